@@ -1,0 +1,281 @@
+"""One population decode step, written as its plain definition (test infrastructure).
+
+What is computed is the step the method section repeats for every candidate
+of a population during LLM aggregation: the assigned model reads the K
+concatenated candidates of its group as context (already in the candidate's
+KV cache) and produces the next token of the refined trajectory, together
+with that token's log-probability under the model (the per-token
+log-probabilities that the fitness signal, Eq. 1, consumes).  Algorithm 1's
+aggregation line runs this step for the whole population at once.
+
+The paper gives no architecture for the models it serves; the decoder below
+is the pre-norm GQA transformer of the Qwen3 family that the workloads are
+shaped after (RMSNorm, per-head QK-RMSNorm, rotate-half RoPE, SwiGLU FFN).
+Sampling is exact full-vocabulary categorical sampling at temperature T (the
+temperature-1, top-k off, top-p 1 row of the generation hyper-parameter
+table), realised as Gumbel-max with counter-based noise (see philox.py).
+
+Paged KV layout (per layer; page size 16):
+    K pool [num_pages][n_kv_heads][16][head_dim]   (token-major tile)
+    V pool [num_pages][n_kv_heads][head_dim][16]   (dim-major tile)
+    logical key t of candidate i -> page page_table[i][t // 16], slot t % 16.
+
+Everything here is float64.  bf16 storage points of the GPU path are mirrored
+with round-to-nearest-even when ``mirror`` is true.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+from .bf16 import round_bf16
+from .philox import gumbel_noise
+
+PAGE = 16
+
+
+def _ident(x):
+    return np.asarray(x, np.float64)
+
+
+def _f32(x):
+    return np.asarray(x, np.float64).astype(np.float32).astype(np.float64)
+
+
+# ------------------------------------------------------------------ elementary ops
+def rms_norm(x, gain, eps):
+    """x / sqrt(mean(x^2) + eps) * gain over the last axis."""
+    x = np.asarray(x, np.float64)
+    inv = 1.0 / np.sqrt(np.mean(x * x, axis=-1, keepdims=True) + eps)
+    return x * inv * np.asarray(gain, np.float64)
+
+
+def rope_rotate(u, position, theta):
+    """Rotate-half RoPE of the last axis (size d) at an integer position.
+
+    For m < d/2 the pair (u[m], u[m + d/2]) is rotated by the angle
+    position * theta^(-2m/d).  ``position`` may be a scalar or broadcast over
+    the leading axes (``position`` broadcastable to ``u.shape[:-1]``).
+    """
+    u = np.asarray(u, np.float64)
+    d = u.shape[-1]
+    h = d // 2
+    inv_freq = np.power(float(theta), -2.0 * np.arange(h, dtype=np.float64) / d)
+    phi = np.asarray(position, np.float64)[..., None] * inv_freq
+    c, s = np.cos(phi), np.sin(phi)
+    a, b = u[..., :h], u[..., h:]
+    return np.concatenate([a * c - b * s, b * c + a * s], axis=-1)
+
+
+def silu(z):
+    z = np.asarray(z, np.float64)
+    return z / (1.0 + np.exp(-z))
+
+
+def log_softmax(z):
+    z = np.asarray(z, np.float64)
+    m = np.max(z, axis=-1, keepdims=True)
+    return z - (m + np.log(np.sum(np.exp(z - m), axis=-1, keepdims=True)))
+
+
+# ------------------------------------------------------------------ attention
+def attention_dense(q, K, V, scale):
+    """Decode attention of one candidate.
+
+    q [hq, d]; K, V [hkv, L, d].  Query head j reads KV head j // (hq / hkv)
+    (contiguous groups).  o_j = softmax(scale * K_c q_j) V_c.  Returns [hq, d].
+    """
+    q = np.asarray(q, np.float64)
+    K = np.asarray(K, np.float64)
+    V = np.asarray(V, np.float64)
+    hq, d = q.shape
+    hkv = K.shape[0]
+    g = hq // hkv
+    out = np.empty((hq, d))
+    for j in range(hq):
+        c = j // g
+        s = (K[c] @ q[j]) * scale
+        a = np.exp(s - s.max())
+        a /= a.sum()
+        out[j] = a @ V[c]
+    return out
+
+
+def split_bounds(n_keys, num_splits, page=PAGE):
+    """Key ranges of a page-granular split: split s owns logical pages
+    [s * ceil(P/S), (s + 1) * ceil(P/S)) of the candidate's P pages."""
+    n_pages = -(-n_keys // page)
+    per = -(-n_pages // num_splits)
+    out = []
+    for s in range(num_splits):
+        lo = min(s * per * page, n_keys)
+        hi = min((s + 1) * per * page, n_keys)
+        out.append((lo, hi))
+    return out
+
+
+def attention_split(q, K, V, scale, bounds):
+    """The same attention computed split-wise and combined.
+
+    Each split s over keys [lo, hi) yields m_s = max score (-inf when empty),
+    l_s = sum exp(score - m_s), acc_s = sum exp(score - m_s) V.  The combine
+    takes m = max_s m_s and o = sum_s e^(m_s - m) acc_s / sum_s e^(m_s - m) l_s.
+    """
+    q = np.asarray(q, np.float64)
+    hq, d = q.shape
+    hkv = K.shape[0]
+    g = hq // hkv
+    out = np.empty((hq, d))
+    for j in range(hq):
+        c = j // g
+        ms, ls, accs = [], [], []
+        for lo, hi in bounds:
+            if hi <= lo:
+                ms.append(-np.inf)
+                ls.append(0.0)
+                accs.append(np.zeros(d))
+                continue
+            s = (np.asarray(K[c, lo:hi], np.float64) @ q[j]) * scale
+            m = s.max()
+            e = np.exp(s - m)
+            ms.append(m)
+            ls.append(e.sum())
+            accs.append(e @ np.asarray(V[c, lo:hi], np.float64))
+        m = max(ms)
+        w = np.array([np.exp(mi - m) if np.isfinite(mi) else 0.0 for mi in ms])
+        out[j] = sum(wi * a for wi, a in zip(w, accs)) / float(np.dot(w, ls))
+    return out
+
+
+def gather_kv(k_pool, v_pool, pages, n_keys):
+    """Logical K, V [hkv, n_keys, d] of one candidate from its page list."""
+    t = np.arange(n_keys)
+    pg = np.asarray(pages, np.int64)[t // PAGE]
+    sl = t % PAGE
+    K = np.asarray(k_pool)[pg, :, sl, :]          # [L, hkv, d]
+    V = np.asarray(v_pool)[pg, :, :, sl]          # [L, hkv, d]
+    return (np.transpose(K, (1, 0, 2)).astype(np.float64),
+            np.transpose(V, (1, 0, 2)).astype(np.float64))
+
+
+def paged_attention(q, k_pool, v_pool, page_table, seq_lens, scale):
+    """Decode attention for a population: q [N, hq, d] -> [N, hq, d]."""
+    q = np.asarray(q, np.float64)
+    out = np.empty_like(q)
+    for i in range(q.shape[0]):
+        K, V = gather_kv(k_pool, v_pool, page_table[i], int(seq_lens[i]))
+        out[i] = attention_dense(q[i], K, V, scale)
+    return out
+
+
+def append_kv(k_pool, v_pool, page_table, positions, k, v):
+    """Write key/value number p_i of every candidate into its page slot."""
+    for i, p in enumerate(np.asarray(positions, np.int64)):
+        page = int(page_table[i][p // PAGE])
+        k_pool[page, :, p % PAGE, :] = k[i]
+        v_pool[page, :, :, p % PAGE] = v[i]
+
+
+# ------------------------------------------------------------------ decoder
+def decoder_layer(shape, lw, x, positions, k_pool, v_pool, page_table, mirror=True):
+    """One pre-norm GQA decoder layer for the population (updates x, appends KV).
+
+    x [N, H] residual stream.  Steps: RMSNorm, QKV projection, per-head
+    QK-RMSNorm, RoPE at p_i, append k and v as key p_i, attention over keys
+    0..p_i, output projection + residual, RMSNorm, SwiGLU FFN + residual.
+    """
+    rb = round_bf16 if mirror else _ident
+    keep32 = _f32 if mirror else _ident
+    N = x.shape[0]
+    hq, hkv, D = shape.n_q_heads, shape.n_kv_heads, shape.head_dim
+    F = shape.ffn
+    eps = shape.rms_eps
+    pos = np.asarray(positions, np.int64)
+
+    h = rb(rms_norm(x, lw["attn_norm"], eps))
+    qkv = h @ np.asarray(lw["w_qkv"], np.float64).T
+    q = qkv[:, : hq * D].reshape(N, hq, D)
+    k = qkv[:, hq * D: (hq + hkv) * D].reshape(N, hkv, D)
+    v = qkv[:, (hq + hkv) * D:].reshape(N, hkv, D)
+    if shape.qk_norm:
+        q = rms_norm(q, lw["q_norm"], eps)
+        k = rms_norm(k, lw["k_norm"], eps)
+    q = rb(rope_rotate(q, pos[:, None], shape.rope_theta))
+    k = rb(rope_rotate(k, pos[:, None], shape.rope_theta))
+    v = rb(v)
+    append_kv(k_pool, v_pool, page_table, pos, k, v)
+    o = paged_attention(q, k_pool, v_pool, page_table, pos + 1, 1.0 / np.sqrt(D))
+    o = rb(o).reshape(N, hq * D)
+    x = keep32(x + o @ np.asarray(lw["w_o"], np.float64).T)
+    h2 = rb(rms_norm(x, lw["ffn_norm"], eps))
+    gu = h2 @ np.asarray(lw["w_gate_up"], np.float64).T
+    a = rb(silu(gu[:, :F]) * gu[:, F:])
+    x = keep32(x + a @ np.asarray(lw["w_down"], np.float64).T)
+    return x
+
+
+def lm_logits(shape, final_norm, lm_head, x, mirror=True, chunk=16384):
+    """logits = RMSNorm(x) * g_final . W_lm^T, computed in vocab chunks."""
+    rb = round_bf16 if mirror else _ident
+    hf = rb(rms_norm(x, final_norm, shape.rms_eps))
+    V = lm_head.shape[0]
+    out = np.empty((x.shape[0], V))
+    for v0 in range(0, V, chunk):
+        out[:, v0:v0 + chunk] = hf @ np.asarray(lm_head[v0:v0 + chunk], np.float64).T
+    return _f32(out) if mirror else out
+
+
+def logprob_sample(logits, temperature, seed, uids, positions, noise=None,
+                   decision_dtype=np.float32):
+    """Gumbel-max sample and its log-probability, per candidate.
+
+    z = logits / T;  id = argmax_v (z_v + G_v) with ties to the lowest v;
+    lp = log_softmax(z)[id].  T == 0 means greedy: id = argmax logits and lp
+    from T = 1.  The argmax decision is taken in ``decision_dtype`` (the
+    kernel's fp32); ``gap`` is the float64 top-1 minus top-2 perturbed value,
+    so a caller can tell decisions that rounding may flip.
+    ``noise`` [N, V] overrides the Philox noise (for pins).
+    Returns ids int64 [N], lps float64 [N], gaps float64 [N].
+    """
+    logits = np.asarray(logits, np.float64)
+    N, V = logits.shape
+    ids = np.empty(N, np.int64)
+    lps = np.empty(N)
+    gaps = np.empty(N)
+    for i in range(N):
+        if temperature == 0:
+            z = logits[i]
+            pert = z
+            pert_dec = z.astype(decision_dtype)
+        else:
+            z = logits[i] / float(temperature)
+            G = (gumbel_noise(V, int(positions[i]), int(uids[i]), int(seed)) if noise is None
+                 else np.asarray(noise[i], np.float64))
+            pert = z + G
+            pert_dec = z.astype(decision_dtype) + G.astype(decision_dtype)
+        ids[i] = int(np.argmax(pert_dec))          # first maximum = lowest index
+        top2 = np.partition(pert, V - 2)[V - 2:] if V > 1 else np.array([-np.inf, pert[0]])
+        gaps[i] = float(top2.max() - top2.min())
+        lps[i] = log_softmax(z)[ids[i]]
+    return ids, lps, gaps
+
+
+def decode_step(shape, weights, k_pools, v_pools, page_table, tokens, positions, uids,
+                seed, temperature, mirror=True, layers=None):
+    """One decode step for a population.
+
+    weights: mapping with "embed" [V, H] (row-indexable), "lm_head" [V, H],
+    "final_norm" [H] and "layers" (sequence of per-layer mappings with
+    attn_norm, w_qkv, q_norm, k_norm, w_o, ffn_norm, w_gate_up, w_down).
+    k_pools / v_pools: per-layer pools in the paged layout (float arrays,
+    modified in place by the KV append).  positions p_i = keys already cached.
+    Returns dict(ids, lps, gaps, logits, x).
+    """
+    tokens = np.asarray(tokens, np.int64)
+    x = np.asarray(weights["embed"][tokens], np.float64)
+    n_layers = shape.n_layers if layers is None else layers
+    for l in range(n_layers):
+        x = decoder_layer(shape, weights["layers"][l], x, positions, k_pools[l], v_pools[l],
+                          page_table, mirror)
+    logits = lm_logits(shape, weights["final_norm"], weights["lm_head"], x, mirror)
+    ids, lps, gaps = logprob_sample(logits, temperature, seed, uids, positions)
+    return {"ids": ids, "lps": lps, "gaps": gaps, "logits": logits, "x": x}

@@ -1,0 +1,170 @@
+"""Whole-step pins of the oracle (CPU only).
+
+The oracle's incremental paged decode, fed one token at a time from an empty
+cache, must reproduce the logits of an independent full-sequence causal
+forward of the same architecture in the ``transformers`` library (Qwen3:
+RMSNorm, per-head QK-RMSNorm, rotate-half RoPE, GQA, SwiGLU) -- a library
+special case that exercises every layer step, the KV append slots and the
+RoPE positions.  Further invariants: page-permutation invariance of a whole
+step, the zero-block special case and determinism.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import decoder as od
+from paper_2604_07725_amd.synth import ModelShape
+
+SHAPE = ModelShape(n_layers=2, hidden=64, n_q_heads=4, n_kv_heads=2, head_dim=16, ffn=96,
+                   vocab=97, rope_theta=1.0e4)
+
+
+def _weights(shape, rng, scale=0.2):
+    H, F, V = shape.hidden, shape.ffn, shape.vocab
+    layers = []
+    for _ in range(shape.n_layers):
+        layers.append({
+            "attn_norm": 1 + 0.1 * rng.standard_normal(H),
+            "w_qkv": scale * rng.standard_normal((shape.qkv_dim, H)),
+            "q_norm": 1 + 0.1 * rng.standard_normal(shape.head_dim),
+            "k_norm": 1 + 0.1 * rng.standard_normal(shape.head_dim),
+            "w_o": scale * rng.standard_normal((H, shape.q_dim)),
+            "ffn_norm": 1 + 0.1 * rng.standard_normal(H),
+            "w_gate_up": scale * rng.standard_normal((2 * F, H)),
+            "w_down": scale * rng.standard_normal((H, F)),
+        })
+    return {"embed": rng.standard_normal((V, H)), "lm_head": scale * rng.standard_normal((V, H)),
+            "final_norm": 1 + 0.1 * rng.standard_normal(H), "layers": layers}
+
+
+def _hf_model(shape, w):
+    from transformers import Qwen3Config, Qwen3ForCausalLM
+    cfg = Qwen3Config(vocab_size=shape.vocab, hidden_size=shape.hidden,
+                      intermediate_size=shape.ffn, num_hidden_layers=shape.n_layers,
+                      num_attention_heads=shape.n_q_heads, num_key_value_heads=shape.n_kv_heads,
+                      head_dim=shape.head_dim, rms_norm_eps=shape.rms_eps,
+                      rope_parameters={"rope_theta": shape.rope_theta, "rope_type": "default"},
+                      max_position_embeddings=256, tie_word_embeddings=False,
+                      attention_bias=False, hidden_act="silu")
+    cfg._attn_implementation = "eager"
+    m = Qwen3ForCausalLM(cfg).to(torch.float64).eval()
+    T = lambda a: torch.from_numpy(np.asarray(a, np.float64))  # noqa: E731
+    qd, kd = shape.q_dim, shape.kv_dim
+    F = shape.ffn
+    with torch.no_grad():
+        m.model.embed_tokens.weight.copy_(T(w["embed"]))
+        m.lm_head.weight.copy_(T(w["lm_head"]))
+        m.model.norm.weight.copy_(T(w["final_norm"]))
+        for l, lw in enumerate(w["layers"]):
+            layer = m.model.layers[l]
+            layer.input_layernorm.weight.copy_(T(lw["attn_norm"]))
+            layer.post_attention_layernorm.weight.copy_(T(lw["ffn_norm"]))
+            a = layer.self_attn
+            a.q_proj.weight.copy_(T(lw["w_qkv"][:qd]))
+            a.k_proj.weight.copy_(T(lw["w_qkv"][qd:qd + kd]))
+            a.v_proj.weight.copy_(T(lw["w_qkv"][qd + kd:]))
+            a.o_proj.weight.copy_(T(lw["w_o"]))
+            a.q_norm.weight.copy_(T(lw["q_norm"]))
+            a.k_norm.weight.copy_(T(lw["k_norm"]))
+            layer.mlp.gate_proj.weight.copy_(T(lw["w_gate_up"][:F]))
+            layer.mlp.up_proj.weight.copy_(T(lw["w_gate_up"][F:]))
+            layer.mlp.down_proj.weight.copy_(T(lw["w_down"]))
+    return m
+
+
+def _empty_pools(shape, n_pages):
+    kp = [np.zeros((n_pages, shape.n_kv_heads, 16, shape.head_dim)) for _ in range(shape.n_layers)]
+    vp = [np.zeros((n_pages, shape.n_kv_heads, shape.head_dim, 16)) for _ in range(shape.n_layers)]
+    return kp, vp
+
+
+def test_incremental_paged_decode_equals_transformers_causal_forward():
+    rng = np.random.default_rng(7)
+    w = _weights(SHAPE, rng)
+    N, T = 2, 37                      # crosses two page boundaries
+    seqs = rng.integers(0, SHAPE.vocab, size=(N, T))
+    pages_per = (T + 15) // 16
+    perm = rng.permutation(N * pages_per)
+    pt = perm.reshape(N, pages_per)
+    kp, vp = _empty_pools(SHAPE, N * pages_per)
+    oracle_logits = np.empty((N, T, SHAPE.vocab))
+    for t in range(T):
+        out = od.decode_step(SHAPE, w, kp, vp, pt, seqs[:, t], np.full(N, t), np.arange(N),
+                             seed=1, temperature=1.0, mirror=False)
+        oracle_logits[:, t] = out["logits"]
+    m = _hf_model(SHAPE, w)
+    with torch.no_grad():
+        ref = m(input_ids=torch.from_numpy(seqs)).logits.numpy()
+    # transformers keeps its RMSNorm and RoPE tables in float32; the bound
+    # covers that, while any structural slip gives O(0.1) differences
+    err = np.abs(oracle_logits - ref).max()
+    assert err < 2e-5 * np.abs(ref).max(), err
+
+
+def test_whole_step_invariant_under_page_permutation_and_deterministic():
+    rng = np.random.default_rng(8)
+    w = _weights(SHAPE, rng)
+    N = 3
+    lens = np.array([5, 33, 20])
+    need = (lens + 1 + 15) // 16
+    P = int(need.sum())
+    kp = [rng.standard_normal((P, 2, 16, 16)) for _ in range(2)]
+    vp = [rng.standard_normal((P, 2, 16, 16)) for _ in range(2)]
+    pt = np.full((N, need.max()), -1)
+    c = 0
+    for i in range(N):
+        pt[i, :need[i]] = np.arange(c, c + need[i])
+        c += need[i]
+    perm = rng.permutation(P)
+    kp2, vp2 = [], []
+    for l in range(2):
+        a = np.empty_like(kp[l]); a[perm] = kp[l]; kp2.append(a)
+        b = np.empty_like(vp[l]); b[perm] = vp[l]; vp2.append(b)
+    pt2 = np.where(pt >= 0, perm[np.maximum(pt, 0)], -1)
+    toks = np.array([1, 50, 96])
+    args = dict(tokens=toks, positions=lens, uids=np.array([10, 11, 12]), seed=3, temperature=1.0)
+    a = od.decode_step(SHAPE, w, [k.copy() for k in kp], [v.copy() for v in vp], pt, **args)
+    b = od.decode_step(SHAPE, w, kp2, vp2, pt2, **args)
+    c2 = od.decode_step(SHAPE, w, [k.copy() for k in kp], [v.copy() for v in vp], pt, **args)
+    np.testing.assert_array_equal(a["logits"], b["logits"])
+    np.testing.assert_array_equal(a["ids"], b["ids"])
+    np.testing.assert_array_equal(a["logits"], c2["logits"])
+
+
+def test_zero_blocks_reduce_to_embedding_head():
+    """With W_o = 0 and W_down = 0 each layer leaves x unchanged, so the logits
+    are RMSNorm(E[t]) * g_final . W_lm^T, whatever the KV cache holds."""
+    rng = np.random.default_rng(9)
+    w = _weights(SHAPE, rng)
+    for lw in w["layers"]:
+        lw["w_o"] = np.zeros_like(lw["w_o"])
+        lw["w_down"] = np.zeros_like(lw["w_down"])
+    kp, vp = _empty_pools(SHAPE, 4)
+    for k in kp + vp:
+        k[:] = rng.standard_normal(k.shape)
+    pt = np.array([[0, 1], [2, 3]])
+    toks = np.array([3, 40])
+    out = od.decode_step(SHAPE, w, kp, vp, pt, toks, np.array([20, 7]), np.array([0, 1]), 0, 1.0,
+                         mirror=False)
+    x = w["embed"][toks]
+    hf = x / np.sqrt((x * x).mean(-1, keepdims=True) + SHAPE.rms_eps) * w["final_norm"]
+    np.testing.assert_allclose(out["logits"], hf @ w["lm_head"].T, rtol=1e-12, atol=1e-12)
+
+
+def test_mirror_rounds_only_storage_points():
+    """mirror=True differs from the pure definition only by bf16 storage rounding:
+    small but non-zero relative change of the logits."""
+    rng = np.random.default_rng(10)
+    w = _weights(SHAPE, rng)
+    kp, vp = _empty_pools(SHAPE, 4)
+    for k in kp + vp:
+        k[:] = rng.standard_normal(k.shape)
+    pt = np.array([[0, 1], [2, 3]])
+    args = dict(tokens=np.array([3, 40]), positions=np.array([20, 7]), uids=np.array([0, 1]),
+                seed=0, temperature=1.0)
+    a = od.decode_step(SHAPE, w, [k.copy() for k in kp], [v.copy() for v in vp], pt,
+                       mirror=False, **args)
+    b = od.decode_step(SHAPE, w, [k.copy() for k in kp], [v.copy() for v in vp], pt,
+                       mirror=True, **args)
+    rel = np.abs(a["logits"] - b["logits"]).max() / np.abs(a["logits"]).max()
+    assert 1e-5 < rel < 5e-2, rel
