@@ -1,0 +1,291 @@
+/*
+ * sevo.h — C ABI of libsevo.so: the population-batched decode step of
+ * verifier-free evolution (Squeeze Evolve, arXiv 2604.07725) on one MI355X.
+ *
+ * What the library computes.  In each evolution loop the method hands every
+ * group of K candidates to a model, which reads them as context and decodes one
+ * refined candidate (method section, "Recombination" paragraph; Algorithm 1,
+ * aggregation line).  The hot path is therefore one autoregressive decode step
+ * for a whole population: N candidates, each with its own KV cache of ragged
+ * length, advanced one token per step, returning the sampled token id and its
+ * log-probability (the per-token log-probabilities the fitness signal of
+ * Eq. 1 is built from; full-vocabulary sampling at temperature T as in the
+ * generation hyper-parameter table).
+ *
+ * Conventions shared by every entry point
+ *   - All tensors are caller-owned DEVICE memory unless a field says "host".
+ *     The library never allocates on the hot path; scratch space comes from a
+ *     caller-provided workspace sized by the matching *_workspace_bytes query.
+ *     sevo_init_model allocates once (the RoPE table) and sevo_free_model
+ *     releases it.
+ *   - bf16 = IEEE binary32 with the low 16 bits dropped, stored as uint16.
+ *   - Calls are stream-ordered and asynchronous: they enqueue kernels on
+ *     `stream` (a hipStream_t; NULL = the legacy default stream) and return
+ *     without synchronising.  Outputs are valid once the stream reaches them.
+ *   - Every device pointer must be 16-byte aligned; row strides are in
+ *     elements.
+ *   - Errors: a non-zero sevo_status; outputs are then undefined.  No C++
+ *     exception or abort crosses the ABI.  sevo_last_error() returns a
+ *     thread-local message describing the most recent failure on the calling
+ *     thread.  Host-visible scalars are validated on every call; the contents
+ *     of device-resident page tables, lengths and positions are NOT validated
+ *     on the hot path (sevo_validate_paging checks them on demand).
+ *   - Paged KV cache, one K pool and one V pool per layer, page size 16:
+ *       K pool  bf16 [num_pages][n_kv_heads][16][head_dim]   token-major tile
+ *       V pool  bf16 [num_pages][n_kv_heads][head_dim][16]   dim-major tile
+ *     Logical key t of candidate i lives in physical page
+ *     page_table[i * max_pages + t / 16], slot t % 16.  One page table serves
+ *     all layers.  Physical page order is arbitrary (any permutation gives
+ *     bit-identical results).
+ *   - GQA: query head j reads KV head j / (n_q_heads / n_kv_heads).
+ */
+#ifndef SEVO_H
+#define SEVO_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t sevo_status;
+#define SEVO_OK 0
+#define SEVO_ERR_INVALID_ARGUMENT 1   /* null pointer, bad size, misalignment   */
+#define SEVO_ERR_UNSUPPORTED 2        /* shape outside the supported set         */
+#define SEVO_ERR_WORKSPACE_TOO_SMALL 3
+#define SEVO_ERR_OUT_OF_MEMORY 4      /* only sevo_init_model allocates          */
+#define SEVO_ERR_HIP 5                /* a HIP runtime call or launch failed     */
+#define SEVO_ERR_BAD_PAGE_TABLE 6     /* sevo_validate_paging found a bad entry  */
+
+#define SEVO_PAGE_SIZE 16
+
+const char* sevo_status_string(sevo_status s);
+/* Thread-local detail of the most recent failure on this thread ("" if none). */
+const char* sevo_last_error(void);
+/* Library version string, e.g. "sevo 0.1 gfx950". */
+const char* sevo_version(void);
+
+/* ------------------------------------------------------------------ model */
+
+/* Decoder shape.  Supported: head_dim in {64, 128}; n_q_heads % n_kv_heads == 0
+ * with n_q_heads / n_kv_heads in {1, 2, 4, 8}; page_size == 16; hidden, ffn and
+ * n_q_heads * head_dim multiples of 32; qk_norm in {0, 1}; rms_eps > 0. */
+typedef struct {
+  int32_t n_layers, hidden, n_q_heads, n_kv_heads, head_dim, ffn, vocab;
+  int32_t page_size;    /* must be 16 */
+  int32_t max_position; /* RoPE table covers positions [0, max_position) */
+  int32_t qk_norm;      /* 1: per-head RMSNorm of q and k before RoPE (Qwen3 style) */
+  float rope_theta;     /* rotate-half RoPE base, e.g. 1e6 */
+  float rms_eps;        /* RMSNorm epsilon, e.g. 1e-6 */
+} sevo_model_config;
+
+/* Borrowed bf16 weight pointers (device); they must outlive the model.  The
+ * per-layer members are HOST arrays of n_layers device pointers.  Matrices are
+ * row-major [out][in]:
+ *   embed, lm_head [vocab][hidden];  final_norm, attn_norm, ffn_norm [hidden]
+ *   w_qkv     [(n_q_heads + 2 n_kv_heads) head_dim][hidden]  rows: q, k, v
+ *   q_norm, k_norm [head_dim]        (unused when qk_norm == 0; may be NULL)
+ *   w_o       [hidden][n_q_heads head_dim]
+ *   w_gate_up [2 ffn][hidden]        rows 0..ffn-1 gate, ffn..2ffn-1 up
+ *   w_down    [hidden][ffn] */
+typedef struct {
+  const void* embed;
+  const void* lm_head;
+  const void* final_norm;
+  const void* const* attn_norm;
+  const void* const* w_qkv;
+  const void* const* q_norm;
+  const void* const* k_norm;
+  const void* const* w_o;
+  const void* const* ffn_norm;
+  const void* const* w_gate_up;
+  const void* const* w_down;
+} sevo_weights;
+
+typedef struct sevo_model sevo_model;
+
+/* Validates the shape, copies the pointer tables and builds the RoPE cos/sin
+ * table (angles in double, stored fp32) on the current device.
+ * Errors: INVALID_ARGUMENT, UNSUPPORTED, OUT_OF_MEMORY, HIP. */
+sevo_status sevo_init_model(const sevo_model_config* cfg, const sevo_weights* w,
+                            sevo_model** out);
+void sevo_free_model(sevo_model* m);
+
+/* ------------------------------------------------------------------ attention */
+
+/* Paged GQA split-KV decode attention (one query token per candidate):
+ *   o[i][j] = softmax_t(scale * q[i][j] . K_i[c][t]) V_i[c][t],  t < seq_lens[i],
+ * c = j / (n_q_heads / n_kv_heads).  Each candidate's pages are cut into
+ * splits of ceil(max_pages / num_splits) logical pages; every split yields an
+ * online-softmax partial (running max, sum, weighted V) that a combine pass
+ * merges in split order, so the result is deterministic.
+ *   q        bf16 [n][n_q_heads][head_dim]
+ *   k_pool, v_pool  paged layout above (bf16)
+ *   page_table int32 [n][max_pages];  seq_lens int32 [n], 1 <= len <= 16 max_pages
+ *   out      bf16 [n][n_q_heads][head_dim]
+ *   num_splits 0 = chosen by the library (see sevo_attn_plan_splits)
+ * A page id outside [0, num_pages) contributes no keys (it is never read).
+ * Errors: INVALID_ARGUMENT, UNSUPPORTED, WORKSPACE_TOO_SMALL, HIP. */
+typedef struct {
+  int32_t n, n_q_heads, n_kv_heads, head_dim, page_size, max_pages, num_splits;
+  int64_t num_pages; /* pages in each pool; ids outside [0, num_pages) are skipped */
+  const void* q;
+  const void* k_pool;
+  const void* v_pool;
+  const int32_t* page_table;
+  const int32_t* seq_lens;
+  float scale;
+  void* out;
+  void* workspace;
+  size_t workspace_bytes;
+} sevo_attn_args;
+
+sevo_status sevo_attn_decode(const sevo_attn_args* a, void* stream);
+/* Split count the library uses when num_splits == 0. */
+int32_t sevo_attn_plan_splits(int32_t n, int32_t n_kv_heads, int32_t max_pages);
+/* Workspace for sevo_attn_decode with the given split count (0 = planned). */
+size_t sevo_attn_workspace_bytes(int32_t n, int32_t n_q_heads, int32_t n_kv_heads,
+                                 int32_t head_dim, int32_t max_pages, int32_t num_splits);
+
+/* ------------------------------------------------------------------ sampling */
+
+/* Full-vocabulary log-softmax and Gumbel-max sample, per candidate i:
+ *   z = logits[i] / T;  id = argmax_v (z_v + G_v)  (ties -> lowest v);
+ *   logprob = z_id - logsumexp(z).
+ * G_v = -log(-log u_v), u_v = ((w >> 9) + 0.5) 2^-23 with w the (v & 3)-th
+ * word of Philox4x32-10 (Salmon et al., SC'11) on counter
+ * (v >> 2, position_i, uid_i lo, uid_i hi) and key (seed lo, seed hi).  Noise
+ * is keyed by candidate uid and position, never by call count, so a resumed or
+ * re-ordered population draws the same tokens.  T == 0: greedy argmax, logprob
+ * under T = 1.  T < 0 or non-finite: INVALID_ARGUMENT.
+ *   logits fp32 [n][ld] (first vocab entries used); cand_uid uint64 [n];
+ *   positions int32 [n];  out_tokens int32 [n];  out_logprobs fp32 [n].
+ * Errors: INVALID_ARGUMENT, WORKSPACE_TOO_SMALL, HIP. */
+typedef struct {
+  const float* logits;
+  int32_t n, vocab;
+  int64_t ld;
+  float temperature;
+  uint64_t seed;
+  const uint64_t* cand_uid;
+  const int32_t* positions;
+  int32_t* out_tokens;
+  float* out_logprobs;
+  void* workspace;
+  size_t workspace_bytes;
+} sevo_sample_args;
+
+sevo_status sevo_logprob_sample(const sevo_sample_args* a, void* stream);
+size_t sevo_sample_workspace_bytes(int32_t n, int32_t vocab);
+
+/* ------------------------------------------------------------------ decode step */
+
+/* One decode step of the whole population through the model:
+ *   x = embed[token];  per layer: h = RMSNorm(x) g_attn;  [q|k|v] = h W_qkv^T;
+ *   (qk_norm) q, k <- per-head RMSNorm * g_q / g_k;  RoPE(q, k) at p_i;
+ *   append k, v as key number p_i;  o = attention over keys 0..p_i;
+ *   x += o W_o^T;  h = RMSNorm(x) g_ffn;  x += (silu(h W_g^T) * (h W_u^T)) W_d^T;
+ * then logits = RMSNorm(x) g_final W_lm^T (fp32) and the sampler above.
+ * Storage: residual x fp32; GEMM inputs, q, K/V, attention output and the
+ * SwiGLU product bf16; logits fp32.
+ *   tokens int32 [n];  positions int32 [n] (p_i = keys cached before the step;
+ *   the caller must have a page for slot p_i, and p_i < max_position);
+ *   page_table int32 [n][max_pages];  k_pools, v_pools: HOST arrays of
+ *   n_layers device pool pointers;  cand_uid uint64 [n];
+ *   out_tokens int32 [n];  out_logprobs fp32 [n];
+ *   out_logits fp32 [n][vocab] or NULL (then kept in the workspace).
+ * The library never changes positions or page tables: the caller advances p_i
+ * and allocates pages.  Errors: INVALID_ARGUMENT, UNSUPPORTED,
+ * WORKSPACE_TOO_SMALL, HIP. */
+typedef struct {
+  int32_t n;
+  const int32_t* tokens;
+  const int32_t* positions;
+  const int32_t* page_table;
+  int32_t max_pages;
+  int64_t num_pages; /* pages in each pool (bounds every page access) */
+  void* const* k_pools;
+  void* const* v_pools;
+  const uint64_t* cand_uid;
+  uint64_t seed;
+  float temperature;
+  int32_t num_splits;
+  int32_t* out_tokens;
+  float* out_logprobs;
+  float* out_logits;
+  void* workspace;
+  size_t workspace_bytes;
+} sevo_step_args;
+
+sevo_status sevo_decode_step(sevo_model* m, const sevo_step_args* a, void* stream);
+size_t sevo_step_workspace_bytes(const sevo_model* m, int32_t n, int32_t max_pages,
+                                 int32_t num_splits);
+
+/* ------------------------------------------------------------------ sub-steps
+ * The steps of sevo_decode_step, exposed one by one so each can be checked
+ * and timed on its own.  Same conventions as above. */
+
+/* x[i][:] = embed[tokens[i]][:] as fp32.  embed bf16 [vocab][hidden]; hidden % 8 == 0.
+ * A token id outside [0, vocab) gives a zero row (the table is never read out of range). */
+sevo_status sevo_embed(const void* embed, const int32_t* tokens, int32_t n, int32_t hidden,
+                       int32_t vocab, float* x, void* stream);
+
+/* out[r][:] = bf16(x[r][:] / sqrt(mean(x[r]^2) + eps) * gain), x fp32 [rows][cols],
+ * gain bf16 [cols].  cols % 4 == 0. */
+sevo_status sevo_rmsnorm(const float* x, const void* gain, int32_t rows, int32_t cols,
+                         float eps, void* out, void* stream);
+
+/* Y = X W^T with X bf16 [m][k] (row stride ldx), W bf16 [n_out][k], fp32
+ * accumulation on the matrix cores, then the epilogue:
+ *   SEVO_LINEAR_STORE  out fp32 [m][n_out]  = Y
+ *   SEVO_LINEAR_ADD    out fp32 [m][n_out] += Y          (residual update)
+ *   SEVO_LINEAR_SWIGLU out bf16 [m][n_out/2] = silu(Y[:, :n_out/2]) * Y[:, n_out/2:]
+ * k % 32 == 0; n_out % 64 == 0 (SWIGLU: n_out % 128 == 0); ldx % 8 == 0.
+ * k_splits 0 = chosen by the library. */
+#define SEVO_LINEAR_STORE 0
+#define SEVO_LINEAR_ADD 1
+#define SEVO_LINEAR_SWIGLU 2
+typedef struct {
+  int32_t m, n_out, k, ldx, mode, k_splits;
+  const void* x;
+  const void* w;
+  void* out;
+  void* workspace;
+  size_t workspace_bytes;
+} sevo_linear_args;
+
+sevo_status sevo_linear(const sevo_linear_args* a, void* stream);
+size_t sevo_linear_workspace_bytes(int32_t m, int32_t n_out, int32_t k, int32_t k_splits);
+
+/* The fused QK-RMSNorm + RoPE + KV append of one layer.
+ *   qkv fp32 [n][(n_q_heads + 2 n_kv_heads) head_dim] (the QKV projection)
+ *   q_out bf16 [n][n_q_heads][head_dim]: RoPE(RMSNorm(q) g_q) at p_i
+ *   K/V pools: slot p_i of every candidate receives RoPE(RMSNorm(k) g_k) and v.
+ * Uses the model's RoPE table, norm gains and shape (layer selects the gains). */
+sevo_status sevo_qk_norm_rope_append(const sevo_model* m, int32_t layer, const float* qkv,
+                                     int32_t n, const int32_t* positions,
+                                     const int32_t* page_table, int32_t max_pages,
+                                     int64_t num_pages, void* q_out, void* k_pool, void* v_pool,
+                                     void* stream);
+
+/* ------------------------------------------------------------------ utilities */
+
+/* Synthetic-input generator (device twin of the host generator): element e of
+ * dst (e < count) = bf16_rne(fp32(s - 131070) * mul [+ add]) with s the sum of
+ * the four 16-bit fields of SplitMix64(key + (offset + e + 1) 0x9E3779B97F4A7C15).
+ * Pure input generation, not part of the decode step. */
+sevo_status sevo_fill_normal_bf16(void* dst, int64_t count, uint64_t key, int64_t offset,
+                                  float mul, float add, int32_t use_add, void* stream);
+
+/* Copies page_table / lengths to the host and checks that every logical page
+ * a candidate needs (ceil(len_i / 16) pages) is in [0, num_pages) and that no
+ * physical page is used twice.  Synchronises the stream.  Returns
+ * SEVO_ERR_BAD_PAGE_TABLE with a message on the first violation. */
+sevo_status sevo_validate_paging(const int32_t* page_table, const int32_t* lengths, int32_t n,
+                                 int32_t max_pages, int64_t num_pages, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SEVO_H */

@@ -1,0 +1,324 @@
+// Paged GQA split-KV decode attention for gfx950 (one query token per
+// candidate), plus the cross-split combine.
+//
+// Work decomposition: one 256-thread workgroup per (split, kv head, candidate).
+// A split is a run of `chunk` logical pages of the candidate; its four waves
+// take every fourth page, each keeping its own online-softmax state for the
+// G = hq / hkv query heads that share the kv head, and merge through LDS at the
+// end.  The combine kernel merges the splits of a (candidate, head) in split
+// order, so results are deterministic and independent of the physical page
+// order.
+//
+// Per page and wave (tile = 16 tokens x D dims, 4 KB at D = 128):
+//   QK  lane (t = lane/4, u = lane%4) loads D/32 16-byte chunks of key t
+//       (chunks u, u+4, ...), forms G partial dot products with v_dot2
+//       (bf16 pairs, fp32 accumulate), and a 2-step quad reduction completes
+//       the score.  Scores are pre-scaled by scale*log2(e) so exp2 is used.
+//   softmax  page max over the 16 tokens by lane shuffles; running max,
+//       rescale factor and p = exp2(s - m) per head (wave-uniform max).
+//   P   lanes holding token t (u == 0) write bf16 p to a per-wave LDS strip;
+//       every lane reads the 8 p values of its token half as 4 packed words.
+//   PV  the V tile is dim-major [D][16] so one 32-bit word holds two tokens of
+//       one dim: lane (dim 32*ii + lane/2, token half lane%2) accumulates
+//       p . v with v_dot2 over token pairs.  Each 16-byte V load is one
+//       contiguous 1 KB wavefront access.
+// Loads for the next page are issued before the current page is consumed
+// (register double buffering), and page ids two pages ahead.
+#include "common.h"
+#include "kernels.h"
+
+namespace sevo {
+
+template <int D>
+struct PageRegs {
+  u32x4 k[D / 32];
+  u32x4 v[D / 32];
+};
+
+template <int D>
+__device__ __forceinline__ void load_page(PageRegs<D>& r, const bf16_t* __restrict__ kpool,
+                                          const bf16_t* __restrict__ vpool, size_t tile, int t,
+                                          int u, int dl, int h) {
+  constexpr int NI = D / 32;
+  const bf16_t* kt = kpool + tile * (kPage * D);
+  const bf16_t* vt = vpool + tile * (kPage * D);
+#pragma unroll
+  for (int ii = 0; ii < NI; ++ii)
+    r.k[ii] = __builtin_nontemporal_load(
+        reinterpret_cast<const u32x4*>(kt + t * D + (u + 4 * ii) * 8));
+#pragma unroll
+  for (int ii = 0; ii < NI; ++ii)
+    r.v[ii] = __builtin_nontemporal_load(
+        reinterpret_cast<const u32x4*>(vt + (32 * ii + dl) * kPage + h * 8));
+}
+
+template <int D, int G>
+__global__ __launch_bounds__(256, (G <= 4 ? 2 : 1)) void attn_split_kernel(
+    const bf16_t* __restrict__ q, const bf16_t* __restrict__ kpool,
+    const bf16_t* __restrict__ vpool, const int32_t* __restrict__ page_table, int max_pages,
+    int64_t num_pages, const int32_t* __restrict__ seq_lens, int len_add, int hkv, int chunk, int S,
+    float qk_scale_log2, float* __restrict__ part_ml, float* __restrict__ part_acc) {
+  constexpr int NI = D / 32;
+  const int s = blockIdx.x;
+  const int c = blockIdx.y;
+  const int i = blockIdx.z;
+  const int hq = hkv * G;
+  int len = seq_lens[i] + len_add;
+  len = len < 0 ? 0 : (len > max_pages * kPage ? max_pages * kPage : len);
+  const int npg = (len + kPage - 1) / kPage;
+  const int pbeg = s * chunk;
+  if (pbeg >= npg) return;  // empty split: the combine pass skips it
+  const int pend = min(npg, pbeg + chunk);
+
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int t = lane >> 2, u = lane & 3;   // QK layout
+  const int dl = lane >> 1, h = lane & 1;  // PV layout
+
+  __shared__ __align__(16) bf16_t p_lds[4][G][kPage];
+  __shared__ float w_m[4][G], w_l[4][G];
+  __shared__ float w_acc[4][G][D];
+
+  // q fragments of the G heads for this lane's dims
+  uint32_t qf[G][NI][4];
+#pragma unroll
+  for (int j = 0; j < G; ++j) {
+    const bf16_t* qh = q + ((size_t)i * hq + (size_t)c * G + j) * D;
+#pragma unroll
+    for (int ii = 0; ii < NI; ++ii) {
+      u32x4 w = *reinterpret_cast<const u32x4*>(qh + (u + 4 * ii) * 8);
+      qf[j][ii][0] = w.x; qf[j][ii][1] = w.y; qf[j][ii][2] = w.z; qf[j][ii][3] = w.w;
+    }
+  }
+
+  float m_run[G], l_run[G], acc[G][NI];
+#pragma unroll
+  for (int j = 0; j < G; ++j) {
+    m_run[j] = -INFINITY;
+    l_run[j] = 0.f;
+#pragma unroll
+    for (int ii = 0; ii < NI; ++ii) acc[j][ii] = 0.f;
+  }
+
+  const int32_t* ptr = page_table + (size_t)i * max_pages;
+  auto tile_of = [&](int pg) -> size_t {
+    int id = ptr[pg];
+    if (id < 0 || (int64_t)id >= num_pages) id = -1;
+    return id < 0 ? (size_t)0xFFFFFFFFFFFFFFFFull : (size_t)id * hkv + c;
+  };
+  auto safe = [](size_t tile) -> size_t { return tile == (size_t)-1 ? 0 : tile; };
+
+  auto consume = [&](const PageRegs<D>& r, int pg, bool bad) {
+    int valid = len - pg * kPage;
+    valid = valid > kPage ? kPage : valid;
+    if (bad) valid = 0;
+    float sc[G];
+#pragma unroll
+    for (int j = 0; j < G; ++j) {
+      float a = 0.f;
+#pragma unroll
+      for (int ii = 0; ii < NI; ++ii) {
+        a = dot2_bf16(r.k[ii].x, qf[j][ii][0], a);
+        a = dot2_bf16(r.k[ii].y, qf[j][ii][1], a);
+        a = dot2_bf16(r.k[ii].z, qf[j][ii][2], a);
+        a = dot2_bf16(r.k[ii].w, qf[j][ii][3], a);
+      }
+      a += __shfl_xor(a, 1, kWave);
+      a += __shfl_xor(a, 2, kWave);
+      sc[j] = (t < valid) ? a * qk_scale_log2 : -INFINITY;
+    }
+    float alpha[G];
+#pragma unroll
+    for (int j = 0; j < G; ++j) {
+      float pm = sc[j];
+      pm = fmaxf(pm, __shfl_xor(pm, 4, kWave));
+      pm = fmaxf(pm, __shfl_xor(pm, 8, kWave));
+      pm = fmaxf(pm, __shfl_xor(pm, 16, kWave));
+      pm = fmaxf(pm, __shfl_xor(pm, 32, kWave));
+      const float mn = fmaxf(m_run[j], pm);
+      float p;
+      if (mn == -INFINITY) {
+        alpha[j] = 1.f;
+        p = 0.f;
+      } else {
+        alpha[j] = exp2f(m_run[j] - mn);
+        p = exp2f(sc[j] - mn);
+      }
+      m_run[j] = mn;
+      const bf16_t pb = f32_to_bf16(p);
+      l_run[j] = l_run[j] * alpha[j] + bf16_to_f32(pb);
+      if (u == 0) p_lds[wave][j][t] = pb;
+    }
+    u32x4 pw[G];
+#pragma unroll
+    for (int j = 0; j < G; ++j) pw[j] = *reinterpret_cast<const u32x4*>(&p_lds[wave][j][h * 8]);
+    u32x4 vv[NI];
+#pragma unroll
+    for (int ii = 0; ii < NI; ++ii) vv[ii] = r.v[ii];
+    if (valid < kPage) {
+      // slots past the last key may hold anything (even NaN patterns): zero them
+#pragma unroll
+      for (int ii = 0; ii < NI; ++ii) {
+        const int t0 = h * 8;
+        vv[ii].x = (t0 + 0 >= valid) ? 0u : ((t0 + 1 >= valid) ? (vv[ii].x & 0xFFFFu) : vv[ii].x);
+        vv[ii].y = (t0 + 2 >= valid) ? 0u : ((t0 + 3 >= valid) ? (vv[ii].y & 0xFFFFu) : vv[ii].y);
+        vv[ii].z = (t0 + 4 >= valid) ? 0u : ((t0 + 5 >= valid) ? (vv[ii].z & 0xFFFFu) : vv[ii].z);
+        vv[ii].w = (t0 + 6 >= valid) ? 0u : ((t0 + 7 >= valid) ? (vv[ii].w & 0xFFFFu) : vv[ii].w);
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < G; ++j) {
+#pragma unroll
+      for (int ii = 0; ii < NI; ++ii) {
+        float a = acc[j][ii] * alpha[j];
+        a = dot2_bf16(vv[ii].x, pw[j].x, a);
+        a = dot2_bf16(vv[ii].y, pw[j].y, a);
+        a = dot2_bf16(vv[ii].z, pw[j].z, a);
+        a = dot2_bf16(vv[ii].w, pw[j].w, a);
+        acc[j][ii] = a;
+      }
+    }
+  };
+
+  int pg = pbeg + wave;
+  if (pg < pend) {
+    // register double buffer: A holds page pg, B the next one of this wave
+    PageRegs<D> A, B;
+    size_t tA = tile_of(pg);
+    size_t tB = tile_of(min(pg + 4, pend - 1));
+    load_page<D>(A, kpool, vpool, safe(tA), t, u, dl, h);
+    while (true) {
+      const size_t tC = tile_of(min(pg + 8, pend - 1));
+      load_page<D>(B, kpool, vpool, safe(tB), t, u, dl, h);
+      consume(A, pg, tA == (size_t)-1);
+      pg += 4;
+      if (pg >= pend) break;
+      const size_t tD = tile_of(min(pg + 8, pend - 1));
+      load_page<D>(A, kpool, vpool, safe(tC), t, u, dl, h);
+      consume(B, pg, tB == (size_t)-1);
+      pg += 4;
+      if (pg >= pend) break;
+      tA = tC;
+      tB = tD;
+    }
+  }
+
+  // finish this wave: sum V partials over the two token halves, l over tokens
+#pragma unroll
+  for (int j = 0; j < G; ++j) {
+#pragma unroll
+    for (int ii = 0; ii < NI; ++ii) acc[j][ii] += __shfl_xor(acc[j][ii], 1, kWave);
+    float l = l_run[j];
+    l += __shfl_xor(l, 4, kWave);
+    l += __shfl_xor(l, 8, kWave);
+    l += __shfl_xor(l, 16, kWave);
+    l += __shfl_xor(l, 32, kWave);
+    l_run[j] = l;
+  }
+  if (lane == 0) {
+#pragma unroll
+    for (int j = 0; j < G; ++j) {
+      w_m[wave][j] = m_run[j];
+      w_l[wave][j] = l_run[j];
+    }
+  }
+  if (h == 0) {
+#pragma unroll
+    for (int j = 0; j < G; ++j)
+#pragma unroll
+      for (int ii = 0; ii < NI; ++ii) w_acc[wave][j][32 * ii + dl] = acc[j][ii];
+  }
+  __syncthreads();
+
+  // merge the four waves (fixed order) and store this split's partial
+  for (int idx = threadIdx.x; idx < G * D; idx += 256) {
+    const int j = idx / D;
+    const int e = idx - j * D;
+    float M = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) M = fmaxf(M, w_m[w][j]);
+    float L = 0.f, A = 0.f;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const float mw = w_m[w][j];
+      if (mw != -INFINITY) {
+        const float f = exp2f(mw - M);
+        L += w_l[w][j] * f;
+        A += w_acc[w][j][e] * f;
+      }
+    }
+    const size_t slot = ((size_t)i * hq + (size_t)c * G + j) * S + s;
+    part_acc[slot * D + e] = A;
+    if (e == 0) {
+      part_ml[slot * 2] = M;
+      part_ml[slot * 2 + 1] = L;
+    }
+  }
+}
+
+// Merge the non-empty splits of one (candidate, query head), in split order.
+template <int D>
+__global__ __launch_bounds__(64) void attn_combine_kernel(const float* __restrict__ part_ml,
+                                                          const float* __restrict__ part_acc,
+                                                          const int32_t* __restrict__ seq_lens,
+                                                          int len_add, int max_pages, int chunk, int S, int hq,
+                                                          bf16_t* __restrict__ out) {
+  constexpr int E = D / 64;
+  const int j = blockIdx.x;
+  const int i = blockIdx.y;
+  int len = seq_lens[i] + len_add;
+  len = len < 0 ? 0 : (len > max_pages * kPage ? max_pages * kPage : len);
+  const int npg = (len + kPage - 1) / kPage;
+  int ns = (npg + chunk - 1) / chunk;
+  ns = ns > S ? S : ns;
+  const size_t base = ((size_t)i * hq + j) * S;
+  float M = -INFINITY;
+  for (int s = 0; s < ns; ++s) M = fmaxf(M, part_ml[(base + s) * 2]);
+  float L = 0.f, a[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) a[e] = 0.f;
+  for (int s = 0; s < ns; ++s) {
+    const float ms = part_ml[(base + s) * 2];
+    if (ms == -INFINITY) continue;
+    const float f = exp2f(ms - M);
+    L += part_ml[(base + s) * 2 + 1] * f;
+#pragma unroll
+    for (int e = 0; e < E; ++e) a[e] += part_acc[(base + s) * D + threadIdx.x + 64 * e] * f;
+  }
+  const float inv = L > 0.f ? 1.0f / L : 0.f;
+  bf16_t* o = out + ((size_t)i * hq + j) * D;
+#pragma unroll
+  for (int e = 0; e < E; ++e) o[threadIdx.x + 64 * e] = f32_to_bf16(a[e] * inv);
+}
+
+template <int D, int G>
+static hipError_t launch_attn_t(const AttnArgs& a, hipStream_t st) {
+  const float log2e = 1.4426950408889634f;
+  hipLaunchKernelGGL((attn_split_kernel<D, G>), dim3(a.num_splits, a.hkv, a.n), dim3(256), 0, st,
+                     a.q, a.k_pool, a.v_pool, a.page_table, a.max_pages, a.num_pages, a.seq_lens,
+                     a.len_add, a.hkv, a.chunk, a.num_splits, a.scale * log2e, a.part_ml, a.part_acc);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((attn_combine_kernel<D>), dim3(a.hq, a.n), dim3(64), 0, st, a.part_ml,
+                     a.part_acc, a.seq_lens, a.len_add, a.max_pages, a.chunk, a.num_splits, a.hq, a.out);
+  return hipGetLastError();
+}
+
+hipError_t launch_attn_decode(const AttnArgs& a, hipStream_t st) {
+  if (a.n == 0) return hipSuccess;
+  const int g = a.hq / a.hkv;
+#define SEVO_ATTN_CASE(DD, GG) \
+  if (a.d == DD && g == GG) return launch_attn_t<DD, GG>(a, st);
+  SEVO_ATTN_CASE(128, 1)
+  SEVO_ATTN_CASE(128, 2)
+  SEVO_ATTN_CASE(128, 4)
+  SEVO_ATTN_CASE(128, 8)
+  SEVO_ATTN_CASE(64, 1)
+  SEVO_ATTN_CASE(64, 2)
+  SEVO_ATTN_CASE(64, 4)
+  SEVO_ATTN_CASE(64, 8)
+#undef SEVO_ATTN_CASE
+  return hipErrorInvalidValue;
+}
+
+}  // namespace sevo

@@ -1,0 +1,74 @@
+// Internal launchers of libsevo (C++ linkage, not part of the ABI).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace sevo {
+
+typedef uint16_t bf16_t;
+
+// ---- norm_rope.hip
+hipError_t launch_embed(const bf16_t* embed, const int32_t* tokens, int n, int hidden,
+                        int vocab, float* x, hipStream_t st);
+hipError_t launch_rmsnorm(const float* x, const bf16_t* gain, int rows, int cols, float eps,
+                          bf16_t* out, hipStream_t st);
+struct RopeAppendArgs {
+  const float* qkv;
+  int n, hq, hkv, d;
+  const int32_t* positions;
+  const int32_t* page_table;
+  int max_pages;
+  int64_t num_pages;
+  const float* rope_cos;  // [max_pos][d/2]
+  const float* rope_sin;
+  int max_pos;
+  const bf16_t* q_gain;   // null when qk_norm == 0
+  const bf16_t* k_gain;
+  int qk_norm;
+  float eps;
+  bf16_t* q_out;
+  bf16_t* k_pool;
+  bf16_t* v_pool;
+};
+hipError_t launch_qk_norm_rope_append(const RopeAppendArgs& a, hipStream_t st);
+hipError_t launch_fill_bf16(bf16_t* dst, int64_t count, uint64_t key, int64_t offset, float mul,
+                            float add, int use_add, hipStream_t st);
+
+// ---- attn_decode.hip
+struct AttnArgs {
+  int n, hq, hkv, d, max_pages, num_splits, chunk;
+  int64_t num_pages;
+  const bf16_t* q;
+  const bf16_t* k_pool;
+  const bf16_t* v_pool;
+  const int32_t* page_table;
+  const int32_t* seq_lens;  // keys per candidate = seq_lens[i] + len_add
+  int len_add;
+  float scale;
+  bf16_t* out;
+  float* part_ml;   // [n][hq][S][2]
+  float* part_acc;  // [n][hq][S][d]
+};
+hipError_t launch_attn_decode(const AttnArgs& a, hipStream_t st);
+
+// ---- linear.hip
+struct LinearPlan {
+  int k_splits;
+  int k_chunk;
+};
+LinearPlan plan_linear(int m, int n_out, int k, int k_splits);
+size_t linear_workspace_bytes(int m, int n_out, int k, int k_splits);
+hipError_t launch_linear(int m, int n_out, int k, int ldx, int mode, const LinearPlan& plan,
+                         const bf16_t* x, const bf16_t* w, void* out, float* workspace,
+                         hipStream_t st);
+
+// ---- sample.hip
+constexpr int kSampleChunk = 4096;  // vocab entries per partial workgroup
+size_t sample_workspace_bytes(int n, int vocab);
+hipError_t launch_logprob_sample(const float* logits, int n, int vocab, int64_t ld, float temp,
+                                 uint64_t seed, const uint64_t* uid, const int32_t* positions,
+                                 int32_t* out_tokens, float* out_lp, float* workspace,
+                                 hipStream_t st);
+
+}  // namespace sevo

@@ -1,0 +1,189 @@
+// Embedding gather, RMSNorm, fused QK-RMSNorm + RoPE + paged KV append, and
+// the device twin of the synthetic-input generator.  All are tiny next to the
+// attention and weight streams of a decode step; they are written for
+// coalesced 16-byte accesses and one workgroup (or wave) per row / head.
+#include "common.h"
+#include "kernels.h"
+
+namespace sevo {
+
+// x[i][:] = embed[tokens[i]][:] (bf16 -> fp32).  One 256-thread block per row,
+// 8 bf16 (16 B) per thread per step.  Out-of-range ids produce a zero row.
+__global__ __launch_bounds__(256) void embed_kernel(const bf16_t* __restrict__ embed,
+                                                    const int32_t* __restrict__ tokens,
+                                                    int hidden, int vocab, float* __restrict__ x) {
+  const int i = blockIdx.x;
+  const int tok = tokens[i];
+  const bool ok = tok >= 0 && tok < vocab;
+  const bf16_t* src = embed + (size_t)(ok ? tok : 0) * hidden;
+  float* dst = x + (size_t)i * hidden;
+  for (int c = threadIdx.x * 8; c < hidden; c += 256 * 8) {
+    u32x4 w = *reinterpret_cast<const u32x4*>(src + c);
+    float4 a, b;
+    a.x = ok ? bf16_lo(w.x) : 0.f; a.y = ok ? bf16_hi(w.x) : 0.f;
+    a.z = ok ? bf16_lo(w.y) : 0.f; a.w = ok ? bf16_hi(w.y) : 0.f;
+    b.x = ok ? bf16_lo(w.z) : 0.f; b.y = ok ? bf16_hi(w.z) : 0.f;
+    b.z = ok ? bf16_lo(w.w) : 0.f; b.w = ok ? bf16_hi(w.w) : 0.f;
+    *reinterpret_cast<float4*>(dst + c) = a;
+    *reinterpret_cast<float4*>(dst + c + 4) = b;
+  }
+}
+
+// out[r][:] = bf16(x[r][:] * (1 / sqrt(mean(x^2) + eps)) * gain).
+__global__ __launch_bounds__(256) void rmsnorm_kernel(const float* __restrict__ x,
+                                                      const bf16_t* __restrict__ gain, int cols,
+                                                      float eps, bf16_t* __restrict__ out) {
+  __shared__ float red[4];
+  const float* xr = x + (size_t)blockIdx.x * cols;
+  float ss = 0.f;
+  for (int c = threadIdx.x * 4; c < cols; c += 1024) {
+    float4 v = *reinterpret_cast<const float4*>(xr + c);
+    ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+  }
+  ss = block_sum<4>(ss, red);
+  const float inv = 1.0f / sqrtf(ss / (float)cols + eps);
+  bf16_t* orow = out + (size_t)blockIdx.x * cols;
+  for (int c = threadIdx.x * 4; c < cols; c += 1024) {
+    float4 v = *reinterpret_cast<const float4*>(xr + c);
+    uint2 g = *reinterpret_cast<const uint2*>(gain + c);
+    uint2 o;
+    o.x = pack_bf16x2(v.x * inv * bf16_lo(g.x), v.y * inv * bf16_hi(g.x));
+    o.y = pack_bf16x2(v.z * inv * bf16_lo(g.y), v.w * inv * bf16_hi(g.y));
+    *reinterpret_cast<uint2*>(orow + c) = o;
+  }
+}
+
+// One wave per (candidate, head) of the fused QKV output.  Lane m < d/2 owns
+// the rotate-half pair (m, m + d/2).  q heads -> q_out; k heads -> K pool slot
+// p_i; v heads -> V pool slot p_i (dim-major tile).  Positions outside the
+// RoPE table or page ids outside the pool skip the write (no fault).
+__global__ __launch_bounds__(64) void qk_norm_rope_append_kernel(RopeAppendArgs a) {
+  const int i = blockIdx.x;
+  const int hh = blockIdx.y;
+  const int m = threadIdx.x;
+  const int half = a.d >> 1;
+  const bool act = m < half;
+  const int qkv_ld = (a.hq + 2 * a.hkv) * a.d;
+  const float* src = a.qkv + (size_t)i * qkv_ld + (size_t)hh * a.d;
+  float u0 = act ? src[m] : 0.f;
+  float u1 = act ? src[m + half] : 0.f;
+  const int p = a.positions[i];
+  const bool pos_ok = p >= 0 && p < a.max_pos;
+  if (hh < a.hq + a.hkv) {
+    if (a.qk_norm) {
+      const float ss = wave_sum(u0 * u0 + u1 * u1);
+      const float inv = 1.0f / sqrtf(ss / (float)a.d + a.eps);
+      const bf16_t* g = hh < a.hq ? a.q_gain : a.k_gain;
+      if (act) {
+        u0 = u0 * inv * bf16_to_f32(g[m]);
+        u1 = u1 * inv * bf16_to_f32(g[m + half]);
+      }
+    }
+    if (!act) return;
+    float r0 = 0.f, r1 = 0.f;
+    if (pos_ok) {
+      const float c = a.rope_cos[(size_t)p * half + m];
+      const float s = a.rope_sin[(size_t)p * half + m];
+      r0 = u0 * c - u1 * s;
+      r1 = u1 * c + u0 * s;
+    }
+    if (hh < a.hq) {
+      bf16_t* dst = a.q_out + ((size_t)i * a.hq + hh) * a.d;
+      dst[m] = f32_to_bf16(r0);
+      dst[m + half] = f32_to_bf16(r1);
+      return;
+    }
+    if (!pos_ok) return;
+    const int pg = p >> 4;
+    if (pg >= a.max_pages) return;
+    const int page = a.page_table[(size_t)i * a.max_pages + pg];
+    if (page < 0 || (int64_t)page >= a.num_pages) return;
+    const int kh = hh - a.hq;
+    bf16_t* dst = a.k_pool + (((size_t)page * a.hkv + kh) * kPage + (p & 15)) * a.d;
+    dst[m] = f32_to_bf16(r0);
+    dst[m + half] = f32_to_bf16(r1);
+  } else {
+    if (!act || !pos_ok) return;
+    const int pg = p >> 4;
+    if (pg >= a.max_pages) return;
+    const int page = a.page_table[(size_t)i * a.max_pages + pg];
+    if (page < 0 || (int64_t)page >= a.num_pages) return;
+    const int vh = hh - a.hq - a.hkv;
+    bf16_t* dst = a.v_pool + ((size_t)page * a.hkv + vh) * a.d * kPage + (p & 15);
+    dst[(size_t)m * kPage] = f32_to_bf16(u0);
+    dst[(size_t)(m + half) * kPage] = f32_to_bf16(u1);
+  }
+}
+
+__device__ __forceinline__ uint64_t mix64(uint64_t z) {
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+
+__device__ __forceinline__ bf16_t synth_value(uint64_t key, int64_t e, float mul, float add,
+                                              int use_add) {
+  const uint64_t r = mix64(key + (uint64_t)(e + 1) * 0x9E3779B97F4A7C15ull);
+  const int32_t s = (int32_t)(r & 0xFFFF) + (int32_t)((r >> 16) & 0xFFFF) +
+                    (int32_t)((r >> 32) & 0xFFFF) + (int32_t)(r >> 48);
+  float v = __fmul_rn((float)(s - 131070), mul);
+  if (use_add) v = __fadd_rn(v, add);
+  return f32_to_bf16(v);
+}
+
+// Eight elements (one 16-byte store) per thread per step; scalar tail.
+__global__ __launch_bounds__(256) void fill_bf16_kernel(bf16_t* __restrict__ dst, int64_t count,
+                                                        uint64_t key, int64_t offset, float mul,
+                                                        float add, int use_add) {
+  const int64_t n8 = count >> 3;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; g < n8; g += stride) {
+    const int64_t e = g << 3;
+    u32x4 w;
+    w.x = synth_value(key, offset + e, mul, add, use_add) |
+          ((uint32_t)synth_value(key, offset + e + 1, mul, add, use_add) << 16);
+    w.y = synth_value(key, offset + e + 2, mul, add, use_add) |
+          ((uint32_t)synth_value(key, offset + e + 3, mul, add, use_add) << 16);
+    w.z = synth_value(key, offset + e + 4, mul, add, use_add) |
+          ((uint32_t)synth_value(key, offset + e + 5, mul, add, use_add) << 16);
+    w.w = synth_value(key, offset + e + 6, mul, add, use_add) |
+          ((uint32_t)synth_value(key, offset + e + 7, mul, add, use_add) << 16);
+    *reinterpret_cast<u32x4*>(dst + e) = w;
+  }
+  const int64_t tail0 = n8 << 3;
+  const int64_t t = tail0 + (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t < count && t - tail0 < 8) dst[t] = synth_value(key, offset + t, mul, add, use_add);
+}
+
+hipError_t launch_embed(const bf16_t* embed, const int32_t* tokens, int n, int hidden, int vocab,
+                        float* x, hipStream_t st) {
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(embed_kernel, dim3(n), dim3(256), 0, st, embed, tokens, hidden, vocab, x);
+  return hipGetLastError();
+}
+
+hipError_t launch_rmsnorm(const float* x, const bf16_t* gain, int rows, int cols, float eps,
+                          bf16_t* out, hipStream_t st) {
+  if (rows == 0) return hipSuccess;
+  hipLaunchKernelGGL(rmsnorm_kernel, dim3(rows), dim3(256), 0, st, x, gain, cols, eps, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_qk_norm_rope_append(const RopeAppendArgs& a, hipStream_t st) {
+  if (a.n == 0) return hipSuccess;
+  hipLaunchKernelGGL(qk_norm_rope_append_kernel, dim3(a.n, a.hq + 2 * a.hkv), dim3(64), 0, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_fill_bf16(bf16_t* dst, int64_t count, uint64_t key, int64_t offset, float mul,
+                            float add, int use_add, hipStream_t st) {
+  if (count == 0) return hipSuccess;
+  int64_t blocks = ((count >> 3) + 255) / 256;
+  if (blocks < 1) blocks = 1;
+  if (blocks > 65536) blocks = 65536;
+  hipLaunchKernelGGL(fill_bf16_kernel, dim3((unsigned)blocks), dim3(256), 0, st, dst, count, key,
+                     offset, mul, add, use_add);
+  return hipGetLastError();
+}
+
+}  // namespace sevo

@@ -1,0 +1,604 @@
+// Host side of the libsevo C ABI: argument validation, split / workspace
+// planning, the model handle (RoPE table) and the decode-step composition.
+// Every entry point catches everything and reports through sevo_status.
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/sevo.h"
+#include "kernels.h"
+
+#define SEVO_API extern "C" __attribute__((visibility("default")))
+
+namespace {
+
+thread_local std::string g_err;
+
+sevo_status fail(sevo_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return s;
+}
+
+sevo_status hip_fail(hipError_t e, const char* where) {
+  return fail(SEVO_ERR_HIP, "%s: %s", where, hipGetErrorString(e));
+}
+
+inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+inline size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+bool supported_group(int hq, int hkv) {
+  if (hkv <= 0 || hq <= 0 || hq % hkv) return false;
+  const int g = hq / hkv;
+  return g == 1 || g == 2 || g == 4 || g == 8;
+}
+
+// Splits per candidate so that (n * hkv * S) workgroups fill the 256 CUs
+// several times over, with at least 32 pages (8 per wave) per split.
+int plan_splits(int n, int hkv, int max_pages) {
+  const int pairs = n * hkv > 0 ? n * hkv : 1;
+  int s = (2048 + pairs - 1) / pairs;
+  const int cap = (max_pages + 31) / 32;
+  if (s > cap) s = cap;
+  if (s < 1) s = 1;
+  if (s > 256) s = 256;
+  return s;
+}
+
+size_t attn_ws(int n, int hq, int d, int S) {
+  return round_up((size_t)n * hq * S * 2 * sizeof(float), 256) +
+         round_up((size_t)n * hq * S * d * sizeof(float), 256);
+}
+
+struct AttnCheck {
+  int S, chunk;
+};
+
+sevo_status check_attn_shape(int n, int hq, int hkv, int d, int page_size, int max_pages) {
+  if (n < 0) return fail(SEVO_ERR_INVALID_ARGUMENT, "n = %d < 0", n);
+  if (page_size != SEVO_PAGE_SIZE)
+    return fail(SEVO_ERR_UNSUPPORTED, "page_size %d != 16", page_size);
+  if (d != 64 && d != 128) return fail(SEVO_ERR_UNSUPPORTED, "head_dim %d not in {64, 128}", d);
+  if (!supported_group(hq, hkv))
+    return fail(SEVO_ERR_UNSUPPORTED, "n_q_heads %d / n_kv_heads %d: group must be 1, 2, 4 or 8",
+                hq, hkv);
+  if (max_pages < 1) return fail(SEVO_ERR_INVALID_ARGUMENT, "max_pages %d < 1", max_pages);
+  return SEVO_OK;
+}
+
+}  // namespace
+
+struct sevo_model {
+  sevo_model_config cfg;
+  const void* embed;
+  const void* lm_head;
+  const void* final_norm;
+  std::vector<const void*> attn_norm, w_qkv, q_norm, k_norm, w_o, ffn_norm, w_gate_up, w_down;
+  float* rope_cos = nullptr;
+  float* rope_sin = nullptr;
+  int device = 0;
+};
+
+SEVO_API const char* sevo_status_string(sevo_status s) {
+  switch (s) {
+    case SEVO_OK: return "ok";
+    case SEVO_ERR_INVALID_ARGUMENT: return "invalid argument";
+    case SEVO_ERR_UNSUPPORTED: return "unsupported";
+    case SEVO_ERR_WORKSPACE_TOO_SMALL: return "workspace too small";
+    case SEVO_ERR_OUT_OF_MEMORY: return "out of memory";
+    case SEVO_ERR_HIP: return "HIP error";
+    case SEVO_ERR_BAD_PAGE_TABLE: return "bad page table";
+    default: return "unknown status";
+  }
+}
+
+SEVO_API const char* sevo_last_error(void) { return g_err.c_str(); }
+
+SEVO_API const char* sevo_version(void) { return "sevo 0.1 gfx950"; }
+
+// ------------------------------------------------------------------ model
+SEVO_API sevo_status sevo_init_model(const sevo_model_config* cfg, const sevo_weights* w,
+                                     sevo_model** out) {
+  try {
+    if (!cfg || !w || !out) return fail(SEVO_ERR_INVALID_ARGUMENT, "null argument");
+    *out = nullptr;
+    const sevo_model_config& c = *cfg;
+    if (c.n_layers < 1 || c.hidden < 1 || c.ffn < 1 || c.vocab < 1)
+      return fail(SEVO_ERR_INVALID_ARGUMENT, "non-positive model size");
+    if (c.max_position < 1) return fail(SEVO_ERR_INVALID_ARGUMENT, "max_position < 1");
+    if (!(c.rms_eps > 0.f) || !(c.rope_theta > 1.f))
+      return fail(SEVO_ERR_INVALID_ARGUMENT, "rms_eps must be > 0 and rope_theta > 1");
+    if (c.qk_norm != 0 && c.qk_norm != 1) return fail(SEVO_ERR_INVALID_ARGUMENT, "qk_norm");
+    sevo_status st = check_attn_shape(1, c.n_q_heads, c.n_kv_heads, c.head_dim, c.page_size, 1);
+    if (st) return st;
+    if (c.hidden % 64 || c.ffn % 64 || (c.n_q_heads * c.head_dim) % 64 || c.vocab % 64)
+      return fail(SEVO_ERR_UNSUPPORTED, "hidden, ffn, n_q_heads*head_dim and vocab must be "
+                                        "multiples of 64");
+    if (!w->embed || !w->lm_head || !w->final_norm)
+      return fail(SEVO_ERR_INVALID_ARGUMENT, "null embed / lm_head / final_norm");
+    const void* const* tabs[] = {w->attn_norm, w->w_qkv, w->w_o, w->ffn_norm, w->w_gate_up,
+                                 w->w_down};
+    for (auto t : tabs)
+      if (!t) return fail(SEVO_ERR_INVALID_ARGUMENT, "null per-layer weight table");
+    if (c.qk_norm && (!w->q_norm || !w->k_norm))
+      return fail(SEVO_ERR_INVALID_ARGUMENT, "qk_norm needs q_norm and k_norm tables");
+    const size_t rope_bytes = (size_t)c.max_position * (c.head_dim / 2) * sizeof(float);
+    if (rope_bytes > (size_t)16 << 30)
+      return fail(SEVO_ERR_OUT_OF_MEMORY, "RoPE table of %zu bytes exceeds 16 GiB", rope_bytes);
+
+    sevo_model* m = new sevo_model();
+    m->cfg = c;
+    m->embed = w->embed;
+    m->lm_head = w->lm_head;
+    m->final_norm = w->final_norm;
+    for (int l = 0; l < c.n_layers; ++l) {
+      m->attn_norm.push_back(w->attn_norm[l]);
+      m->w_qkv.push_back(w->w_qkv[l]);
+      m->q_norm.push_back(c.qk_norm ? w->q_norm[l] : nullptr);
+      m->k_norm.push_back(c.qk_norm ? w->k_norm[l] : nullptr);
+      m->w_o.push_back(w->w_o[l]);
+      m->ffn_norm.push_back(w->ffn_norm[l]);
+      m->w_gate_up.push_back(w->w_gate_up[l]);
+      m->w_down.push_back(w->w_down[l]);
+      const void* need[] = {m->attn_norm[l], m->w_qkv[l], m->w_o[l], m->ffn_norm[l],
+                            m->w_gate_up[l], m->w_down[l]};
+      for (auto p : need)
+        if (!p || !aligned16(p)) {
+          delete m;
+          return fail(SEVO_ERR_INVALID_ARGUMENT, "layer %d: null or misaligned weight", l);
+        }
+    }
+    // RoPE table: angle p * theta^(-2m/d) in double, cos/sin stored fp32
+    const int half = c.head_dim / 2;
+    std::vector<float> hc((size_t)c.max_position * half), hs(hc.size());
+    for (int mm = 0; mm < half; ++mm) {
+      const double inv = std::pow((double)c.rope_theta, -2.0 * mm / c.head_dim);
+      for (int p = 0; p < c.max_position; ++p) {
+        const double a = (double)p * inv;
+        hc[(size_t)p * half + mm] = (float)std::cos(a);
+        hs[(size_t)p * half + mm] = (float)std::sin(a);
+      }
+    }
+    hipError_t e = hipGetDevice(&m->device);
+    if (e == hipSuccess) e = hipMalloc(&m->rope_cos, rope_bytes);
+    if (e == hipSuccess) e = hipMalloc(&m->rope_sin, rope_bytes);
+    if (e == hipSuccess) e = hipMemcpy(m->rope_cos, hc.data(), rope_bytes, hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = hipMemcpy(m->rope_sin, hs.data(), rope_bytes, hipMemcpyHostToDevice);
+    if (e != hipSuccess) {
+      const sevo_status r = e == hipErrorOutOfMemory ? fail(SEVO_ERR_OUT_OF_MEMORY, "RoPE table")
+                                                      : hip_fail(e, "sevo_init_model");
+      if (m->rope_cos) (void)hipFree(m->rope_cos);
+      if (m->rope_sin) (void)hipFree(m->rope_sin);
+      delete m;
+      return r;
+    }
+    *out = m;
+    return SEVO_OK;
+  } catch (...) {
+    return fail(SEVO_ERR_OUT_OF_MEMORY, "host allocation failed in sevo_init_model");
+  }
+}
+
+SEVO_API void sevo_free_model(sevo_model* m) {
+  if (!m) return;
+  if (m->rope_cos) (void)hipFree(m->rope_cos);
+  if (m->rope_sin) (void)hipFree(m->rope_sin);
+  delete m;
+}
+
+// ------------------------------------------------------------------ attention
+SEVO_API int32_t sevo_attn_plan_splits(int32_t n, int32_t n_kv_heads, int32_t max_pages) {
+  return plan_splits(n, n_kv_heads, max_pages);
+}
+
+SEVO_API size_t sevo_attn_workspace_bytes(int32_t n, int32_t n_q_heads, int32_t n_kv_heads,
+                                          int32_t head_dim, int32_t max_pages,
+                                          int32_t num_splits) {
+  if (n <= 0 || n_q_heads <= 0 || head_dim <= 0 || max_pages <= 0) return 0;
+  const int S = num_splits > 0 ? num_splits : plan_splits(n, n_kv_heads, max_pages);
+  return attn_ws(n, n_q_heads, head_dim, S > max_pages ? max_pages : S);
+}
+
+static sevo_status attn_core(int n, int hq, int hkv, int d, int max_pages, int num_splits,
+                             int64_t num_pages, const void* q, const void* kp, const void* vp,
+                             const int32_t* pt, const int32_t* lens, float scale, void* out,
+                             void* ws, size_t ws_bytes, hipStream_t st) {
+  int S = num_splits > 0 ? num_splits : plan_splits(n, hkv, max_pages);
+  if (S > max_pages) S = max_pages;
+  const int chunk = (max_pages + S - 1) / S;
+  S = (max_pages + chunk - 1) / chunk;
+  const size_t need = attn_ws(n, hq, d, S);
+  if (ws_bytes < need)
+    return fail(SEVO_ERR_WORKSPACE_TOO_SMALL, "attention needs %zu workspace bytes, got %zu",
+                need, ws_bytes);
+  sevo::AttnArgs a;
+  a.n = n; a.hq = hq; a.hkv = hkv; a.d = d; a.max_pages = max_pages; a.num_splits = S;
+  a.chunk = chunk; a.num_pages = num_pages;
+  a.q = static_cast<const sevo::bf16_t*>(q);
+  a.k_pool = static_cast<const sevo::bf16_t*>(kp);
+  a.v_pool = static_cast<const sevo::bf16_t*>(vp);
+  a.page_table = pt; a.seq_lens = lens; a.len_add = 0; a.scale = scale;
+  a.out = static_cast<sevo::bf16_t*>(out);
+  a.part_ml = static_cast<float*>(ws);
+  a.part_acc = reinterpret_cast<float*>(static_cast<char*>(ws) +
+                                        round_up((size_t)n * hq * S * 2 * sizeof(float), 256));
+  hipError_t e = sevo::launch_attn_decode(a, st);
+  if (e != hipSuccess) return hip_fail(e, "sevo_attn_decode launch");
+  return SEVO_OK;
+}
+
+SEVO_API sevo_status sevo_attn_decode(const sevo_attn_args* a, void* stream) {
+  if (!a) return fail(SEVO_ERR_INVALID_ARGUMENT, "null args");
+  sevo_status st = check_attn_shape(a->n, a->n_q_heads, a->n_kv_heads, a->head_dim,
+                                    a->page_size, a->max_pages);
+  if (st) return st;
+  if (a->num_splits < 0) return fail(SEVO_ERR_INVALID_ARGUMENT, "num_splits < 0");
+  if (a->num_pages < 1) return fail(SEVO_ERR_INVALID_ARGUMENT, "num_pages < 1");
+  if (!(std::isfinite(a->scale)) || a->scale <= 0.f)
+    return fail(SEVO_ERR_INVALID_ARGUMENT, "scale must be finite and > 0");
+  if (a->n == 0) return SEVO_OK;
+  const void* ptrs[] = {a->q, a->k_pool, a->v_pool, a->page_table, a->seq_lens, a->out,
+                        a->workspace};
+  for (auto p : ptrs)
+    if (!p || !aligned16(p))
+      return fail(SEVO_ERR_INVALID_ARGUMENT, "null or non-16-byte-aligned pointer");
+  return attn_core(a->n, a->n_q_heads, a->n_kv_heads, a->head_dim, a->max_pages, a->num_splits,
+                   a->num_pages, a->q, a->k_pool, a->v_pool, a->page_table, a->seq_lens,
+                   a->scale, a->out, a->workspace, a->workspace_bytes,
+                   static_cast<hipStream_t>(stream));
+}
+
+// ------------------------------------------------------------------ sampling
+SEVO_API size_t sevo_sample_workspace_bytes(int32_t n, int32_t vocab) {
+  if (n <= 0 || vocab <= 0) return 0;
+  return round_up(sevo::sample_workspace_bytes(n, vocab), 256);
+}
+
+static sevo_status sample_check(const float* logits, int n, int vocab, int64_t ld, float temp) {
+  if (n < 0 || vocab < 1 || ld < vocab)
+    return fail(SEVO_ERR_INVALID_ARGUMENT, "bad n / vocab / ld (%d, %d, %lld)", n, vocab,
+                (long long)ld);
+  if (ld % 4) return fail(SEVO_ERR_INVALID_ARGUMENT, "ld must be a multiple of 4");
+  if (!std::isfinite(temp) || temp < 0.f)
+    return fail(SEVO_ERR_INVALID_ARGUMENT, "temperature must be finite and >= 0");
+  if (n > 0 && (!logits || !aligned16(logits)))
+    return fail(SEVO_ERR_INVALID_ARGUMENT, "null or misaligned logits");
+  return SEVO_OK;
+}
+
+SEVO_API sevo_status sevo_logprob_sample(const sevo_sample_args* a, void* stream) {
+  if (!a) return fail(SEVO_ERR_INVALID_ARGUMENT, "null args");
+  sevo_status st = sample_check(a->logits, a->n, a->vocab, a->ld, a->temperature);
+  if (st) return st;
+  if (a->n == 0) return SEVO_OK;
+  if (!a->cand_uid || !a->positions || !a->out_tokens || !a->out_logprobs || !a->workspace)
+    return fail(SEVO_ERR_INVALID_ARGUMENT, "null pointer");
+  if (!aligned16(a->workspace)) return fail(SEVO_ERR_INVALID_ARGUMENT, "misaligned workspace");
+  const size_t need = sevo::sample_workspace_bytes(a->n, a->vocab);
+  if (a->workspace_bytes < need)
+    return fail(SEVO_ERR_WORKSPACE_TOO_SMALL, "sampler needs %zu workspace bytes, got %zu", need,
+                a->workspace_bytes);
+  hipError_t e = sevo::launch_logprob_sample(
+      a->logits, a->n, a->vocab, a->ld, a->temperature, a->seed, a->cand_uid, a->positions,
+      a->out_tokens, a->out_logprobs, static_cast<float*>(a->workspace),
+      static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "sevo_logprob_sample launch");
+  return SEVO_OK;
+}
+
+// ------------------------------------------------------------------ sub-steps
+SEVO_API sevo_status sevo_embed(const void* embed, const int32_t* tokens, int32_t n,
+                                int32_t hidden, int32_t vocab, float* x, void* stream) {
+  if (n < 0 || hidden < 8 || hidden % 8 || vocab < 1)
+    return fail(SEVO_ERR_INVALID_ARGUMENT, "bad n / hidden / vocab");
+  if (n == 0) return SEVO_OK;
+  if (!embed || !tokens || !x || !aligned16(embed) || !aligned16(x))
+    return fail(SEVO_ERR_INVALID_ARGUMENT, "null or misaligned pointer");
+  hipError_t e = sevo::launch_embed(static_cast<const sevo::bf16_t*>(embed), tokens, n, hidden,
+                                    vocab, x, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? SEVO_OK : hip_fail(e, "sevo_embed");
+}
+
+SEVO_API sevo_status sevo_rmsnorm(const float* x, const void* gain, int32_t rows, int32_t cols,
+                                  float eps, void* out, void* stream) {
+  if (rows < 0 || cols < 4 || cols % 4) return fail(SEVO_ERR_INVALID_ARGUMENT, "bad rows / cols");
+  if (!(eps > 0.f)) return fail(SEVO_ERR_INVALID_ARGUMENT, "eps must be > 0");
+  if (rows == 0) return SEVO_OK;
+  if (!x || !gain || !out || !aligned16(x) || (reinterpret_cast<uintptr_t>(gain) & 7) ||
+      (reinterpret_cast<uintptr_t>(out) & 7))
+    return fail(SEVO_ERR_INVALID_ARGUMENT, "null or misaligned pointer");
+  hipError_t e = sevo::launch_rmsnorm(x, static_cast<const sevo::bf16_t*>(gain), rows, cols, eps,
+                                      static_cast<sevo::bf16_t*>(out),
+                                      static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? SEVO_OK : hip_fail(e, "sevo_rmsnorm");
+}
+
+static sevo_status linear_check(int m, int n_out, int k, int ldx, int mode, int k_splits) {
+  if (m < 0 || n_out < 64 || k < 32) return fail(SEVO_ERR_INVALID_ARGUMENT, "bad m / n_out / k");
+  if (k % 32) return fail(SEVO_ERR_UNSUPPORTED, "k %% 32 != 0");
+  if (n_out % 64) return fail(SEVO_ERR_UNSUPPORTED, "n_out %% 64 != 0");
+  if (mode == SEVO_LINEAR_SWIGLU && n_out % 128)
+    return fail(SEVO_ERR_UNSUPPORTED, "SwiGLU needs n_out %% 128 == 0");
+  if (mode < 0 || mode > 2) return fail(SEVO_ERR_INVALID_ARGUMENT, "bad mode %d", mode);
+  if (ldx < k || ldx % 8) return fail(SEVO_ERR_INVALID_ARGUMENT, "ldx must be >= k and %% 8");
+  if (k_splits < 0) return fail(SEVO_ERR_INVALID_ARGUMENT, "k_splits < 0");
+  return SEVO_OK;
+}
+
+SEVO_API size_t sevo_linear_workspace_bytes(int32_t m, int32_t n_out, int32_t k,
+                                            int32_t k_splits) {
+  if (m <= 0 || n_out <= 0 || k <= 0) return 0;
+  return round_up(sevo::linear_workspace_bytes(m, n_out, k, k_splits), 256);
+}
+
+SEVO_API sevo_status sevo_linear(const sevo_linear_args* a, void* stream) {
+  if (!a) return fail(SEVO_ERR_INVALID_ARGUMENT, "null args");
+  sevo_status st = linear_check(a->m, a->n_out, a->k, a->ldx, a->mode, a->k_splits);
+  if (st) return st;
+  if (a->m == 0) return SEVO_OK;
+  if (!a->x || !a->w || !a->out || !aligned16(a->x) || !aligned16(a->w) || !aligned16(a->out))
+    return fail(SEVO_ERR_INVALID_ARGUMENT, "null or misaligned pointer");
+  const sevo::LinearPlan plan = sevo::plan_linear(a->m, a->n_out, a->k, a->k_splits);
+  const bool direct = plan.k_splits == 1 && a->mode != SEVO_LINEAR_SWIGLU;
+  if (!direct) {
+    const size_t need = sevo::linear_workspace_bytes(a->m, a->n_out, a->k, a->k_splits);
+    if (!a->workspace || !aligned16(a->workspace) || a->workspace_bytes < need)
+      return fail(SEVO_ERR_WORKSPACE_TOO_SMALL, "linear needs %zu workspace bytes, got %zu", need,
+                  a->workspace_bytes);
+  }
+  hipError_t e = sevo::launch_linear(a->m, a->n_out, a->k, a->ldx, a->mode, plan,
+                                     static_cast<const sevo::bf16_t*>(a->x),
+                                     static_cast<const sevo::bf16_t*>(a->w), a->out,
+                                     static_cast<float*>(a->workspace),
+                                     static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? SEVO_OK : hip_fail(e, "sevo_linear");
+}
+
+static void fill_rope_args(const sevo_model* m, int layer, const float* qkv, int n,
+                           const int32_t* pos, const int32_t* pt, int max_pages,
+                           int64_t num_pages, void* q_out, void* kp, void* vp,
+                           sevo::RopeAppendArgs& r) {
+  const sevo_model_config& c = m->cfg;
+  r.qkv = qkv; r.n = n; r.hq = c.n_q_heads; r.hkv = c.n_kv_heads; r.d = c.head_dim;
+  r.positions = pos; r.page_table = pt; r.max_pages = max_pages; r.num_pages = num_pages;
+  r.rope_cos = m->rope_cos; r.rope_sin = m->rope_sin; r.max_pos = c.max_position;
+  r.q_gain = static_cast<const sevo::bf16_t*>(m->q_norm[layer]);
+  r.k_gain = static_cast<const sevo::bf16_t*>(m->k_norm[layer]);
+  r.qk_norm = c.qk_norm; r.eps = c.rms_eps;
+  r.q_out = static_cast<sevo::bf16_t*>(q_out);
+  r.k_pool = static_cast<sevo::bf16_t*>(kp);
+  r.v_pool = static_cast<sevo::bf16_t*>(vp);
+}
+
+SEVO_API sevo_status sevo_qk_norm_rope_append(const sevo_model* m, int32_t layer,
+                                              const float* qkv, int32_t n,
+                                              const int32_t* positions,
+                                              const int32_t* page_table, int32_t max_pages,
+                                              int64_t num_pages, void* q_out, void* k_pool,
+                                              void* v_pool, void* stream) {
+  if (!m) return fail(SEVO_ERR_INVALID_ARGUMENT, "null model");
+  if (layer < 0 || layer >= m->cfg.n_layers) return fail(SEVO_ERR_INVALID_ARGUMENT, "bad layer");
+  if (n < 0 || max_pages < 1 || num_pages < 1)
+    return fail(SEVO_ERR_INVALID_ARGUMENT, "bad n / max_pages / num_pages");
+  if (n == 0) return SEVO_OK;
+  if (!qkv || !positions || !page_table || !q_out || !k_pool || !v_pool)
+    return fail(SEVO_ERR_INVALID_ARGUMENT, "null pointer");
+  sevo::RopeAppendArgs r;
+  fill_rope_args(m, layer, qkv, n, positions, page_table, max_pages, num_pages, q_out, k_pool,
+                 v_pool, r);
+  hipError_t e = sevo::launch_qk_norm_rope_append(r, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? SEVO_OK : hip_fail(e, "sevo_qk_norm_rope_append");
+}
+
+// ------------------------------------------------------------------ decode step
+namespace {
+
+struct StepLayout {
+  size_t x, h, qkv, q, o, a, logits, lin, attn, sample, total;
+  int S, chunk;
+};
+
+StepLayout step_layout(const sevo_model_config& c, int n, int max_pages, int num_splits) {
+  StepLayout L;
+  const int qd = c.n_q_heads * c.head_dim;
+  const int qkvd = (c.n_q_heads + 2 * c.n_kv_heads) * c.head_dim;
+  int S = num_splits > 0 ? num_splits : plan_splits(n, c.n_kv_heads, max_pages);
+  if (S > max_pages) S = max_pages;
+  const int chunk = (max_pages + S - 1) / S;
+  L.S = (max_pages + chunk - 1) / chunk;
+  L.chunk = chunk;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off += round_up(bytes, 256);
+    return o;
+  };
+  L.x = take((size_t)n * c.hidden * 4);
+  L.h = take((size_t)n * c.hidden * 2);
+  L.qkv = take((size_t)n * qkvd * 4);
+  L.q = take((size_t)n * qd * 2);
+  L.o = take((size_t)n * qd * 2);
+  L.a = take((size_t)n * c.ffn * 2);
+  L.logits = take((size_t)n * c.vocab * 4);
+  size_t lin = 0;
+  const size_t cand[] = {sevo::linear_workspace_bytes(n, qkvd, c.hidden, 0),
+                         sevo::linear_workspace_bytes(n, c.hidden, qd, 0),
+                         sevo::linear_workspace_bytes(n, 2 * c.ffn, c.hidden, 0),
+                         sevo::linear_workspace_bytes(n, c.hidden, c.ffn, 0),
+                         sevo::linear_workspace_bytes(n, c.vocab, c.hidden, 0)};
+  for (size_t v : cand) lin = v > lin ? v : lin;
+  L.lin = take(lin);
+  L.attn = take(attn_ws(n, c.n_q_heads, c.head_dim, L.S));
+  L.sample = take(sevo::sample_workspace_bytes(n, c.vocab));
+  L.total = off;
+  return L;
+}
+
+}  // namespace
+
+SEVO_API size_t sevo_step_workspace_bytes(const sevo_model* m, int32_t n, int32_t max_pages,
+                                          int32_t num_splits) {
+  if (!m || n <= 0 || max_pages <= 0) return 0;
+  return step_layout(m->cfg, n, max_pages, num_splits).total;
+}
+
+SEVO_API sevo_status sevo_decode_step(sevo_model* m, const sevo_step_args* a, void* stream) {
+  if (!m || !a) return fail(SEVO_ERR_INVALID_ARGUMENT, "null model or args");
+  const sevo_model_config& c = m->cfg;
+  if (a->n < 0 || a->max_pages < 1 || a->num_pages < 1 || a->num_splits < 0)
+    return fail(SEVO_ERR_INVALID_ARGUMENT, "bad n / max_pages / num_pages / num_splits");
+  if (!std::isfinite(a->temperature) || a->temperature < 0.f)
+    return fail(SEVO_ERR_INVALID_ARGUMENT, "temperature must be finite and >= 0");
+  if (a->n == 0) return SEVO_OK;
+  if (!a->tokens || !a->positions || !a->page_table || !a->k_pools || !a->v_pools ||
+      !a->cand_uid || !a->out_tokens || !a->out_logprobs || !a->workspace)
+    return fail(SEVO_ERR_INVALID_ARGUMENT, "null pointer");
+  if (!aligned16(a->workspace)) return fail(SEVO_ERR_INVALID_ARGUMENT, "misaligned workspace");
+  if (a->out_logits && !aligned16(a->out_logits))
+    return fail(SEVO_ERR_INVALID_ARGUMENT, "misaligned out_logits");
+  for (int l = 0; l < c.n_layers; ++l)
+    if (!a->k_pools[l] || !a->v_pools[l] || !aligned16(a->k_pools[l]) ||
+        !aligned16(a->v_pools[l]))
+      return fail(SEVO_ERR_INVALID_ARGUMENT, "layer %d: null or misaligned KV pool", l);
+  const int n = a->n;
+  const StepLayout L = step_layout(c, n, a->max_pages, a->num_splits);
+  if (a->workspace_bytes < L.total)
+    return fail(SEVO_ERR_WORKSPACE_TOO_SMALL, "decode step needs %zu workspace bytes, got %zu",
+                L.total, a->workspace_bytes);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  char* ws = static_cast<char*>(a->workspace);
+  float* x = reinterpret_cast<float*>(ws + L.x);
+  sevo::bf16_t* h = reinterpret_cast<sevo::bf16_t*>(ws + L.h);
+  float* qkv = reinterpret_cast<float*>(ws + L.qkv);
+  sevo::bf16_t* q = reinterpret_cast<sevo::bf16_t*>(ws + L.q);
+  sevo::bf16_t* o = reinterpret_cast<sevo::bf16_t*>(ws + L.o);
+  sevo::bf16_t* act = reinterpret_cast<sevo::bf16_t*>(ws + L.a);
+  float* logits = a->out_logits ? a->out_logits : reinterpret_cast<float*>(ws + L.logits);
+  float* lin = reinterpret_cast<float*>(ws + L.lin);
+  char* attn_ws_ptr = ws + L.attn;
+  float* smp = reinterpret_cast<float*>(ws + L.sample);
+
+  const int H = c.hidden, F = c.ffn, qd = c.n_q_heads * c.head_dim;
+  const int qkvd = (c.n_q_heads + 2 * c.n_kv_heads) * c.head_dim;
+  const sevo::LinearPlan p_qkv = sevo::plan_linear(n, qkvd, H, 0);
+  const sevo::LinearPlan p_o = sevo::plan_linear(n, H, qd, 0);
+  const sevo::LinearPlan p_gu = sevo::plan_linear(n, 2 * F, H, 0);
+  const sevo::LinearPlan p_d = sevo::plan_linear(n, H, F, 0);
+  const sevo::LinearPlan p_lm = sevo::plan_linear(n, c.vocab, H, 0);
+  const float scale = 1.0f / std::sqrt((float)c.head_dim);
+
+  hipError_t e = sevo::launch_embed(static_cast<const sevo::bf16_t*>(m->embed), a->tokens, n, H,
+                                    c.vocab, x, st);
+  if (e != hipSuccess) return hip_fail(e, "embed");
+  for (int l = 0; l < c.n_layers; ++l) {
+    e = sevo::launch_rmsnorm(x, static_cast<const sevo::bf16_t*>(m->attn_norm[l]), n, H,
+                             c.rms_eps, h, st);
+    if (e == hipSuccess)
+      e = sevo::launch_linear(n, qkvd, H, H, SEVO_LINEAR_STORE, p_qkv, h,
+                              static_cast<const sevo::bf16_t*>(m->w_qkv[l]), qkv, lin, st);
+    if (e == hipSuccess) {
+      sevo::RopeAppendArgs r;
+      fill_rope_args(m, l, qkv, n, a->positions, a->page_table, a->max_pages, a->num_pages, q,
+                     a->k_pools[l], a->v_pools[l], r);
+      e = sevo::launch_qk_norm_rope_append(r, st);
+    }
+    if (e != hipSuccess) return hip_fail(e, "decode step (attention input)");
+    // attention over keys 0..p_i: lengths are positions + 1
+    sevo::AttnArgs aa;
+    aa.n = n; aa.hq = c.n_q_heads; aa.hkv = c.n_kv_heads; aa.d = c.head_dim;
+    aa.max_pages = a->max_pages; aa.num_splits = L.S;
+    aa.chunk = L.chunk;
+    aa.num_pages = a->num_pages;
+    aa.q = q;
+    aa.k_pool = static_cast<const sevo::bf16_t*>(a->k_pools[l]);
+    aa.v_pool = static_cast<const sevo::bf16_t*>(a->v_pools[l]);
+    aa.page_table = a->page_table;
+    aa.seq_lens = a->positions;
+    aa.len_add = 1;
+    aa.scale = scale;
+    aa.out = o;
+    aa.part_ml = reinterpret_cast<float*>(attn_ws_ptr);
+    aa.part_acc = reinterpret_cast<float*>(
+        attn_ws_ptr + round_up((size_t)n * c.n_q_heads * L.S * 2 * sizeof(float), 256));
+    e = sevo::launch_attn_decode(aa, st);
+    if (e == hipSuccess)
+      e = sevo::launch_linear(n, H, qd, qd, SEVO_LINEAR_ADD, p_o, o,
+                              static_cast<const sevo::bf16_t*>(m->w_o[l]), x, lin, st);
+    if (e == hipSuccess)
+      e = sevo::launch_rmsnorm(x, static_cast<const sevo::bf16_t*>(m->ffn_norm[l]), n, H,
+                               c.rms_eps, h, st);
+    if (e == hipSuccess)
+      e = sevo::launch_linear(n, 2 * F, H, H, SEVO_LINEAR_SWIGLU, p_gu, h,
+                              static_cast<const sevo::bf16_t*>(m->w_gate_up[l]), act, lin, st);
+    if (e == hipSuccess)
+      e = sevo::launch_linear(n, H, F, F, SEVO_LINEAR_ADD, p_d, act,
+                              static_cast<const sevo::bf16_t*>(m->w_down[l]), x, lin, st);
+    if (e != hipSuccess) return hip_fail(e, "decode step (layer)");
+  }
+  e = sevo::launch_rmsnorm(x, static_cast<const sevo::bf16_t*>(m->final_norm), n, H, c.rms_eps, h,
+                           st);
+  if (e == hipSuccess)
+    e = sevo::launch_linear(n, c.vocab, H, H, SEVO_LINEAR_STORE, p_lm, h,
+                            static_cast<const sevo::bf16_t*>(m->lm_head), logits, lin, st);
+  if (e == hipSuccess)
+    e = sevo::launch_logprob_sample(logits, n, c.vocab, c.vocab, a->temperature, a->seed,
+                                    a->cand_uid, a->positions, a->out_tokens, a->out_logprobs,
+                                    smp, st);
+  if (e != hipSuccess) return hip_fail(e, "decode step (head / sampler)");
+  return SEVO_OK;
+}
+
+// ------------------------------------------------------------------ utilities
+SEVO_API sevo_status sevo_fill_normal_bf16(void* dst, int64_t count, uint64_t key, int64_t offset,
+                                           float mul, float add, int32_t use_add, void* stream) {
+  if (count < 0 || offset < 0) return fail(SEVO_ERR_INVALID_ARGUMENT, "negative count / offset");
+  if (count == 0) return SEVO_OK;
+  if (!dst || !aligned16(dst)) return fail(SEVO_ERR_INVALID_ARGUMENT, "null or misaligned dst");
+  hipError_t e = sevo::launch_fill_bf16(static_cast<sevo::bf16_t*>(dst), count, key, offset, mul,
+                                        add, use_add ? 1 : 0, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? SEVO_OK : hip_fail(e, "sevo_fill_normal_bf16");
+}
+
+SEVO_API sevo_status sevo_validate_paging(const int32_t* page_table, const int32_t* lengths,
+                                          int32_t n, int32_t max_pages, int64_t num_pages,
+                                          void* stream) {
+  if (n < 0 || max_pages < 1 || num_pages < 1)
+    return fail(SEVO_ERR_INVALID_ARGUMENT, "bad n / max_pages / num_pages");
+  if (n == 0) return SEVO_OK;
+  if (!page_table || !lengths) return fail(SEVO_ERR_INVALID_ARGUMENT, "null pointer");
+  try {
+    std::vector<int32_t> pt((size_t)n * max_pages), len(n);
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    hipError_t e = hipMemcpyAsync(pt.data(), page_table, pt.size() * 4, hipMemcpyDeviceToHost, st);
+    if (e == hipSuccess)
+      e = hipMemcpyAsync(len.data(), lengths, len.size() * 4, hipMemcpyDeviceToHost, st);
+    if (e == hipSuccess) e = hipStreamSynchronize(st);
+    if (e != hipSuccess) return hip_fail(e, "sevo_validate_paging copy");
+    std::vector<uint8_t> used((size_t)num_pages, 0);
+    for (int i = 0; i < n; ++i) {
+      if (len[i] < 0 || len[i] > max_pages * SEVO_PAGE_SIZE)
+        return fail(SEVO_ERR_BAD_PAGE_TABLE, "candidate %d: length %d outside [0, %d]", i,
+                    len[i], max_pages * SEVO_PAGE_SIZE);
+      const int np = (len[i] + SEVO_PAGE_SIZE - 1) / SEVO_PAGE_SIZE;
+      for (int p = 0; p < np; ++p) {
+        const int32_t id = pt[(size_t)i * max_pages + p];
+        if (id < 0 || id >= num_pages)
+          return fail(SEVO_ERR_BAD_PAGE_TABLE, "candidate %d page %d: id %d outside [0, %lld)", i,
+                      p, id, (long long)num_pages);
+        if (used[id]) return fail(SEVO_ERR_BAD_PAGE_TABLE, "physical page %d used twice", id);
+        used[id] = 1;
+      }
+    }
+    return SEVO_OK;
+  } catch (...) {
+    return fail(SEVO_ERR_OUT_OF_MEMORY, "host allocation failed in sevo_validate_paging");
+  }
+}

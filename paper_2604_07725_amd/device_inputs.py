@@ -1,0 +1,51 @@
+"""Synthetic inputs materialised in device memory.
+
+The tensors are filled on the GPU by ``sevo_fill_normal_bf16`` (the device
+twin of the seeded generator in ``synth``), so every value equals what the
+host generator gives for the same tensor key and element index.  Population
+metadata (lengths, page tables, tokens, uids) is drawn on the host and copied.
+"""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+from . import synth
+from .sevo import sevo_fill_normal_bf16
+
+
+def _filled(spec: synth.TensorSpec, device) -> torch.Tensor:
+    t = torch.empty(spec.shape, dtype=torch.bfloat16, device=device)
+    sevo_fill_normal_bf16(t, spec.key, 0, spec.std, spec.mean)
+    return t
+
+
+def device_weights(shape: synth.ModelShape, seed: int, device="cuda") -> dict:
+    g = synth.global_specs(shape, seed)
+    out = {k: _filled(s, device) for k, s in g.items()}
+    out["layers"] = [{k: _filled(s, device) for k, s in synth.layer_specs(shape, seed, l).items()}
+                     for l in range(shape.n_layers)]
+    return out
+
+
+def device_pools(shape: synth.ModelShape, seed: int, n_pages: int, device="cuda",
+                 layers=None) -> tuple[list, list]:
+    ks, vs = [], []
+    for l in (range(shape.n_layers) if layers is None else layers):
+        kspec, vspec = synth.kv_specs(shape, seed, l, n_pages)
+        ks.append(_filled(kspec, device))
+        vs.append(_filled(vspec, device))
+    return ks, vs
+
+
+def device_q(shape: synth.ModelShape, seed: int, n: int, device="cuda") -> torch.Tensor:
+    return _filled(synth.q_spec(shape, seed, n), device)
+
+
+def device_population(pop: synth.Population, device="cuda") -> dict:
+    return {
+        "lengths": torch.from_numpy(pop.lengths.astype(np.int32)).to(device),
+        "page_table": torch.from_numpy(pop.page_table.astype(np.int32)).to(device),
+        "tokens": torch.from_numpy(pop.tokens.astype(np.int32)).to(device),
+        "uids": torch.from_numpy(pop.uids.view(np.int64)).to(device),
+    }

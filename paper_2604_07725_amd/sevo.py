@@ -1,0 +1,355 @@
+"""Thin Python binding of libsevo.so (argument marshalling only).
+
+Every function here packs torch tensors into the C structs of
+``include/sevo.h`` and calls the same-named C entry point; all arithmetic of
+the decode step runs in the HIP kernels of the library.  PyTorch provides
+device memory and the current stream.  There is no fallback: a missing or
+unloadable library raises.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+import re
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libsevo.so")
+HEADER = os.path.join(os.path.dirname(_HERE), "include", "sevo.h")
+
+OK, INVALID_ARGUMENT, UNSUPPORTED, WORKSPACE_TOO_SMALL, OUT_OF_MEMORY, HIP, BAD_PAGE_TABLE = range(7)
+LINEAR_STORE, LINEAR_ADD, LINEAR_SWIGLU = 0, 1, 2
+PAGE_SIZE = 16
+
+vp = C.c_void_p
+i32 = C.c_int32
+i64 = C.c_int64
+u64 = C.c_uint64
+f32 = C.c_float
+sz = C.c_size_t
+
+
+class ModelConfig(C.Structure):
+    _fields_ = [("n_layers", i32), ("hidden", i32), ("n_q_heads", i32), ("n_kv_heads", i32),
+                ("head_dim", i32), ("ffn", i32), ("vocab", i32), ("page_size", i32),
+                ("max_position", i32), ("qk_norm", i32), ("rope_theta", f32), ("rms_eps", f32)]
+
+
+class Weights(C.Structure):
+    _fields_ = [("embed", vp), ("lm_head", vp), ("final_norm", vp),
+                ("attn_norm", C.POINTER(vp)), ("w_qkv", C.POINTER(vp)), ("q_norm", C.POINTER(vp)),
+                ("k_norm", C.POINTER(vp)), ("w_o", C.POINTER(vp)), ("ffn_norm", C.POINTER(vp)),
+                ("w_gate_up", C.POINTER(vp)), ("w_down", C.POINTER(vp))]
+
+
+class AttnArgs(C.Structure):
+    _fields_ = [("n", i32), ("n_q_heads", i32), ("n_kv_heads", i32), ("head_dim", i32),
+                ("page_size", i32), ("max_pages", i32), ("num_splits", i32), ("num_pages", i64),
+                ("q", vp), ("k_pool", vp), ("v_pool", vp), ("page_table", vp), ("seq_lens", vp),
+                ("scale", f32), ("out", vp), ("workspace", vp), ("workspace_bytes", sz)]
+
+
+class SampleArgs(C.Structure):
+    _fields_ = [("logits", vp), ("n", i32), ("vocab", i32), ("ld", i64), ("temperature", f32),
+                ("seed", u64), ("cand_uid", vp), ("positions", vp), ("out_tokens", vp),
+                ("out_logprobs", vp), ("workspace", vp), ("workspace_bytes", sz)]
+
+
+class StepArgs(C.Structure):
+    _fields_ = [("n", i32), ("tokens", vp), ("positions", vp), ("page_table", vp),
+                ("max_pages", i32), ("num_pages", i64), ("k_pools", C.POINTER(vp)),
+                ("v_pools", C.POINTER(vp)), ("cand_uid", vp), ("seed", u64),
+                ("temperature", f32), ("num_splits", i32), ("out_tokens", vp),
+                ("out_logprobs", vp), ("out_logits", vp), ("workspace", vp),
+                ("workspace_bytes", sz)]
+
+
+class LinearArgs(C.Structure):
+    _fields_ = [("m", i32), ("n_out", i32), ("k", i32), ("ldx", i32), ("mode", i32),
+                ("k_splits", i32), ("x", vp), ("w", vp), ("out", vp), ("workspace", vp),
+                ("workspace_bytes", sz)]
+
+
+_SIGS = {
+    "sevo_status_string": ([i32], C.c_char_p),
+    "sevo_last_error": ([], C.c_char_p),
+    "sevo_version": ([], C.c_char_p),
+    "sevo_init_model": ([C.POINTER(ModelConfig), C.POINTER(Weights), C.POINTER(vp)], i32),
+    "sevo_free_model": ([vp], None),
+    "sevo_attn_decode": ([C.POINTER(AttnArgs), vp], i32),
+    "sevo_attn_plan_splits": ([i32, i32, i32], i32),
+    "sevo_attn_workspace_bytes": ([i32, i32, i32, i32, i32, i32], sz),
+    "sevo_logprob_sample": ([C.POINTER(SampleArgs), vp], i32),
+    "sevo_sample_workspace_bytes": ([i32, i32], sz),
+    "sevo_decode_step": ([vp, C.POINTER(StepArgs), vp], i32),
+    "sevo_step_workspace_bytes": ([vp, i32, i32, i32], sz),
+    "sevo_embed": ([vp, vp, i32, i32, i32, vp, vp], i32),
+    "sevo_rmsnorm": ([vp, vp, i32, i32, f32, vp, vp], i32),
+    "sevo_linear": ([C.POINTER(LinearArgs), vp], i32),
+    "sevo_linear_workspace_bytes": ([i32, i32, i32, i32], sz),
+    "sevo_qk_norm_rope_append": ([vp, i32, vp, i32, vp, vp, i32, i64, vp, vp, vp, vp], i32),
+    "sevo_fill_normal_bf16": ([vp, i64, u64, i64, f32, f32, i32, vp], i32),
+    "sevo_validate_paging": ([vp, vp, i32, i32, i64, vp], i32),
+}
+
+_lib = None
+
+
+class SevoError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"sevo status {status}: {msg}")
+        self.status = status
+
+
+def lib():
+    """Load libsevo.so (raises if it is missing: there is no fallback path)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} not built: run __graft_entry__.build()")
+        L = C.CDLL(LIB_PATH)
+        for name, (args, res) in _SIGS.items():
+            fn = getattr(L, name)
+            fn.argtypes = args
+            fn.restype = res
+        _lib = L
+    return _lib
+
+
+def header_functions() -> list[str]:
+    """Names of every function declared in include/sevo.h."""
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(sevo_[a-z0-9_]+)\s*\(", text)))
+
+
+def _check(status: int) -> None:
+    if status != OK:
+        raise SevoError(status, lib().sevo_last_error().decode())
+
+
+def _stream(stream):
+    if stream is None:
+        return vp(torch.cuda.current_stream().cuda_stream)
+    if isinstance(stream, torch.cuda.Stream):
+        return vp(stream.cuda_stream)
+    return vp(stream)
+
+
+def _p(t):
+    return None if t is None else vp(t.data_ptr())
+
+
+def _workspace(nbytes: int, device, ws=None):
+    if ws is not None:
+        return ws
+    return torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=device)
+
+
+# ------------------------------------------------------------------ attention
+def sevo_attn_plan_splits(n: int, n_kv_heads: int, max_pages: int) -> int:
+    return int(lib().sevo_attn_plan_splits(n, n_kv_heads, max_pages))
+
+
+def sevo_attn_workspace_bytes(n, n_q_heads, n_kv_heads, head_dim, max_pages, num_splits=0) -> int:
+    return int(lib().sevo_attn_workspace_bytes(n, n_q_heads, n_kv_heads, head_dim, max_pages,
+                                               num_splits))
+
+
+def sevo_attn_decode(q, k_pool, v_pool, page_table, seq_lens, out=None, scale=None,
+                     num_splits=0, workspace=None, stream=None):
+    """o = paged GQA decode attention.  q [n, hq, d] bf16; pools in the paged
+    layouts; page_table int32 [n, max_pages]; seq_lens int32 [n]."""
+    n, hq, d = q.shape
+    hkv = k_pool.shape[1]
+    max_pages = page_table.shape[1]
+    if out is None:
+        out = torch.empty_like(q)
+    need = sevo_attn_workspace_bytes(n, hq, hkv, d, max_pages, num_splits)
+    ws = _workspace(need, q.device, workspace)
+    a = AttnArgs(n=n, n_q_heads=hq, n_kv_heads=hkv, head_dim=d, page_size=PAGE_SIZE,
+                 max_pages=max_pages, num_splits=num_splits, num_pages=k_pool.shape[0],
+                 q=_p(q), k_pool=_p(k_pool), v_pool=_p(v_pool), page_table=_p(page_table),
+                 seq_lens=_p(seq_lens), scale=float(d ** -0.5 if scale is None else scale),
+                 out=_p(out), workspace=_p(ws), workspace_bytes=ws.numel())
+    _check(lib().sevo_attn_decode(C.byref(a), _stream(stream)))
+    return out
+
+
+# ------------------------------------------------------------------ sampling
+def sevo_sample_workspace_bytes(n: int, vocab: int) -> int:
+    return int(lib().sevo_sample_workspace_bytes(n, vocab))
+
+
+def sevo_logprob_sample(logits, temperature, seed, cand_uid, positions, out_tokens=None,
+                        out_logprobs=None, workspace=None, stream=None):
+    """(ids int32 [n], logprobs fp32 [n]) from fp32 logits [n, >=vocab]."""
+    n, vocab = logits.shape
+    if out_tokens is None:
+        out_tokens = torch.empty(n, dtype=torch.int32, device=logits.device)
+    if out_logprobs is None:
+        out_logprobs = torch.empty(n, dtype=torch.float32, device=logits.device)
+    ws = _workspace(sevo_sample_workspace_bytes(n, vocab), logits.device, workspace)
+    a = SampleArgs(logits=_p(logits), n=n, vocab=vocab, ld=logits.stride(0),
+                   temperature=float(temperature), seed=int(seed), cand_uid=_p(cand_uid),
+                   positions=_p(positions), out_tokens=_p(out_tokens),
+                   out_logprobs=_p(out_logprobs), workspace=_p(ws), workspace_bytes=ws.numel())
+    _check(lib().sevo_logprob_sample(C.byref(a), _stream(stream)))
+    return out_tokens, out_logprobs
+
+
+# ------------------------------------------------------------------ sub-steps
+def sevo_embed(embed, tokens, x=None, stream=None):
+    n = tokens.shape[0]
+    hidden = embed.shape[1]
+    if x is None:
+        x = torch.empty(n, hidden, dtype=torch.float32, device=embed.device)
+    _check(lib().sevo_embed(_p(embed), _p(tokens), n, hidden, embed.shape[0], _p(x),
+                            _stream(stream)))
+    return x
+
+
+def sevo_rmsnorm(x, gain, eps, out=None, stream=None):
+    rows, cols = x.shape
+    if out is None:
+        out = torch.empty(rows, cols, dtype=torch.bfloat16, device=x.device)
+    _check(lib().sevo_rmsnorm(_p(x), _p(gain), rows, cols, float(eps), _p(out), _stream(stream)))
+    return out
+
+
+def sevo_linear_workspace_bytes(m, n_out, k, k_splits=0) -> int:
+    return int(lib().sevo_linear_workspace_bytes(m, n_out, k, k_splits))
+
+
+def sevo_linear(x, w, mode=LINEAR_STORE, out=None, k_splits=0, workspace=None, stream=None):
+    """Y = x w^T (bf16 in, fp32 accumulate) with the STORE / ADD / SWIGLU epilogue."""
+    m, k = x.shape
+    n_out = w.shape[0]
+    if out is None:
+        if mode == LINEAR_SWIGLU:
+            out = torch.empty(m, n_out // 2, dtype=torch.bfloat16, device=x.device)
+        else:
+            out = torch.zeros(m, n_out, dtype=torch.float32, device=x.device)
+    ws = _workspace(sevo_linear_workspace_bytes(m, n_out, k, k_splits), x.device, workspace)
+    a = LinearArgs(m=m, n_out=n_out, k=k, ldx=x.stride(0), mode=mode, k_splits=k_splits, x=_p(x),
+                   w=_p(w), out=_p(out), workspace=_p(ws), workspace_bytes=ws.numel())
+    _check(lib().sevo_linear(C.byref(a), _stream(stream)))
+    return out
+
+
+def sevo_qk_norm_rope_append(model, layer, qkv, positions, page_table, k_pool, v_pool,
+                             q_out=None, stream=None):
+    n = qkv.shape[0]
+    cfg = model.config
+    if q_out is None:
+        q_out = torch.empty(n, cfg.n_q_heads, cfg.head_dim, dtype=torch.bfloat16,
+                            device=qkv.device)
+    _check(lib().sevo_qk_norm_rope_append(model.handle, layer, _p(qkv), n, _p(positions),
+                                          _p(page_table), page_table.shape[1], k_pool.shape[0],
+                                          _p(q_out), _p(k_pool), _p(v_pool), _stream(stream)))
+    return q_out
+
+
+def sevo_fill_normal_bf16(dst, key, offset=0, std=1.0, mean=None, stream=None):
+    """Device twin of the seeded input generator: fills a bf16 tensor."""
+    from .synth import ih_mul
+    _check(lib().sevo_fill_normal_bf16(_p(dst), dst.numel(), int(key), int(offset),
+                                       float(ih_mul(std)), 0.0 if mean is None else float(mean),
+                                       0 if mean is None else 1, _stream(stream)))
+    return dst
+
+
+def sevo_validate_paging(page_table, lengths, num_pages, stream=None):
+    n, max_pages = page_table.shape
+    _check(lib().sevo_validate_paging(_p(page_table), _p(lengths), n, max_pages, int(num_pages),
+                                      _stream(stream)))
+
+
+# ------------------------------------------------------------------ model + step
+class Model:
+    """A sevo_model handle plus the bf16 device weights it borrows."""
+
+    def __init__(self, shape, tensors: dict, max_position: int):
+        self.shape = shape
+        self.tensors = tensors  # keeps the weights alive
+        L = shape.n_layers
+        self.config = ModelConfig(
+            n_layers=L, hidden=shape.hidden, n_q_heads=shape.n_q_heads,
+            n_kv_heads=shape.n_kv_heads, head_dim=shape.head_dim, ffn=shape.ffn,
+            vocab=shape.vocab, page_size=PAGE_SIZE, max_position=int(max_position),
+            qk_norm=1 if shape.qk_norm else 0, rope_theta=float(shape.rope_theta),
+            rms_eps=float(shape.rms_eps))
+
+        def table(name):
+            arr = (vp * L)(*[t[name].data_ptr() for t in tensors["layers"]])
+            return arr
+
+        self._tables = {k: table(k) for k in ("attn_norm", "w_qkv", "q_norm", "k_norm", "w_o",
+                                               "ffn_norm", "w_gate_up", "w_down")}
+        self.weights = Weights(embed=_p(tensors["embed"]), lm_head=_p(tensors["lm_head"]),
+                               final_norm=_p(tensors["final_norm"]),
+                               **{k: C.cast(v, C.POINTER(vp)) for k, v in self._tables.items()})
+        h = vp()
+        _check(lib().sevo_init_model(C.byref(self.config), C.byref(self.weights), C.byref(h)))
+        self.handle = h
+
+    def close(self):
+        if self.handle:
+            lib().sevo_free_model(self.handle)
+            self.handle = vp()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def sevo_init_model(shape, tensors: dict, max_position: int) -> Model:
+    return Model(shape, tensors, max_position)
+
+
+def sevo_step_workspace_bytes(model: Model, n: int, max_pages: int, num_splits: int = 0) -> int:
+    return int(lib().sevo_step_workspace_bytes(model.handle, n, max_pages, num_splits))
+
+
+class StepBuffers:
+    """Pre-built argument struct for repeated decode steps (no per-step allocation)."""
+
+    def __init__(self, model: Model, tokens, positions, page_table, k_pools, v_pools, cand_uid,
+                 seed, temperature, num_splits=0, keep_logits=False, workspace=None):
+        n = tokens.shape[0]
+        dev = tokens.device
+        self.model = model
+        self.out_tokens = torch.empty(n, dtype=torch.int32, device=dev)
+        self.out_logprobs = torch.empty(n, dtype=torch.float32, device=dev)
+        self.out_logits = (torch.empty(n, model.shape.vocab, dtype=torch.float32, device=dev)
+                           if keep_logits else None)
+        need = sevo_step_workspace_bytes(model, n, page_table.shape[1], num_splits)
+        self.workspace = _workspace(need, dev, workspace)
+        L = model.shape.n_layers
+        self._k = (vp * L)(*[k.data_ptr() for k in k_pools])
+        self._v = (vp * L)(*[v.data_ptr() for v in v_pools])
+        self.keep = (tokens, positions, page_table, k_pools, v_pools, cand_uid)
+        self.args = StepArgs(
+            n=n, tokens=_p(tokens), positions=_p(positions), page_table=_p(page_table),
+            max_pages=page_table.shape[1], num_pages=k_pools[0].shape[0],
+            k_pools=C.cast(self._k, C.POINTER(vp)), v_pools=C.cast(self._v, C.POINTER(vp)),
+            cand_uid=_p(cand_uid), seed=int(seed), temperature=float(temperature),
+            num_splits=num_splits, out_tokens=_p(self.out_tokens),
+            out_logprobs=_p(self.out_logprobs), out_logits=_p(self.out_logits),
+            workspace=_p(self.workspace), workspace_bytes=self.workspace.numel())
+
+    def run(self, stream=None):
+        _check(lib().sevo_decode_step(self.model.handle, C.byref(self.args), _stream(stream)))
+        return self.out_tokens, self.out_logprobs
+
+
+def sevo_decode_step(model: Model, tokens, positions, page_table, k_pools, v_pools, cand_uid,
+                     seed, temperature=1.0, num_splits=0, keep_logits=False, stream=None):
+    """One decode step of the population; returns (ids, logprobs[, logits])."""
+    b = StepBuffers(model, tokens, positions, page_table, k_pools, v_pools, cand_uid, seed,
+                    temperature, num_splits, keep_logits)
+    ids, lps = b.run(stream)
+    return (ids, lps, b.out_logits) if keep_logits else (ids, lps)

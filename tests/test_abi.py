@@ -1,0 +1,169 @@
+"""C-ABI checks that need no GPU: symbols, struct layouts, host-side validation."""
+import ctypes as C
+import os
+import subprocess
+import tempfile
+
+import pytest
+
+from paper_2604_07725_amd import sevo
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def test_library_exports_every_header_function():
+    names = sevo.header_functions()
+    assert len(names) >= 19
+    L = sevo.lib()
+    for n in names:
+        assert hasattr(L, n), n
+    assert set(names) == set(sevo._SIGS), set(names) ^ set(sevo._SIGS)
+    assert L.sevo_version().startswith(b"sevo")
+
+
+_LAYOUT_C = r"""
+#include <stdio.h>
+#include <stddef.h>
+#include "sevo.h"
+#define P(T, f) printf(#T "." #f " %zu\n", offsetof(T, f));
+#define S(T) printf(#T " %zu\n", sizeof(T));
+int main(void) {
+  S(sevo_model_config) P(sevo_model_config, rope_theta) P(sevo_model_config, rms_eps)
+  S(sevo_weights) P(sevo_weights, w_down)
+  S(sevo_attn_args) P(sevo_attn_args, num_pages) P(sevo_attn_args, q) P(sevo_attn_args, scale)
+  P(sevo_attn_args, out) P(sevo_attn_args, workspace_bytes)
+  S(sevo_sample_args) P(sevo_sample_args, ld) P(sevo_sample_args, temperature)
+  P(sevo_sample_args, seed) P(sevo_sample_args, workspace_bytes)
+  S(sevo_step_args) P(sevo_step_args, max_pages) P(sevo_step_args, num_pages)
+  P(sevo_step_args, k_pools) P(sevo_step_args, seed) P(sevo_step_args, temperature)
+  P(sevo_step_args, num_splits) P(sevo_step_args, out_logits) P(sevo_step_args, workspace_bytes)
+  S(sevo_linear_args) P(sevo_linear_args, x) P(sevo_linear_args, workspace_bytes)
+  return 0;
+}
+"""
+
+_PY = {"sevo_model_config": sevo.ModelConfig, "sevo_weights": sevo.Weights,
+       "sevo_attn_args": sevo.AttnArgs, "sevo_sample_args": sevo.SampleArgs,
+       "sevo_step_args": sevo.StepArgs, "sevo_linear_args": sevo.LinearArgs}
+
+
+def test_ctypes_structs_match_c_layout():
+    with tempfile.TemporaryDirectory() as d:
+        src = os.path.join(d, "layout.c")
+        exe = os.path.join(d, "layout")
+        open(src, "w").write(_LAYOUT_C)
+        subprocess.check_call(["gcc", "-I", os.path.join(ROOT, "include"), src, "-o", exe])
+        out = subprocess.check_output([exe], text=True)
+    for line in out.splitlines():
+        key, val = line.split()
+        val = int(val)
+        if "." in key:
+            t, f = key.split(".")
+            assert getattr(_PY[t], f).offset == val, key
+        else:
+            assert C.sizeof(_PY[key]) == val, key
+
+
+def _attn(**kw):
+    base = dict(n=1, n_q_heads=4, n_kv_heads=2, head_dim=64, page_size=16, max_pages=4,
+                num_splits=0, num_pages=4, scale=0.125)
+    base.update(kw)
+    return sevo.AttnArgs(**base)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(head_dim=96), sevo.UNSUPPORTED),
+    (dict(page_size=8), sevo.UNSUPPORTED),
+    (dict(n_q_heads=6, n_kv_heads=4), sevo.UNSUPPORTED),
+    (dict(n_q_heads=32, n_kv_heads=2), sevo.UNSUPPORTED),
+    (dict(max_pages=0), sevo.INVALID_ARGUMENT),
+    (dict(num_pages=0), sevo.INVALID_ARGUMENT),
+    (dict(num_splits=-1), sevo.INVALID_ARGUMENT),
+    (dict(scale=0.0), sevo.INVALID_ARGUMENT),
+    (dict(), sevo.INVALID_ARGUMENT),           # null pointers
+])
+def test_attention_rejects_bad_arguments(kw, status):
+    a = _attn(**kw)
+    assert sevo.lib().sevo_attn_decode(C.byref(a), None) == status
+    assert sevo.lib().sevo_last_error()
+
+
+def test_attention_workspace_too_small_is_reported_before_launch():
+    fake = 1 << 20  # never dereferenced: the check fails first
+    a = _attn(q=fake, k_pool=fake, v_pool=fake, page_table=fake, seq_lens=fake, out=fake,
+              workspace=fake, workspace_bytes=16)
+    assert sevo.lib().sevo_attn_decode(C.byref(a), None) == sevo.WORKSPACE_TOO_SMALL
+    assert b"workspace" in sevo.lib().sevo_last_error()
+
+
+def test_zero_population_is_a_no_op():
+    assert sevo.lib().sevo_attn_decode(C.byref(_attn(n=0)), None) == sevo.OK
+
+
+def test_split_planning():
+    L = sevo.lib()
+    # enough workgroups for 256 CUs, at least 32 pages per split, at least one split
+    assert L.sevo_attn_plan_splits(64, 8, 2049) == 4
+    assert L.sevo_attn_plan_splits(16, 8, 1024) == 16
+    assert L.sevo_attn_plan_splits(4, 2, 33) == 2
+    assert L.sevo_attn_plan_splits(1, 1, 1) == 1
+    ws = L.sevo_attn_workspace_bytes(64, 32, 8, 128, 2049, 0)
+    assert ws >= 64 * 32 * 4 * 130 * 4
+
+
+@pytest.mark.parametrize("temp", [-1.0, float("nan"), float("inf")])
+def test_sampler_rejects_bad_temperature(temp):
+    a = sevo.SampleArgs(logits=1 << 20, n=1, vocab=8, ld=8, temperature=temp)
+    assert sevo.lib().sevo_logprob_sample(C.byref(a), None) == sevo.INVALID_ARGUMENT
+
+
+def test_sampler_rejects_bad_ld_and_small_workspace():
+    L = sevo.lib()
+    a = sevo.SampleArgs(logits=1 << 20, n=1, vocab=8, ld=6, temperature=1.0)
+    assert L.sevo_logprob_sample(C.byref(a), None) == sevo.INVALID_ARGUMENT
+    f = 1 << 20
+    a = sevo.SampleArgs(logits=f, n=2, vocab=8, ld=8, temperature=1.0, cand_uid=f, positions=f,
+                        out_tokens=f, out_logprobs=f, workspace=f, workspace_bytes=1)
+    assert L.sevo_logprob_sample(C.byref(a), None) == sevo.WORKSPACE_TOO_SMALL
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(k=48), sevo.UNSUPPORTED),
+    (dict(n_out=96), sevo.UNSUPPORTED),
+    (dict(n_out=192, mode=2), sevo.UNSUPPORTED),
+    (dict(mode=3), sevo.INVALID_ARGUMENT),
+    (dict(ldx=100), sevo.INVALID_ARGUMENT),
+])
+def test_linear_rejects_bad_shapes(kw, status):
+    base = dict(m=4, n_out=128, k=64, ldx=64, mode=0, k_splits=0)
+    base.update(kw)
+    a = sevo.LinearArgs(**base)
+    assert sevo.lib().sevo_linear(C.byref(a), None) == status
+
+
+def test_linear_plan_and_workspace():
+    L = sevo.lib()
+    assert L.sevo_linear_workspace_bytes(64, 6144, 4096, 0) == 8 * 64 * 6144 * 4
+    assert L.sevo_linear_workspace_bytes(64, 151936, 4096, 0) == 64 * 151936 * 4
+
+
+def test_init_model_rejects_bad_config():
+    cfg = sevo.ModelConfig(n_layers=1, hidden=256, n_q_heads=4, n_kv_heads=2, head_dim=64,
+                           ffn=1024, vocab=4096, page_size=16, max_position=1024, qk_norm=1,
+                           rope_theta=1e6, rms_eps=1e-6)
+    w = sevo.Weights()
+    h = C.c_void_p()
+    L = sevo.lib()
+    assert L.sevo_init_model(C.byref(cfg), C.byref(w), C.byref(h)) == sevo.INVALID_ARGUMENT
+    cfg.head_dim = 80
+    assert L.sevo_init_model(C.byref(cfg), C.byref(w), C.byref(h)) == sevo.UNSUPPORTED
+    cfg.head_dim = 64
+    cfg.hidden = 200
+    assert L.sevo_init_model(C.byref(cfg), C.byref(w), C.byref(h)) == sevo.UNSUPPORTED
+
+
+def test_status_strings():
+    L = sevo.lib()
+    for s in range(7):
+        assert L.sevo_status_string(s)
+    assert L.sevo_status_string(99) == b"unknown status"
