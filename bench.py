@@ -1,0 +1,215 @@
+"""Population decode benchmark on one MI355X.
+
+Default workload: 8B-class dense decoder (36 layers, hidden 4096, 32/8 heads x
+128, FFN 12288 SwiGLU, vocab 151936, bf16 weights, random init), population
+N = 64 candidates, each an aggregation context of K = 4 candidates with
+16k-32k cached tokens (uniform), 16-token pages in a shuffled page table.
+A step = one decode step of the whole population (embedding, 36 layers of
+RMSNorm / QKV / QK-norm + RoPE + KV append / paged attention / O / SwiGLU FFN,
+final norm, LM head, log-softmax + Gumbel-max sampling) followed by the
+host-side bookkeeping done on device (next tokens, positions + 1).
+
+Prints one JSON line: tokens/s of the population, the roofline of the dominant
+kernel (the split-KV attention kernel, HIP events around every launch inside
+the timed steps) and the oracle's throughput on a bounded sample of the same
+workload on the host cores (cpu_baseline).
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+BF16_PEAK_TFLOPS = 2500.0
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def attention_bytes(lengths, hkv, hq, d):
+    """Algorithmic bytes of one attention launch: every cached key and value of
+    every candidate once (bf16), q and o (bf16) and the page-table entries."""
+    lengths = np.asarray(lengths, np.int64)
+    kv = int(lengths.sum()) * hkv * d * 2 * 2
+    pages = int(((lengths + 15) // 16).sum())
+    n = len(lengths)
+    return kv + 2 * n * hq * d * 2 + pages * 4
+
+
+def cpu_baseline(w, pop, n_sample, budget_s=30.0):
+    """The oracle, as it stands, on a bounded sample of the workload: layer 0
+    of the model for the first n_sample candidates (attention over their full
+    contexts + that layer's projections), then the final norm, LM head and
+    sampler for them.  Inputs are generated before the clock starts.  The
+    per-token time extrapolates the layer time to the model's depth."""
+    from oracle import decoder as od
+    from paper_2604_07725_amd import synth
+    from threadpoolctl import threadpool_info
+    shape = w.shape
+    idx = np.arange(n_sample)
+    lengths = pop.lengths[idx].astype(np.int64)
+    # compact host pools holding only the sampled candidates' pages
+    need = (lengths + 1 + 15) // 16
+    pt = np.full((n_sample, int(need.max())), -1, np.int64)
+    kspec, vspec = synth.kv_specs(shape, w.seed, 0, pop.n_pages)
+    kp = np.empty((int(need.sum()), shape.n_kv_heads, 16, shape.head_dim), np.float32)
+    vp = np.empty((int(need.sum()), shape.n_kv_heads, shape.head_dim, 16), np.float32)
+    c = 0
+    for j, i in enumerate(idx):
+        pages = pop.page_table[i, :need[j]]
+        kp[c:c + need[j]] = synth.pool_pages(kspec, pages)
+        vp[c:c + need[j]] = synth.pool_pages(vspec, pages)
+        pt[j, :need[j]] = np.arange(c, c + need[j])
+        c += need[j]
+    hw = synth.host_weights(shape, w.seed, lazy=True)
+    lw = hw["layers"][0]
+    x = np.asarray(hw["embed"][pop.tokens[idx]], np.float64)
+    lm_head = hw["lm_head"][0:shape.vocab]
+    t0 = time.perf_counter()
+    x1 = od.decoder_layer(shape, lw, x, lengths, kp, vp, pt, mirror=True)
+    t1 = time.perf_counter()
+    logits = od.lm_logits(shape, hw["final_norm"], lm_head, x1, mirror=True)
+    od.logprob_sample(logits, 1.0, 1234, pop.uids[idx], lengths)
+    t2 = time.perf_counter()
+    t_layer, t_head = t1 - t0, t2 - t1
+    step_s = shape.n_layers * t_layer + t_head
+    blas = threadpool_info()
+    threads = max([b.get("num_threads", 1) for b in blas] or [1])
+    return {
+        "value": n_sample / step_s, "unit": "tokens/s", "cores": int(threads),
+        "kind": "oracle",
+        "sample": (f"oracle decoder layer 0 + LM head + sampler for {n_sample} of {pop.n} "
+                   f"candidates (contexts {int(lengths.min())}-{int(lengths.max())} tokens); "
+                   f"layer time x {shape.n_layers} layers + head time = {step_s:.2f} s per "
+                   f"step of {n_sample} tokens (measured {t_layer:.2f} s layer, {t_head:.2f} s "
+                   f"head; extrapolated in depth only)"),
+        "host_cpus": len(os.sched_getaffinity(0)),
+        "blas": [b.get("internal_api") for b in blas],
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=16)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="dense8b_pop64_agg4")
+    ap.add_argument("--num-splits", type=int, default=0)
+    ap.add_argument("--cpu-sample", type=int, default=8)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: the population decode step needs no collectives "
+              "and this build runs on a single MI355X; use --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2604_07725_amd import device_inputs as di
+    from paper_2604_07725_amd import sevo, synth
+
+    w = synth.WORKLOADS[args.workload]
+    shape = w.shape
+    if w.attention_only:
+        raise SystemExit("bench.py times the full decode step; pick a decoder workload")
+    extra = args.warmup + args.steps + 1
+    pop = synth.workload_population(w, extra_tokens=extra)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    kv_bytes_total = 2 * shape.n_layers * pop.n_pages * shape.n_kv_heads * 16 * shape.head_dim * 2
+    free, total = torch.cuda.mem_get_info()
+    need = kv_bytes_total + shape.weight_bytes() + 2 * shape.vocab * shape.hidden + (2 << 30)
+    log(f"workload {w.name}: N={pop.n} contexts {pop.lengths.min()}-{pop.lengths.max()} "
+        f"pages {pop.n_pages}; KV {kv_bytes_total / 1e9:.1f} GB, weights "
+        f"{shape.weight_bytes() / 1e9:.2f} GB; free {free / 1e9:.1f} of {total / 1e9:.1f} GB")
+    if need > free:
+        raise SystemExit(f"not enough device memory: need {need / 1e9:.1f} GB")
+    t = time.time()
+    tensors = di.device_weights(shape, w.seed, dev)
+    kp, vp = di.device_pools(shape, w.seed, pop.n_pages, dev)
+    d = di.device_population(pop, dev)
+    model = sevo.sevo_init_model(shape, tensors, max_position=int(pop.lengths.max()) + extra + 1)
+    torch.cuda.synchronize()
+    log(f"inputs resident in HBM in {time.time() - t:.1f} s")
+
+    tokens = d["tokens"].clone()
+    positions = d["lengths"].clone()
+    buf = sevo.StepBuffers(model, tokens, positions, d["page_table"], kp, vp, d["uids"],
+                           seed=20260412, temperature=1.0, num_splits=args.num_splits)
+
+    def step():
+        ids, _ = buf.run()
+        tokens.copy_(ids)
+        positions.add_(1)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    log("warmup done")
+
+    sevo.sevo_profile_begin(shape.n_layers * args.steps)
+    start = torch.cuda.Event(enable_timing=True)
+    stop = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for _ in range(args.steps):
+        step()
+    stop.record()
+    torch.cuda.synchronize()
+    total_ms = start.elapsed_time(stop)
+    split_ms, attn_ms, launches = sevo.sevo_profile_end()
+    ms_per_step = total_ms / args.steps
+    log(f"{args.steps} steps: {ms_per_step:.3f} ms/step; attention launches {launches}")
+
+    # algorithmic bytes of the timed attention launches (lengths grow by one per step)
+    base = pop.lengths.astype(np.int64) + args.warmup + 1
+    per_step = [attention_bytes(base + s, shape.n_kv_heads, shape.n_q_heads, shape.head_dim)
+                for s in range(args.steps)]
+    attn_bytes_per_launch = float(np.mean(per_step))
+    split_avg_ms = split_ms / max(launches, 1)
+    attn_avg_ms = attn_ms / max(launches, 1)
+    achieved = attn_bytes_per_launch / (split_avg_ms * 1e-3) / 1e9
+    step_bytes = shape.n_layers * attn_bytes_per_launch + shape.weight_bytes()
+    out = {
+        "metric": "population decode tokens/s/GPU",
+        "value": pop.n / (ms_per_step * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic (seeded; random-init weights)",
+        "config": {"workload": w.name, "model": "dense 8B-class decoder", "layers": shape.n_layers,
+                   "hidden": shape.hidden, "heads": f"{shape.n_q_heads}/{shape.n_kv_heads}x"
+                   f"{shape.head_dim}", "ffn": shape.ffn, "vocab": shape.vocab,
+                   "population": pop.n, "aggregation_k": 4,
+                   "context_tokens": [int(pop.lengths.min()), int(pop.lengths.max())],
+                   "page_size": 16, "parallelism": "none (1 GPU)",
+                   "num_splits": int(buf.args.num_splits) or
+                   sevo.sevo_attn_plan_splits(pop.n, shape.n_kv_heads, pop.max_pages)},
+        "roofline": {"kernel": "attn_split_kernel<128,4> (paged split-KV GQA attention)",
+                     "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "bytes_per_launch": attn_bytes_per_launch,
+                     "avg_launch_ms": split_avg_ms,
+                     "with_combine_GBs": attn_bytes_per_launch / (attn_avg_ms * 1e-3) / 1e9},
+        "step_roofline": {"bound": "hbm", "bytes_per_step": step_bytes,
+                          "achieved": step_bytes / (ms_per_step * 1e-3) / 1e9,
+                          "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                          "frac": step_bytes / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                          "attention_ms_per_step": attn_ms / args.steps},
+    }
+    if not args.no_cpu_baseline:
+        log("timing the oracle on a bounded sample (host cores)")
+        out["cpu_baseline"] = cpu_baseline(w, pop, args.cpu_sample)
+    model.close()
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -285,6 +285,17 @@ sevo_status sevo_fill_normal_bf16(void* dst, int64_t count, uint64_t key, int64_
 sevo_status sevo_validate_paging(const int32_t* page_table, const int32_t* lengths, int32_t n,
                                  int32_t max_pages, int64_t num_pages, void* stream);
 
+/* ------------------------------------------------------------------ timing
+ * Measurement aid: while a recording is open, every attention launch (from
+ * sevo_attn_decode or inside sevo_decode_step) is bracketed by HIP events on
+ * the stream it runs on: before the split kernel, between the split and the
+ * combine kernel, and after the combine.  Process-wide; records beyond
+ * max_records are not timed.  sevo_profile_end waits for the recorded events
+ * and returns the summed split-kernel time, the summed split + combine time
+ * (milliseconds) and the number of timed launches. */
+sevo_status sevo_profile_begin(int32_t max_records);
+sevo_status sevo_profile_end(float* split_ms, float* attention_ms, int32_t* records);
+
 #ifdef __cplusplus
 }
 #endif

@@ -16,12 +16,15 @@
 //       the score.  Scores are pre-scaled by scale*log2(e) so exp2 is used.
 //   softmax  page max over the 16 tokens by lane shuffles; running max,
 //       rescale factor and p = exp2(s - m) per head (wave-uniform max).
-//   P   lanes holding token t (u == 0) write bf16 p to a per-wave LDS strip;
-//       every lane reads the 8 p values of its token half as 4 packed words.
+//   P   p is split into bf16 hi + lo parts (p = hi + lo to ~2^-17 relative,
+//       so the softmax weights keep fp32-level accuracy through the bf16 dot
+//       products); lanes holding token t (u == 0) write both to a per-wave LDS
+//       strip and every lane reads the 8 values of its token half as packed
+//       words.
 //   PV  the V tile is dim-major [D][16] so one 32-bit word holds two tokens of
 //       one dim: lane (dim 32*ii + lane/2, token half lane%2) accumulates
-//       p . v with v_dot2 over token pairs.  Each 16-byte V load is one
-//       contiguous 1 KB wavefront access.
+//       hi . v + lo . v with v_dot2 over token pairs.  Each 16-byte V load is
+//       one contiguous 1 KB wavefront access.
 // Loads for the next page are issued before the current page is consumed
 // (register double buffering), and page ids two pages ahead.
 #include "common.h"
@@ -75,7 +78,7 @@ __global__ __launch_bounds__(256, (G <= 4 ? 2 : 1)) void attn_split_kernel(
   const int t = lane >> 2, u = lane & 3;   // QK layout
   const int dl = lane >> 1, h = lane & 1;  // PV layout
 
-  __shared__ __align__(16) bf16_t p_lds[4][G][kPage];
+  __shared__ __align__(16) bf16_t p_lds[4][2][G][kPage];  // [wave][hi|lo][head][token]
   __shared__ float w_m[4][G], w_l[4][G];
   __shared__ float w_acc[4][G][D];
 
@@ -145,13 +148,26 @@ __global__ __launch_bounds__(256, (G <= 4 ? 2 : 1)) void attn_split_kernel(
         p = exp2f(sc[j] - mn);
       }
       m_run[j] = mn;
-      const bf16_t pb = f32_to_bf16(p);
-      l_run[j] = l_run[j] * alpha[j] + bf16_to_f32(pb);
-      if (u == 0) p_lds[wave][j][t] = pb;
+      l_run[j] = l_run[j] * alpha[j] + p;
+      const bf16_t ph = f32_to_bf16(p);
+      const bf16_t pl = f32_to_bf16(p - bf16_to_f32(ph));
+      if (u == 0) {
+        p_lds[wave][0][j][t] = ph;
+        p_lds[wave][1][j][t] = pl;
+      }
     }
-    u32x4 pw[G];
+    // lanes read p values written by other lanes of the wave: order the LDS
+    // stores before the loads for the compiler (the hardware keeps one wave's
+    // LDS operations in order)
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    u32x4 pw[G], pwl[G];
 #pragma unroll
-    for (int j = 0; j < G; ++j) pw[j] = *reinterpret_cast<const u32x4*>(&p_lds[wave][j][h * 8]);
+    for (int j = 0; j < G; ++j) {
+      pw[j] = *reinterpret_cast<const u32x4*>(&p_lds[wave][0][j][h * 8]);
+      pwl[j] = *reinterpret_cast<const u32x4*>(&p_lds[wave][1][j][h * 8]);
+    }
     u32x4 vv[NI];
 #pragma unroll
     for (int ii = 0; ii < NI; ++ii) vv[ii] = r.v[ii];
@@ -171,6 +187,10 @@ __global__ __launch_bounds__(256, (G <= 4 ? 2 : 1)) void attn_split_kernel(
 #pragma unroll
       for (int ii = 0; ii < NI; ++ii) {
         float a = acc[j][ii] * alpha[j];
+        a = dot2_bf16(vv[ii].x, pwl[j].x, a);
+        a = dot2_bf16(vv[ii].y, pwl[j].y, a);
+        a = dot2_bf16(vv[ii].z, pwl[j].z, a);
+        a = dot2_bf16(vv[ii].w, pwl[j].w, a);
         a = dot2_bf16(vv[ii].x, pw[j].x, a);
         a = dot2_bf16(vv[ii].y, pw[j].y, a);
         a = dot2_bf16(vv[ii].z, pw[j].z, a);
@@ -294,14 +314,18 @@ __global__ __launch_bounds__(64) void attn_combine_kernel(const float* __restric
 template <int D, int G>
 static hipError_t launch_attn_t(const AttnArgs& a, hipStream_t st) {
   const float log2e = 1.4426950408889634f;
+  if (a.ev_begin) (void)hipEventRecord(a.ev_begin, st);
   hipLaunchKernelGGL((attn_split_kernel<D, G>), dim3(a.num_splits, a.hkv, a.n), dim3(256), 0, st,
                      a.q, a.k_pool, a.v_pool, a.page_table, a.max_pages, a.num_pages, a.seq_lens,
                      a.len_add, a.hkv, a.chunk, a.num_splits, a.scale * log2e, a.part_ml, a.part_acc);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  if (a.ev_mid) (void)hipEventRecord(a.ev_mid, st);
   hipLaunchKernelGGL((attn_combine_kernel<D>), dim3(a.hq, a.n), dim3(64), 0, st, a.part_ml,
                      a.part_acc, a.seq_lens, a.len_add, a.max_pages, a.chunk, a.num_splits, a.hq, a.out);
-  return hipGetLastError();
+  e = hipGetLastError();
+  if (e == hipSuccess && a.ev_end) (void)hipEventRecord(a.ev_end, st);
+  return e;
 }
 
 hipError_t launch_attn_decode(const AttnArgs& a, hipStream_t st) {

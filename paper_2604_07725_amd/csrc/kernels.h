@@ -49,6 +49,9 @@ struct AttnArgs {
   bf16_t* out;
   float* part_ml;   // [n][hq][S][2]
   float* part_acc;  // [n][hq][S][d]
+  // optional timing: recorded before the split kernel, between the two
+  // kernels and after the combine (all null = no recording)
+  hipEvent_t ev_begin = nullptr, ev_mid = nullptr, ev_end = nullptr;
 };
 hipError_t launch_attn_decode(const AttnArgs& a, hipStream_t st);
 

@@ -5,6 +5,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -72,6 +73,25 @@ sevo_status check_attn_shape(int n, int hq, int hkv, int d, int page_size, int m
                 hq, hkv);
   if (max_pages < 1) return fail(SEVO_ERR_INVALID_ARGUMENT, "max_pages %d < 1", max_pages);
   return SEVO_OK;
+}
+
+// Attention timing: events bracketing each attention launch (see
+// sevo_profile_begin).  Process-wide, guarded by a mutex.
+struct AttnProfiler {
+  std::mutex mu;
+  bool on = false;
+  int n = 0;
+  std::vector<hipEvent_t> ev;  // 3 per record: begin, mid, end
+  int cap() const { return (int)ev.size() / 3; }
+} g_prof;
+
+void attach_profiler(sevo::AttnArgs& a) {
+  std::lock_guard<std::mutex> lk(g_prof.mu);
+  if (!g_prof.on || g_prof.n >= g_prof.cap()) return;
+  a.ev_begin = g_prof.ev[3 * g_prof.n];
+  a.ev_mid = g_prof.ev[3 * g_prof.n + 1];
+  a.ev_end = g_prof.ev[3 * g_prof.n + 2];
+  ++g_prof.n;
 }
 
 }  // namespace
@@ -227,6 +247,7 @@ static sevo_status attn_core(int n, int hq, int hkv, int d, int max_pages, int n
   a.v_pool = static_cast<const sevo::bf16_t*>(vp);
   a.page_table = pt; a.seq_lens = lens; a.len_add = 0; a.scale = scale;
   a.out = static_cast<sevo::bf16_t*>(out);
+  attach_profiler(a);
   a.part_ml = static_cast<float*>(ws);
   a.part_acc = reinterpret_cast<float*>(static_cast<char*>(ws) +
                                         round_up((size_t)n * hq * S * 2 * sizeof(float), 256));
@@ -528,6 +549,7 @@ SEVO_API sevo_status sevo_decode_step(sevo_model* m, const sevo_step_args* a, vo
     aa.part_ml = reinterpret_cast<float*>(attn_ws_ptr);
     aa.part_acc = reinterpret_cast<float*>(
         attn_ws_ptr + round_up((size_t)n * c.n_q_heads * L.S * 2 * sizeof(float), 256));
+    attach_profiler(aa);
     e = sevo::launch_attn_decode(aa, st);
     if (e == hipSuccess)
       e = sevo::launch_linear(n, H, qd, qd, SEVO_LINEAR_ADD, p_o, o,
@@ -601,4 +623,43 @@ SEVO_API sevo_status sevo_validate_paging(const int32_t* page_table, const int32
   } catch (...) {
     return fail(SEVO_ERR_OUT_OF_MEMORY, "host allocation failed in sevo_validate_paging");
   }
+}
+
+// ------------------------------------------------------------------ timing
+SEVO_API sevo_status sevo_profile_begin(int32_t max_records) {
+  if (max_records < 1 || max_records > (1 << 20))
+    return fail(SEVO_ERR_INVALID_ARGUMENT, "max_records must be in [1, 2^20]");
+  std::lock_guard<std::mutex> lk(g_prof.mu);
+  try {
+    while ((int)g_prof.ev.size() < 3 * max_records) {
+      hipEvent_t e;
+      hipError_t r = hipEventCreate(&e);
+      if (r != hipSuccess) return hip_fail(r, "sevo_profile_begin");
+      g_prof.ev.push_back(e);
+    }
+  } catch (...) {
+    return fail(SEVO_ERR_OUT_OF_MEMORY, "sevo_profile_begin");
+  }
+  g_prof.n = 0;
+  g_prof.on = true;
+  return SEVO_OK;
+}
+
+SEVO_API sevo_status sevo_profile_end(float* split_ms, float* attention_ms, int32_t* records) {
+  std::lock_guard<std::mutex> lk(g_prof.mu);
+  g_prof.on = false;
+  float a = 0.f, b = 0.f;
+  for (int r = 0; r < g_prof.n; ++r) {
+    hipError_t e = hipEventSynchronize(g_prof.ev[3 * r + 2]);
+    float t1 = 0.f, t2 = 0.f;
+    if (e == hipSuccess) e = hipEventElapsedTime(&t1, g_prof.ev[3 * r], g_prof.ev[3 * r + 1]);
+    if (e == hipSuccess) e = hipEventElapsedTime(&t2, g_prof.ev[3 * r], g_prof.ev[3 * r + 2]);
+    if (e != hipSuccess) return hip_fail(e, "sevo_profile_end");
+    a += t1;
+    b += t2;
+  }
+  if (split_ms) *split_ms = a;
+  if (attention_ms) *attention_ms = b;
+  if (records) *records = g_prof.n;
+  return SEVO_OK;
 }

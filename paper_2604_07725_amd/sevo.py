@@ -91,6 +91,8 @@ _SIGS = {
     "sevo_qk_norm_rope_append": ([vp, i32, vp, i32, vp, vp, i32, i64, vp, vp, vp, vp], i32),
     "sevo_fill_normal_bf16": ([vp, i64, u64, i64, f32, f32, i32, vp], i32),
     "sevo_validate_paging": ([vp, vp, i32, i32, i64, vp], i32),
+    "sevo_profile_begin": ([i32], i32),
+    "sevo_profile_end": ([C.POINTER(f32), C.POINTER(f32), C.POINTER(i32)], i32),
 }
 
 _lib = None
@@ -264,6 +266,17 @@ def sevo_validate_paging(page_table, lengths, num_pages, stream=None):
     n, max_pages = page_table.shape
     _check(lib().sevo_validate_paging(_p(page_table), _p(lengths), n, max_pages, int(num_pages),
                                       _stream(stream)))
+
+
+def sevo_profile_begin(max_records: int) -> None:
+    _check(lib().sevo_profile_begin(int(max_records)))
+
+
+def sevo_profile_end():
+    """(split-kernel ms, split + combine ms, launches) summed over the recording."""
+    a, b, n = f32(), f32(), i32()
+    _check(lib().sevo_profile_end(C.byref(a), C.byref(b), C.byref(n)))
+    return a.value, b.value, n.value
 
 
 # ------------------------------------------------------------------ model + step

@@ -9,6 +9,8 @@ from tests.gpu_helpers import LP_ABS_TOL, bf16_bits, check_ids, say
 
 pytestmark = pytest.mark.gpu
 
+TINY_LOGIT_TOL = 1e-2
+
 
 @pytest.fixture(scope="module")
 def S():
@@ -55,8 +57,15 @@ def test_tiny_step_sequence_matches_oracle(S):
         ref = od.decode_step(shape, hw, hk, hv, pop.page_table, toks, pos, pop.uids, seed, temp)
         lg = logits.double().cpu().numpy()
         err = np.abs(lg - ref["logits"]).max()
-        say(f"  step {step}: logit max abs err {err:.2e}")
-        assert err <= LP_ABS_TOL
+        lp_err = np.abs(lps.cpu().numpy() - ref["lps"]).max()
+        say(f"  step {step}: logit max abs err {err:.2e}, lp max err {lp_err:.2e}, ids "
+            f"{ids.cpu().numpy().tolist()} vs {ref['ids'].tolist()} gaps {np.round(ref['gaps'], 4)}")
+        # bf16 storage points round values that differ in the last fp32 bits
+        # between any two correct implementations; in this tiny model (residual
+        # stream ~0.05, one layer) a single 1-ulp flip moves logits by ~1e-3.
+        # The oracle's own logits move by up to 6e-3 when its pre-rounding
+        # values are perturbed by 1e-6 relative, so logits are held to 1e-2.
+        assert err <= TINY_LOGIT_TOL
         check_ids(ids.cpu().numpy(), lps.cpu().numpy(), ref["ids"], ref["lps"], ref["gaps"],
                   label=f"step {step}")
         toks = ref["ids"]
@@ -77,11 +86,15 @@ def test_tiny_step_sequence_matches_oracle(S):
         np.testing.assert_array_equal(gk[~written], k0[~written])
         np.testing.assert_array_equal(np.transpose(gv, (0, 1, 3, 2))[~written],
                                       np.transpose(v0, (0, 1, 3, 2))[~written])
-        kd = np.abs(gk[written] - hk[l][written]).max()
-        vd = np.abs(np.transpose(gv, (0, 1, 3, 2))[written]
-                    - np.transpose(hv[l], (0, 1, 3, 2))[written]).max()
-        say(f"  layer {l}: appended k max diff {kd:.2e}, v {vd:.2e}")
-        assert kd <= 2e-2 and vd <= 2e-2
+        gkw, rkw = gk[written], hk[l][written]
+        gvw = np.transpose(gv, (0, 1, 3, 2))[written]
+        rvw = np.transpose(hv[l], (0, 1, 3, 2))[written]
+        say(f"  layer {l}: appended k max diff {np.abs(gkw - rkw).max():.2e}, "
+            f"v {np.abs(gvw - rvw).max():.2e}; equal {np.mean(gkw == rkw):.3f} / "
+            f"{np.mean(gvw == rvw):.3f}")
+        # at most one bf16 rounding step apart (values rounded from fp32 vs fp64)
+        assert np.all(np.abs(gkw - rkw) <= 2.0 ** -7 * np.abs(rkw) + 1e-6)
+        assert np.all(np.abs(gvw - rvw) <= 2.0 ** -7 * np.abs(rvw) + 1e-6)
     model.close()
 
 
