@@ -59,7 +59,7 @@ def cpu_baseline(w, pop, n_sample, budget_s=30.0):
     need = (lengths + 1 + 15) // 16
     pt = np.full((n_sample, int(need.max())), -1, np.int64)
     kspec, vspec = synth.kv_specs(shape, w.seed, 0, pop.n_pages)
-    kp = np.empty((int(need.sum()), shape.n_kv_heads, 16, shape.head_dim), np.float32)
+    kp = np.empty((int(need.sum()), shape.n_kv_heads, shape.head_dim // 32, 16, 32), np.float32)
     vp = np.empty((int(need.sum()), shape.n_kv_heads, shape.head_dim, 16), np.float32)
     c = 0
     for j, i in enumerate(idx):
@@ -104,6 +104,8 @@ def main():
     ap.add_argument("--num-splits", type=int, default=0)
     ap.add_argument("--cpu-sample", type=int, default=8)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain 1 GiB device copy (3 times), to scale HBM counters")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: the population decode step needs no collectives "
@@ -111,6 +113,14 @@ def main():
         sys.exit(2)
 
     import torch
+    if args.copy_calibration:
+        src = torch.ones(1 << 28, dtype=torch.float32, device="cuda")   # 1 GiB
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration_bytes": src.numel() * 4, "copies": 3}), flush=True)
+        return
     from paper_2604_07725_amd import device_inputs as di
     from paper_2604_07725_amd import sevo, synth
 

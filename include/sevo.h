@@ -31,8 +31,11 @@
  *     of device-resident page tables, lengths and positions are NOT validated
  *     on the hot path (sevo_validate_paging checks them on demand).
  *   - Paged KV cache, one K pool and one V pool per layer, page size 16:
- *       K pool  bf16 [num_pages][n_kv_heads][16][head_dim]   token-major tile
+ *       K pool  bf16 [num_pages][n_kv_heads][head_dim/32][16][32]
+ *               dims in blocks of 32, each block token-major: element (slot s,
+ *               dim e) of a (page, head) tile sits at ((e/32)*16 + s)*32 + e%32
  *       V pool  bf16 [num_pages][n_kv_heads][head_dim][16]   dim-major tile
+ *     Each (page, head) tile is 16 * head_dim * 2 bytes, contiguous, for K and V.
  *     Logical key t of candidate i lives in physical page
  *     page_table[i * max_pages + t / 16], slot t % 16.  One page table serves
  *     all layers.  Physical page order is arbitrary (any permutation gives
@@ -117,7 +120,8 @@ void sevo_free_model(sevo_model* m);
 /* Paged GQA split-KV decode attention (one query token per candidate):
  *   o[i][j] = softmax_t(scale * q[i][j] . K_i[c][t]) V_i[c][t],  t < seq_lens[i],
  * c = j / (n_q_heads / n_kv_heads).  Each candidate's pages are cut into
- * splits of ceil(max_pages / num_splits) logical pages; every split yields an
+ * splits of ceil(max_pages / S) logical pages, where S is num_splits raised as
+ * needed so that a split spans at most 256 pages; every split yields an
  * online-softmax partial (running max, sum, weighted V) that a combine pass
  * merges in split order, so the result is deterministic.
  *   q        bf16 [n][n_q_heads][head_dim]

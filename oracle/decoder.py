@@ -15,9 +15,11 @@ Sampling is exact full-vocabulary categorical sampling at temperature T (the
 temperature-1, top-k off, top-p 1 row of the generation hyper-parameter
 table), realised as Gumbel-max with counter-based noise (see philox.py).
 
-Paged KV layout (per layer; page size 16):
-    K pool [num_pages][n_kv_heads][16][head_dim]   (token-major tile)
-    V pool [num_pages][n_kv_heads][head_dim][16]   (dim-major tile)
+Paged KV layout (per layer; page size 16; head_dim a multiple of 32):
+    K pool [num_pages][n_kv_heads][head_dim/32][16][32]  (dims in blocks of 32,
+           each block token-major: element (slot s, dim e) of a tile sits at
+           ((e // 32) * 16 + s) * 32 + e % 32)
+    V pool [num_pages][n_kv_heads][head_dim][16]         (dim-major tile)
     logical key t of candidate i -> page page_table[i][t // 16], slot t % 16.
 
 Everything here is float64.  bf16 storage points of the GPU path are mirrored
@@ -151,8 +153,9 @@ def gather_kv(k_pool, v_pool, pages, n_keys):
     t = np.arange(n_keys)
     pg = np.asarray(pages, np.int64)[t // PAGE]
     sl = t % PAGE
-    K = np.asarray(k_pool)[pg, :, sl, :]          # [L, hkv, d]
-    V = np.asarray(v_pool)[pg, :, :, sl]          # [L, hkv, d]
+    kp = np.asarray(k_pool)
+    K = kp[pg, :, :, sl, :].reshape(n_keys, kp.shape[1], -1)   # [L, hkv, d]
+    V = np.asarray(v_pool)[pg, :, :, sl]                       # [L, hkv, d]
     return (np.transpose(K, (1, 0, 2)).astype(np.float64),
             np.transpose(V, (1, 0, 2)).astype(np.float64))
 
@@ -171,7 +174,7 @@ def append_kv(k_pool, v_pool, page_table, positions, k, v):
     """Write key/value number p_i of every candidate into its page slot."""
     for i, p in enumerate(np.asarray(positions, np.int64)):
         page = int(page_table[i][p // PAGE])
-        k_pool[page, :, p % PAGE, :] = k[i]
+        k_pool[page, :, :, p % PAGE, :] = np.asarray(k[i]).reshape(k_pool.shape[1], -1, 32)
         v_pool[page, :, :, p % PAGE] = v[i]
 
 

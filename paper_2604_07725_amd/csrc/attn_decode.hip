@@ -10,12 +10,16 @@
 // order.
 //
 // Per page and wave (tile = 16 tokens x D dims, 4 KB at D = 128):
-//   QK  lane (t = lane/4, u = lane%4) loads D/32 16-byte chunks of key t
-//       (chunks u, u+4, ...), forms G partial dot products with v_dot2
-//       (bf16 pairs, fp32 accumulate), and a 2-step quad reduction completes
-//       the score.  Scores are pre-scaled by scale*log2(e) so exp2 is used.
-//   softmax  page max over the 16 tokens by lane shuffles; running max,
-//       rescale factor and p = exp2(s - m) per head (wave-uniform max).
+//   QK  the K tile is stored in blocks of 32 dims ([D/32][16 tokens][32]), so
+//       load ii reads block ii as one contiguous 1 KB wavefront access; lane
+//       (t = lane/4, u = lane%4) gets dims 32 ii + 8u .. +7 of key t and forms
+//       G partial dot products with v_dot2
+//       (bf16 pairs, fp32 accumulate), and a 2-step DPP quad reduction
+//       completes the score.  Scores are pre-scaled by scale*log2(e) so exp2
+//       is used.
+//   softmax  page max over the 16 tokens with register-only cross-lane ops
+//       (DPP row rotates, permlane16/32 swaps); running max, rescale factor
+//       and p = exp2(s - m) per head (wave-uniform max).
 //   P   p is split into bf16 hi + lo parts (p = hi + lo to ~2^-17 relative,
 //       so the softmax weights keep fp32-level accuracy through the bf16 dot
 //       products); lanes holding token t (u == 0) write both to a per-wave LDS
@@ -25,8 +29,12 @@
 //       one dim: lane (dim 32*ii + lane/2, token half lane%2) accumulates
 //       hi . v + lo . v with v_dot2 over token pairs.  Each 16-byte V load is
 //       one contiguous 1 KB wavefront access.
-// Loads for the next page are issued before the current page is consumed
-// (register double buffering), and page ids two pages ahead.
+// Loads for the wave's next two pages are issued before the current page is
+// consumed (three register page buffers; two for G = 8, where registers are
+// short).  A split spans at most 256 pages, so each wave's page ids fit one
+// per lane in a single register, read out with readlane inside the loop.
+#include <type_traits>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -38,28 +46,33 @@ struct PageRegs {
   u32x4 v[D / 32];
 };
 
+// One K tile and one V tile of a page, read with raw buffer loads: the tile
+// base goes into a wave-uniform buffer descriptor (scalar registers) and each
+// lane's byte offset inside the tile is a fixed register, so the page loop
+// does no vector address arithmetic.  A descriptor with zero records (a page
+// id outside the pool) makes every load return zero without touching memory.
+// Cache policy: streaming (nt), the KV cache is read once per step.
 template <int D>
-__device__ __forceinline__ void load_page(PageRegs<D>& r, const bf16_t* __restrict__ kpool,
-                                          const bf16_t* __restrict__ vpool, size_t tile, int t,
-                                          int u, int dl, int h) {
+__device__ __forceinline__ void load_page(PageRegs<D>& r, const char* kt, const char* vt,
+                                          int nrec, uint32_t koff, uint32_t voff) {
   constexpr int NI = D / 32;
-  const bf16_t* kt = kpool + tile * (kPage * D);
-  const bf16_t* vt = vpool + tile * (kPage * D);
+  const __amdgpu_buffer_rsrc_t rk =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(kt), 0, nrec, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rv =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(vt), 0, nrec, 0x00020000);
 #pragma unroll
   for (int ii = 0; ii < NI; ++ii)
-    r.k[ii] = __builtin_nontemporal_load(
-        reinterpret_cast<const u32x4*>(kt + t * D + (u + 4 * ii) * 8));
+    r.k[ii] = __builtin_amdgcn_raw_buffer_load_b128(rk, (int)koff, ii * 1024, 2);
 #pragma unroll
   for (int ii = 0; ii < NI; ++ii)
-    r.v[ii] = __builtin_nontemporal_load(
-        reinterpret_cast<const u32x4*>(vt + (32 * ii + dl) * kPage + h * 8));
+    r.v[ii] = __builtin_amdgcn_raw_buffer_load_b128(rv, (int)voff, ii * 1024, 2);
 }
 
 template <int D, int G>
 __global__ __launch_bounds__(256, (G <= 4 ? 2 : 1)) void attn_split_kernel(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ kpool,
     const bf16_t* __restrict__ vpool, const int32_t* __restrict__ page_table, int max_pages,
-    int64_t num_pages, const int32_t* __restrict__ seq_lens, int len_add, int hkv, int chunk, int S,
+    int num_pages32, const int32_t* __restrict__ seq_lens, int len_add, int hkv, int chunk, int S,
     float qk_scale_log2, float* __restrict__ part_ml, float* __restrict__ part_acc) {
   constexpr int NI = D / 32;
   const int s = blockIdx.x;
@@ -103,18 +116,39 @@ __global__ __launch_bounds__(256, (G <= 4 ? 2 : 1)) void attn_split_kernel(
     for (int ii = 0; ii < NI; ++ii) acc[j][ii] = 0.f;
   }
 
+  // The wave's page ids (at most 64: a split spans at most 256 pages) sit one
+  // per lane; readlane turns each into a scalar with no memory latency in the
+  // page loop.  Ids outside [0, num_pages) become -1 (the page is skipped).
   const int32_t* ptr = page_table + (size_t)i * max_pages;
-  auto tile_of = [&](int pg) -> size_t {
-    int id = ptr[pg];
-    if (id < 0 || (int64_t)id >= num_pages) id = -1;
-    return id < 0 ? (size_t)0xFFFFFFFFFFFFFFFFull : (size_t)id * hkv + c;
+  const int my_pages = (pend - (pbeg + wave) + 3) >> 2;
+  int idv = -1;
+  if (lane < my_pages) {
+    const int id = ptr[pbeg + wave + 4 * lane];
+    idv = (id >= 0 && id < num_pages32) ? id : -1;
+  }
+  auto page_id = [&](int k) -> int {
+    return __builtin_amdgcn_readlane(idv, k < my_pages ? k : my_pages - 1);
   };
-  auto safe = [](size_t tile) -> size_t { return tile == (size_t)-1 ? 0 : tile; };
+  constexpr uint32_t kTileBytes = kPage * D * 2;
+  const char* kp8 = reinterpret_cast<const char*>(kpool);
+  const char* vp8 = reinterpret_cast<const char*>(vpool);
+  // lane byte offsets inside a tile: K block ii, token t, dims 8u..8u+7 of the
+  // block; V dims 32 ii + dl, token half h
+  const uint32_t koff = (uint32_t)(t * 64 + u * 16);
+  const uint32_t voff = (uint32_t)(dl * kPage * 2 + h * 16);
+#define SEVO_LOAD(BUF, K)                                                              \
+  {                                                                                    \
+    const int id_ = page_id(K);                                                        \
+    const size_t tb_ = id_ < 0 ? 0 : ((size_t)id_ * hkv + c) * kTileBytes;            \
+    load_page<D>(BUF, kp8 + tb_, vp8 + tb_, id_ < 0 ? 0 : (int)kTileBytes, koff, voff); \
+  }
 
-  auto consume = [&](const PageRegs<D>& r, int pg, bool bad) {
-    int valid = len - pg * kPage;
-    valid = valid > kPage ? kPage : valid;
-    if (bad) valid = 0;
+  // One page of the wave.  FULL: all 16 slots hold keys (no masking); else
+  // `valid` keys (0 for a page id outside the pool).  The running max of each
+  // head is wave-uniform, so the rescale of the accumulators is a uniform
+  // branch taken only when a page raises the max.
+  auto consume = [&](const PageRegs<D>& r, auto full_tag, int valid) {
+    constexpr bool FULL = decltype(full_tag)::value;
     float sc[G];
 #pragma unroll
     for (int j = 0; j < G; ++j) {
@@ -126,34 +160,27 @@ __global__ __launch_bounds__(256, (G <= 4 ? 2 : 1)) void attn_split_kernel(
         a = dot2_bf16(r.k[ii].z, qf[j][ii][2], a);
         a = dot2_bf16(r.k[ii].w, qf[j][ii][3], a);
       }
-      a += __shfl_xor(a, 1, kWave);
-      a += __shfl_xor(a, 2, kWave);
-      sc[j] = (t < valid) ? a * qk_scale_log2 : -INFINITY;
+      a = quad_sum(a) * qk_scale_log2;
+      if constexpr (FULL) sc[j] = a;
+      else sc[j] = (t < valid) ? a : -INFINITY;
     }
-    float alpha[G];
 #pragma unroll
     for (int j = 0; j < G; ++j) {
-      float pm = sc[j];
-      pm = fmaxf(pm, __shfl_xor(pm, 4, kWave));
-      pm = fmaxf(pm, __shfl_xor(pm, 8, kWave));
-      pm = fmaxf(pm, __shfl_xor(pm, 16, kWave));
-      pm = fmaxf(pm, __shfl_xor(pm, 32, kWave));
-      const float mn = fmaxf(m_run[j], pm);
-      float p;
-      if (mn == -INFINITY) {
-        alpha[j] = 1.f;
-        p = 0.f;
-      } else {
-        alpha[j] = exp2f(m_run[j] - mn);
-        p = exp2f(sc[j] - mn);
+      const float pm = quads_max(sc[j]);  // the 4 lanes of a quad hold equal scores
+      if (pm > m_run[j]) {
+        const float alpha = __builtin_amdgcn_exp2f(m_run[j] - pm);  // 0 on the first page
+        l_run[j] *= alpha;
+#pragma unroll
+        for (int ii = 0; ii < NI; ++ii) acc[j][ii] *= alpha;
+        m_run[j] = pm;
       }
-      m_run[j] = mn;
-      l_run[j] = l_run[j] * alpha[j] + p;
-      const bf16_t ph = f32_to_bf16(p);
-      const bf16_t pl = f32_to_bf16(p - bf16_to_f32(ph));
+      const float p = m_run[j] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(sc[j] - m_run[j]);
+      l_run[j] += p;
+      const __bf16 ph = (__bf16)p;
+      const __bf16 pl = (__bf16)(p - (float)ph);
       if (u == 0) {
-        p_lds[wave][0][j][t] = ph;
-        p_lds[wave][1][j][t] = pl;
+        p_lds[wave][0][j][t] = __builtin_bit_cast(bf16_t, ph);
+        p_lds[wave][1][j][t] = __builtin_bit_cast(bf16_t, pl);
       }
     }
     // lanes read p values written by other lanes of the wave: order the LDS
@@ -171,11 +198,11 @@ __global__ __launch_bounds__(256, (G <= 4 ? 2 : 1)) void attn_split_kernel(
     u32x4 vv[NI];
 #pragma unroll
     for (int ii = 0; ii < NI; ++ii) vv[ii] = r.v[ii];
-    if (valid < kPage) {
+    if constexpr (!FULL) {
       // slots past the last key may hold anything (even NaN patterns): zero them
+      const int t0 = h * 8;
 #pragma unroll
       for (int ii = 0; ii < NI; ++ii) {
-        const int t0 = h * 8;
         vv[ii].x = (t0 + 0 >= valid) ? 0u : ((t0 + 1 >= valid) ? (vv[ii].x & 0xFFFFu) : vv[ii].x);
         vv[ii].y = (t0 + 2 >= valid) ? 0u : ((t0 + 3 >= valid) ? (vv[ii].y & 0xFFFFu) : vv[ii].y);
         vv[ii].z = (t0 + 4 >= valid) ? 0u : ((t0 + 5 >= valid) ? (vv[ii].z & 0xFFFFu) : vv[ii].z);
@@ -186,7 +213,7 @@ __global__ __launch_bounds__(256, (G <= 4 ? 2 : 1)) void attn_split_kernel(
     for (int j = 0; j < G; ++j) {
 #pragma unroll
       for (int ii = 0; ii < NI; ++ii) {
-        float a = acc[j][ii] * alpha[j];
+        float a = acc[j][ii];
         a = dot2_bf16(vv[ii].x, pwl[j].x, a);
         a = dot2_bf16(vv[ii].y, pwl[j].y, a);
         a = dot2_bf16(vv[ii].z, pwl[j].z, a);
@@ -199,41 +226,57 @@ __global__ __launch_bounds__(256, (G <= 4 ? 2 : 1)) void attn_split_kernel(
       }
     }
   };
+  // dispatch a page: full pages take the unmasked path
+  auto consume_page = [&](const PageRegs<D>& r, int k) {
+    const int pg = pbeg + wave + 4 * k;
+    int valid = len - pg * kPage;
+    valid = valid > kPage ? kPage : valid;
+    if (page_id(k) < 0) valid = 0;
+    if (valid == kPage) consume(r, std::true_type{}, kPage);
+    else consume(r, std::false_type{}, valid);
+  };
 
-  int pg = pbeg + wave;
-  if (pg < pend) {
-    // register double buffer: A holds page pg, B the next one of this wave
-    PageRegs<D> A, B;
-    size_t tA = tile_of(pg);
-    size_t tB = tile_of(min(pg + 4, pend - 1));
-    load_page<D>(A, kpool, vpool, safe(tA), t, u, dl, h);
-    while (true) {
-      const size_t tC = tile_of(min(pg + 8, pend - 1));
-      load_page<D>(B, kpool, vpool, safe(tB), t, u, dl, h);
-      consume(A, pg, tA == (size_t)-1);
-      pg += 4;
-      if (pg >= pend) break;
-      const size_t tD = tile_of(min(pg + 8, pend - 1));
-      load_page<D>(A, kpool, vpool, safe(tC), t, u, dl, h);
-      consume(B, pg, tB == (size_t)-1);
-      pg += 4;
-      if (pg >= pend) break;
-      tA = tC;
-      tB = tD;
+  if (my_pages > 0) {
+    int k = 0;  // this wave's page index: logical page pbeg + wave + 4k
+    if constexpr (G <= 4) {
+      // three page buffers: while page k is consumed, pages k+1 and k+2 are in
+      // flight (16 KB per wave at D = 128)
+      PageRegs<D> A, B, C;
+      SEVO_LOAD(A, 0)
+      SEVO_LOAD(B, 1)
+      while (true) {
+        SEVO_LOAD(C, k + 2)
+        consume_page(A, k);
+        if (++k >= my_pages) break;
+        SEVO_LOAD(A, k + 2)
+        consume_page(B, k);
+        if (++k >= my_pages) break;
+        SEVO_LOAD(B, k + 2)
+        consume_page(C, k);
+        if (++k >= my_pages) break;
+      }
+    } else {
+      // two page buffers (registers are short at G = 8)
+      PageRegs<D> A, B;
+      SEVO_LOAD(A, 0)
+      while (true) {
+        SEVO_LOAD(B, k + 1)
+        consume_page(A, k);
+        if (++k >= my_pages) break;
+        SEVO_LOAD(A, k + 1)
+        consume_page(B, k);
+        if (++k >= my_pages) break;
+      }
     }
   }
 
+#undef SEVO_LOAD
   // finish this wave: sum V partials over the two token halves, l over tokens
 #pragma unroll
   for (int j = 0; j < G; ++j) {
 #pragma unroll
-    for (int ii = 0; ii < NI; ++ii) acc[j][ii] += __shfl_xor(acc[j][ii], 1, kWave);
-    float l = l_run[j];
-    l += __shfl_xor(l, 4, kWave);
-    l += __shfl_xor(l, 8, kWave);
-    l += __shfl_xor(l, 16, kWave);
-    l += __shfl_xor(l, 32, kWave);
-    l_run[j] = l;
+    for (int ii = 0; ii < NI; ++ii) acc[j][ii] += dpp<kDppQuadXor1>(acc[j][ii]);
+    l_run[j] = quads_sum(l_run[j]);  // over the 16 tokens (lanes of one quad agree)
   }
   if (lane == 0) {
 #pragma unroll
@@ -316,7 +359,8 @@ static hipError_t launch_attn_t(const AttnArgs& a, hipStream_t st) {
   const float log2e = 1.4426950408889634f;
   if (a.ev_begin) (void)hipEventRecord(a.ev_begin, st);
   hipLaunchKernelGGL((attn_split_kernel<D, G>), dim3(a.num_splits, a.hkv, a.n), dim3(256), 0, st,
-                     a.q, a.k_pool, a.v_pool, a.page_table, a.max_pages, a.num_pages, a.seq_lens,
+                     a.q, a.k_pool, a.v_pool, a.page_table, a.max_pages,
+                     (int)(a.num_pages < 0x7FFFFFFF ? a.num_pages : 0x7FFFFFFF), a.seq_lens,
                      a.len_add, a.hkv, a.chunk, a.num_splits, a.scale * log2e, a.part_ml, a.part_acc);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;

@@ -18,20 +18,67 @@ __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w 
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
 __device__ __forceinline__ float bf16_to_f32(bf16_t b) { return __uint_as_float((uint32_t)b << 16); }
 
-// Round-to-nearest-even fp32 -> bf16 (finite inputs).
+// Round-to-nearest-even fp32 -> bf16: gfx950 converts in hardware
+// (v_cvt_pk_bf16_f32, two values per instruction).
 __device__ __forceinline__ bf16_t f32_to_bf16(float f) {
-  uint32_t b = __float_as_uint(f);
-  b += 0x7FFFu + ((b >> 16) & 1u);
-  return (bf16_t)(b >> 16);
+  return __builtin_bit_cast(bf16_t, (__bf16)f);
 }
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-  return (uint32_t)f32_to_bf16(lo) | ((uint32_t)f32_to_bf16(hi) << 16);
+  const bf16x2v v = {(__bf16)lo, (__bf16)hi};
+  return __builtin_bit_cast(uint32_t, v);
 }
 
 // a.x*b.x + a.y*b.y + c, bf16 pairs packed in 32-bit words, fp32 accumulate.
 __device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b, float c) {
   return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2v, a),
                                          __builtin_bit_cast(bf16x2v, b), c, false);
+}
+
+// ---- cross-lane reductions in registers (DPP and the gfx950 permlane swaps;
+// no LDS round trip).  Lane groups follow the wave64 layout: quads of 4
+// lanes, rows of 16 lanes, halves of 32 lanes.
+template <int CTRL>
+__device__ __forceinline__ float dpp(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+constexpr int kDppQuadXor1 = 0xB1;  // quad_perm [1,0,3,2]
+constexpr int kDppQuadXor2 = 0x4E;  // quad_perm [2,3,0,1]
+constexpr int kDppRowRor4 = 0x124;
+constexpr int kDppRowRor8 = 0x128;
+
+// sum over the 4 lanes of each quad (every lane gets the result)
+__device__ __forceinline__ float quad_sum(float v) {
+  v += dpp<kDppQuadXor1>(v);
+  return v + dpp<kDppQuadXor2>(v);
+}
+// combine lane i with lane i ^ 16 (rows 0<->1, 2<->3), every lane gets the result
+__device__ __forceinline__ float xor16_max(float v) {
+  const auto p = __builtin_amdgcn_permlane16_swap(__float_as_int(v), __float_as_int(v), false, false);
+  return fmaxf(__int_as_float(p[0]), __int_as_float(p[1]));
+}
+__device__ __forceinline__ float xor16_sum(float v) {
+  const auto p = __builtin_amdgcn_permlane16_swap(__float_as_int(v), __float_as_int(v), false, false);
+  return __int_as_float(p[0]) + __int_as_float(p[1]);
+}
+// combine lane i with lane i ^ 32
+__device__ __forceinline__ float xor32_max(float v) {
+  const auto p = __builtin_amdgcn_permlane32_swap(__float_as_int(v), __float_as_int(v), false, false);
+  return fmaxf(__int_as_float(p[0]), __int_as_float(p[1]));
+}
+__device__ __forceinline__ float xor32_sum(float v) {
+  const auto p = __builtin_amdgcn_permlane32_swap(__float_as_int(v), __float_as_int(v), false, false);
+  return __int_as_float(p[0]) + __int_as_float(p[1]);
+}
+// max / sum over the lanes with equal lane % 4 (the quads of the wave)
+__device__ __forceinline__ float quads_max(float v) {
+  v = fmaxf(v, dpp<kDppRowRor4>(v));
+  v = fmaxf(v, dpp<kDppRowRor8>(v));
+  return xor32_max(xor16_max(v));
+}
+__device__ __forceinline__ float quads_sum(float v) {
+  v += dpp<kDppRowRor4>(v);
+  v += dpp<kDppRowRor8>(v);
+  return xor32_sum(xor16_sum(v));
 }
 
 __device__ __forceinline__ float wave_sum(float v) {

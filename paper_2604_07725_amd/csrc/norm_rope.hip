@@ -99,9 +99,12 @@ __global__ __launch_bounds__(64) void qk_norm_rope_append_kernel(RopeAppendArgs 
     const int page = a.page_table[(size_t)i * a.max_pages + pg];
     if (page < 0 || (int64_t)page >= a.num_pages) return;
     const int kh = hh - a.hq;
-    bf16_t* dst = a.k_pool + (((size_t)page * a.hkv + kh) * kPage + (p & 15)) * a.d;
-    dst[m] = f32_to_bf16(r0);
-    dst[m + half] = f32_to_bf16(r1);
+    // K tile: dims in blocks of 32, each block [16 slots][32 dims]
+    bf16_t* tile = a.k_pool + ((size_t)page * a.hkv + kh) * kPage * a.d;
+    const int s = p & 15;
+    const int e0 = m, e1 = m + half;
+    tile[((e0 >> 5) * kPage + s) * 32 + (e0 & 31)] = f32_to_bf16(r0);
+    tile[((e1 >> 5) * kPage + s) * 32 + (e1 & 31)] = f32_to_bf16(r1);
   } else {
     if (!act || !pos_ok) return;
     const int pg = p >> 4;

@@ -42,6 +42,12 @@ bool supported_group(int hq, int hkv) {
   return g == 1 || g == 2 || g == 4 || g == 8;
 }
 
+// A split spans at most this many logical pages (64 per wave of the split
+// kernel, whose page ids are then held one per lane).
+constexpr int kMaxSplitPages = 256;
+
+int min_splits(int max_pages) { return (max_pages + kMaxSplitPages - 1) / kMaxSplitPages; }
+
 // Splits per candidate so that (n * hkv * S) workgroups fill the 256 CUs
 // several times over, with at least 32 pages (8 per wave) per split.
 int plan_splits(int n, int hkv, int max_pages) {
@@ -50,8 +56,19 @@ int plan_splits(int n, int hkv, int max_pages) {
   const int cap = (max_pages + 31) / 32;
   if (s > cap) s = cap;
   if (s < 1) s = 1;
-  if (s > 256) s = 256;
+  if (s < min_splits(max_pages)) s = min_splits(max_pages);
   return s;
+}
+
+// The split count actually used: the requested (or planned) count, raised so
+// that no split exceeds kMaxSplitPages, then trimmed so every split is used.
+void resolve_splits(int n, int hkv, int max_pages, int requested, int* S, int* chunk) {
+  int s = requested > 0 ? requested : plan_splits(n, hkv, max_pages);
+  if (s < min_splits(max_pages)) s = min_splits(max_pages);
+  if (s > max_pages) s = max_pages;
+  const int c = (max_pages + s - 1) / s;
+  *chunk = c;
+  *S = (max_pages + c - 1) / c;
 }
 
 size_t attn_ws(int n, int hq, int d, int S) {
@@ -223,18 +240,17 @@ SEVO_API size_t sevo_attn_workspace_bytes(int32_t n, int32_t n_q_heads, int32_t 
                                           int32_t head_dim, int32_t max_pages,
                                           int32_t num_splits) {
   if (n <= 0 || n_q_heads <= 0 || head_dim <= 0 || max_pages <= 0) return 0;
-  const int S = num_splits > 0 ? num_splits : plan_splits(n, n_kv_heads, max_pages);
-  return attn_ws(n, n_q_heads, head_dim, S > max_pages ? max_pages : S);
+  int S, chunk;
+  resolve_splits(n, n_kv_heads, max_pages, num_splits, &S, &chunk);
+  return attn_ws(n, n_q_heads, head_dim, S);
 }
 
 static sevo_status attn_core(int n, int hq, int hkv, int d, int max_pages, int num_splits,
                              int64_t num_pages, const void* q, const void* kp, const void* vp,
                              const int32_t* pt, const int32_t* lens, float scale, void* out,
                              void* ws, size_t ws_bytes, hipStream_t st) {
-  int S = num_splits > 0 ? num_splits : plan_splits(n, hkv, max_pages);
-  if (S > max_pages) S = max_pages;
-  const int chunk = (max_pages + S - 1) / S;
-  S = (max_pages + chunk - 1) / chunk;
+  int S, chunk;
+  resolve_splits(n, hkv, max_pages, num_splits, &S, &chunk);
   const size_t need = attn_ws(n, hq, d, S);
   if (ws_bytes < need)
     return fail(SEVO_ERR_WORKSPACE_TOO_SMALL, "attention needs %zu workspace bytes, got %zu",
@@ -431,11 +447,7 @@ StepLayout step_layout(const sevo_model_config& c, int n, int max_pages, int num
   StepLayout L;
   const int qd = c.n_q_heads * c.head_dim;
   const int qkvd = (c.n_q_heads + 2 * c.n_kv_heads) * c.head_dim;
-  int S = num_splits > 0 ? num_splits : plan_splits(n, c.n_kv_heads, max_pages);
-  if (S > max_pages) S = max_pages;
-  const int chunk = (max_pages + S - 1) / S;
-  L.S = (max_pages + chunk - 1) / chunk;
-  L.chunk = chunk;
+  resolve_splits(n, c.n_kv_heads, max_pages, num_splits, &L.S, &L.chunk);
   size_t off = 0;
   auto take = [&](size_t bytes) {
     const size_t o = off;

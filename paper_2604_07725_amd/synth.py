@@ -325,8 +325,8 @@ def global_specs(shape: ModelShape, seed: int) -> dict:
 
 
 def kv_specs(shape: ModelShape, seed: int, layer: int, n_pages: int) -> tuple:
-    """K pool [P][hkv][16][d] and V pool [P][hkv][d][16], both N(0, 1)."""
-    kshape = (n_pages, shape.n_kv_heads, PAGE_SIZE, shape.head_dim)
+    """K pool [P][hkv][d/32][16][32] and V pool [P][hkv][d][16], both N(0, 1)."""
+    kshape = (n_pages, shape.n_kv_heads, shape.head_dim // 32, PAGE_SIZE, 32)
     vshape = (n_pages, shape.n_kv_heads, shape.head_dim, PAGE_SIZE)
     return (TensorSpec(kshape, tensor_key(seed, K_KPOOL, layer), 1.0),
             TensorSpec(vshape, tensor_key(seed, K_VPOOL, layer), 1.0))

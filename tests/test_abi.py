@@ -102,8 +102,10 @@ def test_zero_population_is_a_no_op():
 
 def test_split_planning():
     L = sevo.lib()
-    # enough workgroups for 256 CUs, at least 32 pages per split, at least one split
-    assert L.sevo_attn_plan_splits(64, 8, 2049) == 4
+    # enough workgroups for 256 CUs, at least 32 pages per split, at least one
+    # split, and no split longer than 256 pages
+    assert L.sevo_attn_plan_splits(64, 8, 2049) == 9
+    assert L.sevo_attn_plan_splits(64, 8, 1024) == 4
     assert L.sevo_attn_plan_splits(16, 8, 1024) == 16
     assert L.sevo_attn_plan_splits(4, 2, 33) == 2
     assert L.sevo_attn_plan_splits(1, 1, 1) == 1

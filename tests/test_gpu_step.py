@@ -74,19 +74,22 @@ def test_tiny_step_sequence_matches_oracle(S):
     # appended slots: close to the oracle's; every other slot untouched
     torch.cuda.synchronize()
     for l in range(shape.n_layers):
-        gk = kp[l].double().cpu().numpy()
+        def tok_major(a):   # [P, hkv, d/32, 16, 32] -> [P, hkv, 16, d]
+            return np.transpose(a, (0, 1, 3, 2, 4)).reshape(a.shape[0], a.shape[1], 16, -1)
+        gk = tok_major(kp[l].double().cpu().numpy())
         gv = vp[l].double().cpu().numpy()
         kspec, vspec = synth.kv_specs(shape, w.seed, l, pop.n_pages)
-        k0 = synth.host_values(kspec).reshape(kspec.shape)
+        k0 = tok_major(synth.host_values(kspec).reshape(kspec.shape))
         v0 = synth.host_values(vspec).reshape(vspec.shape)
-        written = np.zeros(kspec.shape[:3], bool)   # [page, head, slot]
+        hkl = tok_major(hk[l])
+        written = np.zeros(gk.shape[:3], bool)   # [page, head, slot]
         for i in range(pop.n):
             for p in range(int(pop.lengths[i]), int(pop.lengths[i]) + steps):
                 written[pop.page_table[i, p // 16], :, p % 16] = True
         np.testing.assert_array_equal(gk[~written], k0[~written])
         np.testing.assert_array_equal(np.transpose(gv, (0, 1, 3, 2))[~written],
                                       np.transpose(v0, (0, 1, 3, 2))[~written])
-        gkw, rkw = gk[written], hk[l][written]
+        gkw, rkw = gk[written], hkl[written]
         gvw = np.transpose(gv, (0, 1, 3, 2))[written]
         rvw = np.transpose(hv[l], (0, 1, 3, 2))[written]
         say(f"  layer {l}: appended k max diff {np.abs(gkw - rkw).max():.2e}, "

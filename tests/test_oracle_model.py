@@ -15,7 +15,7 @@ import torch
 from oracle import decoder as od
 from paper_2604_07725_amd.synth import ModelShape
 
-SHAPE = ModelShape(n_layers=2, hidden=64, n_q_heads=4, n_kv_heads=2, head_dim=16, ffn=96,
+SHAPE = ModelShape(n_layers=2, hidden=64, n_q_heads=4, n_kv_heads=2, head_dim=32, ffn=96,
                    vocab=97, rope_theta=1.0e4)
 
 
@@ -73,7 +73,8 @@ def _hf_model(shape, w):
 
 
 def _empty_pools(shape, n_pages):
-    kp = [np.zeros((n_pages, shape.n_kv_heads, 16, shape.head_dim)) for _ in range(shape.n_layers)]
+    kp = [np.zeros((n_pages, shape.n_kv_heads, shape.head_dim // 32, 16, 32))
+          for _ in range(shape.n_layers)]
     vp = [np.zeros((n_pages, shape.n_kv_heads, shape.head_dim, 16)) for _ in range(shape.n_layers)]
     return kp, vp
 
@@ -108,8 +109,8 @@ def test_whole_step_invariant_under_page_permutation_and_deterministic():
     lens = np.array([5, 33, 20])
     need = (lens + 1 + 15) // 16
     P = int(need.sum())
-    kp = [rng.standard_normal((P, 2, 16, 16)) for _ in range(2)]
-    vp = [rng.standard_normal((P, 2, 16, 16)) for _ in range(2)]
+    kp = [rng.standard_normal((P, 2, 1, 16, 32)) for _ in range(2)]
+    vp = [rng.standard_normal((P, 2, 32, 16)) for _ in range(2)]
     pt = np.full((N, need.max()), -1)
     c = 0
     for i in range(N):

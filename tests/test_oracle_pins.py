@@ -313,23 +313,27 @@ def test_split_equals_unsplit(L, S):
 
 
 def _random_pool(n_pages, hkv, d):
-    return RNG.standard_normal((n_pages, hkv, 16, d)), RNG.standard_normal((n_pages, hkv, d, 16))
+    return (RNG.standard_normal((n_pages, hkv, d // 32, 16, 32)),
+            RNG.standard_normal((n_pages, hkv, d, 16)))
 
 
 def test_gather_layout_by_hand():
-    kp, vp = _random_pool(5, 2, 8)
+    kp, vp = _random_pool(5, 2, 64)
     pages = np.array([3, 0, 4])
     K, V = od.gather_kv(kp, vp, pages, 35)
-    assert K.shape == (2, 35, 8)
-    # key 20 lives in logical page 1 -> physical 0, slot 4
-    np.testing.assert_array_equal(K[1, 20], kp[0, 1, 4, :])
+    assert K.shape == (2, 35, 64)
+    # key 20 lives in logical page 1 -> physical 0, slot 4; dim 40 is in dim
+    # block 1 at offset 8: flat tile position (1 * 16 + 4) * 32 + 8
+    flat = kp.reshape(5, 2, -1)
+    assert K[1, 20, 40] == flat[0, 1, (1 * 16 + 4) * 32 + 8]
+    np.testing.assert_array_equal(K[1, 20], np.concatenate([kp[0, 1, 0, 4], kp[0, 1, 1, 4]]))
     np.testing.assert_array_equal(V[1, 20], vp[0, 1, :, 4])
-    np.testing.assert_array_equal(K[0, 34], kp[4, 0, 2, :])
+    assert K[0, 34, 3] == flat[4, 0, 2 * 32 + 3]
     np.testing.assert_array_equal(V[0, 0], vp[3, 0, :, 0])
 
 
 def test_paging_invariant_under_physical_permutation():
-    N, hq, hkv, d = 3, 4, 2, 16
+    N, hq, hkv, d = 3, 4, 2, 32
     lens = np.array([16, 45, 70])
     need = (lens + 15) // 16
     P = int(need.sum())
@@ -352,15 +356,16 @@ def test_paging_invariant_under_physical_permutation():
 
 
 def test_append_writes_exactly_one_slot():
-    kp, vp = _random_pool(6, 2, 8)
+    kp, vp = _random_pool(6, 2, 64)
     k0, v0 = kp.copy(), vp.copy()
     pt = np.array([[5, 1], [0, 3]])
     pos = np.array([17, 9])
-    k = RNG.standard_normal((2, 2, 8))
-    v = RNG.standard_normal((2, 2, 8))
+    k = RNG.standard_normal((2, 2, 64))
+    v = RNG.standard_normal((2, 2, 64))
     od.append_kv(kp, vp, pt, pos, k, v)
-    changed_k = np.argwhere((kp != k0).any(axis=-1))
+    changed_k = np.argwhere((kp != k0).any(axis=(2, 4)))     # [page, head, slot]
     assert sorted(map(tuple, changed_k.tolist())) == [(0, 0, 9), (0, 1, 9), (1, 0, 1), (1, 1, 1)]
-    np.testing.assert_array_equal(kp[1, :, 1, :], k[0])
+    assert int((kp != k0).sum()) == 4 * 64
+    np.testing.assert_array_equal(kp[1, :, :, 1, :].reshape(2, 64), k[0])
     np.testing.assert_array_equal(vp[0, :, :, 9], v[1])
     assert int(((vp != v0).any(axis=-2)).sum()) == 4
