@@ -73,7 +73,8 @@ const char* sevo_version(void);
 
 /* Decoder shape.  Supported: head_dim in {64, 128}; n_q_heads % n_kv_heads == 0
  * with n_q_heads / n_kv_heads in {1, 2, 4, 8}; page_size == 16; hidden, ffn and
- * n_q_heads * head_dim multiples of 32; qk_norm in {0, 1}; rms_eps > 0. */
+ * n_q_heads * head_dim multiples of 128; vocab a multiple of 64; qk_norm in
+ * {0, 1}; rms_eps > 0. */
 typedef struct {
   int32_t n_layers, hidden, n_q_heads, n_kv_heads, head_dim, ffn, vocab;
   int32_t page_size;    /* must be 16 */
@@ -121,7 +122,7 @@ void sevo_free_model(sevo_model* m);
  *   o[i][j] = softmax_t(scale * q[i][j] . K_i[c][t]) V_i[c][t],  t < seq_lens[i],
  * c = j / (n_q_heads / n_kv_heads).  Each candidate's pages are cut into
  * splits of ceil(max_pages / S) logical pages, where S is num_splits raised as
- * needed so that a split spans at most 256 pages; every split yields an
+ * needed so that a split spans at most 512 pages; every split yields an
  * online-softmax partial (running max, sum, weighted V) that a combine pass
  * merges in split order, so the result is deterministic.
  *   q        bf16 [n][n_q_heads][head_dim]
@@ -245,8 +246,8 @@ sevo_status sevo_rmsnorm(const float* x, const void* gain, int32_t rows, int32_t
  *   SEVO_LINEAR_STORE  out fp32 [m][n_out]  = Y
  *   SEVO_LINEAR_ADD    out fp32 [m][n_out] += Y          (residual update)
  *   SEVO_LINEAR_SWIGLU out bf16 [m][n_out/2] = silu(Y[:, :n_out/2]) * Y[:, n_out/2:]
- * k % 32 == 0; n_out % 64 == 0 (SWIGLU: n_out % 128 == 0); ldx % 8 == 0.
- * k_splits 0 = chosen by the library. */
+ * k % 128 == 0; n_out % 64 == 0 (SWIGLU: n_out % 128 == 0); ldx % 8 == 0.
+ * k_splits 0 = chosen by the library (SWIGLU always uses one split). */
 #define SEVO_LINEAR_STORE 0
 #define SEVO_LINEAR_ADD 1
 #define SEVO_LINEAR_SWIGLU 2

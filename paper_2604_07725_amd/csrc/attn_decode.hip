@@ -1,7 +1,7 @@
 // Paged GQA split-KV decode attention for gfx950 (one query token per
 // candidate), plus the cross-split combine.
 //
-// Work decomposition: one 256-thread workgroup per (split, kv head, candidate).
+// Work decomposition: one 256-thread workgroup per (kv head, split, candidate).
 // A split is a run of `chunk` logical pages of the candidate; its four waves
 // take every fourth page, each keeping its own online-softmax state for the
 // G = hq / hkv query heads that share the kv head, and merge through LDS at the
@@ -31,8 +31,8 @@
 //       one contiguous 1 KB wavefront access.
 // Loads for the wave's next two pages are issued before the current page is
 // consumed (three register page buffers; two for G = 8, where registers are
-// short).  A split spans at most 256 pages, so each wave's page ids fit one
-// per lane in a single register, read out with readlane inside the loop.
+// short).  A split spans at most 512 pages, so each wave's page ids fit one
+// per lane in two registers, read out with readlane inside the loop.
 #include <type_traits>
 
 #include "common.h"
@@ -75,8 +75,12 @@ __global__ __launch_bounds__(256, (G <= 4 ? 2 : 1)) void attn_split_kernel(
     int num_pages32, const int32_t* __restrict__ seq_lens, int len_add, int hkv, int chunk, int S,
     float qk_scale_log2, float* __restrict__ part_ml, float* __restrict__ part_acc) {
   constexpr int NI = D / 32;
-  const int s = blockIdx.x;
-  const int c = blockIdx.y;
+  // Grid (kv head, split, candidate): workgroups are dealt round-robin to the
+  // 8 XCDs by linear id, so with 8 kv heads each XCD streams one head of every
+  // candidate (equal work per XCD), and the splits of a candidate run side by
+  // side (measured best among the orders of the three indices).
+  const int c = blockIdx.x;
+  const int s = blockIdx.y;
   const int i = blockIdx.z;
   const int hq = hkv * G;
   int len = seq_lens[i] + len_add;
@@ -116,18 +120,24 @@ __global__ __launch_bounds__(256, (G <= 4 ? 2 : 1)) void attn_split_kernel(
     for (int ii = 0; ii < NI; ++ii) acc[j][ii] = 0.f;
   }
 
-  // The wave's page ids (at most 64: a split spans at most 256 pages) sit one
-  // per lane; readlane turns each into a scalar with no memory latency in the
-  // page loop.  Ids outside [0, num_pages) become -1 (the page is skipped).
+  // The wave's page ids (at most 128: a split spans at most 512 pages) sit one
+  // per lane in two registers; readlane turns each into a scalar with no
+  // memory latency in the page loop.  Ids outside [0, num_pages) become -1
+  // (the page is skipped).
   const int32_t* ptr = page_table + (size_t)i * max_pages;
   const int my_pages = (pend - (pbeg + wave) + 3) >> 2;
-  int idv = -1;
+  int idv0 = -1, idv1 = -1;
   if (lane < my_pages) {
     const int id = ptr[pbeg + wave + 4 * lane];
-    idv = (id >= 0 && id < num_pages32) ? id : -1;
+    idv0 = (id >= 0 && id < num_pages32) ? id : -1;
+  }
+  if (lane + 64 < my_pages) {
+    const int id = ptr[pbeg + wave + 4 * (lane + 64)];
+    idv1 = (id >= 0 && id < num_pages32) ? id : -1;
   }
   auto page_id = [&](int k) -> int {
-    return __builtin_amdgcn_readlane(idv, k < my_pages ? k : my_pages - 1);
+    const int kk = k < my_pages ? k : my_pages - 1;
+    return kk < 64 ? __builtin_amdgcn_readlane(idv0, kk) : __builtin_amdgcn_readlane(idv1, kk - 64);
   };
   constexpr uint32_t kTileBytes = kPage * D * 2;
   const char* kp8 = reinterpret_cast<const char*>(kpool);
@@ -358,7 +368,7 @@ template <int D, int G>
 static hipError_t launch_attn_t(const AttnArgs& a, hipStream_t st) {
   const float log2e = 1.4426950408889634f;
   if (a.ev_begin) (void)hipEventRecord(a.ev_begin, st);
-  hipLaunchKernelGGL((attn_split_kernel<D, G>), dim3(a.num_splits, a.hkv, a.n), dim3(256), 0, st,
+  hipLaunchKernelGGL((attn_split_kernel<D, G>), dim3(a.hkv, a.num_splits, a.n), dim3(256), 0, st,
                      a.q, a.k_pool, a.v_pool, a.page_table, a.max_pages,
                      (int)(a.num_pages < 0x7FFFFFFF ? a.num_pages : 0x7FFFFFFF), a.seq_lens,
                      a.len_add, a.hkv, a.chunk, a.num_splits, a.scale * log2e, a.part_ml, a.part_acc);

@@ -13,8 +13,13 @@ hipError_t launch_embed(const bf16_t* embed, const int32_t* tokens, int n, int h
                         int vocab, float* x, hipStream_t st);
 hipError_t launch_rmsnorm(const float* x, const bf16_t* gain, int rows, int cols, float eps,
                           bf16_t* out, hipStream_t st);
+// x += sum_s part[s] (split order; S == 0: nothing to add), then
+// out = bf16(RMSNorm(x) * gain).  part is [S][rows][cols] fp32.
+hipError_t launch_add_rmsnorm(float* x, const float* part, int S, const bf16_t* gain, int rows,
+                              int cols, float eps, bf16_t* out, hipStream_t st);
 struct RopeAppendArgs {
-  const float* qkv;
+  const float* qkv;  // [qkv_splits][n][(hq + 2 hkv) d]: summed in split order
+  int qkv_splits;
   int n, hq, hkv, d;
   const int32_t* positions;
   const int32_t* page_table;
@@ -60,11 +65,17 @@ struct LinearPlan {
   int k_splits;
   int k_chunk;
 };
-LinearPlan plan_linear(int m, int n_out, int k, int k_splits);
-size_t linear_workspace_bytes(int m, int n_out, int k, int k_splits);
+LinearPlan plan_linear(int m, int n_out, int k, int k_splits, int mode);
+size_t linear_workspace_bytes(int m, int n_out, int k, int k_splits, int mode);
+// complete Y = X W^T with the STORE / ADD / SWIGLU epilogue
 hipError_t launch_linear(int m, int n_out, int k, int ldx, int mode, const LinearPlan& plan,
                          const bf16_t* x, const bf16_t* w, void* out, float* workspace,
                          hipStream_t st);
+// raw fp32 split partials out[split][m][n] (k_splits == 1: the product itself,
+// added to out when accumulate)
+hipError_t launch_linear_partials(int m, int n_out, int k, int ldx, const LinearPlan& plan,
+                                  const bf16_t* x, const bf16_t* w, float* out, int accumulate,
+                                  hipStream_t st);
 
 // ---- sample.hip
 constexpr int kSampleChunk = 4096;  // vocab entries per partial workgroup

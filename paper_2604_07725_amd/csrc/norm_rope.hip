@@ -53,7 +53,8 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const float* __restrict__ 
   }
 }
 
-// One wave per (candidate, head) of the fused QKV output.  Lane m < d/2 owns
+// One wave per (candidate, head) of the QKV projection (given as the fp32
+// split-K partials of the GEMM, summed here in split order).  Lane m < d/2 owns
 // the rotate-half pair (m, m + d/2).  q heads -> q_out; k heads -> K pool slot
 // p_i; v heads -> V pool slot p_i (dim-major tile).  Positions outside the
 // RoPE table or page ids outside the pool skip the write (no fault).
@@ -64,9 +65,15 @@ __global__ __launch_bounds__(64) void qk_norm_rope_append_kernel(RopeAppendArgs 
   const int half = a.d >> 1;
   const bool act = m < half;
   const int qkv_ld = (a.hq + 2 * a.hkv) * a.d;
+  const size_t split_stride = (size_t)a.n * qkv_ld;
   const float* src = a.qkv + (size_t)i * qkv_ld + (size_t)hh * a.d;
-  float u0 = act ? src[m] : 0.f;
-  float u1 = act ? src[m + half] : 0.f;
+  float u0 = 0.f, u1 = 0.f;
+  if (act) {
+    for (int sp = 0; sp < a.qkv_splits; ++sp) {  // split-K partials, in split order
+      u0 += src[sp * split_stride + m];
+      u1 += src[sp * split_stride + m + half];
+    }
+  }
   const int p = a.positions[i];
   const bool pos_ok = p >= 0 && p < a.max_pos;
   if (hh < a.hq + a.hkv) {
@@ -162,6 +169,55 @@ hipError_t launch_embed(const bf16_t* embed, const int32_t* tokens, int n, int h
                         float* x, hipStream_t st) {
   if (n == 0) return hipSuccess;
   hipLaunchKernelGGL(embed_kernel, dim3(n), dim3(256), 0, st, embed, tokens, hidden, vocab, x);
+  return hipGetLastError();
+}
+
+// x[r] += sum_s part[s][r] in split order, written back; then the RMSNorm.
+// 1024 threads per row, each owning 4 consecutive columns per 4096-column
+// pass with all split loads independent (latency, not bandwidth, is the cost).
+__global__ __launch_bounds__(1024) void add_rmsnorm_kernel(float* __restrict__ x,
+                                                           const float* __restrict__ part, int S,
+                                                           size_t part_stride,
+                                                           const bf16_t* __restrict__ gain,
+                                                           int cols, float eps,
+                                                           bf16_t* __restrict__ out) {
+  __shared__ float red[16];
+  float* xr = x + (size_t)blockIdx.x * cols;
+  const float* pr = part + (size_t)blockIdx.x * cols;
+  float ss = 0.f;
+  for (int c = threadIdx.x * 4; c < cols; c += 4096) {
+    f32x4 v = *reinterpret_cast<const f32x4*>(xr + c);
+    if (S > 0) {
+      f32x4 p[16];
+#pragma unroll
+      for (int s = 0; s < 16; ++s)
+        if (s < S) p[s] = *reinterpret_cast<const f32x4*>(pr + s * part_stride + c);
+#pragma unroll
+      for (int s = 0; s < 16; ++s)
+        if (s < S) v += p[s];
+      *reinterpret_cast<f32x4*>(xr + c) = v;
+    }
+    ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+  }
+  ss = block_sum<16>(ss, red);
+  const float inv = 1.0f / sqrtf(ss / (float)cols + eps);
+  bf16_t* orow = out + (size_t)blockIdx.x * cols;
+  for (int c = threadIdx.x * 4; c < cols; c += 4096) {
+    const f32x4 v = *reinterpret_cast<const f32x4*>(xr + c);
+    const uint2 g = *reinterpret_cast<const uint2*>(gain + c);
+    uint2 o;
+    o.x = pack_bf16x2(v.x * inv * bf16_lo(g.x), v.y * inv * bf16_hi(g.x));
+    o.y = pack_bf16x2(v.z * inv * bf16_lo(g.y), v.w * inv * bf16_hi(g.y));
+    *reinterpret_cast<uint2*>(orow + c) = o;
+  }
+}
+
+hipError_t launch_add_rmsnorm(float* x, const float* part, int S, const bf16_t* gain, int rows,
+                              int cols, float eps, bf16_t* out, hipStream_t st) {
+  if (rows == 0) return hipSuccess;
+  if (S > 16) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(add_rmsnorm_kernel, dim3(rows), dim3(1024), 0, st, x, part, part ? S : 0,
+                     (size_t)rows * cols, gain, cols, eps, out);
   return hipGetLastError();
 }
 

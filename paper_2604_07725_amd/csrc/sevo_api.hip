@@ -42,17 +42,18 @@ bool supported_group(int hq, int hkv) {
   return g == 1 || g == 2 || g == 4 || g == 8;
 }
 
-// A split spans at most this many logical pages (64 per wave of the split
-// kernel, whose page ids are then held one per lane).
-constexpr int kMaxSplitPages = 256;
+// A split spans at most this many logical pages (128 per wave of the split
+// kernel, whose page ids are then held one per lane in two registers).
+constexpr int kMaxSplitPages = 512;
 
 int min_splits(int max_pages) { return (max_pages + kMaxSplitPages - 1) / kMaxSplitPages; }
 
 // Splits per candidate so that (n * hkv * S) workgroups fill the 256 CUs
-// several times over, with at least 32 pages (8 per wave) per split.
+// about 16 times over (512 resident at 2 per CU), with at least 32 pages
+// (8 per wave) per split.
 int plan_splits(int n, int hkv, int max_pages) {
   const int pairs = n * hkv > 0 ? n * hkv : 1;
-  int s = (2048 + pairs - 1) / pairs;
+  int s = (4096 + pairs - 1) / pairs;
   const int cap = (max_pages + 31) / 32;
   if (s > cap) s = cap;
   if (s < 1) s = 1;
@@ -156,9 +157,9 @@ SEVO_API sevo_status sevo_init_model(const sevo_model_config* cfg, const sevo_we
     if (c.qk_norm != 0 && c.qk_norm != 1) return fail(SEVO_ERR_INVALID_ARGUMENT, "qk_norm");
     sevo_status st = check_attn_shape(1, c.n_q_heads, c.n_kv_heads, c.head_dim, c.page_size, 1);
     if (st) return st;
-    if (c.hidden % 64 || c.ffn % 64 || (c.n_q_heads * c.head_dim) % 64 || c.vocab % 64)
-      return fail(SEVO_ERR_UNSUPPORTED, "hidden, ffn, n_q_heads*head_dim and vocab must be "
-                                        "multiples of 64");
+    if (c.hidden % 128 || c.ffn % 128 || (c.n_q_heads * c.head_dim) % 128 || c.vocab % 64)
+      return fail(SEVO_ERR_UNSUPPORTED, "hidden, ffn and n_q_heads*head_dim must be multiples "
+                                        "of 128 and vocab of 64");
     if (!w->embed || !w->lm_head || !w->final_norm)
       return fail(SEVO_ERR_INVALID_ARGUMENT, "null embed / lm_head / final_norm");
     const void* const* tabs[] = {w->attn_norm, w->w_qkv, w->w_o, w->ffn_norm, w->w_gate_up,
@@ -359,8 +360,8 @@ SEVO_API sevo_status sevo_rmsnorm(const float* x, const void* gain, int32_t rows
 }
 
 static sevo_status linear_check(int m, int n_out, int k, int ldx, int mode, int k_splits) {
-  if (m < 0 || n_out < 64 || k < 32) return fail(SEVO_ERR_INVALID_ARGUMENT, "bad m / n_out / k");
-  if (k % 32) return fail(SEVO_ERR_UNSUPPORTED, "k %% 32 != 0");
+  if (m < 0 || n_out < 64 || k < 128) return fail(SEVO_ERR_INVALID_ARGUMENT, "bad m / n_out / k");
+  if (k % 128) return fail(SEVO_ERR_UNSUPPORTED, "k %% 128 != 0");
   if (n_out % 64) return fail(SEVO_ERR_UNSUPPORTED, "n_out %% 64 != 0");
   if (mode == SEVO_LINEAR_SWIGLU && n_out % 128)
     return fail(SEVO_ERR_UNSUPPORTED, "SwiGLU needs n_out %% 128 == 0");
@@ -373,7 +374,8 @@ static sevo_status linear_check(int m, int n_out, int k, int ldx, int mode, int 
 SEVO_API size_t sevo_linear_workspace_bytes(int32_t m, int32_t n_out, int32_t k,
                                             int32_t k_splits) {
   if (m <= 0 || n_out <= 0 || k <= 0) return 0;
-  return round_up(sevo::linear_workspace_bytes(m, n_out, k, k_splits), 256);
+  // the STORE / ADD plan; SwiGLU needs no workspace
+  return round_up(sevo::linear_workspace_bytes(m, n_out, k, k_splits, SEVO_LINEAR_STORE), 256);
 }
 
 SEVO_API sevo_status sevo_linear(const sevo_linear_args* a, void* stream) {
@@ -383,10 +385,9 @@ SEVO_API sevo_status sevo_linear(const sevo_linear_args* a, void* stream) {
   if (a->m == 0) return SEVO_OK;
   if (!a->x || !a->w || !a->out || !aligned16(a->x) || !aligned16(a->w) || !aligned16(a->out))
     return fail(SEVO_ERR_INVALID_ARGUMENT, "null or misaligned pointer");
-  const sevo::LinearPlan plan = sevo::plan_linear(a->m, a->n_out, a->k, a->k_splits);
-  const bool direct = plan.k_splits == 1 && a->mode != SEVO_LINEAR_SWIGLU;
-  if (!direct) {
-    const size_t need = sevo::linear_workspace_bytes(a->m, a->n_out, a->k, a->k_splits);
+  const sevo::LinearPlan plan = sevo::plan_linear(a->m, a->n_out, a->k, a->k_splits, a->mode);
+  const size_t need = sevo::linear_workspace_bytes(a->m, a->n_out, a->k, a->k_splits, a->mode);
+  if (need > 0) {
     if (!a->workspace || !aligned16(a->workspace) || a->workspace_bytes < need)
       return fail(SEVO_ERR_WORKSPACE_TOO_SMALL, "linear needs %zu workspace bytes, got %zu", need,
                   a->workspace_bytes);
@@ -399,12 +400,12 @@ SEVO_API sevo_status sevo_linear(const sevo_linear_args* a, void* stream) {
   return e == hipSuccess ? SEVO_OK : hip_fail(e, "sevo_linear");
 }
 
-static void fill_rope_args(const sevo_model* m, int layer, const float* qkv, int n,
-                           const int32_t* pos, const int32_t* pt, int max_pages,
+static void fill_rope_args(const sevo_model* m, int layer, const float* qkv, int qkv_splits,
+                           int n, const int32_t* pos, const int32_t* pt, int max_pages,
                            int64_t num_pages, void* q_out, void* kp, void* vp,
                            sevo::RopeAppendArgs& r) {
   const sevo_model_config& c = m->cfg;
-  r.qkv = qkv; r.n = n; r.hq = c.n_q_heads; r.hkv = c.n_kv_heads; r.d = c.head_dim;
+  r.qkv = qkv; r.qkv_splits = qkv_splits; r.n = n; r.hq = c.n_q_heads; r.hkv = c.n_kv_heads; r.d = c.head_dim;
   r.positions = pos; r.page_table = pt; r.max_pages = max_pages; r.num_pages = num_pages;
   r.rope_cos = m->rope_cos; r.rope_sin = m->rope_sin; r.max_pos = c.max_position;
   r.q_gain = static_cast<const sevo::bf16_t*>(m->q_norm[layer]);
@@ -429,7 +430,7 @@ SEVO_API sevo_status sevo_qk_norm_rope_append(const sevo_model* m, int32_t layer
   if (!qkv || !positions || !page_table || !q_out || !k_pool || !v_pool)
     return fail(SEVO_ERR_INVALID_ARGUMENT, "null pointer");
   sevo::RopeAppendArgs r;
-  fill_rope_args(m, layer, qkv, n, positions, page_table, max_pages, num_pages, q_out, k_pool,
+  fill_rope_args(m, layer, qkv, 1, n, positions, page_table, max_pages, num_pages, q_out, k_pool,
                  v_pool, r);
   hipError_t e = sevo::launch_qk_norm_rope_append(r, static_cast<hipStream_t>(stream));
   return e == hipSuccess ? SEVO_OK : hip_fail(e, "sevo_qk_norm_rope_append");
@@ -439,8 +440,9 @@ SEVO_API sevo_status sevo_qk_norm_rope_append(const sevo_model* m, int32_t layer
 namespace {
 
 struct StepLayout {
-  size_t x, h, qkv, q, o, a, logits, lin, attn, sample, total;
+  size_t x, h, part_qkv, q, o, a, logits, part_x, attn, sample, total;
   int S, chunk;
+  sevo::LinearPlan p_qkv, p_o, p_gu, p_d, p_lm;
 };
 
 StepLayout step_layout(const sevo_model_config& c, int n, int max_pages, int num_splits) {
@@ -448,27 +450,26 @@ StepLayout step_layout(const sevo_model_config& c, int n, int max_pages, int num
   const int qd = c.n_q_heads * c.head_dim;
   const int qkvd = (c.n_q_heads + 2 * c.n_kv_heads) * c.head_dim;
   resolve_splits(n, c.n_kv_heads, max_pages, num_splits, &L.S, &L.chunk);
+  L.p_qkv = sevo::plan_linear(n, qkvd, c.hidden, 0, SEVO_LINEAR_STORE);
+  L.p_o = sevo::plan_linear(n, c.hidden, qd, 0, SEVO_LINEAR_STORE);
+  L.p_gu = sevo::plan_linear(n, 2 * c.ffn, c.hidden, 0, SEVO_LINEAR_SWIGLU);
+  L.p_d = sevo::plan_linear(n, c.hidden, c.ffn, 0, SEVO_LINEAR_STORE);
+  L.p_lm = sevo::plan_linear(n, c.vocab, c.hidden, 1, SEVO_LINEAR_STORE);
   size_t off = 0;
   auto take = [&](size_t bytes) {
     const size_t o = off;
     off += round_up(bytes, 256);
     return o;
   };
+  const int sx = L.p_o.k_splits > L.p_d.k_splits ? L.p_o.k_splits : L.p_d.k_splits;
   L.x = take((size_t)n * c.hidden * 4);
   L.h = take((size_t)n * c.hidden * 2);
-  L.qkv = take((size_t)n * qkvd * 4);
+  L.part_qkv = take((size_t)L.p_qkv.k_splits * n * qkvd * 4);
   L.q = take((size_t)n * qd * 2);
   L.o = take((size_t)n * qd * 2);
   L.a = take((size_t)n * c.ffn * 2);
   L.logits = take((size_t)n * c.vocab * 4);
-  size_t lin = 0;
-  const size_t cand[] = {sevo::linear_workspace_bytes(n, qkvd, c.hidden, 0),
-                         sevo::linear_workspace_bytes(n, c.hidden, qd, 0),
-                         sevo::linear_workspace_bytes(n, 2 * c.ffn, c.hidden, 0),
-                         sevo::linear_workspace_bytes(n, c.hidden, c.ffn, 0),
-                         sevo::linear_workspace_bytes(n, c.vocab, c.hidden, 0)};
-  for (size_t v : cand) lin = v > lin ? v : lin;
-  L.lin = take(lin);
+  L.part_x = take((size_t)sx * n * c.hidden * 4);
   L.attn = take(attn_ws(n, c.n_q_heads, c.head_dim, L.S));
   L.sample = take(sevo::sample_workspace_bytes(n, c.vocab));
   L.total = off;
@@ -510,37 +511,38 @@ SEVO_API sevo_status sevo_decode_step(sevo_model* m, const sevo_step_args* a, vo
   char* ws = static_cast<char*>(a->workspace);
   float* x = reinterpret_cast<float*>(ws + L.x);
   sevo::bf16_t* h = reinterpret_cast<sevo::bf16_t*>(ws + L.h);
-  float* qkv = reinterpret_cast<float*>(ws + L.qkv);
+  float* part_qkv = reinterpret_cast<float*>(ws + L.part_qkv);
   sevo::bf16_t* q = reinterpret_cast<sevo::bf16_t*>(ws + L.q);
   sevo::bf16_t* o = reinterpret_cast<sevo::bf16_t*>(ws + L.o);
   sevo::bf16_t* act = reinterpret_cast<sevo::bf16_t*>(ws + L.a);
   float* logits = a->out_logits ? a->out_logits : reinterpret_cast<float*>(ws + L.logits);
-  float* lin = reinterpret_cast<float*>(ws + L.lin);
+  float* part_x = reinterpret_cast<float*>(ws + L.part_x);
   char* attn_ws_ptr = ws + L.attn;
   float* smp = reinterpret_cast<float*>(ws + L.sample);
 
   const int H = c.hidden, F = c.ffn, qd = c.n_q_heads * c.head_dim;
   const int qkvd = (c.n_q_heads + 2 * c.n_kv_heads) * c.head_dim;
-  const sevo::LinearPlan p_qkv = sevo::plan_linear(n, qkvd, H, 0);
-  const sevo::LinearPlan p_o = sevo::plan_linear(n, H, qd, 0);
-  const sevo::LinearPlan p_gu = sevo::plan_linear(n, 2 * F, H, 0);
-  const sevo::LinearPlan p_d = sevo::plan_linear(n, H, F, 0);
-  const sevo::LinearPlan p_lm = sevo::plan_linear(n, c.vocab, H, 0);
   const float scale = 1.0f / std::sqrt((float)c.head_dim);
 
+  // Split-K partials of a projection are summed (in split order) by the
+  // kernel that consumes them: QKV by the QK-norm / RoPE / append kernel, the
+  // output and down projections by the next residual add + RMSNorm.
   hipError_t e = sevo::launch_embed(static_cast<const sevo::bf16_t*>(m->embed), a->tokens, n, H,
                                     c.vocab, x, st);
   if (e != hipSuccess) return hip_fail(e, "embed");
+  int pending = 0;  // split partials of the last down projection, not yet in x
   for (int l = 0; l < c.n_layers; ++l) {
-    e = sevo::launch_rmsnorm(x, static_cast<const sevo::bf16_t*>(m->attn_norm[l]), n, H,
-                             c.rms_eps, h, st);
+    e = sevo::launch_add_rmsnorm(x, pending ? part_x : nullptr, pending,
+                                 static_cast<const sevo::bf16_t*>(m->attn_norm[l]), n, H,
+                                 c.rms_eps, h, st);
     if (e == hipSuccess)
-      e = sevo::launch_linear(n, qkvd, H, H, SEVO_LINEAR_STORE, p_qkv, h,
-                              static_cast<const sevo::bf16_t*>(m->w_qkv[l]), qkv, lin, st);
+      e = sevo::launch_linear_partials(n, qkvd, H, H, L.p_qkv, h,
+                                       static_cast<const sevo::bf16_t*>(m->w_qkv[l]), part_qkv, 0,
+                                       st);
     if (e == hipSuccess) {
       sevo::RopeAppendArgs r;
-      fill_rope_args(m, l, qkv, n, a->positions, a->page_table, a->max_pages, a->num_pages, q,
-                     a->k_pools[l], a->v_pools[l], r);
+      fill_rope_args(m, l, part_qkv, L.p_qkv.k_splits, n, a->positions, a->page_table,
+                     a->max_pages, a->num_pages, q, a->k_pools[l], a->v_pools[l], r);
       e = sevo::launch_qk_norm_rope_append(r, st);
     }
     if (e != hipSuccess) return hip_fail(e, "decode step (attention input)");
@@ -564,24 +566,28 @@ SEVO_API sevo_status sevo_decode_step(sevo_model* m, const sevo_step_args* a, vo
     attach_profiler(aa);
     e = sevo::launch_attn_decode(aa, st);
     if (e == hipSuccess)
-      e = sevo::launch_linear(n, H, qd, qd, SEVO_LINEAR_ADD, p_o, o,
-                              static_cast<const sevo::bf16_t*>(m->w_o[l]), x, lin, st);
+      e = sevo::launch_linear_partials(n, H, qd, qd, L.p_o, o,
+                                       static_cast<const sevo::bf16_t*>(m->w_o[l]), part_x, 0, st);
     if (e == hipSuccess)
-      e = sevo::launch_rmsnorm(x, static_cast<const sevo::bf16_t*>(m->ffn_norm[l]), n, H,
-                               c.rms_eps, h, st);
+      e = sevo::launch_add_rmsnorm(x, part_x, L.p_o.k_splits,
+                                   static_cast<const sevo::bf16_t*>(m->ffn_norm[l]), n, H,
+                                   c.rms_eps, h, st);
     if (e == hipSuccess)
-      e = sevo::launch_linear(n, 2 * F, H, H, SEVO_LINEAR_SWIGLU, p_gu, h,
-                              static_cast<const sevo::bf16_t*>(m->w_gate_up[l]), act, lin, st);
+      e = sevo::launch_linear(n, 2 * F, H, H, SEVO_LINEAR_SWIGLU, L.p_gu, h,
+                              static_cast<const sevo::bf16_t*>(m->w_gate_up[l]), act, nullptr,
+                              st);
     if (e == hipSuccess)
-      e = sevo::launch_linear(n, H, F, F, SEVO_LINEAR_ADD, p_d, act,
-                              static_cast<const sevo::bf16_t*>(m->w_down[l]), x, lin, st);
+      e = sevo::launch_linear_partials(n, H, F, F, L.p_d, act,
+                                       static_cast<const sevo::bf16_t*>(m->w_down[l]), part_x, 0,
+                                       st);
+    pending = L.p_d.k_splits;
     if (e != hipSuccess) return hip_fail(e, "decode step (layer)");
   }
-  e = sevo::launch_rmsnorm(x, static_cast<const sevo::bf16_t*>(m->final_norm), n, H, c.rms_eps, h,
-                           st);
+  e = sevo::launch_add_rmsnorm(x, part_x, pending, static_cast<const sevo::bf16_t*>(m->final_norm),
+                               n, H, c.rms_eps, h, st);
   if (e == hipSuccess)
-    e = sevo::launch_linear(n, c.vocab, H, H, SEVO_LINEAR_STORE, p_lm, h,
-                            static_cast<const sevo::bf16_t*>(m->lm_head), logits, lin, st);
+    e = sevo::launch_linear_partials(n, c.vocab, H, H, L.p_lm, h,
+                                     static_cast<const sevo::bf16_t*>(m->lm_head), logits, 0, st);
   if (e == hipSuccess)
     e = sevo::launch_logprob_sample(logits, n, c.vocab, c.vocab, a->temperature, a->seed,
                                     a->cand_uid, a->positions, a->out_tokens, a->out_logprobs,

@@ -103,10 +103,11 @@ def test_zero_population_is_a_no_op():
 def test_split_planning():
     L = sevo.lib()
     # enough workgroups for 256 CUs, at least 32 pages per split, at least one
-    # split, and no split longer than 256 pages
-    assert L.sevo_attn_plan_splits(64, 8, 2049) == 9
-    assert L.sevo_attn_plan_splits(64, 8, 1024) == 4
-    assert L.sevo_attn_plan_splits(16, 8, 1024) == 16
+    # split, and no split longer than 512 pages
+    assert L.sevo_attn_plan_splits(64, 8, 2049) == 8
+    assert L.sevo_attn_plan_splits(64, 8, 1024) == 8
+    assert L.sevo_attn_plan_splits(16, 8, 1024) == 32
+    assert L.sevo_attn_plan_splits(64, 8, 4100) == 9
     assert L.sevo_attn_plan_splits(4, 2, 33) == 2
     assert L.sevo_attn_plan_splits(1, 1, 1) == 1
     ws = L.sevo_attn_workspace_bytes(64, 32, 8, 128, 2049, 0)
@@ -130,14 +131,14 @@ def test_sampler_rejects_bad_ld_and_small_workspace():
 
 
 @pytest.mark.parametrize("kw,status", [
-    (dict(k=48), sevo.UNSUPPORTED),
+    (dict(k=192), sevo.UNSUPPORTED),
     (dict(n_out=96), sevo.UNSUPPORTED),
     (dict(n_out=192, mode=2), sevo.UNSUPPORTED),
     (dict(mode=3), sevo.INVALID_ARGUMENT),
     (dict(ldx=100), sevo.INVALID_ARGUMENT),
 ])
 def test_linear_rejects_bad_shapes(kw, status):
-    base = dict(m=4, n_out=128, k=64, ldx=64, mode=0, k_splits=0)
+    base = dict(m=4, n_out=128, k=128, ldx=128, mode=0, k_splits=0)
     base.update(kw)
     a = sevo.LinearArgs(**base)
     assert sevo.lib().sevo_linear(C.byref(a), None) == status
@@ -145,8 +146,10 @@ def test_linear_rejects_bad_shapes(kw, status):
 
 def test_linear_plan_and_workspace():
     L = sevo.lib()
-    assert L.sevo_linear_workspace_bytes(64, 6144, 4096, 0) == 8 * 64 * 6144 * 4
-    assert L.sevo_linear_workspace_bytes(64, 151936, 4096, 0) == 64 * 151936 * 4
+    # split K while fewer than 512 workgroups and each split keeps >= 1024 k
+    assert L.sevo_linear_workspace_bytes(64, 6144, 4096, 0) == 4 * 64 * 6144 * 4
+    assert L.sevo_linear_workspace_bytes(64, 4096, 12288, 0) == 8 * 64 * 4096 * 4
+    assert L.sevo_linear_workspace_bytes(64, 151936, 4096, 0) == 0      # one split: no partials
 
 
 def test_init_model_rejects_bad_config():
