@@ -41,6 +41,20 @@
  *     all layers.  Physical page order is arbitrary (any permutation gives
  *     bit-identical results).
  *   - GQA: query head j reads KV head j / (n_q_heads / n_kv_heads).
+ *   - GEMM operand layouts.  Both are built from the operand fragment of one
+ *     16x16x32 bf16 matrix-core instruction: 16 rows x 32 columns stored as
+ *     64 runs of 8 values, run index 16 ((c / 8) % 4) + r % 16, so a fragment
+ *     is one contiguous 1 KB block.
+ *       packed weight W [n_out][k] (n_out % 64 == 0, k % 32 == 0): element
+ *         (r, c) at ((r/64 * k/32 + c/32) * 4 + (r/16) % 4) * 512
+ *                   + (16 ((c/8) % 4) + r % 16) * 8 + c % 8
+ *         (superblocks of 64 rows; per 32-column step the four 16-row
+ *         fragments of a superblock are adjacent).  sevo_pack_weight builds it
+ *         from row-major [n_out][k].
+ *       tiled activation X [m][k] (k % 32 == 0): element (r, c) at
+ *         (r/16 * k/32 + c/32) * 512 + (16 ((c/8) % 4) + r % 16) * 8 + c % 8,
+ *         with m rounded up to a multiple of 16 rows (padding rows are never
+ *         read into a stored result and need no initialisation).
  */
 #ifndef SEVO_H
 #define SEVO_H
@@ -85,13 +99,16 @@ typedef struct {
 } sevo_model_config;
 
 /* Borrowed bf16 weight pointers (device); they must outlive the model.  The
- * per-layer members are HOST arrays of n_layers device pointers.  Matrices are
- * row-major [out][in]:
- *   embed, lm_head [vocab][hidden];  final_norm, attn_norm, ffn_norm [hidden]
+ * per-layer members are HOST arrays of n_layers device pointers.  Shapes are
+ * [out][in]; embed is row-major, the projection matrices are in the packed
+ * weight layout (sevo_pack_weight, kind SEVO_PACK_PLAIN unless noted):
+ *   embed [vocab][hidden] (row-major);  lm_head [vocab][hidden] (packed)
+ *   final_norm, attn_norm, ffn_norm [hidden]
  *   w_qkv     [(n_q_heads + 2 n_kv_heads) head_dim][hidden]  rows: q, k, v
  *   q_norm, k_norm [head_dim]        (unused when qk_norm == 0; may be NULL)
  *   w_o       [hidden][n_q_heads head_dim]
- *   w_gate_up [2 ffn][hidden]        rows 0..ffn-1 gate, ffn..2ffn-1 up
+ *   w_gate_up [2 ffn][hidden]        rows 0..ffn-1 gate, ffn..2ffn-1 up, packed
+ *                                    with kind SEVO_PACK_GATE_UP
  *   w_down    [hidden][ffn] */
 typedef struct {
   const void* embed;
@@ -241,18 +258,24 @@ sevo_status sevo_embed(const void* embed, const int32_t* tokens, int32_t n, int3
 sevo_status sevo_rmsnorm(const float* x, const void* gain, int32_t rows, int32_t cols,
                          float eps, void* out, void* stream);
 
-/* Y = X W^T with X bf16 [m][k] (row stride ldx), W bf16 [n_out][k], fp32
- * accumulation on the matrix cores, then the epilogue:
+/* Y = X W^T with X bf16 [m][k], W bf16 [n_out][k] in the packed weight layout
+ * (for SWIGLU packed with kind SEVO_PACK_GATE_UP), fp32 accumulation on the
+ * matrix cores, then the epilogue:
  *   SEVO_LINEAR_STORE  out fp32 [m][n_out]  = Y
  *   SEVO_LINEAR_ADD    out fp32 [m][n_out] += Y          (residual update)
  *   SEVO_LINEAR_SWIGLU out bf16 [m][n_out/2] = silu(Y[:, :n_out/2]) * Y[:, n_out/2:]
- * k % 128 == 0; n_out % 64 == 0 (SWIGLU: n_out % 128 == 0); ldx % 8 == 0.
- * k_splits 0 = chosen by the library (SWIGLU always uses one split). */
+ * flags: SEVO_LINEAR_X_TILED     X in the tiled activation layout (ldx unused;
+ *                                else row-major with row stride ldx, ldx % 8 == 0)
+ *        SEVO_LINEAR_OUT_TILED   SWIGLU output in the tiled activation layout
+ * k % 32 == 0; n_out % 64 == 0.  k_splits 0 = chosen by the library (SWIGLU
+ * always uses one split). */
 #define SEVO_LINEAR_STORE 0
 #define SEVO_LINEAR_ADD 1
 #define SEVO_LINEAR_SWIGLU 2
+#define SEVO_LINEAR_X_TILED 1
+#define SEVO_LINEAR_OUT_TILED 2
 typedef struct {
-  int32_t m, n_out, k, ldx, mode, k_splits;
+  int32_t m, n_out, k, ldx, mode, k_splits, flags;
   const void* x;
   const void* w;
   void* out;
@@ -262,6 +285,17 @@ typedef struct {
 
 sevo_status sevo_linear(const sevo_linear_args* a, void* stream);
 size_t sevo_linear_workspace_bytes(int32_t m, int32_t n_out, int32_t k, int32_t k_splits);
+
+/* Row-major bf16 [n_out][k] (src) -> packed weight layout (dst, a separate
+ * buffer of the same size).  SEVO_PACK_GATE_UP treats rows 0..n_out/2-1 as
+ * gate rows and the rest as up rows and puts gate rows 32 s..32 s+31 and up
+ * rows n_out/2 + 32 s.. in superblock s (logical order gate, then up), the form
+ * the SWIGLU epilogue reads.  n_out % 64 == 0, k % 32 == 0.  A one-time
+ * preparation of model weights, not part of the decode step. */
+#define SEVO_PACK_PLAIN 0
+#define SEVO_PACK_GATE_UP 1
+sevo_status sevo_pack_weight(const void* src, void* dst, int32_t n_out, int32_t k, int32_t kind,
+                             void* stream);
 
 /* The fused QK-RMSNorm + RoPE + KV append of one layer.
  *   qkv fp32 [n][(n_q_heads + 2 n_kv_heads) head_dim] (the QKV projection)

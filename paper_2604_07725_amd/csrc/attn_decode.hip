@@ -335,7 +335,7 @@ __global__ __launch_bounds__(64) void attn_combine_kernel(const float* __restric
                                                           const float* __restrict__ part_acc,
                                                           const int32_t* __restrict__ seq_lens,
                                                           int len_add, int max_pages, int chunk, int S, int hq,
-                                                          bf16_t* __restrict__ out) {
+                                                          bf16_t* __restrict__ out, int out_tiled) {
   constexpr int E = D / 64;
   const int j = blockIdx.x;
   const int i = blockIdx.y;
@@ -359,9 +359,14 @@ __global__ __launch_bounds__(64) void attn_combine_kernel(const float* __restric
     for (int e = 0; e < E; ++e) a[e] += part_acc[(base + s) * D + threadIdx.x + 64 * e] * f;
   }
   const float inv = L > 0.f ? 1.0f / L : 0.f;
-  bf16_t* o = out + ((size_t)i * hq + j) * D;
+  // row-major [n][hq][D], or the tiled activation layout of [n][hq D] (the
+  // output projection's input)
 #pragma unroll
-  for (int e = 0; e < E; ++e) o[threadIdx.x + 64 * e] = f32_to_bf16(a[e] * inv);
+  for (int e = 0; e < E; ++e) {
+    const int c = j * D + threadIdx.x + 64 * e;
+    const size_t off = out_tiled ? act_tile_offset(i, c, hq * D) : (size_t)i * hq * D + c;
+    out[off] = f32_to_bf16(a[e] * inv);
+  }
 }
 
 template <int D, int G>
@@ -376,7 +381,8 @@ static hipError_t launch_attn_t(const AttnArgs& a, hipStream_t st) {
   if (e != hipSuccess) return e;
   if (a.ev_mid) (void)hipEventRecord(a.ev_mid, st);
   hipLaunchKernelGGL((attn_combine_kernel<D>), dim3(a.hq, a.n), dim3(64), 0, st, a.part_ml,
-                     a.part_acc, a.seq_lens, a.len_add, a.max_pages, a.chunk, a.num_splits, a.hq, a.out);
+                     a.part_acc, a.seq_lens, a.len_add, a.max_pages, a.chunk, a.num_splits, a.hq, a.out,
+                     a.out_tiled);
   e = hipGetLastError();
   if (e == hipSuccess && a.ev_end) (void)hipEventRecord(a.ev_end, st);
   return e;

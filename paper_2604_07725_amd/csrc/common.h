@@ -14,6 +14,25 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 constexpr int kWave = 64;
 constexpr int kPage = 16;
 
+// ---- GEMM operand layouts (bf16), built around one MFMA 16x16x32 fragment:
+// 16 rows x 32 columns stored as 64 lanes x 8 values, lane = 16 (c/8 % 4) + r % 16,
+// so a wave loads a whole fragment as one contiguous 1 KB read.
+//
+// Packed weight [n_out][k]: superblocks of 64 rows; for each 32-column step
+// the superblock's four 16-row fragments are adjacent (2048 elements), so a
+// workgroup streaming a superblock reads one contiguous region.
+__host__ __device__ __forceinline__ size_t packed_weight_offset(int r, int c, int k) {
+  return (((size_t)(r >> 6) * (k >> 5) + (c >> 5)) * 4 + ((r >> 4) & 3)) * 512 +
+         (((c >> 3) & 3) * 16 + (r & 15)) * 8 + (c & 7);
+}
+// Tiled activation [m][k]: 16-row blocks, each a run of k/32 fragments.
+// Rows are padded to a multiple of 16 (padding rows are never read into a
+// stored output).
+__host__ __device__ __forceinline__ size_t act_tile_offset(int m, int c, int k) {
+  return ((size_t)(m >> 4) * (k >> 5) + (c >> 5)) * 512 + (((c >> 3) & 3) * 16 + (m & 15)) * 8 +
+         (c & 7);
+}
+
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
 __device__ __forceinline__ float bf16_to_f32(bf16_t b) { return __uint_as_float((uint32_t)b << 16); }

@@ -14,9 +14,10 @@ hipError_t launch_embed(const bf16_t* embed, const int32_t* tokens, int n, int h
 hipError_t launch_rmsnorm(const float* x, const bf16_t* gain, int rows, int cols, float eps,
                           bf16_t* out, hipStream_t st);
 // x += sum_s part[s] (split order; S == 0: nothing to add), then
-// out = bf16(RMSNorm(x) * gain).  part is [S][rows][cols] fp32.
+// out = bf16(RMSNorm(x) * gain) in the tiled activation layout (the GEMM
+// input).  part is [S][rows][cols] fp32.
 hipError_t launch_add_rmsnorm(float* x, const float* part, int S, const bf16_t* gain, int rows,
-                              int cols, float eps, bf16_t* out, hipStream_t st);
+                              int cols, float eps, bf16_t* out_tiled, hipStream_t st);
 struct RopeAppendArgs {
   const float* qkv;  // [qkv_splits][n][(hq + 2 hkv) d]: summed in split order
   int qkv_splits;
@@ -52,6 +53,7 @@ struct AttnArgs {
   int len_add;
   float scale;
   bf16_t* out;
+  int out_tiled = 0;  // 1: out in the tiled activation layout of [n][hq d]
   float* part_ml;   // [n][hq][S][2]
   float* part_acc;  // [n][hq][S][d]
   // optional timing: recorded before the split kernel, between the two
@@ -67,15 +69,22 @@ struct LinearPlan {
 };
 LinearPlan plan_linear(int m, int n_out, int k, int k_splits, int mode);
 size_t linear_workspace_bytes(int m, int n_out, int k, int k_splits, int mode);
-// complete Y = X W^T with the STORE / ADD / SWIGLU epilogue
-hipError_t launch_linear(int m, int n_out, int k, int ldx, int mode, const LinearPlan& plan,
-                         const bf16_t* x, const bf16_t* w, void* out, float* workspace,
-                         hipStream_t st);
+// X operand: row-major with row stride ldx (x_tiled == 0) or the tiled
+// activation layout; W: the packed weight layout (gate/up interleaved for SWIGLU).
+// complete Y = X W^T with the STORE / ADD / SWIGLU epilogue (SWIGLU output
+// bf16, row-major or tiled per out_tiled)
+hipError_t launch_linear(int m, int n_out, int k, int ldx, int x_tiled, int mode,
+                         const LinearPlan& plan, const bf16_t* x, const bf16_t* w, void* out,
+                         int out_tiled, float* workspace, hipStream_t st);
 // raw fp32 split partials out[split][m][n] (k_splits == 1: the product itself,
 // added to out when accumulate)
-hipError_t launch_linear_partials(int m, int n_out, int k, int ldx, const LinearPlan& plan,
-                                  const bf16_t* x, const bf16_t* w, float* out, int accumulate,
-                                  hipStream_t st);
+hipError_t launch_linear_partials(int m, int n_out, int k, int ldx, int x_tiled,
+                                  const LinearPlan& plan, const bf16_t* x, const bf16_t* w,
+                                  float* out, int accumulate, hipStream_t st);
+// row-major [n_out][k] -> packed weight layout; gate_up: rows 0..n_out/2-1 are
+// gate rows and the rest up rows, interleaved per superblock (32 + 32)
+hipError_t launch_pack_weight(const bf16_t* src, bf16_t* dst, int n_out, int k, int gate_up,
+                              hipStream_t st);
 
 // ---- sample.hip
 constexpr int kSampleChunk = 4096;  // vocab entries per partial workgroup

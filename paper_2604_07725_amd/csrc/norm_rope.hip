@@ -172,7 +172,8 @@ hipError_t launch_embed(const bf16_t* embed, const int32_t* tokens, int n, int h
   return hipGetLastError();
 }
 
-// x[r] += sum_s part[s][r] in split order, written back; then the RMSNorm.
+// x[r] += sum_s part[s][r] in split order, written back; then the RMSNorm,
+// stored in the tiled activation layout that the projections read.
 // 1024 threads per row, each owning 4 consecutive columns per 4096-column
 // pass with all split loads independent (latency, not bandwidth, is the cost).
 __global__ __launch_bounds__(1024) void add_rmsnorm_kernel(float* __restrict__ x,
@@ -201,23 +202,23 @@ __global__ __launch_bounds__(1024) void add_rmsnorm_kernel(float* __restrict__ x
   }
   ss = block_sum<16>(ss, red);
   const float inv = 1.0f / sqrtf(ss / (float)cols + eps);
-  bf16_t* orow = out + (size_t)blockIdx.x * cols;
   for (int c = threadIdx.x * 4; c < cols; c += 4096) {
     const f32x4 v = *reinterpret_cast<const f32x4*>(xr + c);
     const uint2 g = *reinterpret_cast<const uint2*>(gain + c);
     uint2 o;
     o.x = pack_bf16x2(v.x * inv * bf16_lo(g.x), v.y * inv * bf16_hi(g.x));
     o.y = pack_bf16x2(v.z * inv * bf16_lo(g.y), v.w * inv * bf16_hi(g.y));
-    *reinterpret_cast<uint2*>(orow + c) = o;
+    // 4 consecutive columns are contiguous in the tiled activation layout
+    *reinterpret_cast<uint2*>(out + act_tile_offset(blockIdx.x, c, cols)) = o;
   }
 }
 
 hipError_t launch_add_rmsnorm(float* x, const float* part, int S, const bf16_t* gain, int rows,
-                              int cols, float eps, bf16_t* out, hipStream_t st) {
+                              int cols, float eps, bf16_t* out_tiled, hipStream_t st) {
   if (rows == 0) return hipSuccess;
   if (S > 16) return hipErrorInvalidValue;
   hipLaunchKernelGGL(add_rmsnorm_kernel, dim3(rows), dim3(1024), 0, st, x, part, part ? S : 0,
-                     (size_t)rows * cols, gain, cols, eps, out);
+                     (size_t)rows * cols, gain, cols, eps, out_tiled);
   return hipGetLastError();
 }
 

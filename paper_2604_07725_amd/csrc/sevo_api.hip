@@ -359,14 +359,18 @@ SEVO_API sevo_status sevo_rmsnorm(const float* x, const void* gain, int32_t rows
   return e == hipSuccess ? SEVO_OK : hip_fail(e, "sevo_rmsnorm");
 }
 
-static sevo_status linear_check(int m, int n_out, int k, int ldx, int mode, int k_splits) {
-  if (m < 0 || n_out < 64 || k < 128) return fail(SEVO_ERR_INVALID_ARGUMENT, "bad m / n_out / k");
-  if (k % 128) return fail(SEVO_ERR_UNSUPPORTED, "k %% 128 != 0");
+static sevo_status linear_check(int m, int n_out, int k, int ldx, int mode, int k_splits,
+                                int flags) {
+  if (m < 0 || n_out < 64 || k < 32) return fail(SEVO_ERR_INVALID_ARGUMENT, "bad m / n_out / k");
+  if (k % 32) return fail(SEVO_ERR_UNSUPPORTED, "k %% 32 != 0");
   if (n_out % 64) return fail(SEVO_ERR_UNSUPPORTED, "n_out %% 64 != 0");
-  if (mode == SEVO_LINEAR_SWIGLU && n_out % 128)
-    return fail(SEVO_ERR_UNSUPPORTED, "SwiGLU needs n_out %% 128 == 0");
   if (mode < 0 || mode > 2) return fail(SEVO_ERR_INVALID_ARGUMENT, "bad mode %d", mode);
-  if (ldx < k || ldx % 8) return fail(SEVO_ERR_INVALID_ARGUMENT, "ldx must be >= k and %% 8");
+  if (flags & ~(SEVO_LINEAR_X_TILED | SEVO_LINEAR_OUT_TILED))
+    return fail(SEVO_ERR_INVALID_ARGUMENT, "unknown flags 0x%x", flags);
+  if ((flags & SEVO_LINEAR_OUT_TILED) && mode != SEVO_LINEAR_SWIGLU)
+    return fail(SEVO_ERR_INVALID_ARGUMENT, "SEVO_LINEAR_OUT_TILED needs SEVO_LINEAR_SWIGLU");
+  if (!(flags & SEVO_LINEAR_X_TILED) && (ldx < k || ldx % 8))
+    return fail(SEVO_ERR_INVALID_ARGUMENT, "ldx must be >= k and %% 8");
   if (k_splits < 0) return fail(SEVO_ERR_INVALID_ARGUMENT, "k_splits < 0");
   return SEVO_OK;
 }
@@ -380,7 +384,7 @@ SEVO_API size_t sevo_linear_workspace_bytes(int32_t m, int32_t n_out, int32_t k,
 
 SEVO_API sevo_status sevo_linear(const sevo_linear_args* a, void* stream) {
   if (!a) return fail(SEVO_ERR_INVALID_ARGUMENT, "null args");
-  sevo_status st = linear_check(a->m, a->n_out, a->k, a->ldx, a->mode, a->k_splits);
+  sevo_status st = linear_check(a->m, a->n_out, a->k, a->ldx, a->mode, a->k_splits, a->flags);
   if (st) return st;
   if (a->m == 0) return SEVO_OK;
   if (!a->x || !a->w || !a->out || !aligned16(a->x) || !aligned16(a->w) || !aligned16(a->out))
@@ -392,12 +396,31 @@ SEVO_API sevo_status sevo_linear(const sevo_linear_args* a, void* stream) {
       return fail(SEVO_ERR_WORKSPACE_TOO_SMALL, "linear needs %zu workspace bytes, got %zu", need,
                   a->workspace_bytes);
   }
-  hipError_t e = sevo::launch_linear(a->m, a->n_out, a->k, a->ldx, a->mode, plan,
-                                     static_cast<const sevo::bf16_t*>(a->x),
-                                     static_cast<const sevo::bf16_t*>(a->w), a->out,
-                                     static_cast<float*>(a->workspace),
-                                     static_cast<hipStream_t>(stream));
+  hipError_t e = sevo::launch_linear(
+      a->m, a->n_out, a->k, a->ldx, (a->flags & SEVO_LINEAR_X_TILED) ? 1 : 0, a->mode, plan,
+      static_cast<const sevo::bf16_t*>(a->x), static_cast<const sevo::bf16_t*>(a->w), a->out,
+      (a->flags & SEVO_LINEAR_OUT_TILED) ? 1 : 0, static_cast<float*>(a->workspace),
+      static_cast<hipStream_t>(stream));
   return e == hipSuccess ? SEVO_OK : hip_fail(e, "sevo_linear");
+}
+
+SEVO_API sevo_status sevo_pack_weight(const void* src, void* dst, int32_t n_out, int32_t k,
+                                      int32_t kind, void* stream) {
+  if (n_out < 64 || k < 32) return fail(SEVO_ERR_INVALID_ARGUMENT, "bad n_out / k");
+  if (n_out % 64 || k % 32) return fail(SEVO_ERR_UNSUPPORTED, "n_out %% 64 and k %% 32 must be 0");
+  if (kind != SEVO_PACK_PLAIN && kind != SEVO_PACK_GATE_UP)
+    return fail(SEVO_ERR_INVALID_ARGUMENT, "bad kind %d", kind);
+  if (!src || !dst || !aligned16(src) || !aligned16(dst))
+    return fail(SEVO_ERR_INVALID_ARGUMENT, "null or misaligned pointer");
+  const size_t bytes = (size_t)n_out * k * 2;
+  const uintptr_t s0 = reinterpret_cast<uintptr_t>(src), d0 = reinterpret_cast<uintptr_t>(dst);
+  if (s0 < d0 + bytes && d0 < s0 + bytes)
+    return fail(SEVO_ERR_INVALID_ARGUMENT, "src and dst overlap");
+  hipError_t e = sevo::launch_pack_weight(static_cast<const sevo::bf16_t*>(src),
+                                          static_cast<sevo::bf16_t*>(dst), n_out, k,
+                                          kind == SEVO_PACK_GATE_UP ? 1 : 0,
+                                          static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? SEVO_OK : hip_fail(e, "sevo_pack_weight");
 }
 
 static void fill_rope_args(const sevo_model* m, int layer, const float* qkv, int qkv_splits,
@@ -462,12 +485,13 @@ StepLayout step_layout(const sevo_model_config& c, int n, int max_pages, int num
     return o;
   };
   const int sx = L.p_o.k_splits > L.p_d.k_splits ? L.p_o.k_splits : L.p_d.k_splits;
+  const size_t n16 = round_up((size_t)n, 16);  // tiled activations: 16-row blocks
   L.x = take((size_t)n * c.hidden * 4);
-  L.h = take((size_t)n * c.hidden * 2);
+  L.h = take(n16 * c.hidden * 2);
   L.part_qkv = take((size_t)L.p_qkv.k_splits * n * qkvd * 4);
   L.q = take((size_t)n * qd * 2);
-  L.o = take((size_t)n * qd * 2);
-  L.a = take((size_t)n * c.ffn * 2);
+  L.o = take(n16 * qd * 2);
+  L.a = take(n16 * c.ffn * 2);
   L.logits = take((size_t)n * c.vocab * 4);
   L.part_x = take((size_t)sx * n * c.hidden * 4);
   L.attn = take(attn_ws(n, c.n_q_heads, c.head_dim, L.S));
@@ -536,7 +560,7 @@ SEVO_API sevo_status sevo_decode_step(sevo_model* m, const sevo_step_args* a, vo
                                  static_cast<const sevo::bf16_t*>(m->attn_norm[l]), n, H,
                                  c.rms_eps, h, st);
     if (e == hipSuccess)
-      e = sevo::launch_linear_partials(n, qkvd, H, H, L.p_qkv, h,
+      e = sevo::launch_linear_partials(n, qkvd, H, H, 1, L.p_qkv, h,
                                        static_cast<const sevo::bf16_t*>(m->w_qkv[l]), part_qkv, 0,
                                        st);
     if (e == hipSuccess) {
@@ -560,24 +584,25 @@ SEVO_API sevo_status sevo_decode_step(sevo_model* m, const sevo_step_args* a, vo
     aa.len_add = 1;
     aa.scale = scale;
     aa.out = o;
+    aa.out_tiled = 1;
     aa.part_ml = reinterpret_cast<float*>(attn_ws_ptr);
     aa.part_acc = reinterpret_cast<float*>(
         attn_ws_ptr + round_up((size_t)n * c.n_q_heads * L.S * 2 * sizeof(float), 256));
     attach_profiler(aa);
     e = sevo::launch_attn_decode(aa, st);
     if (e == hipSuccess)
-      e = sevo::launch_linear_partials(n, H, qd, qd, L.p_o, o,
+      e = sevo::launch_linear_partials(n, H, qd, qd, 1, L.p_o, o,
                                        static_cast<const sevo::bf16_t*>(m->w_o[l]), part_x, 0, st);
     if (e == hipSuccess)
       e = sevo::launch_add_rmsnorm(x, part_x, L.p_o.k_splits,
                                    static_cast<const sevo::bf16_t*>(m->ffn_norm[l]), n, H,
                                    c.rms_eps, h, st);
     if (e == hipSuccess)
-      e = sevo::launch_linear(n, 2 * F, H, H, SEVO_LINEAR_SWIGLU, L.p_gu, h,
-                              static_cast<const sevo::bf16_t*>(m->w_gate_up[l]), act, nullptr,
+      e = sevo::launch_linear(n, 2 * F, H, H, 1, SEVO_LINEAR_SWIGLU, L.p_gu, h,
+                              static_cast<const sevo::bf16_t*>(m->w_gate_up[l]), act, 1, nullptr,
                               st);
     if (e == hipSuccess)
-      e = sevo::launch_linear_partials(n, H, F, F, L.p_d, act,
+      e = sevo::launch_linear_partials(n, H, F, F, 1, L.p_d, act,
                                        static_cast<const sevo::bf16_t*>(m->w_down[l]), part_x, 0,
                                        st);
     pending = L.p_d.k_splits;
@@ -586,7 +611,7 @@ SEVO_API sevo_status sevo_decode_step(sevo_model* m, const sevo_step_args* a, vo
   e = sevo::launch_add_rmsnorm(x, part_x, pending, static_cast<const sevo::bf16_t*>(m->final_norm),
                                n, H, c.rms_eps, h, st);
   if (e == hipSuccess)
-    e = sevo::launch_linear_partials(n, c.vocab, H, H, L.p_lm, h,
+    e = sevo::launch_linear_partials(n, c.vocab, H, H, 1, L.p_lm, h,
                                      static_cast<const sevo::bf16_t*>(m->lm_head), logits, 0, st);
   if (e == hipSuccess)
     e = sevo::launch_logprob_sample(logits, n, c.vocab, c.vocab, a->temperature, a->seed,

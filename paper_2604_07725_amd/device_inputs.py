@@ -11,7 +11,7 @@ import numpy as np
 import torch
 
 from . import synth
-from .sevo import sevo_fill_normal_bf16
+from .sevo import PACKED_WEIGHTS, sevo_fill_normal_bf16, sevo_pack_weight
 
 
 def _filled(spec: synth.TensorSpec, device) -> torch.Tensor:
@@ -21,9 +21,27 @@ def _filled(spec: synth.TensorSpec, device) -> torch.Tensor:
 
 
 def device_weights(shape: synth.ModelShape, seed: int, device="cuda") -> dict:
+    """The model's weights as the library takes them: projection matrices are
+    generated row-major (the generator's element order) into a scratch tensor
+    and packed; the rest stay row-major."""
+    scratch = {}
+
+    def make(name, spec):
+        if name not in PACKED_WEIGHTS:
+            return _filled(spec, device)
+        n = 1
+        for d in spec.shape:
+            n *= d
+        buf = scratch.get("buf")
+        if buf is None or buf.numel() < n:
+            buf = scratch["buf"] = torch.empty(n, dtype=torch.bfloat16, device=device)
+        src = buf[:n].view(spec.shape)
+        sevo_fill_normal_bf16(src, spec.key, 0, spec.std, spec.mean)
+        return sevo_pack_weight(src, PACKED_WEIGHTS[name])
+
     g = synth.global_specs(shape, seed)
-    out = {k: _filled(s, device) for k, s in g.items()}
-    out["layers"] = [{k: _filled(s, device) for k, s in synth.layer_specs(shape, seed, l).items()}
+    out = {k: make(k, s) for k, s in g.items()}
+    out["layers"] = [{k: make(k, s) for k, s in synth.layer_specs(shape, seed, l).items()}
                      for l in range(shape.n_layers)]
     return out
 

@@ -20,6 +20,11 @@ HEADER = os.path.join(os.path.dirname(_HERE), "include", "sevo.h")
 
 OK, INVALID_ARGUMENT, UNSUPPORTED, WORKSPACE_TOO_SMALL, OUT_OF_MEMORY, HIP, BAD_PAGE_TABLE = range(7)
 LINEAR_STORE, LINEAR_ADD, LINEAR_SWIGLU = 0, 1, 2
+LINEAR_X_TILED, LINEAR_OUT_TILED = 1, 2
+PACK_PLAIN, PACK_GATE_UP = 0, 1
+# projection weights held in the packed layout, and how each is packed
+PACKED_WEIGHTS = {"w_qkv": PACK_PLAIN, "w_o": PACK_PLAIN, "w_gate_up": PACK_GATE_UP,
+                  "w_down": PACK_PLAIN, "lm_head": PACK_PLAIN}
 PAGE_SIZE = 16
 
 vp = C.c_void_p
@@ -67,8 +72,8 @@ class StepArgs(C.Structure):
 
 class LinearArgs(C.Structure):
     _fields_ = [("m", i32), ("n_out", i32), ("k", i32), ("ldx", i32), ("mode", i32),
-                ("k_splits", i32), ("x", vp), ("w", vp), ("out", vp), ("workspace", vp),
-                ("workspace_bytes", sz)]
+                ("k_splits", i32), ("flags", i32), ("x", vp), ("w", vp), ("out", vp),
+                ("workspace", vp), ("workspace_bytes", sz)]
 
 
 _SIGS = {
@@ -88,6 +93,7 @@ _SIGS = {
     "sevo_rmsnorm": ([vp, vp, i32, i32, f32, vp, vp], i32),
     "sevo_linear": ([C.POINTER(LinearArgs), vp], i32),
     "sevo_linear_workspace_bytes": ([i32, i32, i32, i32], sz),
+    "sevo_pack_weight": ([vp, vp, i32, i32, i32, vp], i32),
     "sevo_qk_norm_rope_append": ([vp, i32, vp, i32, vp, vp, i32, i64, vp, vp, vp, vp], i32),
     "sevo_fill_normal_bf16": ([vp, i64, u64, i64, f32, f32, i32, vp], i32),
     "sevo_validate_paging": ([vp, vp, i32, i32, i64, vp], i32),
@@ -224,20 +230,43 @@ def sevo_linear_workspace_bytes(m, n_out, k, k_splits=0) -> int:
     return int(lib().sevo_linear_workspace_bytes(m, n_out, k, k_splits))
 
 
-def sevo_linear(x, w, mode=LINEAR_STORE, out=None, k_splits=0, workspace=None, stream=None):
-    """Y = x w^T (bf16 in, fp32 accumulate) with the STORE / ADD / SWIGLU epilogue."""
-    m, k = x.shape
-    n_out = w.shape[0]
+def sevo_linear(x, w, mode=LINEAR_STORE, out=None, k_splits=0, workspace=None, stream=None,
+                m=None, x_tiled=False, out_tiled=False):
+    """Y = x w^T (bf16 in, fp32 accumulate) with the STORE / ADD / SWIGLU epilogue.
+
+    w [n_out, k] is in the packed weight layout (``sevo_pack_weight``).  x is
+    row-major [m, k] (row stride from the tensor), or with ``x_tiled`` a buffer
+    in the tiled activation layout, whose row count ``m`` must be given.
+    ``out_tiled`` (SWIGLU only) writes the bf16 product in the tiled layout."""
+    n_out, k = w.shape
+    if x_tiled:
+        if m is None:
+            raise ValueError("x_tiled needs m")
+        ldx = k
+    else:
+        m = x.shape[0]
+        ldx = x.stride(0)
     if out is None:
         if mode == LINEAR_SWIGLU:
-            out = torch.empty(m, n_out // 2, dtype=torch.bfloat16, device=x.device)
+            rows = -(-m // 16) * 16 if out_tiled else m
+            out = torch.empty(rows, n_out // 2, dtype=torch.bfloat16, device=x.device)
         else:
             out = torch.zeros(m, n_out, dtype=torch.float32, device=x.device)
     ws = _workspace(sevo_linear_workspace_bytes(m, n_out, k, k_splits), x.device, workspace)
-    a = LinearArgs(m=m, n_out=n_out, k=k, ldx=x.stride(0), mode=mode, k_splits=k_splits, x=_p(x),
-                   w=_p(w), out=_p(out), workspace=_p(ws), workspace_bytes=ws.numel())
+    flags = (LINEAR_X_TILED if x_tiled else 0) | (LINEAR_OUT_TILED if out_tiled else 0)
+    a = LinearArgs(m=m, n_out=n_out, k=k, ldx=ldx, mode=mode, k_splits=k_splits, flags=flags,
+                   x=_p(x), w=_p(w), out=_p(out), workspace=_p(ws), workspace_bytes=ws.numel())
     _check(lib().sevo_linear(C.byref(a), _stream(stream)))
     return out
+
+
+def sevo_pack_weight(src, kind=PACK_PLAIN, dst=None, stream=None):
+    """Row-major bf16 [n_out, k] -> a new tensor of the same shape in the packed layout."""
+    n_out, k = src.shape
+    if dst is None:
+        dst = torch.empty_like(src)
+    _check(lib().sevo_pack_weight(_p(src), _p(dst), n_out, k, int(kind), _stream(stream)))
+    return dst
 
 
 def sevo_qk_norm_rope_append(model, layer, qkv, positions, page_table, k_pool, v_pool,

@@ -63,3 +63,49 @@ def check_ids(gpu_ids, gpu_lps, ref_ids, ref_lps, ref_gaps, pert=None, label="")
     # compare the log-prob of the GPU's own id when a near-tie made it differ
     assert lp_err[exact].max(initial=0.0) <= LP_ABS_TOL, f"{label}: lp err {lp_err.max()}"
     return float(lp_err.max(initial=0.0)), int(exact.sum())
+
+
+# ---- GEMM operand layouts, written out from their definition in include/sevo.h
+def packed_weight_offsets(n_out: int, k: int) -> np.ndarray:
+    """Flat offset of every element (r, c) of W [n_out][k] in the packed layout."""
+    r = np.arange(n_out)[:, None]
+    c = np.arange(k)[None, :]
+    return ((((r // 64) * (k // 32) + c // 32) * 4 + (r // 16) % 4) * 512
+            + (16 * ((c // 8) % 4) + r % 16) * 8 + c % 8)
+
+
+def gate_up_row_order(n_out: int) -> np.ndarray:
+    """Logical row order of a SEVO_PACK_GATE_UP weight: per superblock s the gate
+    rows 32s..32s+31, then the up rows n_out/2 + 32s.."""
+    F = n_out // 2
+    order = []
+    for s in range(n_out // 64):
+        order += list(range(32 * s, 32 * s + 32)) + list(range(F + 32 * s, F + 32 * s + 32))
+    return np.array(order)
+
+
+def pack_weight_host(w: np.ndarray, gate_up: bool = False) -> np.ndarray:
+    n_out, k = w.shape
+    if gate_up:
+        w = w[gate_up_row_order(n_out)]
+    out = np.empty(n_out * k, w.dtype)
+    out[packed_weight_offsets(n_out, k).ravel()] = w.ravel()
+    return out.reshape(n_out, k)
+
+
+def act_tile_offsets(m: int, k: int) -> np.ndarray:
+    r = np.arange(m)[:, None]
+    c = np.arange(k)[None, :]
+    return ((r // 16) * (k // 32) + c // 32) * 512 + (16 * ((c // 8) % 4) + r % 16) * 8 + c % 8
+
+
+def tile_activations_host(x: np.ndarray) -> np.ndarray:
+    """x [m][k] -> flat tiled buffer of ceil(m/16)*16 rows (padding rows zero)."""
+    m, k = x.shape
+    out = np.zeros(-(-m // 16) * 16 * k, x.dtype)
+    out[act_tile_offsets(m, k).ravel()] = x.ravel()
+    return out
+
+
+def untile_activations_host(t: np.ndarray, m: int, k: int) -> np.ndarray:
+    return np.asarray(t).reshape(-1)[act_tile_offsets(m, k)]

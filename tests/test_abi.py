@@ -37,7 +37,8 @@ int main(void) {
   S(sevo_step_args) P(sevo_step_args, max_pages) P(sevo_step_args, num_pages)
   P(sevo_step_args, k_pools) P(sevo_step_args, seed) P(sevo_step_args, temperature)
   P(sevo_step_args, num_splits) P(sevo_step_args, out_logits) P(sevo_step_args, workspace_bytes)
-  S(sevo_linear_args) P(sevo_linear_args, x) P(sevo_linear_args, workspace_bytes)
+  S(sevo_linear_args) P(sevo_linear_args, flags) P(sevo_linear_args, x)
+  P(sevo_linear_args, workspace_bytes)
   return 0;
 }
 """
@@ -131,11 +132,12 @@ def test_sampler_rejects_bad_ld_and_small_workspace():
 
 
 @pytest.mark.parametrize("kw,status", [
-    (dict(k=192), sevo.UNSUPPORTED),
+    (dict(k=200, ldx=200), sevo.UNSUPPORTED),
     (dict(n_out=96), sevo.UNSUPPORTED),
-    (dict(n_out=192, mode=2), sevo.UNSUPPORTED),
     (dict(mode=3), sevo.INVALID_ARGUMENT),
     (dict(ldx=100), sevo.INVALID_ARGUMENT),
+    (dict(flags=4), sevo.INVALID_ARGUMENT),
+    (dict(flags=2, mode=0), sevo.INVALID_ARGUMENT),     # tiled output needs SWIGLU
 ])
 def test_linear_rejects_bad_shapes(kw, status):
     base = dict(m=4, n_out=128, k=128, ldx=128, mode=0, k_splits=0)
@@ -146,10 +148,26 @@ def test_linear_rejects_bad_shapes(kw, status):
 
 def test_linear_plan_and_workspace():
     L = sevo.lib()
-    # split K while fewer than 512 workgroups and each split keeps >= 1024 k
-    assert L.sevo_linear_workspace_bytes(64, 6144, 4096, 0) == 4 * 64 * 6144 * 4
-    assert L.sevo_linear_workspace_bytes(64, 4096, 12288, 0) == 8 * 64 * 4096 * 4
+    # split K while fewer than 192 workgroups and each split keeps >= 1024 k
+    assert L.sevo_linear_workspace_bytes(64, 6144, 4096, 0) == 2 * 64 * 6144 * 4
+    assert L.sevo_linear_workspace_bytes(64, 4096, 4096, 0) == 4 * 64 * 4096 * 4
+    assert L.sevo_linear_workspace_bytes(64, 4096, 12288, 0) == 4 * 64 * 4096 * 4
     assert L.sevo_linear_workspace_bytes(64, 151936, 4096, 0) == 0      # one split: no partials
+    assert L.sevo_linear_workspace_bytes(4, 512, 256, 0) == 0           # short k: one split
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(n_out=96), sevo.UNSUPPORTED),
+    (dict(k=48), sevo.UNSUPPORTED),
+    (dict(kind=2), sevo.INVALID_ARGUMENT),
+    (dict(src=0), sevo.INVALID_ARGUMENT),
+    (dict(dst=(1 << 20) + 4096), sevo.INVALID_ARGUMENT),                # overlapping buffers
+])
+def test_pack_weight_rejects_bad_arguments(kw, status):
+    a = dict(src=1 << 20, dst=1 << 24, n_out=64, k=64, kind=0)
+    a.update(kw)
+    assert sevo.lib().sevo_pack_weight(a["src"], a["dst"], a["n_out"], a["k"], a["kind"],
+                                       None) == status
 
 
 def test_init_model_rejects_bad_config():

@@ -12,7 +12,8 @@ from oracle import decoder as od
 from oracle.bf16 import round_bf16
 from paper_2604_07725_amd import synth
 from tests.gpu_helpers import (ATTN_REL_TOL, attn_rel_err, bf16_bits, check_ids,
-                               host_candidate_kv, make_population, say, to_np)
+                               host_candidate_kv, make_population, pack_weight_host, say,
+                               tile_activations_host, to_np, untile_activations_host)
 
 pytestmark = pytest.mark.gpu
 
@@ -223,28 +224,40 @@ def test_logprob_sample_is_keyed_by_uid_and_position(S):
 
 # ------------------------------------------------------------------ linear
 LINEAR_CASES = [
-    # m, n_out, k, mode, k_splits
-    (4, 512, 256, 0, 0), (4, 256, 256, 1, 0), (4, 2048, 256, 2, 0), (4, 256, 1024, 1, 0),
-    (17, 128, 1024, 0, 3), (33, 192, 512, 1, 0), (64, 256, 4096, 0, 1), (64, 6144, 4096, 0, 0),
-    (64, 4096, 12288, 1, 0), (64, 24576, 4096, 2, 0), (16, 4096, 4096, 1, 0), (100, 128, 256, 0, 2),
+    # m, n_out, k, mode, k_splits, x_tiled
+    (4, 512, 256, 0, 0, 0), (4, 256, 256, 1, 0, 1), (4, 2048, 256, 2, 0, 0),
+    (4, 256, 1024, 1, 0, 0), (17, 128, 1024, 0, 3, 1), (33, 192, 512, 1, 0, 0),
+    (64, 256, 4096, 0, 1, 1), (64, 6144, 4096, 0, 0, 1), (64, 4096, 12288, 1, 0, 1),
+    (64, 24576, 4096, 2, 0, 1), (16, 4096, 4096, 1, 0, 0), (100, 128, 256, 0, 2, 1),
+    # k not a multiple of 128: per-wave step counts differ, short tails
+    (5, 128, 96, 0, 0, 0), (20, 256, 160, 1, 0, 1), (3, 128, 32, 2, 0, 1), (40, 192, 352, 0, 2, 0),
 ]
 
 
-@pytest.mark.parametrize("m,n_out,k,mode,ks", LINEAR_CASES)
-def test_linear_matches_float64_matmul(S, m, n_out, k, mode, ks):
-    sevo, _ = S
-    say(f"linear m={m} n={n_out} k={k} mode={mode} ks={ks}")
+def _linear_inputs(sevo, m, n_out, k, mode):
     x = torch.empty(m, k, dtype=torch.bfloat16, device="cuda")
     w = torch.empty(n_out, k, dtype=torch.bfloat16, device="cuda")
     kx, kw = synth.tensor_key(m, 50, k), synth.tensor_key(n_out, 51, k)
     sevo.sevo_fill_normal_bf16(x, kx, 0, 1.0)
     sevo.sevo_fill_normal_bf16(w, kw, 0, 0.02)
-    xh = synth.host_values(synth.TensorSpec((m, k), kx, 1.0)).reshape(m, k).astype(np.float64)
-    wh = synth.host_values(synth.TensorSpec((n_out, k), kw, 0.02)).reshape(n_out, k).astype(
-        np.float64)
-    y = xh @ wh.T
+    wp = sevo.sevo_pack_weight(w, sevo.PACK_GATE_UP if mode == 2 else sevo.PACK_PLAIN)
+    xh = synth.host_values(synth.TensorSpec((m, k), kx, 1.0)).reshape(m, k)
+    wh = synth.host_values(synth.TensorSpec((n_out, k), kw, 0.02)).reshape(n_out, k)
+    return x, w, wp, xh, wh
+
+
+@pytest.mark.parametrize("m,n_out,k,mode,ks,xt", LINEAR_CASES)
+def test_linear_matches_float64_matmul(S, m, n_out, k, mode, ks, xt):
+    sevo, _ = S
+    say(f"linear m={m} n={n_out} k={k} mode={mode} ks={ks} x_tiled={xt}")
+    x, _, wp, xh, wh = _linear_inputs(sevo, m, n_out, k, mode)
+    if xt:
+        xb = tile_activations_host(bf16_bits(x).reshape(m, k))
+        x = torch.from_numpy(xb.view(np.int16)).cuda().view(torch.bfloat16)
+    kw = dict(k_splits=ks, x_tiled=bool(xt), m=m)
+    y = xh.astype(np.float64) @ wh.astype(np.float64).T
     if mode == 2:
-        out = sevo.sevo_linear(x, w, mode=2, k_splits=ks)
+        out = sevo.sevo_linear(x, wp, mode=2, **kw)
         torch.cuda.synchronize()
         F = n_out // 2
         ref = od.silu(y[:, :F]) * y[:, F:]
@@ -252,20 +265,58 @@ def test_linear_matches_float64_matmul(S, m, n_out, k, mode, ks):
         # one bf16 rounding of the product plus fp32 accumulation error
         assert np.all(np.abs(got - ref) <= 2 ** -8 * np.abs(ref) + 1e-4 * np.abs(ref).max())
         return
-    base = None
     if mode == 1:
         base = synth.host_values(synth.TensorSpec((m, n_out), synth.tensor_key(1, 52), 1.0))
         base = base.reshape(m, n_out).astype(np.float32)
         out = torch.from_numpy(base.copy()).cuda()
-        sevo.sevo_linear(x, w, mode=1, out=out, k_splits=ks)
+        sevo.sevo_linear(x, wp, mode=1, out=out, **kw)
         ref = base.astype(np.float64) + y
     else:
-        out = sevo.sevo_linear(x, w, mode=0, k_splits=ks)
+        out = sevo.sevo_linear(x, wp, mode=0, **kw)
         ref = y
     torch.cuda.synchronize()
     got = out.double().cpu().numpy()
     scale = np.sqrt(k) * 0.02
     np.testing.assert_allclose(got, ref, rtol=0, atol=2e-5 * scale + 1e-6 * np.abs(ref).max())
+
+
+@pytest.mark.parametrize("n_out,k,gate_up", [(64, 32, False), (192, 160, False),
+                                             (4096, 4096, False), (256, 96, True),
+                                             (24576, 4096, True)])
+def test_pack_weight_bit_exact(S, n_out, k, gate_up):
+    sevo, _ = S
+    say(f"pack n={n_out} k={k} gate_up={gate_up}")
+    w = torch.empty(n_out, k, dtype=torch.bfloat16, device="cuda")
+    kw = synth.tensor_key(n_out, 53, k)
+    sevo.sevo_fill_normal_bf16(w, kw, 0, 0.02)
+    wp = sevo.sevo_pack_weight(w, sevo.PACK_GATE_UP if gate_up else sevo.PACK_PLAIN)
+    wh = synth.host_values(synth.TensorSpec((n_out, k), kw, 0.02)).reshape(n_out, k)
+    torch.cuda.synchronize()
+    # bf16 bit patterns (the host values are exactly representable in bf16)
+    bits = (np.ascontiguousarray(wh, np.float32).view(np.uint32) >> 16).astype(np.uint16)
+    np.testing.assert_array_equal(bf16_bits(wp).reshape(n_out, k), pack_weight_host(bits, gate_up))
+
+
+def test_swiglu_tiled_output_and_tiled_chain(S):
+    """SwiGLU written in the tiled layout equals the row-major result, and feeds
+    the next projection as a tiled input (the decode step's FFN chain)."""
+    sevo, _ = S
+    m, F2, H = 37, 512, 256
+    say("swiglu tiled chain")
+    x, _, wp, _, _ = _linear_inputs(sevo, m, F2, H, 2)
+    a_row = sevo.sevo_linear(x, wp, mode=2)
+    a_til = sevo.sevo_linear(x, wp, mode=2, out_tiled=True)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(untile_activations_host(bf16_bits(a_til), m, F2 // 2),
+                                  bf16_bits(a_row))
+    wd = torch.empty(H, F2 // 2, dtype=torch.bfloat16, device="cuda")
+    sevo.sevo_fill_normal_bf16(wd, synth.tensor_key(9, 54), 0, 0.02)
+    wdp = sevo.sevo_pack_weight(wd)
+    y_row = sevo.sevo_linear(a_row, wdp, mode=0, k_splits=1)
+    y_til = sevo.sevo_linear(a_til, wdp, mode=0, k_splits=1, x_tiled=True, m=m)
+    torch.cuda.synchronize()
+    # same operands, same kernel schedule: identical sums
+    np.testing.assert_array_equal(y_row.cpu().numpy(), y_til.cpu().numpy())
 
 
 # ------------------------------------------------------------------ norm / embed / rope
