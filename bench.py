@@ -15,6 +15,7 @@ the timed steps) and the oracle's throughput on a bounded sample of the same
 workload on the host cores (cpu_baseline).
 """
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -27,6 +28,10 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
 BF16_PEAK_TFLOPS = 2500.0
+# sources of the attention split kernel; the HBM-counter traffic recorded under
+# profiles/ is reported only while they are unchanged
+ATTN_SOURCES = ["paper_2604_07725_amd/csrc/attn_decode.hip", "paper_2604_07725_amd/csrc/common.h"]
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_split_kernel_traffic.json")
 
 
 def log(msg):
@@ -41,6 +46,22 @@ def attention_bytes(lengths, hkv, hq, d):
     pages = int(((lengths + 15) // 16).sum())
     n = len(lengths)
     return kv + 2 * n * hq * d * 2 + pages * 4
+
+
+def measured_traffic(workload):
+    """HBM bytes per attention launch from the rocprofv3 FETCH_SIZE / WRITE_SIZE
+    passes (copy-kernel calibrated) recorded under profiles/, or None when they
+    were taken on another workload or the kernel sources changed since."""
+    try:
+        rec = json.load(open(TRAFFIC_FILE))
+    except (OSError, ValueError):
+        return None
+    h = hashlib.sha256()
+    for f in ATTN_SOURCES:
+        h.update(open(os.path.join(ROOT, f), "rb").read())
+    if rec.get("source_sha256") != h.hexdigest() or rec.get("workload") != workload:
+        return None
+    return rec
 
 
 def cpu_baseline(w, pop, n_sample, budget_s=30.0):
@@ -186,6 +207,7 @@ def main():
     attn_avg_ms = attn_ms / max(launches, 1)
     achieved = attn_bytes_per_launch / (split_avg_ms * 1e-3) / 1e9
     step_bytes = shape.n_layers * attn_bytes_per_launch + shape.weight_bytes()
+    tr = measured_traffic(w.name)
     out = {
         "metric": "population decode tokens/s/GPU",
         "value": pop.n / (ms_per_step * 1e-3),
@@ -204,7 +226,10 @@ def main():
                    sevo.sevo_attn_plan_splits(pop.n, shape.n_kv_heads, pop.max_pages)},
         "roofline": {"kernel": "attn_split_kernel<128,4> (paged split-KV GQA attention)",
                      "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": None if tr is None else tr["traffic_bytes_per_launch"],
+                     "traffic_over_algorithmic": None if tr is None else
+                     tr["traffic_bytes_per_launch"] / tr["algorithmic_bytes_per_launch"],
                      "bytes_per_launch": attn_bytes_per_launch,
                      "avg_launch_ms": split_avg_ms,
                      "with_combine_GBs": attn_bytes_per_launch / (attn_avg_ms * 1e-3) / 1e9},
