@@ -144,7 +144,8 @@ void sevo_free_model(sevo_model* m);
  * merges in split order, so the result is deterministic.
  *   q        bf16 [n][n_q_heads][head_dim]
  *   k_pool, v_pool  paged layout above (bf16)
- *   page_table int32 [n][max_pages];  seq_lens int32 [n], 1 <= len <= 16 max_pages
+ *   page_table int32 [n][max_pages];  seq_lens int32 [n], 0 <= len <= 16 max_pages
+ *   (a candidate with len 0 gets o = 0)
  *   out      bf16 [n][n_q_heads][head_dim]
  *   num_splits 0 = chosen by the library (see sevo_attn_plan_splits)
  * A page id outside [0, num_pages) contributes no keys (it is never read).

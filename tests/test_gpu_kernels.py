@@ -144,8 +144,20 @@ def test_attention_out_of_range_page_ids_are_skipped(S):
         assert attn_rel_err(o[i], ref) <= 8e-3
 
 
+def test_attention_zero_length_candidate_gives_zero(S):
+    """A candidate with no cached keys yields o = 0 and never disturbs the others."""
+    shape = synth.ModelShape(1, 256, 32, 8, 128, 256, 256)
+    say("attention with a zero-length candidate")
+    pop, q, kp, vp, pt, lens, out = _attn_case(S, shape, [0, 40, 0, 300], seed=12)
+    o = to_np(out)
+    assert np.all(o[0] == 0) and np.all(o[2] == 0)
+    for i in (1, 3):
+        assert attn_rel_err(o[i], _oracle_attn(shape, 12, pop, i)) <= 8e-3
+
+
 @pytest.mark.parametrize("workload,sample", [("attn_pop16_agg4", [0, 5, 11, 15]),
-                                             ("dense8b_pop64_agg4", None)])
+                                             ("dense8b_pop64_agg4", None),
+                                             ("dense8b_pop16_agg8", None)])
 def test_attention_full_size_sampled(S, workload, sample):
     """Full-size pools and the benchmark's launch configuration (auto splits);
     the oracle checks sampled candidates (all heads), including the shortest
