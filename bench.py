@@ -125,6 +125,8 @@ def main():
     ap.add_argument("--num-splits", type=int, default=0)
     ap.add_argument("--cpu-sample", type=int, default=8)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--conf-topk", type=int, default=0,
+                    help="also compute the per-token self-confidence (top-K log-probs) each step")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device copy (3 times), to scale HBM counters")
     args = ap.parse_args()
@@ -171,8 +173,10 @@ def main():
 
     tokens = d["tokens"].clone()
     positions = d["lengths"].clone()
+    conf_sum = torch.zeros(pop.n, dtype=torch.float32, device=dev) if args.conf_topk else None
     buf = sevo.StepBuffers(model, tokens, positions, d["page_table"], kp, vp, d["uids"],
-                           seed=20260412, temperature=1.0, num_splits=args.num_splits)
+                           seed=20260412, temperature=1.0, num_splits=args.num_splits,
+                           conf_topk=args.conf_topk, conf_sum=conf_sum)
 
     def step():
         ids, _ = buf.run()
@@ -223,7 +227,8 @@ def main():
                    "context_tokens": [int(pop.lengths.min()), int(pop.lengths.max())],
                    "page_size": 16, "parallelism": "none (1 GPU)",
                    "num_splits": int(buf.args.num_splits) or
-                   sevo.sevo_attn_plan_splits(pop.n, shape.n_kv_heads, pop.max_pages)},
+                   sevo.sevo_attn_plan_splits(pop.n, shape.n_kv_heads, pop.max_pages),
+                   "self_confidence_topk": args.conf_topk},
         "roofline": {"kernel": "attn_split_kernel<128,4> (paged split-KV GQA attention)",
                      "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,

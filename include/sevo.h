@@ -184,7 +184,15 @@ size_t sevo_attn_workspace_bytes(int32_t n, int32_t n_q_heads, int32_t n_kv_head
  * under T = 1.  T < 0 or non-finite: INVALID_ARGUMENT.
  *   logits fp32 [n][ld] (first vocab entries used); cand_uid uint64 [n];
  *   positions int32 [n];  out_tokens int32 [n];  out_logprobs fp32 [n].
- * Errors: INVALID_ARGUMENT, WORKSPACE_TOO_SMALL, HIP. */
+ * Self-confidence (the group-confidence fitness signal, Eq. 1), computed in
+ * the same passes when conf_topk > 0 (1..32, and at most vocab):
+ *   c_i = -(1/K) * sum of the K largest log_softmax(logits[i]) entries
+ *       = logsumexp(logits[i]) - mean of the K largest logits[i],
+ * under the model's own distribution (T = 1) whatever the sampling T.
+ *   out_conf fp32 [n] (nullable) receives c_i; conf_sum fp32 [n] (nullable) gets
+ *   c_i added (a running sum over a trajectory's tokens: C = conf_sum / tokens).
+ * Errors: INVALID_ARGUMENT, UNSUPPORTED (conf_topk * ceil(vocab / 4096) > 6144),
+ * WORKSPACE_TOO_SMALL, HIP. */
 typedef struct {
   const float* logits;
   int32_t n, vocab;
@@ -195,12 +203,26 @@ typedef struct {
   const int32_t* positions;
   int32_t* out_tokens;
   float* out_logprobs;
+  int32_t conf_topk; /* 0 = no confidence */
+  float* out_conf;
+  float* conf_sum;
   void* workspace;
   size_t workspace_bytes;
 } sevo_sample_args;
 
 sevo_status sevo_logprob_sample(const sevo_sample_args* a, void* stream);
 size_t sevo_sample_workspace_bytes(int32_t n, int32_t vocab);
+
+/* Group confidence of Eq. 2 from the per-candidate running sums:
+ *   GC[g] = (1/K) sum_{k<K} conf_sum[c] / token_counts[c],  c = groups[g*K + k]
+ * (C(tau) = conf_sum / token count is the candidate confidence).
+ *   conf_sum fp32 [n];  token_counts int32 [n] (> 0 for every grouped
+ *   candidate);  groups int32 [n_groups][group_size];  out_gc fp32 [n_groups].
+ * Candidate indices are not validated on the device.
+ * Errors: INVALID_ARGUMENT, HIP. */
+sevo_status sevo_group_confidence(const float* conf_sum, const int32_t* token_counts,
+                                  const int32_t* groups, int32_t n_groups, int32_t group_size,
+                                  float* out_gc, void* stream);
 
 /* ------------------------------------------------------------------ decode step */
 
@@ -217,7 +239,8 @@ size_t sevo_sample_workspace_bytes(int32_t n, int32_t vocab);
  *   page_table int32 [n][max_pages];  k_pools, v_pools: HOST arrays of
  *   n_layers device pool pointers;  cand_uid uint64 [n];
  *   out_tokens int32 [n];  out_logprobs fp32 [n];
- *   out_logits fp32 [n][vocab] or NULL (then kept in the workspace).
+ *   out_logits fp32 [n][vocab] or NULL (then kept in the workspace);
+ *   conf_topk, out_conf, conf_sum: the sampler's self-confidence (above).
  * The library never changes positions or page tables: the caller advances p_i
  * and allocates pages.  Errors: INVALID_ARGUMENT, UNSUPPORTED,
  * WORKSPACE_TOO_SMALL, HIP. */
@@ -237,6 +260,9 @@ typedef struct {
   int32_t* out_tokens;
   float* out_logprobs;
   float* out_logits;
+  int32_t conf_topk;
+  float* out_conf;
+  float* conf_sum;
   void* workspace;
   size_t workspace_bytes;
 } sevo_step_args;

@@ -282,3 +282,29 @@ def decode_step(shape, weights, k_pools, v_pools, page_table, tokens, positions,
     logits = lm_logits(shape, weights["final_norm"], weights["lm_head"], x, mirror)
     ids, lps, gaps = logprob_sample(logits, temperature, seed, uids, positions)
     return {"ids": ids, "lps": lps, "gaps": gaps, "logits": logits, "x": x}
+
+
+# ------------------------------------------------------------------ fitness signal
+def token_confidence(logits, k_l):
+    """Per-token confidence of Eq. 1 from the scoring model's logits.
+
+    c = -(1/K_l) * sum of the K_l largest log-probabilities log p(v | prefix),
+    where p is the model's own distribution (softmax of the logits at T = 1).
+    logits [N, V] -> c [N].
+    """
+    lp = log_softmax(np.asarray(logits, np.float64))
+    k_l = int(k_l)
+    top = -np.sort(-lp, axis=-1)[:, :k_l]
+    return -np.mean(top, axis=-1)
+
+
+def candidate_confidence(token_conf_sum, n_tokens):
+    """C(tau) of Eq. 2: the mean of c(i) over the trajectory's tokens."""
+    return np.asarray(token_conf_sum, np.float64) / np.asarray(n_tokens, np.float64)
+
+
+def group_confidence(cand_conf, groups):
+    """GC(g) of Eq. 2: the mean of C(tau) over the K candidates of each group.
+    groups [M, K] holds candidate indices."""
+    cand_conf = np.asarray(cand_conf, np.float64)
+    return cand_conf[np.asarray(groups, np.int64)].mean(axis=-1)

@@ -300,6 +300,19 @@ SEVO_API size_t sevo_sample_workspace_bytes(int32_t n, int32_t vocab) {
   return round_up(sevo::sample_workspace_bytes(n, vocab), 256);
 }
 
+static sevo_status conf_check(int conf_topk, int vocab, const float* out_conf,
+                              const float* conf_sum) {
+  if (conf_topk < 0 || conf_topk > 32)
+    return fail(SEVO_ERR_INVALID_ARGUMENT, "conf_topk %d outside [0, 32]", conf_topk);
+  if (conf_topk > vocab)
+    return fail(SEVO_ERR_INVALID_ARGUMENT, "conf_topk %d > vocab %d", conf_topk, vocab);
+  if (!sevo::sample_conf_supported(vocab, conf_topk))
+    return fail(SEVO_ERR_UNSUPPORTED, "confidence over a vocabulary of %d entries", vocab);
+  if (conf_topk > 0 && !out_conf && !conf_sum)
+    return fail(SEVO_ERR_INVALID_ARGUMENT, "conf_topk > 0 needs out_conf or conf_sum");
+  return SEVO_OK;
+}
+
 static sevo_status sample_check(const float* logits, int n, int vocab, int64_t ld, float temp) {
   if (n < 0 || vocab < 1 || ld < vocab)
     return fail(SEVO_ERR_INVALID_ARGUMENT, "bad n / vocab / ld (%d, %d, %lld)", n, vocab,
@@ -320,16 +333,32 @@ SEVO_API sevo_status sevo_logprob_sample(const sevo_sample_args* a, void* stream
   if (!a->cand_uid || !a->positions || !a->out_tokens || !a->out_logprobs || !a->workspace)
     return fail(SEVO_ERR_INVALID_ARGUMENT, "null pointer");
   if (!aligned16(a->workspace)) return fail(SEVO_ERR_INVALID_ARGUMENT, "misaligned workspace");
+  st = conf_check(a->conf_topk, a->vocab, a->out_conf, a->conf_sum);
+  if (st) return st;
   const size_t need = sevo::sample_workspace_bytes(a->n, a->vocab);
   if (a->workspace_bytes < need)
     return fail(SEVO_ERR_WORKSPACE_TOO_SMALL, "sampler needs %zu workspace bytes, got %zu", need,
                 a->workspace_bytes);
   hipError_t e = sevo::launch_logprob_sample(
       a->logits, a->n, a->vocab, a->ld, a->temperature, a->seed, a->cand_uid, a->positions,
-      a->out_tokens, a->out_logprobs, static_cast<float*>(a->workspace),
-      static_cast<hipStream_t>(stream));
+      a->out_tokens, a->out_logprobs, static_cast<float*>(a->workspace), a->conf_topk,
+      a->out_conf, a->conf_sum, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "sevo_logprob_sample launch");
   return SEVO_OK;
+}
+
+SEVO_API sevo_status sevo_group_confidence(const float* conf_sum, const int32_t* token_counts,
+                                           const int32_t* groups, int32_t n_groups,
+                                           int32_t group_size, float* out_gc, void* stream) {
+  if (n_groups < 0 || group_size < 1)
+    return fail(SEVO_ERR_INVALID_ARGUMENT, "bad n_groups / group_size");
+  if (n_groups == 0) return SEVO_OK;
+  if (!conf_sum || !token_counts || !groups || !out_gc)
+    return fail(SEVO_ERR_INVALID_ARGUMENT, "null pointer");
+  hipError_t e = sevo::launch_group_confidence(conf_sum, token_counts, groups, n_groups,
+                                               group_size, out_gc,
+                                               static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? SEVO_OK : hip_fail(e, "sevo_group_confidence");
 }
 
 // ------------------------------------------------------------------ sub-steps
@@ -515,6 +544,7 @@ SEVO_API sevo_status sevo_decode_step(sevo_model* m, const sevo_step_args* a, vo
     return fail(SEVO_ERR_INVALID_ARGUMENT, "bad n / max_pages / num_pages / num_splits");
   if (!std::isfinite(a->temperature) || a->temperature < 0.f)
     return fail(SEVO_ERR_INVALID_ARGUMENT, "temperature must be finite and >= 0");
+  if (sevo_status cs = conf_check(a->conf_topk, c.vocab, a->out_conf, a->conf_sum)) return cs;
   if (a->n == 0) return SEVO_OK;
   if (!a->tokens || !a->positions || !a->page_table || !a->k_pools || !a->v_pools ||
       !a->cand_uid || !a->out_tokens || !a->out_logprobs || !a->workspace)
@@ -616,7 +646,7 @@ SEVO_API sevo_status sevo_decode_step(sevo_model* m, const sevo_step_args* a, vo
   if (e == hipSuccess)
     e = sevo::launch_logprob_sample(logits, n, c.vocab, c.vocab, a->temperature, a->seed,
                                     a->cand_uid, a->positions, a->out_tokens, a->out_logprobs,
-                                    smp, st);
+                                    smp, a->conf_topk, a->out_conf, a->conf_sum, st);
   if (e != hipSuccess) return hip_fail(e, "decode step (head / sampler)");
   return SEVO_OK;
 }

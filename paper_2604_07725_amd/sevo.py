@@ -58,7 +58,8 @@ class AttnArgs(C.Structure):
 class SampleArgs(C.Structure):
     _fields_ = [("logits", vp), ("n", i32), ("vocab", i32), ("ld", i64), ("temperature", f32),
                 ("seed", u64), ("cand_uid", vp), ("positions", vp), ("out_tokens", vp),
-                ("out_logprobs", vp), ("workspace", vp), ("workspace_bytes", sz)]
+                ("out_logprobs", vp), ("conf_topk", i32), ("out_conf", vp), ("conf_sum", vp),
+                ("workspace", vp), ("workspace_bytes", sz)]
 
 
 class StepArgs(C.Structure):
@@ -66,8 +67,8 @@ class StepArgs(C.Structure):
                 ("max_pages", i32), ("num_pages", i64), ("k_pools", C.POINTER(vp)),
                 ("v_pools", C.POINTER(vp)), ("cand_uid", vp), ("seed", u64),
                 ("temperature", f32), ("num_splits", i32), ("out_tokens", vp),
-                ("out_logprobs", vp), ("out_logits", vp), ("workspace", vp),
-                ("workspace_bytes", sz)]
+                ("out_logprobs", vp), ("out_logits", vp), ("conf_topk", i32),
+                ("out_conf", vp), ("conf_sum", vp), ("workspace", vp), ("workspace_bytes", sz)]
 
 
 class LinearArgs(C.Structure):
@@ -87,6 +88,7 @@ _SIGS = {
     "sevo_attn_workspace_bytes": ([i32, i32, i32, i32, i32, i32], sz),
     "sevo_logprob_sample": ([C.POINTER(SampleArgs), vp], i32),
     "sevo_sample_workspace_bytes": ([i32, i32], sz),
+    "sevo_group_confidence": ([vp, vp, vp, i32, i32, vp, vp], i32),
     "sevo_decode_step": ([vp, C.POINTER(StepArgs), vp], i32),
     "sevo_step_workspace_bytes": ([vp, i32, i32, i32], sz),
     "sevo_embed": ([vp, vp, i32, i32, i32, vp, vp], i32),
@@ -191,9 +193,16 @@ def sevo_sample_workspace_bytes(n: int, vocab: int) -> int:
 
 
 def sevo_logprob_sample(logits, temperature, seed, cand_uid, positions, out_tokens=None,
-                        out_logprobs=None, workspace=None, stream=None):
-    """(ids int32 [n], logprobs fp32 [n]) from fp32 logits [n, >=vocab]."""
-    n, vocab = logits.shape
+                        out_logprobs=None, workspace=None, stream=None, vocab=None,
+                        conf_topk=0, out_conf=None, conf_sum=None):
+    """(ids int32 [n], logprobs fp32 [n]) from fp32 logits [n, ld] (the first
+    ``vocab`` columns, default all).  With ``conf_topk`` > 0 also the per-token
+    self-confidence: returned as a third element (``out_conf``) and/or added to
+    ``conf_sum``."""
+    n = logits.shape[0]
+    vocab = logits.shape[1] if vocab is None else vocab
+    if conf_topk and out_conf is None:
+        out_conf = torch.empty(n, dtype=torch.float32, device=logits.device)
     if out_tokens is None:
         out_tokens = torch.empty(n, dtype=torch.int32, device=logits.device)
     if out_logprobs is None:
@@ -202,9 +211,23 @@ def sevo_logprob_sample(logits, temperature, seed, cand_uid, positions, out_toke
     a = SampleArgs(logits=_p(logits), n=n, vocab=vocab, ld=logits.stride(0),
                    temperature=float(temperature), seed=int(seed), cand_uid=_p(cand_uid),
                    positions=_p(positions), out_tokens=_p(out_tokens),
-                   out_logprobs=_p(out_logprobs), workspace=_p(ws), workspace_bytes=ws.numel())
+                   out_logprobs=_p(out_logprobs), conf_topk=int(conf_topk), out_conf=_p(out_conf),
+                   conf_sum=_p(conf_sum), workspace=_p(ws), workspace_bytes=ws.numel())
     _check(lib().sevo_logprob_sample(C.byref(a), _stream(stream)))
+    if conf_topk:
+        return out_tokens, out_logprobs, out_conf
     return out_tokens, out_logprobs
+
+
+def sevo_group_confidence(conf_sum, token_counts, groups, out=None, stream=None):
+    """GC [n_groups] from per-candidate confidence sums, token counts (int32)
+    and groups int32 [n_groups, K] of candidate indices."""
+    n_groups, k = groups.shape
+    if out is None:
+        out = torch.empty(n_groups, dtype=torch.float32, device=conf_sum.device)
+    _check(lib().sevo_group_confidence(_p(conf_sum), _p(token_counts), _p(groups), n_groups, k,
+                                       _p(out), _stream(stream)))
+    return out
 
 
 # ------------------------------------------------------------------ sub-steps
@@ -360,7 +383,8 @@ class StepBuffers:
     """Pre-built argument struct for repeated decode steps (no per-step allocation)."""
 
     def __init__(self, model: Model, tokens, positions, page_table, k_pools, v_pools, cand_uid,
-                 seed, temperature, num_splits=0, keep_logits=False, workspace=None):
+                 seed, temperature, num_splits=0, keep_logits=False, workspace=None,
+                 conf_topk=0, conf_sum=None):
         n = tokens.shape[0]
         dev = tokens.device
         self.model = model
@@ -368,6 +392,8 @@ class StepBuffers:
         self.out_logprobs = torch.empty(n, dtype=torch.float32, device=dev)
         self.out_logits = (torch.empty(n, model.shape.vocab, dtype=torch.float32, device=dev)
                            if keep_logits else None)
+        self.out_conf = (torch.empty(n, dtype=torch.float32, device=dev) if conf_topk else None)
+        self.conf_sum = conf_sum
         need = sevo_step_workspace_bytes(model, n, page_table.shape[1], num_splits)
         self.workspace = _workspace(need, dev, workspace)
         L = model.shape.n_layers
@@ -381,6 +407,7 @@ class StepBuffers:
             cand_uid=_p(cand_uid), seed=int(seed), temperature=float(temperature),
             num_splits=num_splits, out_tokens=_p(self.out_tokens),
             out_logprobs=_p(self.out_logprobs), out_logits=_p(self.out_logits),
+            conf_topk=int(conf_topk), out_conf=_p(self.out_conf), conf_sum=_p(conf_sum),
             workspace=_p(self.workspace), workspace_bytes=self.workspace.numel())
 
     def run(self, stream=None):
@@ -389,9 +416,12 @@ class StepBuffers:
 
 
 def sevo_decode_step(model: Model, tokens, positions, page_table, k_pools, v_pools, cand_uid,
-                     seed, temperature=1.0, num_splits=0, keep_logits=False, stream=None):
-    """One decode step of the population; returns (ids, logprobs[, logits])."""
+                     seed, temperature=1.0, num_splits=0, keep_logits=False, stream=None,
+                     conf_topk=0, conf_sum=None):
+    """One decode step of the population; returns (ids, logprobs[, logits][, conf])."""
     b = StepBuffers(model, tokens, positions, page_table, k_pools, v_pools, cand_uid, seed,
-                    temperature, num_splits, keep_logits)
+                    temperature, num_splits, keep_logits, conf_topk=conf_topk, conf_sum=conf_sum)
     ids, lps = b.run(stream)
-    return (ids, lps, b.out_logits) if keep_logits else (ids, lps)
+    out = (ids, lps) + ((b.out_logits,) if keep_logits else ()) + \
+        ((b.out_conf,) if conf_topk else ())
+    return out

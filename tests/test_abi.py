@@ -33,10 +33,12 @@ int main(void) {
   S(sevo_attn_args) P(sevo_attn_args, num_pages) P(sevo_attn_args, q) P(sevo_attn_args, scale)
   P(sevo_attn_args, out) P(sevo_attn_args, workspace_bytes)
   S(sevo_sample_args) P(sevo_sample_args, ld) P(sevo_sample_args, temperature)
-  P(sevo_sample_args, seed) P(sevo_sample_args, workspace_bytes)
+  P(sevo_sample_args, seed) P(sevo_sample_args, conf_topk) P(sevo_sample_args, conf_sum)
+  P(sevo_sample_args, workspace_bytes)
   S(sevo_step_args) P(sevo_step_args, max_pages) P(sevo_step_args, num_pages)
   P(sevo_step_args, k_pools) P(sevo_step_args, seed) P(sevo_step_args, temperature)
-  P(sevo_step_args, num_splits) P(sevo_step_args, out_logits) P(sevo_step_args, workspace_bytes)
+  P(sevo_step_args, num_splits) P(sevo_step_args, out_logits) P(sevo_step_args, conf_topk)
+  P(sevo_step_args, out_conf) P(sevo_step_args, workspace_bytes)
   S(sevo_linear_args) P(sevo_linear_args, flags) P(sevo_linear_args, x)
   P(sevo_linear_args, workspace_bytes)
   return 0;
@@ -190,3 +192,26 @@ def test_status_strings():
     for s in range(7):
         assert L.sevo_status_string(s)
     assert L.sevo_status_string(99) == b"unknown status"
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(conf_topk=33, out_conf=1 << 20), sevo.INVALID_ARGUMENT),
+    (dict(conf_topk=-1, out_conf=1 << 20), sevo.INVALID_ARGUMENT),
+    (dict(conf_topk=9, out_conf=1 << 20), sevo.INVALID_ARGUMENT),     # more than vocab
+    (dict(conf_topk=4), sevo.INVALID_ARGUMENT),                       # no output
+])
+def test_sampler_rejects_bad_confidence_arguments(kw, status):
+    f = 1 << 20
+    a = dict(logits=f, n=2, vocab=8, ld=8, temperature=1.0, cand_uid=f, positions=f,
+             out_tokens=f, out_logprobs=f, workspace=f, workspace_bytes=1 << 20)
+    a.update(kw)
+    assert sevo.lib().sevo_logprob_sample(C.byref(sevo.SampleArgs(**a)), None) == status
+
+
+def test_group_confidence_rejects_bad_arguments():
+    L = sevo.lib()
+    f = 1 << 20
+    assert L.sevo_group_confidence(f, f, f, -1, 4, f, None) == sevo.INVALID_ARGUMENT
+    assert L.sevo_group_confidence(f, f, f, 3, 0, f, None) == sevo.INVALID_ARGUMENT
+    assert L.sevo_group_confidence(None, f, f, 3, 4, f, None) == sevo.INVALID_ARGUMENT
+    assert L.sevo_group_confidence(None, None, None, 0, 4, None, None) == sevo.OK

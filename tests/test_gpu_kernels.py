@@ -234,6 +234,66 @@ def test_logprob_sample_is_keyed_by_uid_and_position(S):
     np.testing.assert_array_equal(la.cpu().numpy()[perm], lb.cpu().numpy())
 
 
+@pytest.mark.parametrize("n,vocab,ld,temp,k", [(64, 151936, 151936, 1.0, 20),
+                                               (64, 151936, 151936, 0.7, 32),
+                                               (16, 151936, 151936, 0.0, 1),
+                                               (4, 4093, 4096, 1.3, 8), (3, 40, 40, 1.0, 32),
+                                               (5, 9000, 9000, 1.0, 5)])
+def test_self_confidence_matches_oracle(S, n, vocab, ld, temp, k):
+    """Per-token confidence (Eq. 1) fused in the sampler, on identical logits:
+    c = -(1/K) sum of the K largest log-probabilities at T = 1, whatever T;
+    the running sum adds it; ids and log-probs are unchanged by it."""
+    sevo, _ = S
+    say(f"confidence n={n} vocab={vocab} T={temp} K={k}")
+    host, dev = _logits(n, vocab, ld, 7)
+    uid = torch.from_numpy(np.arange(n, dtype=np.int64) * 977 + 5).cuda()
+    pos = torch.from_numpy(np.arange(n, dtype=np.int32) + 100).cuda()
+    base = np.linspace(-1.0, 1.0, n).astype(np.float32)
+    acc = torch.from_numpy(base.copy()).cuda()
+    ids, lps, conf = sevo.sevo_logprob_sample(dev, temp, 31, uid, pos, vocab=vocab, conf_topk=k,
+                                              conf_sum=acc)
+    ids0, lps0 = sevo.sevo_logprob_sample(dev, temp, 31, uid, pos, vocab=vocab)
+    torch.cuda.synchronize()
+    ref = od.token_confidence(host.astype(np.float64), k)
+    got = conf.cpu().numpy().astype(np.float64)
+    err = np.abs(got - ref).max()
+    say(f"  max |c - c_ref| {err:.2e} (c in [{ref.min():.3f}, {ref.max():.3f}])")
+    assert err <= 2e-4
+    np.testing.assert_allclose(acc.cpu().numpy(), base + conf.cpu().numpy(), rtol=0, atol=1e-6)
+    np.testing.assert_array_equal(ids.cpu().numpy(), ids0.cpu().numpy())
+    np.testing.assert_array_equal(lps.cpu().numpy(), lps0.cpu().numpy())
+
+
+def test_self_confidence_ties_and_uniform(S):
+    """Uniform logits give c = log V exactly; many equal maxima count once each."""
+    sevo, _ = S
+    n, vocab = 3, 10000
+    dev = torch.zeros(n, vocab, dtype=torch.float32, device="cuda")
+    dev[1, 123:163] = 2.5            # 40 tied maxima
+    dev[2, ::1000] = 4.0             # 10 tied maxima, K = 16 also takes 6 zeros
+    uid = torch.arange(n, dtype=torch.int64, device="cuda")
+    pos = torch.zeros(n, dtype=torch.int32, device="cuda")
+    _, _, conf = sevo.sevo_logprob_sample(dev, 1.0, 1, uid, pos, conf_topk=16)
+    torch.cuda.synchronize()
+    ref = od.token_confidence(dev.double().cpu().numpy(), 16)
+    np.testing.assert_allclose(conf.cpu().numpy(), ref, rtol=0, atol=2e-5)
+    assert abs(float(conf[0]) - np.log(vocab)) < 2e-5
+
+
+def test_group_confidence_matches_oracle(S):
+    sevo, _ = S
+    rng = np.random.default_rng(3)
+    n, M, K = 64, 16, 4
+    csum = rng.uniform(1, 50, n).astype(np.float32)
+    cnt = rng.integers(1, 500, n).astype(np.int32)
+    groups = np.stack([rng.choice(n, K, replace=False) for _ in range(M)]).astype(np.int32)
+    gc = sevo.sevo_group_confidence(torch.from_numpy(csum).cuda(), torch.from_numpy(cnt).cuda(),
+                                    torch.from_numpy(groups).cuda())
+    torch.cuda.synchronize()
+    ref = od.group_confidence(od.candidate_confidence(csum, cnt), groups)
+    np.testing.assert_allclose(gc.cpu().numpy(), ref, rtol=2e-6)
+
+
 # ------------------------------------------------------------------ linear
 LINEAR_CASES = [
     # m, n_out, k, mode, k_splits, x_tiled

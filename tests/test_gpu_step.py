@@ -49,12 +49,18 @@ def test_tiny_step_sequence_matches_oracle(S):
     toks = pop.tokens.astype(np.int64)
     pos = pop.lengths.astype(np.int64)
     pos_d = d["lengths"].clone()
+    conf_sum = torch.zeros(pop.n, dtype=torch.float32, device="cuda")
+    ref_conf_sum = np.zeros(pop.n)
     for step in range(steps):
-        ids, lps, logits = sevo.sevo_decode_step(model, torch.from_numpy(toks.astype(np.int32)).cuda(),
-                                                 pos_d, d["page_table"], kp, vp, d["uids"], seed,
-                                                 temp, keep_logits=True)
+        ids, lps, logits, conf = sevo.sevo_decode_step(
+            model, torch.from_numpy(toks.astype(np.int32)).cuda(), pos_d, d["page_table"], kp, vp,
+            d["uids"], seed, temp, keep_logits=True, conf_topk=20, conf_sum=conf_sum)
         torch.cuda.synchronize()
         ref = od.decode_step(shape, hw, hk, hv, pop.page_table, toks, pos, pop.uids, seed, temp)
+        # the step's self-confidence (Eq. 1) follows the logits it came from
+        rc = od.token_confidence(ref["logits"], 20)
+        ref_conf_sum += rc
+        assert np.abs(conf.cpu().numpy() - rc).max() <= 2 * TINY_LOGIT_TOL
         lg = logits.double().cpu().numpy()
         err = np.abs(lg - ref["logits"]).max()
         lp_err = np.abs(lps.cpu().numpy() - ref["lps"]).max()
@@ -71,6 +77,8 @@ def test_tiny_step_sequence_matches_oracle(S):
         toks = ref["ids"]
         pos = pos + 1
         pos_d += 1
+    # running sum over the trajectory's tokens (C(tau) numerator, Eq. 2)
+    assert np.abs(conf_sum.cpu().numpy() - ref_conf_sum).max() <= 2 * steps * TINY_LOGIT_TOL
     # appended slots: close to the oracle's; every other slot untouched
     torch.cuda.synchronize()
     for l in range(shape.n_layers):

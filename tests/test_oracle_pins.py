@@ -369,3 +369,45 @@ def test_append_writes_exactly_one_slot():
     np.testing.assert_array_equal(kp[1, :, :, 1, :].reshape(2, 64), k[0])
     np.testing.assert_array_equal(vp[0, :, :, 9], v[1])
     assert int(((vp != v0).any(axis=-2)).sum()) == 4
+
+
+# ---------------------------------------------------------------- confidence (Eq. 1, 2)
+def test_token_confidence_uniform_is_log_vocab():
+    for V, k in ((7, 1), (7, 7), (4096, 20)):
+        c = od.token_confidence(np.full((2, V), 3.25), k)
+        np.testing.assert_allclose(c, math.log(V), rtol=0, atol=1e-12)
+
+
+def test_token_confidence_all_tokens_is_lse_minus_mean():
+    z = RNG.standard_normal((3, 50)) * 2
+    lse = np.log(np.exp(z).sum(-1))
+    np.testing.assert_allclose(od.token_confidence(z, 50), lse - z.mean(-1), atol=1e-12)
+
+
+def test_token_confidence_dominant_token_and_brute_force():
+    z = np.zeros((1, 10))
+    z[0, 3] = 1000.0
+    assert abs(od.token_confidence(z, 1)[0]) < 1e-12        # log p(top) = 0
+    np.testing.assert_allclose(od.token_confidence(z, 2), [500.0 + 0.5 * math.log(1.0)],
+                               atol=1e-9)
+    z = RNG.standard_normal((4, 9))
+    for k in (1, 3, 9):
+        for i in range(4):
+            p = [math.exp(v) for v in z[i]]
+            s = sum(p)
+            lps = sorted((math.log(v / s) for v in p), reverse=True)
+            want = -sum(lps[:k]) / k
+            assert abs(od.token_confidence(z[i:i + 1], k)[0] - want) < 1e-12
+
+
+def test_token_confidence_shift_and_permutation_invariant():
+    z = RNG.standard_normal((2, 64))
+    c = od.token_confidence(z, 5)
+    np.testing.assert_allclose(od.token_confidence(z + 17.5, 5), c, atol=1e-12)
+    np.testing.assert_allclose(od.token_confidence(z[:, RNG.permutation(64)], 5), c, atol=1e-12)
+
+
+def test_candidate_and_group_confidence_by_hand():
+    C = od.candidate_confidence([6.0, 9.0, 2.0, 8.0], [3, 3, 1, 4])
+    np.testing.assert_allclose(C, [2.0, 3.0, 2.0, 2.0])
+    np.testing.assert_allclose(od.group_confidence(C, [[0, 1], [2, 3], [1, 3]]), [2.5, 2.0, 2.5])
