@@ -48,6 +48,34 @@ def attention_bytes(lengths, hkv, hq, d):
     return kv + 2 * n * hq * d * 2 + pages * 4
 
 
+def kernel_table(shape, n, kprof, attn_bytes):
+    """Average time per launch of each kernel kind of the step, with the
+    projections' weight-streaming rate and matrix-core utilisation (algorithmic
+    bytes: weights + activations in + outputs out; flops 2 M N K)."""
+    H, F, V = shape.hidden, shape.ffn, shape.vocab
+    qd = shape.n_q_heads * shape.head_dim
+    qkvd = qd + 2 * shape.n_kv_heads * shape.head_dim
+    gemms = {"qkv": (qkvd, H, 4), "attn_out": (H, qd, 4), "gate_up": (2 * F, H, None),
+             "down": (H, F, 4), "lm_head": (V, H, 4)}
+    table = {}
+    for kind, (ms, cnt) in kprof.items():
+        avg = ms / cnt
+        row = {"avg_us": avg * 1e3, "launches": cnt}
+        if kind in gemms:
+            N, K, ob = gemms[kind]
+            out_bytes = n * (F * 2 if ob is None else N * ob)
+            byts = N * K * 2 + n * K * 2 + out_bytes
+            flops = 2.0 * n * N * K
+            row.update({"GB_s": byts / (avg * 1e-3) / 1e9,
+                        "hbm_frac": byts / (avg * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                        "TFLOP_s": flops / (avg * 1e-3) / 1e12,
+                        "mfma_frac": flops / (avg * 1e-3) / 1e12 / BF16_PEAK_TFLOPS})
+        elif kind == "attn_split":
+            row["GB_s"] = attn_bytes / (avg * 1e-3) / 1e9
+        table[kind] = row
+    return table
+
+
 def measured_traffic(workload):
     """HBM bytes per attention launch from the rocprofv3 FETCH_SIZE / WRITE_SIZE
     passes (copy-kernel calibrated) recorded under profiles/, or None when they
@@ -188,7 +216,7 @@ def main():
     torch.cuda.synchronize()
     log("warmup done")
 
-    sevo.sevo_profile_begin(shape.n_layers * args.steps)
+    sevo.sevo_profile_begin(shape.n_layers * args.steps, ("attn_split", "attn_combine"))
     start = torch.cuda.Event(enable_timing=True)
     stop = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -198,8 +226,18 @@ def main():
     stop.record()
     torch.cuda.synchronize()
     total_ms = start.elapsed_time(stop)
-    split_ms, attn_ms, launches = sevo.sevo_profile_end()
+    prof = sevo.sevo_profile_end()
+    split_ms, launches = prof["attn_split"]
+    attn_ms = split_ms + prof["attn_combine"][0]
     ms_per_step = total_ms / args.steps
+
+    # per-kernel breakdown: two more steps with every launch of the step timed
+    # (outside the timed region: the extra event records cost a little time)
+    sevo.sevo_profile_begin(400 * 2, sevo.PROF_KINDS)
+    for _ in range(2):
+        step()
+    torch.cuda.synchronize()
+    kprof = sevo.sevo_profile_end()
     log(f"{args.steps} steps: {ms_per_step:.3f} ms/step; attention launches {launches}")
 
     # algorithmic bytes of the timed attention launches (lengths grow by one per step)
@@ -244,6 +282,7 @@ def main():
                           "frac": step_bytes / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS,
                           "attention_ms_per_step": attn_ms / args.steps},
     }
+    out["kernels"] = kernel_table(shape, pop.n, kprof, attn_bytes_per_launch)
     if not args.no_cpu_baseline:
         log("timing the oracle on a bounded sample (host cores)")
         out["cpu_baseline"] = cpu_baseline(w, pop, args.cpu_sample)

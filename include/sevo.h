@@ -352,15 +352,28 @@ sevo_status sevo_validate_paging(const int32_t* page_table, const int32_t* lengt
                                  int32_t max_pages, int64_t num_pages, void* stream);
 
 /* ------------------------------------------------------------------ timing
- * Measurement aid: while a recording is open, every attention launch (from
- * sevo_attn_decode or inside sevo_decode_step) is bracketed by HIP events on
- * the stream it runs on: before the split kernel, between the split and the
- * combine kernel, and after the combine.  Process-wide; records beyond
- * max_records are not timed.  sevo_profile_end waits for the recorded events
- * and returns the summed split-kernel time, the summed split + combine time
- * (milliseconds) and the number of timed launches. */
-sevo_status sevo_profile_begin(int32_t max_records);
-sevo_status sevo_profile_end(float* split_ms, float* attention_ms, int32_t* records);
+ * Measurement aid: while a recording is open, the launches of the selected
+ * kinds (inside sevo_decode_step; the attention kinds also in
+ * sevo_attn_decode) are bracketed by HIP events on the stream they run on.
+ * Process-wide; launches beyond max_launches are not timed; one recording at a
+ * time.  kinds is a mask of (1u << SEVO_PROF_*).  sevo_profile_end waits for
+ * the recorded events and returns, per kind, the summed milliseconds and the
+ * number of timed launches (arrays of SEVO_PROF_NUM_KINDS entries; either may
+ * be NULL).  Recording adds two event records per timed launch. */
+#define SEVO_PROF_ATTN_SPLIT 0    /* split-KV attention kernel           */
+#define SEVO_PROF_ATTN_COMBINE 1  /* cross-split combine                 */
+#define SEVO_PROF_QKV 2           /* QKV projection                      */
+#define SEVO_PROF_ATTN_OUT 3      /* output projection                   */
+#define SEVO_PROF_GATE_UP 4       /* gate/up projection + SwiGLU         */
+#define SEVO_PROF_DOWN 5          /* down projection                     */
+#define SEVO_PROF_LM_HEAD 6       /* LM head                             */
+#define SEVO_PROF_NORM 7          /* residual add + RMSNorm              */
+#define SEVO_PROF_ROPE_APPEND 8   /* QK-norm + RoPE + KV append          */
+#define SEVO_PROF_SAMPLE 9        /* log-softmax + Gumbel-max (+ confidence) */
+#define SEVO_PROF_EMBED 10        /* embedding gather                    */
+#define SEVO_PROF_NUM_KINDS 11
+sevo_status sevo_profile_begin(int32_t max_launches, uint32_t kinds);
+sevo_status sevo_profile_end(float* total_ms, int32_t* launches);
 
 #ifdef __cplusplus
 }

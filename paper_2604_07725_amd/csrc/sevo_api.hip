@@ -93,24 +93,60 @@ sevo_status check_attn_shape(int n, int hq, int hkv, int d, int page_size, int m
   return SEVO_OK;
 }
 
-// Attention timing: events bracketing each attention launch (see
-// sevo_profile_begin).  Process-wide, guarded by a mutex.
-struct AttnProfiler {
+// Kernel timing (see sevo_profile_begin): HIP events recorded on the launch
+// stream around the launches of the selected kinds.  Process-wide, guarded by
+// a mutex; events come from a pool created by sevo_profile_begin.
+struct ProfRecord {
+  int kind;
+  hipEvent_t b, e;
+};
+struct Profiler {
   std::mutex mu;
   bool on = false;
-  int n = 0;
-  std::vector<hipEvent_t> ev;  // 3 per record: begin, mid, end
-  int cap() const { return (int)ev.size() / 3; }
+  uint32_t mask = 0;
+  std::vector<hipEvent_t> pool;
+  size_t used = 0;
+  std::vector<ProfRecord> recs;
+  bool want(int kind) const { return on && ((mask >> kind) & 1u); }
+  hipEvent_t take() { return used < pool.size() ? pool[used++] : nullptr; }
 } g_prof;
 
 void attach_profiler(sevo::AttnArgs& a) {
   std::lock_guard<std::mutex> lk(g_prof.mu);
-  if (!g_prof.on || g_prof.n >= g_prof.cap()) return;
-  a.ev_begin = g_prof.ev[3 * g_prof.n];
-  a.ev_mid = g_prof.ev[3 * g_prof.n + 1];
-  a.ev_end = g_prof.ev[3 * g_prof.n + 2];
-  ++g_prof.n;
+  const bool ws = g_prof.want(SEVO_PROF_ATTN_SPLIT), wc = g_prof.want(SEVO_PROF_ATTN_COMBINE);
+  if (!ws && !wc) return;
+  if (g_prof.used + 3 > g_prof.pool.size()) return;
+  a.ev_begin = g_prof.take();
+  a.ev_mid = g_prof.take();
+  a.ev_end = g_prof.take();
+  if (ws) g_prof.recs.push_back({SEVO_PROF_ATTN_SPLIT, a.ev_begin, a.ev_mid});
+  if (wc) g_prof.recs.push_back({SEVO_PROF_ATTN_COMBINE, a.ev_mid, a.ev_end});
 }
+
+// Brackets one launch (or a few) of the given kind on stream st.
+class ProfScope {
+ public:
+  ProfScope(int kind, hipStream_t st) : kind_(kind), st_(st) {
+    std::lock_guard<std::mutex> lk(g_prof.mu);
+    if (!g_prof.want(kind) || g_prof.used + 2 > g_prof.pool.size()) return;
+    b_ = g_prof.take();
+    e_ = g_prof.take();
+    (void)hipEventRecord(b_, st_);
+  }
+  ~ProfScope() {
+    if (!b_) return;
+    (void)hipEventRecord(e_, st_);
+    std::lock_guard<std::mutex> lk(g_prof.mu);
+    g_prof.recs.push_back({kind_, b_, e_});
+  }
+  ProfScope(const ProfScope&) = delete;
+  ProfScope& operator=(const ProfScope&) = delete;
+
+ private:
+  int kind_;
+  hipStream_t st_;
+  hipEvent_t b_ = nullptr, e_ = nullptr;
+};
 
 }  // namespace
 
@@ -581,19 +617,29 @@ SEVO_API sevo_status sevo_decode_step(sevo_model* m, const sevo_step_args* a, vo
   // Split-K partials of a projection are summed (in split order) by the
   // kernel that consumes them: QKV by the QK-norm / RoPE / append kernel, the
   // output and down projections by the next residual add + RMSNorm.
-  hipError_t e = sevo::launch_embed(static_cast<const sevo::bf16_t*>(m->embed), a->tokens, n, H,
-                                    c.vocab, x, st);
+  hipError_t e;
+  {
+    ProfScope ps(SEVO_PROF_EMBED, st);
+    e = sevo::launch_embed(static_cast<const sevo::bf16_t*>(m->embed), a->tokens, n, H, c.vocab,
+                           x, st);
+  }
   if (e != hipSuccess) return hip_fail(e, "embed");
   int pending = 0;  // split partials of the last down projection, not yet in x
   for (int l = 0; l < c.n_layers; ++l) {
-    e = sevo::launch_add_rmsnorm(x, pending ? part_x : nullptr, pending,
-                                 static_cast<const sevo::bf16_t*>(m->attn_norm[l]), n, H,
-                                 c.rms_eps, h, st);
-    if (e == hipSuccess)
+    {
+      ProfScope ps(SEVO_PROF_NORM, st);
+      e = sevo::launch_add_rmsnorm(x, pending ? part_x : nullptr, pending,
+                                   static_cast<const sevo::bf16_t*>(m->attn_norm[l]), n, H,
+                                   c.rms_eps, h, st);
+    }
+    if (e == hipSuccess) {
+      ProfScope ps(SEVO_PROF_QKV, st);
       e = sevo::launch_linear_partials(n, qkvd, H, H, 1, L.p_qkv, h,
                                        static_cast<const sevo::bf16_t*>(m->w_qkv[l]), part_qkv, 0,
                                        st);
+    }
     if (e == hipSuccess) {
+      ProfScope ps(SEVO_PROF_ROPE_APPEND, st);
       sevo::RopeAppendArgs r;
       fill_rope_args(m, l, part_qkv, L.p_qkv.k_splits, n, a->positions, a->page_table,
                      a->max_pages, a->num_pages, q, a->k_pools[l], a->v_pools[l], r);
@@ -620,33 +666,49 @@ SEVO_API sevo_status sevo_decode_step(sevo_model* m, const sevo_step_args* a, vo
         attn_ws_ptr + round_up((size_t)n * c.n_q_heads * L.S * 2 * sizeof(float), 256));
     attach_profiler(aa);
     e = sevo::launch_attn_decode(aa, st);
-    if (e == hipSuccess)
+    if (e == hipSuccess) {
+      ProfScope ps(SEVO_PROF_ATTN_OUT, st);
       e = sevo::launch_linear_partials(n, H, qd, qd, 1, L.p_o, o,
                                        static_cast<const sevo::bf16_t*>(m->w_o[l]), part_x, 0, st);
-    if (e == hipSuccess)
+    }
+    if (e == hipSuccess) {
+      ProfScope ps(SEVO_PROF_NORM, st);
       e = sevo::launch_add_rmsnorm(x, part_x, L.p_o.k_splits,
                                    static_cast<const sevo::bf16_t*>(m->ffn_norm[l]), n, H,
                                    c.rms_eps, h, st);
-    if (e == hipSuccess)
+    }
+    if (e == hipSuccess) {
+      ProfScope ps(SEVO_PROF_GATE_UP, st);
       e = sevo::launch_linear(n, 2 * F, H, H, 1, SEVO_LINEAR_SWIGLU, L.p_gu, h,
                               static_cast<const sevo::bf16_t*>(m->w_gate_up[l]), act, 1, nullptr,
                               st);
-    if (e == hipSuccess)
+    }
+    if (e == hipSuccess) {
+      ProfScope ps(SEVO_PROF_DOWN, st);
       e = sevo::launch_linear_partials(n, H, F, F, 1, L.p_d, act,
                                        static_cast<const sevo::bf16_t*>(m->w_down[l]), part_x, 0,
                                        st);
+    }
     pending = L.p_d.k_splits;
     if (e != hipSuccess) return hip_fail(e, "decode step (layer)");
   }
-  e = sevo::launch_add_rmsnorm(x, part_x, pending, static_cast<const sevo::bf16_t*>(m->final_norm),
-                               n, H, c.rms_eps, h, st);
-  if (e == hipSuccess)
+  {
+    ProfScope ps(SEVO_PROF_NORM, st);
+    e = sevo::launch_add_rmsnorm(x, part_x, pending,
+                                 static_cast<const sevo::bf16_t*>(m->final_norm), n, H, c.rms_eps,
+                                 h, st);
+  }
+  if (e == hipSuccess) {
+    ProfScope ps(SEVO_PROF_LM_HEAD, st);
     e = sevo::launch_linear_partials(n, c.vocab, H, H, 1, L.p_lm, h,
                                      static_cast<const sevo::bf16_t*>(m->lm_head), logits, 0, st);
-  if (e == hipSuccess)
+  }
+  if (e == hipSuccess) {
+    ProfScope ps(SEVO_PROF_SAMPLE, st);
     e = sevo::launch_logprob_sample(logits, n, c.vocab, c.vocab, a->temperature, a->seed,
                                     a->cand_uid, a->positions, a->out_tokens, a->out_logprobs,
                                     smp, a->conf_topk, a->out_conf, a->conf_sum, st);
+  }
   if (e != hipSuccess) return hip_fail(e, "decode step (head / sampler)");
   return SEVO_OK;
 }
@@ -699,40 +761,48 @@ SEVO_API sevo_status sevo_validate_paging(const int32_t* page_table, const int32
 }
 
 // ------------------------------------------------------------------ timing
-SEVO_API sevo_status sevo_profile_begin(int32_t max_records) {
-  if (max_records < 1 || max_records > (1 << 20))
-    return fail(SEVO_ERR_INVALID_ARGUMENT, "max_records must be in [1, 2^20]");
+SEVO_API sevo_status sevo_profile_begin(int32_t max_launches, uint32_t kinds) {
+  if (max_launches < 1 || max_launches > (1 << 20))
+    return fail(SEVO_ERR_INVALID_ARGUMENT, "max_launches must be in [1, 2^20]");
+  if (kinds == 0 || (kinds >> SEVO_PROF_NUM_KINDS) != 0)
+    return fail(SEVO_ERR_INVALID_ARGUMENT, "bad kinds mask 0x%x", kinds);
   std::lock_guard<std::mutex> lk(g_prof.mu);
+  if (g_prof.on) return fail(SEVO_ERR_INVALID_ARGUMENT, "a recording is already open");
   try {
-    while ((int)g_prof.ev.size() < 3 * max_records) {
+    while (g_prof.pool.size() < (size_t)3 * max_launches) {
       hipEvent_t e;
       hipError_t r = hipEventCreate(&e);
       if (r != hipSuccess) return hip_fail(r, "sevo_profile_begin");
-      g_prof.ev.push_back(e);
+      g_prof.pool.push_back(e);
     }
+    g_prof.recs.clear();
+    g_prof.recs.reserve((size_t)max_launches * 2);
   } catch (...) {
     return fail(SEVO_ERR_OUT_OF_MEMORY, "sevo_profile_begin");
   }
-  g_prof.n = 0;
+  g_prof.used = 0;
+  g_prof.mask = kinds;
   g_prof.on = true;
   return SEVO_OK;
 }
 
-SEVO_API sevo_status sevo_profile_end(float* split_ms, float* attention_ms, int32_t* records) {
+SEVO_API sevo_status sevo_profile_end(float* total_ms, int32_t* launches) {
   std::lock_guard<std::mutex> lk(g_prof.mu);
   g_prof.on = false;
-  float a = 0.f, b = 0.f;
-  for (int r = 0; r < g_prof.n; ++r) {
-    hipError_t e = hipEventSynchronize(g_prof.ev[3 * r + 2]);
-    float t1 = 0.f, t2 = 0.f;
-    if (e == hipSuccess) e = hipEventElapsedTime(&t1, g_prof.ev[3 * r], g_prof.ev[3 * r + 1]);
-    if (e == hipSuccess) e = hipEventElapsedTime(&t2, g_prof.ev[3 * r], g_prof.ev[3 * r + 2]);
+  float ms[SEVO_PROF_NUM_KINDS] = {};
+  int32_t cnt[SEVO_PROF_NUM_KINDS] = {};
+  for (const ProfRecord& r : g_prof.recs) {
+    hipError_t e = hipEventSynchronize(r.e);
+    float t = 0.f;
+    if (e == hipSuccess) e = hipEventElapsedTime(&t, r.b, r.e);
     if (e != hipSuccess) return hip_fail(e, "sevo_profile_end");
-    a += t1;
-    b += t2;
+    ms[r.kind] += t;
+    ++cnt[r.kind];
   }
-  if (split_ms) *split_ms = a;
-  if (attention_ms) *attention_ms = b;
-  if (records) *records = g_prof.n;
+  g_prof.recs.clear();
+  for (int k = 0; k < SEVO_PROF_NUM_KINDS; ++k) {
+    if (total_ms) total_ms[k] = ms[k];
+    if (launches) launches[k] = cnt[k];
+  }
   return SEVO_OK;
 }

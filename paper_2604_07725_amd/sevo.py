@@ -26,6 +26,8 @@ PACK_PLAIN, PACK_GATE_UP = 0, 1
 PACKED_WEIGHTS = {"w_qkv": PACK_PLAIN, "w_o": PACK_PLAIN, "w_gate_up": PACK_GATE_UP,
                   "w_down": PACK_PLAIN, "lm_head": PACK_PLAIN}
 PAGE_SIZE = 16
+PROF_KINDS = ["attn_split", "attn_combine", "qkv", "attn_out", "gate_up", "down", "lm_head",
+              "norm", "rope_append", "sample", "embed"]   # SEVO_PROF_* order
 
 vp = C.c_void_p
 i32 = C.c_int32
@@ -99,8 +101,8 @@ _SIGS = {
     "sevo_qk_norm_rope_append": ([vp, i32, vp, i32, vp, vp, i32, i64, vp, vp, vp, vp], i32),
     "sevo_fill_normal_bf16": ([vp, i64, u64, i64, f32, f32, i32, vp], i32),
     "sevo_validate_paging": ([vp, vp, i32, i32, i64, vp], i32),
-    "sevo_profile_begin": ([i32], i32),
-    "sevo_profile_end": ([C.POINTER(f32), C.POINTER(f32), C.POINTER(i32)], i32),
+    "sevo_profile_begin": ([i32, C.c_uint32], i32),
+    "sevo_profile_end": ([C.POINTER(f32), C.POINTER(i32)], i32),
 }
 
 _lib = None
@@ -320,15 +322,21 @@ def sevo_validate_paging(page_table, lengths, num_pages, stream=None):
                                       _stream(stream)))
 
 
-def sevo_profile_begin(max_records: int) -> None:
-    _check(lib().sevo_profile_begin(int(max_records)))
+def sevo_profile_begin(max_launches: int, kinds=("attn_split", "attn_combine")) -> None:
+    """Open a recording that times the launches of the named kinds (PROF_KINDS)."""
+    mask = 0
+    for k in kinds:
+        mask |= 1 << PROF_KINDS.index(k)
+    _check(lib().sevo_profile_begin(int(max_launches), mask))
 
 
-def sevo_profile_end():
-    """(split-kernel ms, split + combine ms, launches) summed over the recording."""
-    a, b, n = f32(), f32(), i32()
-    _check(lib().sevo_profile_end(C.byref(a), C.byref(b), C.byref(n)))
-    return a.value, b.value, n.value
+def sevo_profile_end() -> dict:
+    """{kind: (summed ms, launches)} of the recording, for kinds with launches."""
+    n = len(PROF_KINDS)
+    ms = (f32 * n)()
+    cnt = (i32 * n)()
+    _check(lib().sevo_profile_end(ms, cnt))
+    return {k: (ms[i], cnt[i]) for i, k in enumerate(PROF_KINDS) if cnt[i]}
 
 
 # ------------------------------------------------------------------ model + step

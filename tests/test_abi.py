@@ -215,3 +215,15 @@ def test_group_confidence_rejects_bad_arguments():
     assert L.sevo_group_confidence(f, f, f, 3, 0, f, None) == sevo.INVALID_ARGUMENT
     assert L.sevo_group_confidence(None, f, f, 3, 4, f, None) == sevo.INVALID_ARGUMENT
     assert L.sevo_group_confidence(None, None, None, 0, 4, None, None) == sevo.OK
+
+
+def test_profile_begin_rejects_bad_arguments():
+    L = sevo.lib()
+    assert L.sevo_profile_begin(0, 1) == sevo.INVALID_ARGUMENT
+    assert L.sevo_profile_begin(8, 0) == sevo.INVALID_ARGUMENT
+    assert L.sevo_profile_begin(8, 1 << 11) == sevo.INVALID_ARGUMENT
+    # ending without a recording returns empty totals
+    import ctypes as CT
+    ms = (CT.c_float * 11)()
+    cnt = (CT.c_int32 * 11)()
+    assert L.sevo_profile_end(ms, cnt) == sevo.OK and sum(cnt) == 0

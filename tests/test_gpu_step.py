@@ -242,3 +242,26 @@ def test_full_width_step_reduced_depth(S, workload, layers):
             z = ref["logits"][j] / temp + od.gumbel_noise(shape.vocab, int(pop.lengths[i]),
                                                            int(pop.uids[i]), seed)
             assert z.max() - z[g_ids[j]] <= FULL_GAP_EXACT
+
+
+def test_step_kernel_timing_counts_every_launch(S):
+    """The per-kind timing records one launch of each kind where the step makes
+    one (per layer or per step) and positive times."""
+    sevo, di = S
+    w = synth.WORKLOADS["tiny_step"]
+    say("step kernel timing")
+    pop, model, kp, vp, d = _setup(S, w, extra=2)
+    toks = torch.from_numpy(pop.tokens).cuda()
+    L = w.shape.n_layers
+    sevo.sevo_profile_begin(64, sevo.PROF_KINDS)
+    sevo.sevo_decode_step(model, toks, d["lengths"], d["page_table"], kp, vp, d["uids"], 5, 1.0)
+    prof = sevo.sevo_profile_end()
+    want = {"attn_split": L, "attn_combine": L, "qkv": L, "attn_out": L, "gate_up": L, "down": L,
+            "lm_head": 1, "norm": 2 * L + 1, "rope_append": L, "sample": 1, "embed": 1}
+    assert {k: c for k, (ms, c) in prof.items()} == want
+    assert all(ms > 0 for ms, c in prof.values())
+    # a recording of one kind times only that kind
+    sevo.sevo_profile_begin(8, ["lm_head"])
+    sevo.sevo_decode_step(model, toks, d["lengths"], d["page_table"], kp, vp, d["uids"], 5, 1.0)
+    assert list(sevo.sevo_profile_end()) == ["lm_head"]
+    model.close()
