@@ -153,6 +153,10 @@ def main():
     ap.add_argument("--num-splits", type=int, default=0)
     ap.add_argument("--cpu-sample", type=int, default=8)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--temperature", type=float, default=1.0)
+    ap.add_argument("--top-k", type=int, default=0, help="0 = full-vocabulary sampling")
+    ap.add_argument("--top-p", type=float, default=1.0)
+    ap.add_argument("--min-p", type=float, default=0.0)
     ap.add_argument("--conf-topk", type=int, default=0,
                     help="also compute the per-token self-confidence (top-K log-probs) each step")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -203,8 +207,10 @@ def main():
     positions = d["lengths"].clone()
     conf_sum = torch.zeros(pop.n, dtype=torch.float32, device=dev) if args.conf_topk else None
     buf = sevo.StepBuffers(model, tokens, positions, d["page_table"], kp, vp, d["uids"],
-                           seed=20260412, temperature=1.0, num_splits=args.num_splits,
-                           conf_topk=args.conf_topk, conf_sum=conf_sum)
+                           seed=20260412, temperature=args.temperature,
+                           num_splits=args.num_splits, conf_topk=args.conf_topk,
+                           conf_sum=conf_sum, top_k=args.top_k, top_p=args.top_p,
+                           min_p=args.min_p)
 
     def step():
         ids, _ = buf.run()
@@ -266,6 +272,9 @@ def main():
                    "page_size": 16, "parallelism": "none (1 GPU)",
                    "num_splits": int(buf.args.num_splits) or
                    sevo.sevo_attn_plan_splits(pop.n, shape.n_kv_heads, pop.max_pages),
+                   "temperature": args.temperature,
+                   "sampling": ("full vocabulary" if args.top_k == 0 else
+                                f"top-k {args.top_k}, top-p {args.top_p}, min-p {args.min_p}"),
                    "self_confidence_topk": args.conf_topk},
         "roofline": {"kernel": "attn_split_kernel<128,4> (paged split-KV GQA attention)",
                      "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,

@@ -184,6 +184,17 @@ size_t sevo_attn_workspace_bytes(int32_t n, int32_t n_q_heads, int32_t n_kv_head
  * under T = 1.  T < 0 or non-finite: INVALID_ARGUMENT.
  *   logits fp32 [n][ld] (first vocab entries used); cand_uid uint64 [n];
  *   positions int32 [n];  out_tokens int32 [n];  out_logprobs fp32 [n].
+ * Truncated sampling (the top-k / top-p / min-p rows of the generation
+ * hyper-parameter table), active when top_k > 0 (1..32, at most vocab):
+ *   kept = the top_k logits in (value desc, index asc) order -- temperature
+ *   does not change the set; with z = logit / T over it, min-p keeps
+ *   z_j >= z_0 + log(min_p) (min_p in [0, 1], 0 = off), then top-p keeps, in
+ *   that order, each entry whose preceding cumulative probability
+ *   (renormalised over the min-p set) is below top_p (top_p in (0, 1], 1 = off);
+ *   id = argmax over kept of (z_v + G_v) with the noise above;
+ *   logprob = z_id - logsumexp(kept z), the distribution that is sampled.
+ *   T == 0: the first entry; truncation and logprob evaluated at T = 1.
+ *   top_k == 0 needs top_p == 1 and min_p == 0 (UNSUPPORTED otherwise).
  * Self-confidence (the group-confidence fitness signal, Eq. 1), computed in
  * the same passes when conf_topk > 0 (1..32, and at most vocab):
  *   c_i = -(1/K) * sum of the K largest log_softmax(logits[i]) entries
@@ -191,8 +202,8 @@ size_t sevo_attn_workspace_bytes(int32_t n, int32_t n_q_heads, int32_t n_kv_head
  * under the model's own distribution (T = 1) whatever the sampling T.
  *   out_conf fp32 [n] (nullable) receives c_i; conf_sum fp32 [n] (nullable) gets
  *   c_i added (a running sum over a trajectory's tokens: C = conf_sum / tokens).
- * Errors: INVALID_ARGUMENT, UNSUPPORTED (conf_topk * ceil(vocab / 4096) > 6144),
- * WORKSPACE_TOO_SMALL, HIP. */
+ * Errors: INVALID_ARGUMENT, UNSUPPORTED (max(top_k, conf_topk) * ceil(vocab /
+ * 4096) > 6144; top_p / min_p without top_k), WORKSPACE_TOO_SMALL, HIP. */
 typedef struct {
   const float* logits;
   int32_t n, vocab;
@@ -203,6 +214,9 @@ typedef struct {
   const int32_t* positions;
   int32_t* out_tokens;
   float* out_logprobs;
+  int32_t top_k;     /* 0 = full vocabulary */
+  float top_p;       /* 1 = off */
+  float min_p;       /* 0 = off */
   int32_t conf_topk; /* 0 = no confidence */
   float* out_conf;
   float* conf_sum;
@@ -240,7 +254,8 @@ sevo_status sevo_group_confidence(const float* conf_sum, const int32_t* token_co
  *   n_layers device pool pointers;  cand_uid uint64 [n];
  *   out_tokens int32 [n];  out_logprobs fp32 [n];
  *   out_logits fp32 [n][vocab] or NULL (then kept in the workspace);
- *   conf_topk, out_conf, conf_sum: the sampler's self-confidence (above).
+ *   top_k, top_p, min_p: truncated sampling; conf_topk, out_conf, conf_sum:
+ *   the sampler's self-confidence (both above).
  * The library never changes positions or page tables: the caller advances p_i
  * and allocates pages.  Errors: INVALID_ARGUMENT, UNSUPPORTED,
  * WORKSPACE_TOO_SMALL, HIP. */
@@ -260,6 +275,9 @@ typedef struct {
   int32_t* out_tokens;
   float* out_logprobs;
   float* out_logits;
+  int32_t top_k;
+  float top_p;
+  float min_p;
   int32_t conf_topk;
   float* out_conf;
   float* conf_sum;

@@ -308,3 +308,58 @@ def group_confidence(cand_conf, groups):
     groups [M, K] holds candidate indices."""
     cand_conf = np.asarray(cand_conf, np.float64)
     return cand_conf[np.asarray(groups, np.int64)].mean(axis=-1)
+
+
+def truncated_logprob_sample(logits, temperature, seed, uids, positions, top_k, top_p=1.0,
+                             min_p=0.0, decision_dtype=np.float32):
+    """Top-k sampling with min-p and top-p applied inside the top-k set.
+
+    The kept list is the top_k logits in (value desc, index asc) order -- a
+    temperature does not change it.  With z = logit / T on that list, min-p
+    keeps z_j >= z_0 + log(min_p) (a probability at least min_p times the
+    largest); top-p then keeps, in list order, each entry whose preceding
+    cumulative probability (renormalised over the min-p set) is below top_p.
+    The token is the Gumbel-max over the kept entries with the same noise as
+    ``logprob_sample``; lp = z_id - logsumexp(kept z).  T == 0 takes the first
+    entry and evaluates the truncation and lp at T = 1.  Decisions in
+    ``decision_dtype``; ``gap`` = float64 top-1 minus top-2 perturbed value
+    among the kept entries (inf when one is kept).
+    Returns ids int64 [N], lps float64 [N], gaps float64 [N].
+    """
+    logits = np.asarray(logits, np.float64)
+    N, V = logits.shape
+    tdiv = 1.0 if temperature == 0 else float(temperature)
+    ids = np.empty(N, np.int64)
+    lps = np.empty(N)
+    gaps = np.empty(N)
+    for i in range(N):
+        order = np.lexsort((np.arange(V), -logits[i]))[:int(top_k)]
+        z = logits[i][order] / tdiv
+        keep = np.ones(len(order), bool)
+        if min_p > 0:
+            keep &= z - z[0] >= np.log(min_p)
+        if top_p < 1:
+            p = np.exp(z - z[0]) * keep
+            tot = p.sum()
+            cum = 0.0
+            for j in range(len(order)):
+                if not keep[j]:
+                    continue
+                if cum < top_p * tot:
+                    cum += p[j]
+                else:
+                    keep[j] = False
+        kz, kv = z[keep], order[keep]
+        if temperature == 0:
+            pert = kz
+            pert_dec = kz.astype(decision_dtype)
+        else:
+            G = gumbel_noise(V, int(positions[i]), int(uids[i]), int(seed))[kv]
+            pert = kz + G
+            pert_dec = kz.astype(decision_dtype) + G.astype(decision_dtype)
+        best = np.lexsort((kv, -pert_dec.astype(np.float64)))[0]   # ties -> lowest vocab index
+        ids[i] = int(kv[best])
+        srt = np.sort(pert)[::-1]
+        gaps[i] = float(srt[0] - srt[1]) if len(srt) > 1 else np.inf
+        lps[i] = kz[best] - (kz.max() + np.log(np.sum(np.exp(kz - kz.max()))))
+    return ids, lps, gaps

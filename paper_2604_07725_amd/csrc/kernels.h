@@ -90,12 +90,15 @@ hipError_t launch_pack_weight(const bf16_t* src, bf16_t* dst, int n_out, int k, 
 constexpr int kSampleChunk = 4096;  // vocab entries per partial workgroup
 size_t sample_workspace_bytes(int n, int vocab);
 // conf_k > 0: also the per-token confidence (written to out_conf and/or added
-// to conf_sum, either may be null)
+// to conf_sum, either may be null).  top_k > 0: truncated sampling (top-k, then
+// min-p and top-p inside the top-k set).
 hipError_t launch_logprob_sample(const float* logits, int n, int vocab, int64_t ld, float temp,
                                  uint64_t seed, const uint64_t* uid, const int32_t* positions,
                                  int32_t* out_tokens, float* out_lp, float* workspace,
-                                 int conf_k, float* out_conf, float* conf_sum, hipStream_t st);
-bool sample_conf_supported(int vocab, int conf_k);
+                                 int conf_k, float* out_conf, float* conf_sum, hipStream_t st,
+                                 int top_k = 0, float top_p = 1.f, float min_p = 0.f);
+// a top-k / confidence list of list_len entries fits the chunk merge
+bool sample_conf_supported(int vocab, int list_len);
 hipError_t launch_group_confidence(const float* conf_sum, const int32_t* counts,
                                    const int32_t* groups, int n_groups, int K, float* out,
                                    hipStream_t st);

@@ -322,30 +322,281 @@ __global__ __launch_bounds__(256) void group_confidence_kernel(
   out[g] = a / (float)K;
 }
 
+// ---- truncated sampling (top-k, then min-p and top-p inside the top-k set)
+//
+// The kept set is the top_k logits in (value desc, vocab index asc) order --
+// temperature does not change it.  With z = logit / T over that set, min-p
+// keeps z_j >= z_0 + log(min_p); top-p keeps, in list order, the entries whose
+// preceding cumulative probability (renormalised over the min-p set) is below
+// top_p.  The token is the Gumbel-max over the kept entries (same Philox noise
+// as the full sampler), lp = z_id - logsumexp(kept z).  T = 0: the first entry,
+// with the truncation and lp evaluated at T = 1.
+__device__ __forceinline__ bool pair_before(float a, int ia, float b, int ib) {
+  return a > b || (a == b && ia < ib);
+}
+
+// The K first (value, index) pairs of a wave in pair_before order (NV per
+// lane; empty = (-inf, INT_MAX)), written by lane 0 to out_v / out_i.
+template <int NV>
+__device__ __forceinline__ void wave_topk_pairs(float (&x)[NV], int (&xi)[NV], int K, float* out_v,
+                                                int* out_i) {
+  const int lane = threadIdx.x & 63;
+  for (int r = 0; r < K; ++r) {
+    float bv = -INFINITY;
+    int bi = 0x7FFFFFFF;
+#pragma unroll
+    for (int e = 0; e < NV; ++e)
+      if (pair_before(x[e], xi[e], bv, bi)) {
+        bv = x[e];
+        bi = xi[e];
+      }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      const float ov = __shfl_xor(bv, o, kWave);
+      const int oi = __shfl_xor(bi, o, kWave);
+      if (pair_before(ov, oi, bv, bi)) {
+        bv = ov;
+        bi = oi;
+      }
+    }
+    // vocab indices are unique: exactly one slot holds a real winner
+#pragma unroll
+    for (int e = 0; e < NV; ++e)
+      if (xi[e] == bi && x[e] == bv) {
+        x[e] = -INFINITY;
+        xi[e] = 0x7FFFFFFF;
+      }
+    if (lane == 0) {
+      out_v[r] = bv;
+      out_i[r] = bi;
+    }
+  }
+}
+
+__global__ __launch_bounds__(256) void sample_trunc_partial_kernel(
+    const float* __restrict__ logits, int vocab, int64_t ld, int L, SamplePartial* __restrict__ part,
+    float* __restrict__ topv, int* __restrict__ topi) {
+  __shared__ SamplePartial red[4];
+  __shared__ float wv[4][kConfMaxK];
+  __shared__ int wi[4][kConfMaxK];
+  const int chunk = blockIdx.x;
+  const int i = blockIdx.y;
+  const float* row = logits + (size_t)i * ld;
+  float x[16];
+  int xi[16];
+  float m1 = -INFINITY;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int v0 = (chunk * (kSampleChunk / 4) + r * 256 + threadIdx.x) * 4;
+    float4 lv;
+    if (v0 + 3 < vocab) {
+      lv = *reinterpret_cast<const float4*>(row + v0);
+    } else {
+      lv.x = v0 + 0 < vocab ? row[v0 + 0] : -INFINITY;
+      lv.y = v0 + 1 < vocab ? row[v0 + 1] : -INFINITY;
+      lv.z = v0 + 2 < vocab ? row[v0 + 2] : -INFINITY;
+      lv.w = v0 + 3 < vocab ? row[v0 + 3] : -INFINITY;
+    }
+    const float vals[4] = {lv.x, lv.y, lv.z, lv.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      x[r * 4 + e] = vals[e];
+      xi[r * 4 + e] = v0 + e < vocab ? v0 + e : 0x7FFFFFFF;
+      m1 = fmaxf(m1, vals[e]);
+    }
+  }
+  float s1 = 0.f;
+  if (m1 != -INFINITY) {
+#pragma unroll
+    for (int e = 0; e < 16; ++e) s1 += (x[e] == -INFINITY) ? 0.f : expf(x[e] - m1);
+  }
+  SamplePartial p{m1, s1, -INFINITY, 0x7FFFFFFF, m1, s1};
+  p = block_merge<4>(p, red);
+  if (threadIdx.x == 0) part[(size_t)i * gridDim.x + chunk] = p;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  wave_topk_pairs<16>(x, xi, L, wv[wave], wi[wave]);
+  __syncthreads();
+  if (wave == 0) {
+    float x2[2];
+    int i2[2];
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+      const int q = lane * 2 + e;
+      const int w = q / kConfMaxK, r = q - w * kConfMaxK;
+      const bool ok = w < 4 && r < L;
+      x2[e] = ok ? wv[w][r] : -INFINITY;
+      i2[e] = ok ? wi[w][r] : 0x7FFFFFFF;
+    }
+    const size_t o = ((size_t)i * gridDim.x + chunk) * kConfMaxK;
+    wave_topk_pairs<2>(x2, i2, L, topv + o, topi + o);
+  }
+}
+
+__global__ __launch_bounds__(256) void sample_trunc_final_kernel(
+    const SamplePartial* __restrict__ part, int nchunks, int L, const float* __restrict__ topv,
+    const int* __restrict__ topi, float temp, int top_k, float top_p, float min_p, uint64_t seed,
+    const uint64_t* __restrict__ uid, const int32_t* __restrict__ positions,
+    int32_t* __restrict__ out_tokens, float* __restrict__ out_lp, int conf_k,
+    float* __restrict__ out_conf, float* __restrict__ conf_sum) {
+  __shared__ SamplePartial red[4];
+  __shared__ float wv[4][kConfMaxK];
+  __shared__ int wi[4][kConfMaxK];
+  __shared__ float fv[kConfMaxK];
+  __shared__ int fi[kConfMaxK];
+  __shared__ int keep[kConfMaxK];
+  const int i = blockIdx.x;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  // logsumexp of the raw logits (confidence)
+  SamplePartial p{-INFINITY, 0.f, -INFINITY, 0x7FFFFFFF, -INFINITY, 0.f};
+  for (int c = threadIdx.x; c < nchunks; c += 256) {
+    const SamplePartial o = part[(size_t)i * nchunks + c];
+    lse_merge(p.m1, p.s1, o.m1, o.s1);
+  }
+  p.m = p.m1;
+  p.s = p.s1;
+  p = block_merge<4>(p, red);
+  // merge the chunks' lists: a quarter per wave, then wave 0 merges the four
+  const int total = nchunks * L;
+  const int per = (total + 3) / 4;
+  const size_t base = (size_t)i * nchunks * kConfMaxK;
+  float x[kConfMergeNV];
+  int xi[kConfMergeNV];
+#pragma unroll
+  for (int e = 0; e < kConfMergeNV; ++e) {
+    const int q = wave * per + lane * kConfMergeNV + e;
+    const bool ok = lane * kConfMergeNV + e < per && q < total;
+    const int c = ok ? q / L : 0;
+    x[e] = ok ? topv[base + (size_t)c * kConfMaxK + (q - c * L)] : -INFINITY;
+    xi[e] = ok ? topi[base + (size_t)c * kConfMaxK + (q - c * L)] : 0x7FFFFFFF;
+  }
+  wave_topk_pairs<kConfMergeNV>(x, xi, L, wv[wave], wi[wave]);
+  __syncthreads();
+  if (wave != 0) return;
+  {
+    float x2[2];
+    int i2[2];
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+      const int q = lane * 2 + e;
+      const int w = q / kConfMaxK, r = q - w * kConfMaxK;
+      const bool ok = w < 4 && r < L;
+      x2[e] = ok ? wv[w][r] : -INFINITY;
+      i2[e] = ok ? wi[w][r] : 0x7FFFFFFF;
+    }
+    wave_topk_pairs<2>(x2, i2, L, fv, fi);
+  }
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  const float tdiv = temp == 0.f ? 1.f : temp;  // T = 0: truncation and lp at T = 1
+  if (lane == 0) {
+    // min-p, then top-p in list order over the renormalised min-p set
+    const float z0 = fv[0] / tdiv;
+    float tot = 0.f;
+    for (int j = 0; j < top_k; ++j) {
+      const float d = fv[j] / tdiv - z0;
+      const bool k = !(min_p > 0.f) || d >= logf(min_p);
+      keep[j] = k;
+      if (k) tot += expf(d);
+    }
+    if (top_p < 1.f) {
+      float cum = 0.f;
+      for (int j = 0; j < top_k; ++j) {
+        if (!keep[j]) continue;
+        if (!(cum < top_p * tot)) keep[j] = 0;
+        else cum += expf(fv[j] / tdiv - z0);
+      }
+    }
+  }
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  // Gumbel-max over the kept entries (lane j holds entry j)
+  float pv = -INFINITY, ez = 0.f;
+  int pid = 0x7FFFFFFF;
+  if (lane < top_k && keep[lane]) {
+    const int v = fi[lane];
+    const float z = fv[lane] / tdiv;
+    ez = expf(z - fv[0] / tdiv);
+    float g = 0.f;
+    if (temp != 0.f) {
+      const uint64_t cu = uid[i];
+      const u32x4 w = philox4x32_10(
+          u32x4{(uint32_t)(v >> 2), (uint32_t)positions[i], (uint32_t)cu, (uint32_t)(cu >> 32)},
+          (uint32_t)seed, (uint32_t)(seed >> 32));
+      const uint32_t word = (v & 3) == 0 ? w.x : (v & 3) == 1 ? w.y : (v & 3) == 2 ? w.z : w.w;
+      g = gumbel_from_bits(word);
+    }
+    pv = z + g;
+    pid = v;
+  }
+  float zme = (lane < top_k && keep[lane]) ? fv[lane] / tdiv : -INFINITY;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float ov = __shfl_xor(pv, o, kWave);
+    const int oi = __shfl_xor(pid, o, kWave);
+    const float oz = __shfl_xor(zme, o, kWave);
+    if (pair_before(ov, oi, pv, pid)) {
+      pv = ov;
+      pid = oi;
+      zme = oz;
+    }
+    ez += __shfl_xor(ez, o, kWave);
+  }
+  if (lane == 0) {
+    out_tokens[i] = pid;
+    out_lp[i] = zme - (fv[0] / tdiv + logf(ez));
+    if (conf_k > 0) {
+      float sum = 0.f;
+      for (int r = 0; r < conf_k; ++r) sum += fv[r];
+      const float c = (p.m1 + logf(p.s1)) - sum / (float)conf_k;
+      if (out_conf) out_conf[i] = c;
+      if (conf_sum) conf_sum[i] += c;
+    }
+  }
+}
+
 static size_t partial_bytes(int n, int nchunks) {
   return ((size_t)n * nchunks * sizeof(SamplePartial) + 255) / 256 * 256;
 }
 
-size_t sample_workspace_bytes(int n, int vocab) {
-  const int nchunks = (vocab + kSampleChunk - 1) / kSampleChunk;
-  return partial_bytes(n, nchunks) + (size_t)n * nchunks * kConfMaxK * sizeof(float);
+static size_t list_bytes(int n, int nchunks) {
+  return ((size_t)n * nchunks * kConfMaxK * sizeof(float) + 255) / 256 * 256;
 }
 
-bool sample_conf_supported(int vocab, int conf_k) {
+size_t sample_workspace_bytes(int n, int vocab) {
   const int nchunks = (vocab + kSampleChunk - 1) / kSampleChunk;
-  return conf_k >= 0 && conf_k <= kConfMaxK && conf_k <= vocab &&
-         (size_t)nchunks * conf_k <= (size_t)4 * kWave * kConfMergeNV;
+  return partial_bytes(n, nchunks) + 2 * list_bytes(n, nchunks);
+}
+
+bool sample_conf_supported(int vocab, int list_len) {
+  const int nchunks = (vocab + kSampleChunk - 1) / kSampleChunk;
+  return list_len >= 0 && list_len <= kConfMaxK && list_len <= vocab &&
+         (size_t)nchunks * list_len <= (size_t)4 * kWave * kConfMergeNV;
 }
 
 hipError_t launch_logprob_sample(const float* logits, int n, int vocab, int64_t ld, float temp,
                                  uint64_t seed, const uint64_t* uid, const int32_t* positions,
                                  int32_t* out_tokens, float* out_lp, float* workspace,
-                                 int conf_k, float* out_conf, float* conf_sum, hipStream_t st) {
+                                 int conf_k, float* out_conf, float* conf_sum, hipStream_t st,
+                                 int top_k, float top_p, float min_p) {
   if (n == 0) return hipSuccess;
   const int nchunks = (vocab + kSampleChunk - 1) / kSampleChunk;
   SamplePartial* part = reinterpret_cast<SamplePartial*>(workspace);
-  float* topk = reinterpret_cast<float*>(reinterpret_cast<char*>(workspace) +
-                                         partial_bytes(n, nchunks));
+  char* lists = reinterpret_cast<char*>(workspace) + partial_bytes(n, nchunks);
+  float* topk = reinterpret_cast<float*>(lists);
+  int* topi = reinterpret_cast<int*>(lists + list_bytes(n, nchunks));
+  if (top_k > 0) {
+    const int L = top_k > conf_k ? top_k : conf_k;
+    hipLaunchKernelGGL(sample_trunc_partial_kernel, dim3(nchunks, n), dim3(256), 0, st, logits,
+                       vocab, ld, L, part, topk, topi);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(sample_trunc_final_kernel, dim3(n), dim3(256), 0, st, part, nchunks, L,
+                       topk, topi, temp, top_k, top_p, min_p, seed, uid, positions, out_tokens,
+                       out_lp, conf_k, out_conf, conf_sum);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL(sample_partial_kernel, dim3(nchunks, n), dim3(256), 0, st, logits, vocab, ld,
                      temp, seed, uid, positions, part, conf_k, topk);
   hipError_t e = hipGetLastError();

@@ -337,15 +337,24 @@ SEVO_API size_t sevo_sample_workspace_bytes(int32_t n, int32_t vocab) {
 }
 
 static sevo_status conf_check(int conf_topk, int vocab, const float* out_conf,
-                              const float* conf_sum) {
+                              const float* conf_sum, int top_k, float top_p, float min_p) {
   if (conf_topk < 0 || conf_topk > 32)
     return fail(SEVO_ERR_INVALID_ARGUMENT, "conf_topk %d outside [0, 32]", conf_topk);
   if (conf_topk > vocab)
     return fail(SEVO_ERR_INVALID_ARGUMENT, "conf_topk %d > vocab %d", conf_topk, vocab);
-  if (!sevo::sample_conf_supported(vocab, conf_topk))
-    return fail(SEVO_ERR_UNSUPPORTED, "confidence over a vocabulary of %d entries", vocab);
   if (conf_topk > 0 && !out_conf && !conf_sum)
     return fail(SEVO_ERR_INVALID_ARGUMENT, "conf_topk > 0 needs out_conf or conf_sum");
+  if (top_k < 0 || top_k > 32 || top_k > vocab)
+    return fail(SEVO_ERR_INVALID_ARGUMENT, "top_k %d outside [0, min(32, vocab)]", top_k);
+  if (!(top_p > 0.f && top_p <= 1.f))
+    return fail(SEVO_ERR_INVALID_ARGUMENT, "top_p must be in (0, 1]");
+  if (!(min_p >= 0.f && min_p <= 1.f))
+    return fail(SEVO_ERR_INVALID_ARGUMENT, "min_p must be in [0, 1]");
+  if (top_k == 0 && (top_p < 1.f || min_p > 0.f))
+    return fail(SEVO_ERR_UNSUPPORTED, "top_p / min_p need top_k > 0");
+  const int L = top_k > conf_topk ? top_k : conf_topk;
+  if (!sevo::sample_conf_supported(vocab, L))
+    return fail(SEVO_ERR_UNSUPPORTED, "top-k / confidence lists over a vocabulary of %d", vocab);
   return SEVO_OK;
 }
 
@@ -369,7 +378,8 @@ SEVO_API sevo_status sevo_logprob_sample(const sevo_sample_args* a, void* stream
   if (!a->cand_uid || !a->positions || !a->out_tokens || !a->out_logprobs || !a->workspace)
     return fail(SEVO_ERR_INVALID_ARGUMENT, "null pointer");
   if (!aligned16(a->workspace)) return fail(SEVO_ERR_INVALID_ARGUMENT, "misaligned workspace");
-  st = conf_check(a->conf_topk, a->vocab, a->out_conf, a->conf_sum);
+  st = conf_check(a->conf_topk, a->vocab, a->out_conf, a->conf_sum, a->top_k, a->top_p,
+                  a->min_p);
   if (st) return st;
   const size_t need = sevo::sample_workspace_bytes(a->n, a->vocab);
   if (a->workspace_bytes < need)
@@ -378,7 +388,7 @@ SEVO_API sevo_status sevo_logprob_sample(const sevo_sample_args* a, void* stream
   hipError_t e = sevo::launch_logprob_sample(
       a->logits, a->n, a->vocab, a->ld, a->temperature, a->seed, a->cand_uid, a->positions,
       a->out_tokens, a->out_logprobs, static_cast<float*>(a->workspace), a->conf_topk,
-      a->out_conf, a->conf_sum, static_cast<hipStream_t>(stream));
+      a->out_conf, a->conf_sum, static_cast<hipStream_t>(stream), a->top_k, a->top_p, a->min_p);
   if (e != hipSuccess) return hip_fail(e, "sevo_logprob_sample launch");
   return SEVO_OK;
 }
@@ -580,7 +590,9 @@ SEVO_API sevo_status sevo_decode_step(sevo_model* m, const sevo_step_args* a, vo
     return fail(SEVO_ERR_INVALID_ARGUMENT, "bad n / max_pages / num_pages / num_splits");
   if (!std::isfinite(a->temperature) || a->temperature < 0.f)
     return fail(SEVO_ERR_INVALID_ARGUMENT, "temperature must be finite and >= 0");
-  if (sevo_status cs = conf_check(a->conf_topk, c.vocab, a->out_conf, a->conf_sum)) return cs;
+  if (sevo_status cs = conf_check(a->conf_topk, c.vocab, a->out_conf, a->conf_sum, a->top_k,
+                                  a->top_p, a->min_p))
+    return cs;
   if (a->n == 0) return SEVO_OK;
   if (!a->tokens || !a->positions || !a->page_table || !a->k_pools || !a->v_pools ||
       !a->cand_uid || !a->out_tokens || !a->out_logprobs || !a->workspace)
@@ -707,7 +719,8 @@ SEVO_API sevo_status sevo_decode_step(sevo_model* m, const sevo_step_args* a, vo
     ProfScope ps(SEVO_PROF_SAMPLE, st);
     e = sevo::launch_logprob_sample(logits, n, c.vocab, c.vocab, a->temperature, a->seed,
                                     a->cand_uid, a->positions, a->out_tokens, a->out_logprobs,
-                                    smp, a->conf_topk, a->out_conf, a->conf_sum, st);
+                                    smp, a->conf_topk, a->out_conf, a->conf_sum, st, a->top_k,
+                                    a->top_p, a->min_p);
   }
   if (e != hipSuccess) return hip_fail(e, "decode step (head / sampler)");
   return SEVO_OK;

@@ -60,8 +60,9 @@ class AttnArgs(C.Structure):
 class SampleArgs(C.Structure):
     _fields_ = [("logits", vp), ("n", i32), ("vocab", i32), ("ld", i64), ("temperature", f32),
                 ("seed", u64), ("cand_uid", vp), ("positions", vp), ("out_tokens", vp),
-                ("out_logprobs", vp), ("conf_topk", i32), ("out_conf", vp), ("conf_sum", vp),
-                ("workspace", vp), ("workspace_bytes", sz)]
+                ("out_logprobs", vp), ("top_k", i32), ("top_p", f32), ("min_p", f32),
+                ("conf_topk", i32), ("out_conf", vp), ("conf_sum", vp), ("workspace", vp),
+                ("workspace_bytes", sz)]
 
 
 class StepArgs(C.Structure):
@@ -69,8 +70,9 @@ class StepArgs(C.Structure):
                 ("max_pages", i32), ("num_pages", i64), ("k_pools", C.POINTER(vp)),
                 ("v_pools", C.POINTER(vp)), ("cand_uid", vp), ("seed", u64),
                 ("temperature", f32), ("num_splits", i32), ("out_tokens", vp),
-                ("out_logprobs", vp), ("out_logits", vp), ("conf_topk", i32),
-                ("out_conf", vp), ("conf_sum", vp), ("workspace", vp), ("workspace_bytes", sz)]
+                ("out_logprobs", vp), ("out_logits", vp), ("top_k", i32), ("top_p", f32),
+                ("min_p", f32), ("conf_topk", i32), ("out_conf", vp), ("conf_sum", vp),
+                ("workspace", vp), ("workspace_bytes", sz)]
 
 
 class LinearArgs(C.Structure):
@@ -196,11 +198,13 @@ def sevo_sample_workspace_bytes(n: int, vocab: int) -> int:
 
 def sevo_logprob_sample(logits, temperature, seed, cand_uid, positions, out_tokens=None,
                         out_logprobs=None, workspace=None, stream=None, vocab=None,
-                        conf_topk=0, out_conf=None, conf_sum=None):
+                        conf_topk=0, out_conf=None, conf_sum=None, top_k=0, top_p=1.0,
+                        min_p=0.0):
     """(ids int32 [n], logprobs fp32 [n]) from fp32 logits [n, ld] (the first
-    ``vocab`` columns, default all).  With ``conf_topk`` > 0 also the per-token
-    self-confidence: returned as a third element (``out_conf``) and/or added to
-    ``conf_sum``."""
+    ``vocab`` columns, default all).  ``top_k`` > 0: truncated sampling with
+    ``top_p`` / ``min_p`` inside the top-k set.  With ``conf_topk`` > 0 also the
+    per-token self-confidence: returned as a third element (``out_conf``) and/or
+    added to ``conf_sum``."""
     n = logits.shape[0]
     vocab = logits.shape[1] if vocab is None else vocab
     if conf_topk and out_conf is None:
@@ -213,7 +217,8 @@ def sevo_logprob_sample(logits, temperature, seed, cand_uid, positions, out_toke
     a = SampleArgs(logits=_p(logits), n=n, vocab=vocab, ld=logits.stride(0),
                    temperature=float(temperature), seed=int(seed), cand_uid=_p(cand_uid),
                    positions=_p(positions), out_tokens=_p(out_tokens),
-                   out_logprobs=_p(out_logprobs), conf_topk=int(conf_topk), out_conf=_p(out_conf),
+                   out_logprobs=_p(out_logprobs), top_k=int(top_k), top_p=float(top_p),
+                   min_p=float(min_p), conf_topk=int(conf_topk), out_conf=_p(out_conf),
                    conf_sum=_p(conf_sum), workspace=_p(ws), workspace_bytes=ws.numel())
     _check(lib().sevo_logprob_sample(C.byref(a), _stream(stream)))
     if conf_topk:
@@ -392,7 +397,7 @@ class StepBuffers:
 
     def __init__(self, model: Model, tokens, positions, page_table, k_pools, v_pools, cand_uid,
                  seed, temperature, num_splits=0, keep_logits=False, workspace=None,
-                 conf_topk=0, conf_sum=None):
+                 conf_topk=0, conf_sum=None, top_k=0, top_p=1.0, min_p=0.0):
         n = tokens.shape[0]
         dev = tokens.device
         self.model = model
@@ -415,6 +420,7 @@ class StepBuffers:
             cand_uid=_p(cand_uid), seed=int(seed), temperature=float(temperature),
             num_splits=num_splits, out_tokens=_p(self.out_tokens),
             out_logprobs=_p(self.out_logprobs), out_logits=_p(self.out_logits),
+            top_k=int(top_k), top_p=float(top_p), min_p=float(min_p),
             conf_topk=int(conf_topk), out_conf=_p(self.out_conf), conf_sum=_p(conf_sum),
             workspace=_p(self.workspace), workspace_bytes=self.workspace.numel())
 
@@ -425,10 +431,11 @@ class StepBuffers:
 
 def sevo_decode_step(model: Model, tokens, positions, page_table, k_pools, v_pools, cand_uid,
                      seed, temperature=1.0, num_splits=0, keep_logits=False, stream=None,
-                     conf_topk=0, conf_sum=None):
+                     conf_topk=0, conf_sum=None, top_k=0, top_p=1.0, min_p=0.0):
     """One decode step of the population; returns (ids, logprobs[, logits][, conf])."""
     b = StepBuffers(model, tokens, positions, page_table, k_pools, v_pools, cand_uid, seed,
-                    temperature, num_splits, keep_logits, conf_topk=conf_topk, conf_sum=conf_sum)
+                    temperature, num_splits, keep_logits, conf_topk=conf_topk, conf_sum=conf_sum,
+                    top_k=top_k, top_p=top_p, min_p=min_p)
     ids, lps = b.run(stream)
     out = (ids, lps) + ((b.out_logits,) if keep_logits else ()) + \
         ((b.out_conf,) if conf_topk else ())

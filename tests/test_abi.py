@@ -33,11 +33,13 @@ int main(void) {
   S(sevo_attn_args) P(sevo_attn_args, num_pages) P(sevo_attn_args, q) P(sevo_attn_args, scale)
   P(sevo_attn_args, out) P(sevo_attn_args, workspace_bytes)
   S(sevo_sample_args) P(sevo_sample_args, ld) P(sevo_sample_args, temperature)
-  P(sevo_sample_args, seed) P(sevo_sample_args, conf_topk) P(sevo_sample_args, conf_sum)
+  P(sevo_sample_args, seed) P(sevo_sample_args, top_k) P(sevo_sample_args, min_p)
+  P(sevo_sample_args, conf_topk) P(sevo_sample_args, conf_sum)
   P(sevo_sample_args, workspace_bytes)
   S(sevo_step_args) P(sevo_step_args, max_pages) P(sevo_step_args, num_pages)
   P(sevo_step_args, k_pools) P(sevo_step_args, seed) P(sevo_step_args, temperature)
-  P(sevo_step_args, num_splits) P(sevo_step_args, out_logits) P(sevo_step_args, conf_topk)
+  P(sevo_step_args, num_splits) P(sevo_step_args, out_logits) P(sevo_step_args, top_p)
+  P(sevo_step_args, conf_topk)
   P(sevo_step_args, out_conf) P(sevo_step_args, workspace_bytes)
   S(sevo_linear_args) P(sevo_linear_args, flags) P(sevo_linear_args, x)
   P(sevo_linear_args, workspace_bytes)
@@ -125,11 +127,11 @@ def test_sampler_rejects_bad_temperature(temp):
 
 def test_sampler_rejects_bad_ld_and_small_workspace():
     L = sevo.lib()
-    a = sevo.SampleArgs(logits=1 << 20, n=1, vocab=8, ld=6, temperature=1.0)
+    a = sevo.SampleArgs(logits=1 << 20, n=1, vocab=8, ld=6, temperature=1.0, top_p=1.0)
     assert L.sevo_logprob_sample(C.byref(a), None) == sevo.INVALID_ARGUMENT
     f = 1 << 20
     a = sevo.SampleArgs(logits=f, n=2, vocab=8, ld=8, temperature=1.0, cand_uid=f, positions=f,
-                        out_tokens=f, out_logprobs=f, workspace=f, workspace_bytes=1)
+                        out_tokens=f, out_logprobs=f, workspace=f, workspace_bytes=1, top_p=1.0)
     assert L.sevo_logprob_sample(C.byref(a), None) == sevo.WORKSPACE_TOO_SMALL
 
 
@@ -199,11 +201,18 @@ def test_status_strings():
     (dict(conf_topk=-1, out_conf=1 << 20), sevo.INVALID_ARGUMENT),
     (dict(conf_topk=9, out_conf=1 << 20), sevo.INVALID_ARGUMENT),     # more than vocab
     (dict(conf_topk=4), sevo.INVALID_ARGUMENT),                       # no output
+    (dict(top_k=33), sevo.INVALID_ARGUMENT),
+    (dict(top_k=9), sevo.INVALID_ARGUMENT),                           # more than vocab
+    (dict(top_k=4, top_p=0.0), sevo.INVALID_ARGUMENT),
+    (dict(top_k=4, top_p=1.5), sevo.INVALID_ARGUMENT),
+    (dict(top_k=4, min_p=-0.1), sevo.INVALID_ARGUMENT),
+    (dict(top_p=0.9), sevo.UNSUPPORTED),                              # top-p without top-k
+    (dict(min_p=0.1), sevo.UNSUPPORTED),
 ])
 def test_sampler_rejects_bad_confidence_arguments(kw, status):
     f = 1 << 20
     a = dict(logits=f, n=2, vocab=8, ld=8, temperature=1.0, cand_uid=f, positions=f,
-             out_tokens=f, out_logprobs=f, workspace=f, workspace_bytes=1 << 20)
+             out_tokens=f, out_logprobs=f, workspace=f, workspace_bytes=1 << 20, top_p=1.0)
     a.update(kw)
     assert sevo.lib().sevo_logprob_sample(C.byref(sevo.SampleArgs(**a)), None) == status
 

@@ -264,6 +264,53 @@ def test_self_confidence_matches_oracle(S, n, vocab, ld, temp, k):
     np.testing.assert_array_equal(lps.cpu().numpy(), lps0.cpu().numpy())
 
 
+@pytest.mark.parametrize("n,vocab,ld,temp,top_k,top_p,min_p,conf", [
+    (64, 151936, 151936, 0.7, 20, 0.8, 0.0, 0),     # instruct rows of the table
+    (64, 151936, 151936, 0.6, 20, 0.95, 0.0, 20),   # thinking rows, with confidence
+    (16, 151936, 151936, 1.0, 20, 0.95, 0.0, 0),
+    (16, 151936, 151936, 0.0, 20, 0.8, 0.0, 0),     # greedy
+    (8, 4093, 4096, 1.0, 32, 1.0, 0.1, 32),         # min-p
+    (3, 40, 40, 1.3, 5, 0.5, 0.2, 3),
+    (4, 9000, 9000, 2.0, 1, 1.0, 0.0, 0)])
+def test_truncated_sampling_matches_oracle(S, n, vocab, ld, temp, top_k, top_p, min_p, conf):
+    """Top-k with min-p and top-p inside the top-k set, on identical logits."""
+    sevo, _ = S
+    say(f"truncated sampling n={n} V={vocab} T={temp} k={top_k} p={top_p} min_p={min_p}")
+    host, dev = _logits(n, vocab, ld, 11, std=2.0)
+    uid = torch.from_numpy(np.arange(n, dtype=np.int64) * 7919 + 3).cuda()
+    pos = torch.from_numpy(np.arange(n, dtype=np.int32) * 13 + 2).cuda()
+    out = sevo.sevo_logprob_sample(dev, temp, 99, uid, pos, vocab=vocab, top_k=top_k,
+                                   top_p=top_p, min_p=min_p, conf_topk=conf)
+    torch.cuda.synchronize()
+    ids, lps = out[0].cpu().numpy(), out[1].cpu().numpy()
+    rid, rlp, gap = od.truncated_logprob_sample(host, temp, 99, np.arange(n) * 7919 + 3,
+                                                np.arange(n) * 13 + 2, top_k, top_p, min_p)
+    exact = gap > 1e-3
+    say(f"  ids equal {np.mean(ids == rid):.3f}, lp err {np.abs(lps - rlp).max():.2e}")
+    assert np.all(ids[exact] == rid[exact])
+    assert np.abs(lps - rlp)[ids == rid].max() <= 3e-3
+    if conf:
+        ref = od.token_confidence(host.astype(np.float64), conf)
+        assert np.abs(out[2].cpu().numpy() - ref).max() <= 2e-4
+
+
+def test_truncated_sampling_tied_logits_use_index_order(S):
+    """Equal logits at the top-k boundary: the lower vocabulary indices are kept."""
+    sevo, _ = S
+    n, vocab = 2, 5000
+    dev = torch.zeros(n, vocab, dtype=torch.float32, device="cuda")
+    dev[:, 100:140] = 3.0            # 40 tied maxima: top-8 keeps indices 100..107
+    uid = torch.arange(n, dtype=torch.int64, device="cuda") + 5
+    seen = set()
+    for seed in range(40):
+        ids, lps = sevo.sevo_logprob_sample(dev, 1.0, seed, uid, torch.zeros(n, dtype=torch.int32,
+                                                                             device="cuda"),
+                                            top_k=8)
+        seen |= set(ids.cpu().numpy().tolist())
+        np.testing.assert_allclose(lps.cpu().numpy(), np.log(1 / 8), atol=1e-6)
+    assert seen <= set(range(100, 108)) and len(seen) > 4
+
+
 def test_self_confidence_ties_and_uniform(S):
     """Uniform logits give c = log V exactly; many equal maxima count once each."""
     sevo, _ = S

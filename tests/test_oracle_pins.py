@@ -411,3 +411,80 @@ def test_candidate_and_group_confidence_by_hand():
     C = od.candidate_confidence([6.0, 9.0, 2.0, 8.0], [3, 3, 1, 4])
     np.testing.assert_allclose(C, [2.0, 3.0, 2.0, 2.0])
     np.testing.assert_allclose(od.group_confidence(C, [[0, 1], [2, 3], [1, 3]]), [2.5, 2.0, 2.5])
+
+
+# ---------------------------------------------------------------- truncated sampling
+def test_truncated_with_everything_kept_is_the_plain_sampler():
+    z = RNG.standard_normal((6, 300)) * 2
+    uids = np.arange(6) + 40
+    pos = np.arange(6) + 7
+    for T in (1.0, 0.7, 0.0):
+        a = od.logprob_sample(z, T, 3, uids, pos)
+        b = od.truncated_logprob_sample(z, T, 3, uids, pos, top_k=300)
+        np.testing.assert_array_equal(a[0], b[0])
+        np.testing.assert_allclose(a[1], b[1], atol=1e-12)
+
+
+def test_truncated_top1_is_greedy_with_zero_logprob():
+    z = np.array([[0.5, 2.0, 2.0, -1.0], [3.0, 1.0, 0.0, 3.0]])
+    ids, lps, _ = od.truncated_logprob_sample(z, 1.0, 5, [1, 2], [0, 0], top_k=1)
+    assert list(ids) == [1, 0] and np.all(lps == 0.0)
+
+
+def test_truncated_top_p_and_min_p_boundaries_by_hand():
+    p = np.array([0.5, 0.3, 0.15, 0.05])
+    z = np.log(p)[None, :]
+    def kept(**kw):
+        seen = set()
+        for s in range(400):
+            ids, lps, _ = od.truncated_logprob_sample(z, 1.0, s, [9], [0], top_k=4, **kw)
+            seen.add(int(ids[0]))
+        return seen
+    assert kept(top_p=0.79) == {0, 1}           # cumulative before token 2 is 0.8: not below
+    assert kept(top_p=0.81) == {0, 1, 2}
+    assert kept(min_p=0.31) == {0, 1}           # 0.15 < 0.31 * 0.5
+    assert kept(min_p=0.29) == {0, 1, 2}
+    # the log-prob is renormalised over the kept set
+    ids, lps, _ = od.truncated_logprob_sample(z, 1.0, 0, [9], [0], top_k=4, top_p=0.79)
+    assert abs(lps[0] - np.log(p[ids[0]] / 0.8)) < 1e-12
+
+
+def test_truncated_frequencies_match_renormalised_softmax():
+    V = 10
+    z = np.array([[1.2, 0.3, 2.0, -0.5, 1.9, 0.0, -3.0, 1.0, 0.9, 0.2]])
+    T, k, top_p, min_p = 0.8, 5, 0.9, 0.05
+    order = np.lexsort((np.arange(V), -z[0]))[:k]
+    w = np.exp(z[0][order] / T)
+    w = w / w.sum()
+    keep = w >= min_p * w.max()
+    cum, kp = 0.0, []
+    tot = w[keep].sum()
+    for j in range(k):
+        if keep[j] and cum < top_p * tot:
+            kp.append(j)
+            cum += w[j]
+    probs = np.zeros(V)
+    probs[order[kp]] = w[kp] / w[kp].sum()
+    n = 6000
+    counts = np.zeros(V)
+    for u in range(n):
+        ids, _, _ = od.truncated_logprob_sample(z, T, 77, [u], [3], top_k=k, top_p=top_p,
+                                                min_p=min_p)
+        counts[ids[0]] += 1
+    assert np.all(counts[probs == 0] == 0)
+    m = probs > 0
+    chi2 = np.sum((counts[m] - n * probs[m]) ** 2 / (n * probs[m]))
+    assert chi2 < 25.0, (chi2, counts, probs)        # df <= 4: p ~ 1e-4
+
+
+def test_truncated_set_does_not_depend_on_temperature():
+    z = RNG.standard_normal((1, 64))
+    sets = []
+    for T in (0.3, 1.0, 2.5):
+        seen = set()
+        for s in range(200):
+            ids, _, _ = od.truncated_logprob_sample(z, T, s, [1], [0], top_k=3)
+            seen.add(int(ids[0]))
+        sets.append(seen)
+    top3 = set(np.argsort(-z[0])[:3].tolist())
+    assert all(s <= top3 for s in sets)
