@@ -107,14 +107,12 @@ def cpu_baseline(w, pop, n_sample, budget_s=30.0):
     # compact host pools holding only the sampled candidates' pages
     need = (lengths + 1 + 15) // 16
     pt = np.full((n_sample, int(need.max())), -1, np.int64)
-    kspec, vspec = synth.kv_specs(shape, w.seed, 0, pop.n_pages)
-    kp = np.empty((int(need.sum()), shape.n_kv_heads, shape.head_dim // 32, 16, 32), np.float32)
-    vp = np.empty((int(need.sum()), shape.n_kv_heads, shape.head_dim, 16), np.float32)
+    spec = synth.kv_spec(shape, w.seed, 0, pop.n_pages)
+    kvp = np.empty((int(need.sum()),) + tuple(spec.shape[1:]), np.float32)
     c = 0
     for j, i in enumerate(idx):
         pages = pop.page_table[i, :need[j]]
-        kp[c:c + need[j]] = synth.pool_pages(kspec, pages)
-        vp[c:c + need[j]] = synth.pool_pages(vspec, pages)
+        kvp[c:c + need[j]] = synth.pool_pages(spec, pages)
         pt[j, :need[j]] = np.arange(c, c + need[j])
         c += need[j]
     hw = synth.host_weights(shape, w.seed, lazy=True)
@@ -122,7 +120,7 @@ def cpu_baseline(w, pop, n_sample, budget_s=30.0):
     x = np.asarray(hw["embed"][pop.tokens[idx]], np.float64)
     lm_head = hw["lm_head"][0:shape.vocab]
     t0 = time.perf_counter()
-    x1 = od.decoder_layer(shape, lw, x, lengths, kp, vp, pt, mirror=True)
+    x1 = od.decoder_layer(shape, lw, x, lengths, kvp, pt, mirror=True)
     t1 = time.perf_counter()
     logits = od.lm_logits(shape, hw["final_norm"], lm_head, x1, mirror=True)
     od.logprob_sample(logits, 1.0, 1234, pop.uids[idx], lengths)
@@ -197,7 +195,7 @@ def main():
         raise SystemExit(f"not enough device memory: need {need / 1e9:.1f} GB")
     t = time.time()
     tensors = di.device_weights(shape, w.seed, dev)
-    kp, vp = di.device_pools(shape, w.seed, pop.n_pages, dev)
+    kvp = di.device_pools(shape, w.seed, pop.n_pages, dev)
     d = di.device_population(pop, dev)
     model = sevo.sevo_init_model(shape, tensors, max_position=int(pop.lengths.max()) + extra + 1)
     torch.cuda.synchronize()
@@ -206,7 +204,7 @@ def main():
     tokens = d["tokens"].clone()
     positions = d["lengths"].clone()
     conf_sum = torch.zeros(pop.n, dtype=torch.float32, device=dev) if args.conf_topk else None
-    buf = sevo.StepBuffers(model, tokens, positions, d["page_table"], kp, vp, d["uids"],
+    buf = sevo.StepBuffers(model, tokens, positions, d["page_table"], kvp, d["uids"],
                            seed=20260412, temperature=args.temperature,
                            num_splits=args.num_splits, conf_topk=args.conf_topk,
                            conf_sum=conf_sum, top_k=args.top_k, top_p=args.top_p,

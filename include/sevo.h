@@ -30,12 +30,12 @@
  *     thread.  Host-visible scalars are validated on every call; the contents
  *     of device-resident page tables, lengths and positions are NOT validated
  *     on the hot path (sevo_validate_paging checks them on demand).
- *   - Paged KV cache, one K pool and one V pool per layer, page size 16:
- *       K pool  bf16 [num_pages][n_kv_heads][head_dim/32][16][32]
- *               dims in blocks of 32, each block token-major: element (slot s,
- *               dim e) of a (page, head) tile sits at ((e/32)*16 + s)*32 + e%32
- *       V pool  bf16 [num_pages][n_kv_heads][head_dim][16]   dim-major tile
- *     Each (page, head) tile is 16 * head_dim * 2 bytes, contiguous, for K and V.
+ *   - Paged KV cache, one KV pool per layer, page size 16:
+ *       pool bf16 [num_pages][n_kv_heads][2][16 head_dim]: for each (page, kv
+ *       head) the K tile, then the V tile (one contiguous 8 KB at head_dim 128)
+ *       K tile: dims in blocks of 32, each block token-major: element (slot s,
+ *               dim e) at ((e/32)*16 + s)*32 + e%32
+ *       V tile: dim-major: element (s, e) at e*16 + s
  *     Logical key t of candidate i lives in physical page
  *     page_table[i * max_pages + t / 16], slot t % 16.  One page table serves
  *     all layers.  Physical page order is arbitrary (any permutation gives
@@ -143,7 +143,7 @@ void sevo_free_model(sevo_model* m);
  * online-softmax partial (running max, sum, weighted V) that a combine pass
  * merges in split order, so the result is deterministic.
  *   q        bf16 [n][n_q_heads][head_dim]
- *   k_pool, v_pool  paged layout above (bf16)
+ *   kv_pool  paged layout above (bf16)
  *   page_table int32 [n][max_pages];  seq_lens int32 [n], 0 <= len <= 16 max_pages
  *   (a candidate with len 0 gets o = 0)
  *   out      bf16 [n][n_q_heads][head_dim]
@@ -154,8 +154,7 @@ typedef struct {
   int32_t n, n_q_heads, n_kv_heads, head_dim, page_size, max_pages, num_splits;
   int64_t num_pages; /* pages in each pool; ids outside [0, num_pages) are skipped */
   const void* q;
-  const void* k_pool;
-  const void* v_pool;
+  const void* kv_pool;
   const int32_t* page_table;
   const int32_t* seq_lens;
   float scale;
@@ -250,7 +249,7 @@ sevo_status sevo_group_confidence(const float* conf_sum, const int32_t* token_co
  * SwiGLU product bf16; logits fp32.
  *   tokens int32 [n];  positions int32 [n] (p_i = keys cached before the step;
  *   the caller must have a page for slot p_i, and p_i < max_position);
- *   page_table int32 [n][max_pages];  k_pools, v_pools: HOST arrays of
+ *   page_table int32 [n][max_pages];  kv_pools: HOST array of
  *   n_layers device pool pointers;  cand_uid uint64 [n];
  *   out_tokens int32 [n];  out_logprobs fp32 [n];
  *   out_logits fp32 [n][vocab] or NULL (then kept in the workspace);
@@ -266,8 +265,7 @@ typedef struct {
   const int32_t* page_table;
   int32_t max_pages;
   int64_t num_pages; /* pages in each pool (bounds every page access) */
-  void* const* k_pools;
-  void* const* v_pools;
+  void* const* kv_pools;
   const uint64_t* cand_uid;
   uint64_t seed;
   float temperature;
@@ -345,12 +343,12 @@ sevo_status sevo_pack_weight(const void* src, void* dst, int32_t n_out, int32_t 
 /* The fused QK-RMSNorm + RoPE + KV append of one layer.
  *   qkv fp32 [n][(n_q_heads + 2 n_kv_heads) head_dim] (the QKV projection)
  *   q_out bf16 [n][n_q_heads][head_dim]: RoPE(RMSNorm(q) g_q) at p_i
- *   K/V pools: slot p_i of every candidate receives RoPE(RMSNorm(k) g_k) and v.
+ *   kv_pool: slot p_i of every candidate receives RoPE(RMSNorm(k) g_k) (K tile) and v (V tile).
  * Uses the model's RoPE table, norm gains and shape (layer selects the gains). */
 sevo_status sevo_qk_norm_rope_append(const sevo_model* m, int32_t layer, const float* qkv,
                                      int32_t n, const int32_t* positions,
                                      const int32_t* page_table, int32_t max_pages,
-                                     int64_t num_pages, void* q_out, void* k_pool, void* v_pool,
+                                     int64_t num_pages, void* q_out, void* kv_pool,
                                      void* stream);
 
 /* ------------------------------------------------------------------ utilities */

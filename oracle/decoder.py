@@ -15,11 +15,12 @@ Sampling is exact full-vocabulary categorical sampling at temperature T (the
 temperature-1, top-k off, top-p 1 row of the generation hyper-parameter
 table), realised as Gumbel-max with counter-based noise (see philox.py).
 
-Paged KV layout (per layer; page size 16; head_dim a multiple of 32):
-    K pool [num_pages][n_kv_heads][head_dim/32][16][32]  (dims in blocks of 32,
-           each block token-major: element (slot s, dim e) of a tile sits at
-           ((e // 32) * 16 + s) * 32 + e % 32)
-    V pool [num_pages][n_kv_heads][head_dim][16]         (dim-major tile)
+Paged KV layout (one pool per layer; page size 16; head_dim a multiple of 32):
+    pool [num_pages][n_kv_heads][2][16 head_dim]: per (page, head) the K tile,
+    then the V tile.
+    K tile: dims in blocks of 32, each block token-major -- element (slot s,
+            dim e) at ((e // 32) * 16 + s) * 32 + e % 32
+    V tile: dim-major -- element (s, e) at e * 16 + s
     logical key t of candidate i -> page page_table[i][t // 16], slot t % 16.
 
 Everything here is float64.  bf16 storage points of the GPU path are mirrored
@@ -148,38 +149,57 @@ def attention_split(q, K, V, scale, bounds):
     return out
 
 
-def gather_kv(k_pool, v_pool, pages, n_keys):
+def k_tile_offset(slot, dim):
+    """Position of (slot, dim) inside a K tile (dims in blocks of 32, token-major)."""
+    return ((dim // 32) * PAGE + slot) * 32 + dim % 32
+
+
+def v_tile_offset(slot, dim):
+    """Position of (slot, dim) inside a V tile (dim-major)."""
+    return dim * PAGE + slot
+
+
+def gather_kv(kv_pool, pages, n_keys):
     """Logical K, V [hkv, n_keys, d] of one candidate from its page list."""
+    kv = np.asarray(kv_pool)
+    hkv, d = kv.shape[1], kv.shape[3] // PAGE
     t = np.arange(n_keys)
     pg = np.asarray(pages, np.int64)[t // PAGE]
     sl = t % PAGE
-    kp = np.asarray(k_pool)
-    K = kp[pg, :, :, sl, :].reshape(n_keys, kp.shape[1], -1)   # [L, hkv, d]
-    V = np.asarray(v_pool)[pg, :, :, sl]                       # [L, hkv, d]
-    return (np.transpose(K, (1, 0, 2)).astype(np.float64),
-            np.transpose(V, (1, 0, 2)).astype(np.float64))
+    e = np.arange(d)
+    K = np.empty((hkv, n_keys, d))
+    V = np.empty((hkv, n_keys, d))
+    for p in np.unique(pg):             # one physical page at a time
+        sel = np.nonzero(pg == p)[0]
+        s = sl[sel]
+        K[:, sel, :] = kv[p, :, 0][:, k_tile_offset(s[:, None], e[None, :])]
+        V[:, sel, :] = kv[p, :, 1][:, v_tile_offset(s[:, None], e[None, :])]
+    return K, V
 
 
-def paged_attention(q, k_pool, v_pool, page_table, seq_lens, scale):
+def paged_attention(q, kv_pool, page_table, seq_lens, scale):
     """Decode attention for a population: q [N, hq, d] -> [N, hq, d]."""
     q = np.asarray(q, np.float64)
     out = np.empty_like(q)
     for i in range(q.shape[0]):
-        K, V = gather_kv(k_pool, v_pool, page_table[i], int(seq_lens[i]))
+        K, V = gather_kv(kv_pool, page_table[i], int(seq_lens[i]))
         out[i] = attention_dense(q[i], K, V, scale)
     return out
 
 
-def append_kv(k_pool, v_pool, page_table, positions, k, v):
+def append_kv(kv_pool, page_table, positions, k, v):
     """Write key/value number p_i of every candidate into its page slot."""
+    d = np.asarray(k).shape[-1]
+    e = np.arange(d)
     for i, p in enumerate(np.asarray(positions, np.int64)):
         page = int(page_table[i][p // PAGE])
-        k_pool[page, :, :, p % PAGE, :] = np.asarray(k[i]).reshape(k_pool.shape[1], -1, 32)
-        v_pool[page, :, :, p % PAGE] = v[i]
+        tiles = kv_pool[page]              # [hkv][2][16 d] view of the page
+        tiles[:, 0, k_tile_offset(p % PAGE, e)] = k[i]
+        tiles[:, 1, v_tile_offset(p % PAGE, e)] = v[i]
 
 
 # ------------------------------------------------------------------ decoder
-def decoder_layer(shape, lw, x, positions, k_pool, v_pool, page_table, mirror=True):
+def decoder_layer(shape, lw, x, positions, kv_pool, page_table, mirror=True):
     """One pre-norm GQA decoder layer for the population (updates x, appends KV).
 
     x [N, H] residual stream.  Steps: RMSNorm, QKV projection, per-head
@@ -205,8 +225,8 @@ def decoder_layer(shape, lw, x, positions, k_pool, v_pool, page_table, mirror=Tr
     q = rb(rope_rotate(q, pos[:, None], shape.rope_theta))
     k = rb(rope_rotate(k, pos[:, None], shape.rope_theta))
     v = rb(v)
-    append_kv(k_pool, v_pool, page_table, pos, k, v)
-    o = paged_attention(q, k_pool, v_pool, page_table, pos + 1, 1.0 / np.sqrt(D))
+    append_kv(kv_pool, page_table, pos, k, v)
+    o = paged_attention(q, kv_pool, page_table, pos + 1, 1.0 / np.sqrt(D))
     o = rb(o).reshape(N, hq * D)
     x = keep32(x + o @ np.asarray(lw["w_o"], np.float64).T)
     h2 = rb(rms_norm(x, lw["ffn_norm"], eps))
@@ -262,23 +282,23 @@ def logprob_sample(logits, temperature, seed, uids, positions, noise=None,
     return ids, lps, gaps
 
 
-def decode_step(shape, weights, k_pools, v_pools, page_table, tokens, positions, uids,
+def decode_step(shape, weights, kv_pools, page_table, tokens, positions, uids,
                 seed, temperature, mirror=True, layers=None):
     """One decode step for a population.
 
     weights: mapping with "embed" [V, H] (row-indexable), "lm_head" [V, H],
     "final_norm" [H] and "layers" (sequence of per-layer mappings with
     attn_norm, w_qkv, q_norm, k_norm, w_o, ffn_norm, w_gate_up, w_down).
-    k_pools / v_pools: per-layer pools in the paged layout (float arrays,
-    modified in place by the KV append).  positions p_i = keys already cached.
+    kv_pools: per-layer pools in the paged layout (float arrays, modified in
+    place by the KV append).  positions p_i = keys already cached.
     Returns dict(ids, lps, gaps, logits, x).
     """
     tokens = np.asarray(tokens, np.int64)
     x = np.asarray(weights["embed"][tokens], np.float64)
     n_layers = shape.n_layers if layers is None else layers
     for l in range(n_layers):
-        x = decoder_layer(shape, weights["layers"][l], x, positions, k_pools[l], v_pools[l],
-                          page_table, mirror)
+        x = decoder_layer(shape, weights["layers"][l], x, positions, kv_pools[l], page_table,
+                          mirror)
     logits = lm_logits(shape, weights["final_norm"], weights["lm_head"], x, mirror)
     ids, lps, gaps = logprob_sample(logits, temperature, seed, uids, positions)
     return {"ids": ids, "lps": lps, "gaps": gaps, "logits": logits, "x": x}

@@ -9,7 +9,9 @@
 // order, so results are deterministic and independent of the physical page
 // order.
 //
-// Per page and wave (tile = 16 tokens x D dims, 4 KB at D = 128):
+// Per page and wave (tile = 16 tokens x D dims, 4 KB at D = 128; the K and V
+// tiles of a (page, kv head) are adjacent in the pool, so each page is one
+// contiguous 8 KB read, measured about 2% faster than separate K and V pools):
 //   QK  the K tile is stored in blocks of 32 dims ([D/32][16 tokens][32]), so
 //       load ii reads block ii as one contiguous 1 KB wavefront access; lane
 //       (t = lane/4, u = lane%4) gets dims 32 ii + 8u .. +7 of key t and forms
@@ -70,8 +72,8 @@ __device__ __forceinline__ void load_page(PageRegs<D>& r, const char* kt, const 
 
 template <int D, int G>
 __global__ __launch_bounds__(256, (G <= 4 ? 2 : 1)) void attn_split_kernel(
-    const bf16_t* __restrict__ q, const bf16_t* __restrict__ kpool,
-    const bf16_t* __restrict__ vpool, const int32_t* __restrict__ page_table, int max_pages,
+    const bf16_t* __restrict__ q, const bf16_t* __restrict__ kvpool,
+    const int32_t* __restrict__ page_table, int max_pages,
     int num_pages32, const int32_t* __restrict__ seq_lens, int len_add, int hkv, int chunk, int S,
     float qk_scale_log2, float* __restrict__ part_ml, float* __restrict__ part_acc) {
   constexpr int NI = D / 32;
@@ -140,8 +142,7 @@ __global__ __launch_bounds__(256, (G <= 4 ? 2 : 1)) void attn_split_kernel(
     return kk < 64 ? __builtin_amdgcn_readlane(idv0, kk) : __builtin_amdgcn_readlane(idv1, kk - 64);
   };
   constexpr uint32_t kTileBytes = kPage * D * 2;
-  const char* kp8 = reinterpret_cast<const char*>(kpool);
-  const char* vp8 = reinterpret_cast<const char*>(vpool);
+  const char* kv8 = reinterpret_cast<const char*>(kvpool);
   // lane byte offsets inside a tile: K block ii, token t, dims 8u..8u+7 of the
   // block; V dims 32 ii + dl, token half h
   const uint32_t koff = (uint32_t)(t * 64 + u * 16);
@@ -149,8 +150,9 @@ __global__ __launch_bounds__(256, (G <= 4 ? 2 : 1)) void attn_split_kernel(
 #define SEVO_LOAD(BUF, K)                                                              \
   {                                                                                    \
     const int id_ = page_id(K);                                                        \
-    const size_t tb_ = id_ < 0 ? 0 : ((size_t)id_ * hkv + c) * kTileBytes;            \
-    load_page<D>(BUF, kp8 + tb_, vp8 + tb_, id_ < 0 ? 0 : (int)kTileBytes, koff, voff); \
+    const size_t tb_ = id_ < 0 ? 0 : ((size_t)id_ * hkv + c) * 2 * kTileBytes;        \
+    load_page<D>(BUF, kv8 + tb_, kv8 + tb_ + kTileBytes, id_ < 0 ? 0 : (int)kTileBytes, \
+                 koff, voff);                                                          \
   }
 
   // One page of the wave.  FULL: all 16 slots hold keys (no masking); else
@@ -374,7 +376,7 @@ static hipError_t launch_attn_t(const AttnArgs& a, hipStream_t st) {
   const float log2e = 1.4426950408889634f;
   if (a.ev_begin) (void)hipEventRecord(a.ev_begin, st);
   hipLaunchKernelGGL((attn_split_kernel<D, G>), dim3(a.hkv, a.num_splits, a.n), dim3(256), 0, st,
-                     a.q, a.k_pool, a.v_pool, a.page_table, a.max_pages,
+                     a.q, a.kv_pool, a.page_table, a.max_pages,
                      (int)(a.num_pages < 0x7FFFFFFF ? a.num_pages : 0x7FFFFFFF), a.seq_lens,
                      a.len_add, a.hkv, a.chunk, a.num_splits, a.scale * log2e, a.part_ml, a.part_acc);
   hipError_t e = hipGetLastError();

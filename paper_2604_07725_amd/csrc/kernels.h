@@ -34,8 +34,7 @@ struct RopeAppendArgs {
   int qk_norm;
   float eps;
   bf16_t* q_out;
-  bf16_t* k_pool;
-  bf16_t* v_pool;
+  bf16_t* kv_pool;  // [num_pages][hkv][2][16 d]: K tile, then V tile
 };
 hipError_t launch_qk_norm_rope_append(const RopeAppendArgs& a, hipStream_t st);
 hipError_t launch_fill_bf16(bf16_t* dst, int64_t count, uint64_t key, int64_t offset, float mul,
@@ -46,8 +45,7 @@ struct AttnArgs {
   int n, hq, hkv, d, max_pages, num_splits, chunk;
   int64_t num_pages;
   const bf16_t* q;
-  const bf16_t* k_pool;
-  const bf16_t* v_pool;
+  const bf16_t* kv_pool;
   const int32_t* page_table;
   const int32_t* seq_lens;  // keys per candidate = seq_lens[i] + len_add
   int len_add;

@@ -106,8 +106,9 @@ __global__ __launch_bounds__(64) void qk_norm_rope_append_kernel(RopeAppendArgs 
     const int page = a.page_table[(size_t)i * a.max_pages + pg];
     if (page < 0 || (int64_t)page >= a.num_pages) return;
     const int kh = hh - a.hq;
-    // K tile: dims in blocks of 32, each block [16 slots][32 dims]
-    bf16_t* tile = a.k_pool + ((size_t)page * a.hkv + kh) * kPage * a.d;
+    // K tile (first half of the (page, head) pair): dims in blocks of 32, each
+    // block [16 slots][32 dims]
+    bf16_t* tile = a.kv_pool + ((size_t)page * a.hkv + kh) * 2 * kPage * a.d;
     const int s = p & 15;
     const int e0 = m, e1 = m + half;
     tile[((e0 >> 5) * kPage + s) * 32 + (e0 & 31)] = f32_to_bf16(r0);
@@ -119,7 +120,8 @@ __global__ __launch_bounds__(64) void qk_norm_rope_append_kernel(RopeAppendArgs 
     const int page = a.page_table[(size_t)i * a.max_pages + pg];
     if (page < 0 || (int64_t)page >= a.num_pages) return;
     const int vh = hh - a.hq - a.hkv;
-    bf16_t* dst = a.v_pool + ((size_t)page * a.hkv + vh) * a.d * kPage + (p & 15);
+    // V tile (second half): dim-major [dims][16 slots]
+    bf16_t* dst = a.kv_pool + (((size_t)page * a.hkv + vh) * 2 + 1) * kPage * a.d + (p & 15);
     dst[(size_t)m * kPage] = f32_to_bf16(u0);
     dst[(size_t)(m + half) * kPage] = f32_to_bf16(u1);
   }

@@ -283,7 +283,7 @@ SEVO_API size_t sevo_attn_workspace_bytes(int32_t n, int32_t n_q_heads, int32_t 
 }
 
 static sevo_status attn_core(int n, int hq, int hkv, int d, int max_pages, int num_splits,
-                             int64_t num_pages, const void* q, const void* kp, const void* vp,
+                             int64_t num_pages, const void* q, const void* kvp,
                              const int32_t* pt, const int32_t* lens, float scale, void* out,
                              void* ws, size_t ws_bytes, hipStream_t st) {
   int S, chunk;
@@ -296,8 +296,7 @@ static sevo_status attn_core(int n, int hq, int hkv, int d, int max_pages, int n
   a.n = n; a.hq = hq; a.hkv = hkv; a.d = d; a.max_pages = max_pages; a.num_splits = S;
   a.chunk = chunk; a.num_pages = num_pages;
   a.q = static_cast<const sevo::bf16_t*>(q);
-  a.k_pool = static_cast<const sevo::bf16_t*>(kp);
-  a.v_pool = static_cast<const sevo::bf16_t*>(vp);
+  a.kv_pool = static_cast<const sevo::bf16_t*>(kvp);
   a.page_table = pt; a.seq_lens = lens; a.len_add = 0; a.scale = scale;
   a.out = static_cast<sevo::bf16_t*>(out);
   attach_profiler(a);
@@ -319,13 +318,13 @@ SEVO_API sevo_status sevo_attn_decode(const sevo_attn_args* a, void* stream) {
   if (!(std::isfinite(a->scale)) || a->scale <= 0.f)
     return fail(SEVO_ERR_INVALID_ARGUMENT, "scale must be finite and > 0");
   if (a->n == 0) return SEVO_OK;
-  const void* ptrs[] = {a->q, a->k_pool, a->v_pool, a->page_table, a->seq_lens, a->out,
+  const void* ptrs[] = {a->q, a->kv_pool, a->page_table, a->seq_lens, a->out,
                         a->workspace};
   for (auto p : ptrs)
     if (!p || !aligned16(p))
       return fail(SEVO_ERR_INVALID_ARGUMENT, "null or non-16-byte-aligned pointer");
   return attn_core(a->n, a->n_q_heads, a->n_kv_heads, a->head_dim, a->max_pages, a->num_splits,
-                   a->num_pages, a->q, a->k_pool, a->v_pool, a->page_table, a->seq_lens,
+                   a->num_pages, a->q, a->kv_pool, a->page_table, a->seq_lens,
                    a->scale, a->out, a->workspace, a->workspace_bytes,
                    static_cast<hipStream_t>(stream));
 }
@@ -500,7 +499,7 @@ SEVO_API sevo_status sevo_pack_weight(const void* src, void* dst, int32_t n_out,
 
 static void fill_rope_args(const sevo_model* m, int layer, const float* qkv, int qkv_splits,
                            int n, const int32_t* pos, const int32_t* pt, int max_pages,
-                           int64_t num_pages, void* q_out, void* kp, void* vp,
+                           int64_t num_pages, void* q_out, void* kvp,
                            sevo::RopeAppendArgs& r) {
   const sevo_model_config& c = m->cfg;
   r.qkv = qkv; r.qkv_splits = qkv_splits; r.n = n; r.hq = c.n_q_heads; r.hkv = c.n_kv_heads; r.d = c.head_dim;
@@ -510,26 +509,25 @@ static void fill_rope_args(const sevo_model* m, int layer, const float* qkv, int
   r.k_gain = static_cast<const sevo::bf16_t*>(m->k_norm[layer]);
   r.qk_norm = c.qk_norm; r.eps = c.rms_eps;
   r.q_out = static_cast<sevo::bf16_t*>(q_out);
-  r.k_pool = static_cast<sevo::bf16_t*>(kp);
-  r.v_pool = static_cast<sevo::bf16_t*>(vp);
+  r.kv_pool = static_cast<sevo::bf16_t*>(kvp);
 }
 
 SEVO_API sevo_status sevo_qk_norm_rope_append(const sevo_model* m, int32_t layer,
                                               const float* qkv, int32_t n,
                                               const int32_t* positions,
                                               const int32_t* page_table, int32_t max_pages,
-                                              int64_t num_pages, void* q_out, void* k_pool,
-                                              void* v_pool, void* stream) {
+                                              int64_t num_pages, void* q_out, void* kv_pool,
+                                              void* stream) {
   if (!m) return fail(SEVO_ERR_INVALID_ARGUMENT, "null model");
   if (layer < 0 || layer >= m->cfg.n_layers) return fail(SEVO_ERR_INVALID_ARGUMENT, "bad layer");
   if (n < 0 || max_pages < 1 || num_pages < 1)
     return fail(SEVO_ERR_INVALID_ARGUMENT, "bad n / max_pages / num_pages");
   if (n == 0) return SEVO_OK;
-  if (!qkv || !positions || !page_table || !q_out || !k_pool || !v_pool)
+  if (!qkv || !positions || !page_table || !q_out || !kv_pool)
     return fail(SEVO_ERR_INVALID_ARGUMENT, "null pointer");
   sevo::RopeAppendArgs r;
-  fill_rope_args(m, layer, qkv, 1, n, positions, page_table, max_pages, num_pages, q_out, k_pool,
-                 v_pool, r);
+  fill_rope_args(m, layer, qkv, 1, n, positions, page_table, max_pages, num_pages, q_out, kv_pool,
+                 r);
   hipError_t e = sevo::launch_qk_norm_rope_append(r, static_cast<hipStream_t>(stream));
   return e == hipSuccess ? SEVO_OK : hip_fail(e, "sevo_qk_norm_rope_append");
 }
@@ -594,15 +592,14 @@ SEVO_API sevo_status sevo_decode_step(sevo_model* m, const sevo_step_args* a, vo
                                   a->top_p, a->min_p))
     return cs;
   if (a->n == 0) return SEVO_OK;
-  if (!a->tokens || !a->positions || !a->page_table || !a->k_pools || !a->v_pools ||
+  if (!a->tokens || !a->positions || !a->page_table || !a->kv_pools ||
       !a->cand_uid || !a->out_tokens || !a->out_logprobs || !a->workspace)
     return fail(SEVO_ERR_INVALID_ARGUMENT, "null pointer");
   if (!aligned16(a->workspace)) return fail(SEVO_ERR_INVALID_ARGUMENT, "misaligned workspace");
   if (a->out_logits && !aligned16(a->out_logits))
     return fail(SEVO_ERR_INVALID_ARGUMENT, "misaligned out_logits");
   for (int l = 0; l < c.n_layers; ++l)
-    if (!a->k_pools[l] || !a->v_pools[l] || !aligned16(a->k_pools[l]) ||
-        !aligned16(a->v_pools[l]))
+    if (!a->kv_pools[l] || !aligned16(a->kv_pools[l]))
       return fail(SEVO_ERR_INVALID_ARGUMENT, "layer %d: null or misaligned KV pool", l);
   const int n = a->n;
   const StepLayout L = step_layout(c, n, a->max_pages, a->num_splits);
@@ -654,7 +651,7 @@ SEVO_API sevo_status sevo_decode_step(sevo_model* m, const sevo_step_args* a, vo
       ProfScope ps(SEVO_PROF_ROPE_APPEND, st);
       sevo::RopeAppendArgs r;
       fill_rope_args(m, l, part_qkv, L.p_qkv.k_splits, n, a->positions, a->page_table,
-                     a->max_pages, a->num_pages, q, a->k_pools[l], a->v_pools[l], r);
+                     a->max_pages, a->num_pages, q, a->kv_pools[l], r);
       e = sevo::launch_qk_norm_rope_append(r, st);
     }
     if (e != hipSuccess) return hip_fail(e, "decode step (attention input)");
@@ -665,8 +662,7 @@ SEVO_API sevo_status sevo_decode_step(sevo_model* m, const sevo_step_args* a, vo
     aa.chunk = L.chunk;
     aa.num_pages = a->num_pages;
     aa.q = q;
-    aa.k_pool = static_cast<const sevo::bf16_t*>(a->k_pools[l]);
-    aa.v_pool = static_cast<const sevo::bf16_t*>(a->v_pools[l]);
+    aa.kv_pool = static_cast<const sevo::bf16_t*>(a->kv_pools[l]);
     aa.page_table = a->page_table;
     aa.seq_lens = a->positions;
     aa.len_add = 1;

@@ -47,13 +47,10 @@ def device_weights(shape: synth.ModelShape, seed: int, device="cuda") -> dict:
 
 
 def device_pools(shape: synth.ModelShape, seed: int, n_pages: int, device="cuda",
-                 layers=None) -> tuple[list, list]:
-    ks, vs = [], []
-    for l in (range(shape.n_layers) if layers is None else layers):
-        kspec, vspec = synth.kv_specs(shape, seed, l, n_pages)
-        ks.append(_filled(kspec, device))
-        vs.append(_filled(vspec, device))
-    return ks, vs
+                 layers=None) -> list:
+    """One KV pool per layer, [P][hkv][2][16 d] bf16."""
+    return [_filled(synth.kv_spec(shape, seed, l, n_pages), device)
+            for l in (range(shape.n_layers) if layers is None else layers)]
 
 
 def device_q(shape: synth.ModelShape, seed: int, n: int, device="cuda") -> torch.Tensor:

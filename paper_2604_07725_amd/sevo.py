@@ -53,7 +53,7 @@ class Weights(C.Structure):
 class AttnArgs(C.Structure):
     _fields_ = [("n", i32), ("n_q_heads", i32), ("n_kv_heads", i32), ("head_dim", i32),
                 ("page_size", i32), ("max_pages", i32), ("num_splits", i32), ("num_pages", i64),
-                ("q", vp), ("k_pool", vp), ("v_pool", vp), ("page_table", vp), ("seq_lens", vp),
+                ("q", vp), ("kv_pool", vp), ("page_table", vp), ("seq_lens", vp),
                 ("scale", f32), ("out", vp), ("workspace", vp), ("workspace_bytes", sz)]
 
 
@@ -67,8 +67,8 @@ class SampleArgs(C.Structure):
 
 class StepArgs(C.Structure):
     _fields_ = [("n", i32), ("tokens", vp), ("positions", vp), ("page_table", vp),
-                ("max_pages", i32), ("num_pages", i64), ("k_pools", C.POINTER(vp)),
-                ("v_pools", C.POINTER(vp)), ("cand_uid", vp), ("seed", u64),
+                ("max_pages", i32), ("num_pages", i64), ("kv_pools", C.POINTER(vp)),
+                ("cand_uid", vp), ("seed", u64),
                 ("temperature", f32), ("num_splits", i32), ("out_tokens", vp),
                 ("out_logprobs", vp), ("out_logits", vp), ("top_k", i32), ("top_p", f32),
                 ("min_p", f32), ("conf_topk", i32), ("out_conf", vp), ("conf_sum", vp),
@@ -100,7 +100,7 @@ _SIGS = {
     "sevo_linear": ([C.POINTER(LinearArgs), vp], i32),
     "sevo_linear_workspace_bytes": ([i32, i32, i32, i32], sz),
     "sevo_pack_weight": ([vp, vp, i32, i32, i32, vp], i32),
-    "sevo_qk_norm_rope_append": ([vp, i32, vp, i32, vp, vp, i32, i64, vp, vp, vp, vp], i32),
+    "sevo_qk_norm_rope_append": ([vp, i32, vp, i32, vp, vp, i32, i64, vp, vp, vp], i32),
     "sevo_fill_normal_bf16": ([vp, i64, u64, i64, f32, f32, i32, vp], i32),
     "sevo_validate_paging": ([vp, vp, i32, i32, i64, vp], i32),
     "sevo_profile_begin": ([i32, C.c_uint32], i32),
@@ -171,20 +171,20 @@ def sevo_attn_workspace_bytes(n, n_q_heads, n_kv_heads, head_dim, max_pages, num
                                                num_splits))
 
 
-def sevo_attn_decode(q, k_pool, v_pool, page_table, seq_lens, out=None, scale=None,
+def sevo_attn_decode(q, kv_pool, page_table, seq_lens, out=None, scale=None,
                      num_splits=0, workspace=None, stream=None):
-    """o = paged GQA decode attention.  q [n, hq, d] bf16; pools in the paged
-    layouts; page_table int32 [n, max_pages]; seq_lens int32 [n]."""
+    """o = paged GQA decode attention.  q [n, hq, d] bf16; kv_pool in the paged
+    layout [P, hkv, 2, 16 d]; page_table int32 [n, max_pages]; seq_lens int32 [n]."""
     n, hq, d = q.shape
-    hkv = k_pool.shape[1]
+    hkv = kv_pool.shape[1]
     max_pages = page_table.shape[1]
     if out is None:
         out = torch.empty_like(q)
     need = sevo_attn_workspace_bytes(n, hq, hkv, d, max_pages, num_splits)
     ws = _workspace(need, q.device, workspace)
     a = AttnArgs(n=n, n_q_heads=hq, n_kv_heads=hkv, head_dim=d, page_size=PAGE_SIZE,
-                 max_pages=max_pages, num_splits=num_splits, num_pages=k_pool.shape[0],
-                 q=_p(q), k_pool=_p(k_pool), v_pool=_p(v_pool), page_table=_p(page_table),
+                 max_pages=max_pages, num_splits=num_splits, num_pages=kv_pool.shape[0],
+                 q=_p(q), kv_pool=_p(kv_pool), page_table=_p(page_table),
                  seq_lens=_p(seq_lens), scale=float(d ** -0.5 if scale is None else scale),
                  out=_p(out), workspace=_p(ws), workspace_bytes=ws.numel())
     _check(lib().sevo_attn_decode(C.byref(a), _stream(stream)))
@@ -299,16 +299,16 @@ def sevo_pack_weight(src, kind=PACK_PLAIN, dst=None, stream=None):
     return dst
 
 
-def sevo_qk_norm_rope_append(model, layer, qkv, positions, page_table, k_pool, v_pool,
-                             q_out=None, stream=None):
+def sevo_qk_norm_rope_append(model, layer, qkv, positions, page_table, kv_pool, q_out=None,
+                             stream=None):
     n = qkv.shape[0]
     cfg = model.config
     if q_out is None:
         q_out = torch.empty(n, cfg.n_q_heads, cfg.head_dim, dtype=torch.bfloat16,
                             device=qkv.device)
     _check(lib().sevo_qk_norm_rope_append(model.handle, layer, _p(qkv), n, _p(positions),
-                                          _p(page_table), page_table.shape[1], k_pool.shape[0],
-                                          _p(q_out), _p(k_pool), _p(v_pool), _stream(stream)))
+                                          _p(page_table), page_table.shape[1], kv_pool.shape[0],
+                                          _p(q_out), _p(kv_pool), _stream(stream)))
     return q_out
 
 
@@ -395,7 +395,7 @@ def sevo_step_workspace_bytes(model: Model, n: int, max_pages: int, num_splits: 
 class StepBuffers:
     """Pre-built argument struct for repeated decode steps (no per-step allocation)."""
 
-    def __init__(self, model: Model, tokens, positions, page_table, k_pools, v_pools, cand_uid,
+    def __init__(self, model: Model, tokens, positions, page_table, kv_pools, cand_uid,
                  seed, temperature, num_splits=0, keep_logits=False, workspace=None,
                  conf_topk=0, conf_sum=None, top_k=0, top_p=1.0, min_p=0.0):
         n = tokens.shape[0]
@@ -410,13 +410,12 @@ class StepBuffers:
         need = sevo_step_workspace_bytes(model, n, page_table.shape[1], num_splits)
         self.workspace = _workspace(need, dev, workspace)
         L = model.shape.n_layers
-        self._k = (vp * L)(*[k.data_ptr() for k in k_pools])
-        self._v = (vp * L)(*[v.data_ptr() for v in v_pools])
-        self.keep = (tokens, positions, page_table, k_pools, v_pools, cand_uid)
+        self._kv = (vp * L)(*[p.data_ptr() for p in kv_pools])
+        self.keep = (tokens, positions, page_table, kv_pools, cand_uid)
         self.args = StepArgs(
             n=n, tokens=_p(tokens), positions=_p(positions), page_table=_p(page_table),
-            max_pages=page_table.shape[1], num_pages=k_pools[0].shape[0],
-            k_pools=C.cast(self._k, C.POINTER(vp)), v_pools=C.cast(self._v, C.POINTER(vp)),
+            max_pages=page_table.shape[1], num_pages=kv_pools[0].shape[0],
+            kv_pools=C.cast(self._kv, C.POINTER(vp)),
             cand_uid=_p(cand_uid), seed=int(seed), temperature=float(temperature),
             num_splits=num_splits, out_tokens=_p(self.out_tokens),
             out_logprobs=_p(self.out_logprobs), out_logits=_p(self.out_logits),
@@ -429,11 +428,11 @@ class StepBuffers:
         return self.out_tokens, self.out_logprobs
 
 
-def sevo_decode_step(model: Model, tokens, positions, page_table, k_pools, v_pools, cand_uid,
+def sevo_decode_step(model: Model, tokens, positions, page_table, kv_pools, cand_uid,
                      seed, temperature=1.0, num_splits=0, keep_logits=False, stream=None,
                      conf_topk=0, conf_sum=None, top_k=0, top_p=1.0, min_p=0.0):
     """One decode step of the population; returns (ids, logprobs[, logits][, conf])."""
-    b = StepBuffers(model, tokens, positions, page_table, k_pools, v_pools, cand_uid, seed,
+    b = StepBuffers(model, tokens, positions, page_table, kv_pools, cand_uid, seed,
                     temperature, num_splits, keep_logits, conf_topk=conf_topk, conf_sum=conf_sum,
                     top_k=top_k, top_p=top_p, min_p=min_p)
     ids, lps = b.run(stream)

@@ -281,7 +281,7 @@ def workload_population(w: Workload, extra_tokens: int = 0, shuffle: bool = True
 # ---------------------------------------------------------------- tensor kinds
 K_EMBED, K_LMHEAD, K_FINAL_NORM = 1, 2, 3
 K_ATTN_NORM, K_WQKV, K_QNORM, K_KNORM, K_WO, K_FFN_NORM, K_WGU, K_WDOWN = range(10, 18)
-K_KPOOL, K_VPOOL, K_Q = 30, 31, 32
+K_KVPOOL, K_Q = 30, 32
 
 WEIGHT_STD = 0.02
 GAIN_STD = 0.02
@@ -324,12 +324,10 @@ def global_specs(shape: ModelShape, seed: int) -> dict:
     }
 
 
-def kv_specs(shape: ModelShape, seed: int, layer: int, n_pages: int) -> tuple:
-    """K pool [P][hkv][d/32][16][32] and V pool [P][hkv][d][16], both N(0, 1)."""
-    kshape = (n_pages, shape.n_kv_heads, shape.head_dim // 32, PAGE_SIZE, 32)
-    vshape = (n_pages, shape.n_kv_heads, shape.head_dim, PAGE_SIZE)
-    return (TensorSpec(kshape, tensor_key(seed, K_KPOOL, layer), 1.0),
-            TensorSpec(vshape, tensor_key(seed, K_VPOOL, layer), 1.0))
+def kv_spec(shape: ModelShape, seed: int, layer: int, n_pages: int) -> TensorSpec:
+    """The layer's KV pool [P][hkv][2][16 d] (K tile, then V tile), N(0, 1)."""
+    return TensorSpec((n_pages, shape.n_kv_heads, 2, PAGE_SIZE * shape.head_dim),
+                      tensor_key(seed, K_KVPOOL, layer), 1.0)
 
 
 def q_spec(shape: ModelShape, seed: int, n: int) -> TensorSpec:
@@ -407,11 +405,10 @@ def host_weights(shape: ModelShape, seed: int, lazy: bool = False) -> dict:
             "layers": [layers[l] for l in range(shape.n_layers)]}
 
 
-def host_pools(shape: ModelShape, seed: int, n_pages: int, layers=None) -> tuple:
-    """Full host K and V pools (fp32 values) for the given layers."""
-    ks, vs = [], []
+def host_pools(shape: ModelShape, seed: int, n_pages: int, layers=None) -> list:
+    """Full host KV pools (fp32 values) for the given layers."""
+    out = []
     for l in (range(shape.n_layers) if layers is None else layers):
-        kspec, vspec = kv_specs(shape, seed, l, n_pages)
-        ks.append(host_values(kspec).reshape(kspec.shape))
-        vs.append(host_values(vspec).reshape(vspec.shape))
-    return ks, vs
+        spec = kv_spec(shape, seed, l, n_pages)
+        out.append(host_values(spec).reshape(spec.shape))
+    return out

@@ -27,10 +27,8 @@ def tiny_step_expected():
     shape = w.shape
     pop = synth.workload_population(w, extra_tokens=1)
     weights = synth.host_weights(shape, w.seed)
-    kp, vp = synth.host_pools(shape, w.seed, pop.n_pages)
-    kp = [k.astype(np.float64) for k in kp]
-    vp = [v.astype(np.float64) for v in vp]
-    out = od.decode_step(shape, weights, kp, vp, pop.page_table, pop.tokens, pop.lengths,
+    kvp = [p.astype(np.float64) for p in synth.host_pools(shape, w.seed, pop.n_pages)]
+    out = od.decode_step(shape, weights, kvp, pop.page_table, pop.tokens, pop.lengths,
                          pop.uids, SEED_SAMPLE, 1.0, mirror=True)
     return {
         "workload": "tiny_step", "sample_seed": SEED_SAMPLE, "temperature": 1.0,

@@ -38,11 +38,10 @@ def make_population(lengths, shuffle=True, seed=0, extra=0, vocab=4096):
 
 def host_candidate_kv(shape, seed, layer, pop, i, n_keys, n_pages_total):
     """Logical K, V [hkv, n_keys, d] of candidate i regenerated on the host."""
-    kspec, vspec = synth.kv_specs(shape, seed, layer, n_pages_total)
+    spec = synth.kv_spec(shape, seed, layer, n_pages_total)
     pages = pop.page_table[i, : (n_keys + 15) // 16]
-    kp = synth.pool_pages(kspec, pages)
-    vp = synth.pool_pages(vspec, pages)
-    return od.gather_kv(kp, vp, np.arange(len(pages)), n_keys)
+    pool = synth.pool_pages(spec, pages)
+    return od.gather_kv(pool, np.arange(len(pages)), n_keys)
 
 
 def attn_rel_err(o, ref):

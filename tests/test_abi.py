@@ -37,7 +37,7 @@ int main(void) {
   P(sevo_sample_args, conf_topk) P(sevo_sample_args, conf_sum)
   P(sevo_sample_args, workspace_bytes)
   S(sevo_step_args) P(sevo_step_args, max_pages) P(sevo_step_args, num_pages)
-  P(sevo_step_args, k_pools) P(sevo_step_args, seed) P(sevo_step_args, temperature)
+  P(sevo_step_args, kv_pools) P(sevo_step_args, seed) P(sevo_step_args, temperature)
   P(sevo_step_args, num_splits) P(sevo_step_args, out_logits) P(sevo_step_args, top_p)
   P(sevo_step_args, conf_topk)
   P(sevo_step_args, out_conf) P(sevo_step_args, workspace_bytes)
@@ -95,7 +95,7 @@ def test_attention_rejects_bad_arguments(kw, status):
 
 def test_attention_workspace_too_small_is_reported_before_launch():
     fake = 1 << 20  # never dereferenced: the check fails first
-    a = _attn(q=fake, k_pool=fake, v_pool=fake, page_table=fake, seq_lens=fake, out=fake,
+    a = _attn(q=fake, kv_pool=fake, page_table=fake, seq_lens=fake, out=fake,
               workspace=fake, workspace_bytes=16)
     assert sevo.lib().sevo_attn_decode(C.byref(a), None) == sevo.WORKSPACE_TOO_SMALL
     assert b"workspace" in sevo.lib().sevo_last_error()

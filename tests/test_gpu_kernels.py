@@ -46,13 +46,13 @@ def _attn_case(S, shape, lengths, seed, num_splits=0, shuffle=True, pt_override=
     sevo, di = S
     pop = make_population(lengths, shuffle=shuffle, seed=seed)
     pt = pop.page_table if pt_override is None else pt_override
-    ks, vs = di.device_pools(shape, seed, pop.n_pages, layers=[0])
+    kvp = di.device_pools(shape, seed, pop.n_pages, layers=[0])[0]
     q = di.device_q(shape, seed, pop.n)
     lens = torch.from_numpy(pop.lengths.astype(np.int32)).cuda()
     ptd = torch.from_numpy(pt.astype(np.int32)).cuda()
-    out = sevo.sevo_attn_decode(q, ks[0], vs[0], ptd, lens, num_splits=num_splits)
+    out = sevo.sevo_attn_decode(q, kvp, ptd, lens, num_splits=num_splits)
     torch.cuda.synchronize()
-    return pop, q, ks[0], vs[0], ptd, lens, out
+    return pop, q, kvp, ptd, lens, out
 
 
 def _oracle_attn(shape, seed, pop, i, n_keys=None):
@@ -80,7 +80,7 @@ ATTN_SMALL = [
 def test_attention_small_matches_oracle(S, hq, hkv, d, lengths, splits):
     shape = synth.ModelShape(1, 256, hq, hkv, d, 256, 256)
     say(f"attention hq={hq} hkv={hkv} d={d} lens={lengths} splits={splits}")
-    pop, q, kp, vp, pt, lens, out = _attn_case(S, shape, lengths, seed=11, num_splits=splits)
+    pop, q, kvp, pt, lens, out = _attn_case(S, shape, lengths, seed=11, num_splits=splits)
     o = to_np(out)
     for i in range(pop.n):
         ref = _oracle_attn(shape, 11, pop, i)
@@ -95,17 +95,15 @@ def test_attention_page_permutation_and_determinism_bit_exact(S):
     shape = synth.ModelShape(1, 256, 32, 8, 128, 256, 256)
     lengths = [900, 33, 1600, 17]
     say("attention permutation / determinism")
-    pop, q, kp, vp, pt, lens, out1 = _attn_case(S, shape, lengths, seed=5, shuffle=False)
-    out2 = sevo.sevo_attn_decode(q, kp, vp, pt, lens)
+    pop, q, kvp, pt, lens, out1 = _attn_case(S, shape, lengths, seed=5, shuffle=False)
+    out2 = sevo.sevo_attn_decode(q, kvp, pt, lens)
     # physically permute the pages and the page table the same way
     perm = torch.randperm(pop.n_pages, generator=torch.Generator().manual_seed(3))
-    kp2 = torch.empty_like(kp)
-    vp2 = torch.empty_like(vp)
-    kp2[perm.cuda()] = kp
-    vp2[perm.cuda()] = vp
+    kvp2 = torch.empty_like(kvp)
+    kvp2[perm.cuda()] = kvp
     pt_np = pop.page_table.copy()
     pt_np[pt_np >= 0] = perm.numpy()[pt_np[pt_np >= 0]]
-    out3 = sevo.sevo_attn_decode(q, kp2, vp2, torch.from_numpy(pt_np).cuda(), lens)
+    out3 = sevo.sevo_attn_decode(q, kvp2, torch.from_numpy(pt_np).cuda(), lens)
     torch.cuda.synchronize()
     np.testing.assert_array_equal(bf16_bits(out1), bf16_bits(out2))
     np.testing.assert_array_equal(bf16_bits(out1), bf16_bits(out3))
@@ -115,10 +113,10 @@ def test_attention_split_count_changes_only_rounding(S):
     sevo, di = S
     shape = synth.ModelShape(1, 256, 32, 8, 128, 256, 256)
     say("attention split counts")
-    pop, q, kp, vp, pt, lens, out1 = _attn_case(S, shape, [3000, 2500, 100], seed=6,
-                                                num_splits=1)
+    pop, q, kvp, pt, lens, out1 = _attn_case(S, shape, [3000, 2500, 100], seed=6,
+                                             num_splits=1)
     for s in (2, 5, 16, 0):
-        o = sevo.sevo_attn_decode(q, kp, vp, pt, lens, num_splits=s)
+        o = sevo.sevo_attn_decode(q, kvp, pt, lens, num_splits=s)
         torch.cuda.synchronize()
         d = np.abs(to_np(o) - to_np(out1)).max() / np.abs(to_np(out1)).max()
         assert d < 4e-3, (s, d)
@@ -134,7 +132,7 @@ def test_attention_out_of_range_page_ids_are_skipped(S):
     bad[0, 3] = pop.n_pages + 1000      # keys 48..63 of candidate 0
     bad[1, 0] = -7                      # keys 0..15 of candidate 1
     say("attention bad page ids")
-    _, q, kp, vp, pt, lens, out = _attn_case(S, shape, lengths, seed=8, pt_override=bad)
+    _, q, kvp, pt, lens, out = _attn_case(S, shape, lengths, seed=8, pt_override=bad)
     o = to_np(out)
     qh = synth.host_values(synth.q_spec(shape, 8, 2)).reshape(2, 16, 128)
     for i, drop in ((0, range(48, 64)), (1, range(0, 16))):
@@ -148,7 +146,7 @@ def test_attention_zero_length_candidate_gives_zero(S):
     """A candidate with no cached keys yields o = 0 and never disturbs the others."""
     shape = synth.ModelShape(1, 256, 32, 8, 128, 256, 256)
     say("attention with a zero-length candidate")
-    pop, q, kp, vp, pt, lens, out = _attn_case(S, shape, [0, 40, 0, 300], seed=12)
+    pop, q, kvp, pt, lens, out = _attn_case(S, shape, [0, 40, 0, 300], seed=12)
     o = to_np(out)
     assert np.all(o[0] == 0) and np.all(o[2] == 0)
     for i in (1, 3):
@@ -167,11 +165,11 @@ def test_attention_full_size_sampled(S, workload, sample):
     shape = w.shape
     pop = synth.workload_population(w)
     say(f"attention full size {workload}: N={pop.n} pages={pop.n_pages}")
-    ks, vs = di.device_pools(shape, w.seed, pop.n_pages, layers=[0])
+    kvp = di.device_pools(shape, w.seed, pop.n_pages, layers=[0])[0]
     q = di.device_q(shape, w.seed, pop.n)
     lens = torch.from_numpy(pop.lengths.astype(np.int32)).cuda()
     pt = torch.from_numpy(pop.page_table).cuda()
-    out = sevo.sevo_attn_decode(q, ks[0], vs[0], pt, lens)
+    out = sevo.sevo_attn_decode(q, kvp, pt, lens)
     torch.cuda.synchronize()
     o = to_np(out)
     if sample is None:

@@ -27,9 +27,18 @@ def _setup(S, w, extra, n=None, shape=None):
     pop = synth.workload_population(w, extra_tokens=extra, n=n)
     tensors = di.device_weights(shape, w.seed)
     model = sevo.sevo_init_model(shape, tensors, max_position=int(pop.lengths.max()) + extra + 1)
-    kp, vp = di.device_pools(shape, w.seed, pop.n_pages)
+    kvp = di.device_pools(shape, w.seed, pop.n_pages)
     d = di.device_population(pop)
-    return pop, model, kp, vp, d
+    return pop, model, kvp, d
+
+
+def _token_major(pool, d):
+    """K and V of every (page, head, slot) of a pool [P, hkv, 2, 16 d] as
+    [P, hkv, 16, d] arrays (tile offsets of the documented layout)."""
+    s = np.arange(16)[:, None]
+    e = np.arange(d)[None, :]
+    return (pool[:, :, 0, :][:, :, ((e // 32) * 16 + s) * 32 + e % 32],
+            pool[:, :, 1, :][:, :, e * 16 + s])
 
 
 def test_tiny_step_sequence_matches_oracle(S):
@@ -40,11 +49,9 @@ def test_tiny_step_sequence_matches_oracle(S):
     shape = w.shape
     steps = 3
     say("tiny step sequence")
-    pop, model, kp, vp, d = _setup(S, w, extra=steps)
+    pop, model, kvp, d = _setup(S, w, extra=steps)
     hw = synth.host_weights(shape, w.seed)
-    hk, hv = synth.host_pools(shape, w.seed, pop.n_pages)
-    hk = [k.astype(np.float64) for k in hk]
-    hv = [v.astype(np.float64) for v in hv]
+    hkv = [p.astype(np.float64) for p in synth.host_pools(shape, w.seed, pop.n_pages)]
     seed, temp = 99, 1.0
     toks = pop.tokens.astype(np.int64)
     pos = pop.lengths.astype(np.int64)
@@ -53,10 +60,10 @@ def test_tiny_step_sequence_matches_oracle(S):
     ref_conf_sum = np.zeros(pop.n)
     for step in range(steps):
         ids, lps, logits, conf = sevo.sevo_decode_step(
-            model, torch.from_numpy(toks.astype(np.int32)).cuda(), pos_d, d["page_table"], kp, vp,
+            model, torch.from_numpy(toks.astype(np.int32)).cuda(), pos_d, d["page_table"], kvp,
             d["uids"], seed, temp, keep_logits=True, conf_topk=20, conf_sum=conf_sum)
         torch.cuda.synchronize()
-        ref = od.decode_step(shape, hw, hk, hv, pop.page_table, toks, pos, pop.uids, seed, temp)
+        ref = od.decode_step(shape, hw, hkv, pop.page_table, toks, pos, pop.uids, seed, temp)
         # the step's self-confidence (Eq. 1) follows the logits it came from
         rc = od.token_confidence(ref["logits"], 20)
         ref_conf_sum += rc
@@ -82,24 +89,19 @@ def test_tiny_step_sequence_matches_oracle(S):
     # appended slots: close to the oracle's; every other slot untouched
     torch.cuda.synchronize()
     for l in range(shape.n_layers):
-        def tok_major(a):   # [P, hkv, d/32, 16, 32] -> [P, hkv, 16, d]
-            return np.transpose(a, (0, 1, 3, 2, 4)).reshape(a.shape[0], a.shape[1], 16, -1)
-        gk = tok_major(kp[l].double().cpu().numpy())
-        gv = vp[l].double().cpu().numpy()
-        kspec, vspec = synth.kv_specs(shape, w.seed, l, pop.n_pages)
-        k0 = tok_major(synth.host_values(kspec).reshape(kspec.shape))
-        v0 = synth.host_values(vspec).reshape(vspec.shape)
-        hkl = tok_major(hk[l])
+        D = shape.head_dim
+        gk, gv = _token_major(kvp[l].double().cpu().numpy(), D)
+        spec = synth.kv_spec(shape, w.seed, l, pop.n_pages)
+        k0, v0 = _token_major(synth.host_values(spec).reshape(spec.shape), D)
+        hk, hv = _token_major(hkv[l], D)
         written = np.zeros(gk.shape[:3], bool)   # [page, head, slot]
         for i in range(pop.n):
             for p in range(int(pop.lengths[i]), int(pop.lengths[i]) + steps):
                 written[pop.page_table[i, p // 16], :, p % 16] = True
         np.testing.assert_array_equal(gk[~written], k0[~written])
-        np.testing.assert_array_equal(np.transpose(gv, (0, 1, 3, 2))[~written],
-                                      np.transpose(v0, (0, 1, 3, 2))[~written])
-        gkw, rkw = gk[written], hkl[written]
-        gvw = np.transpose(gv, (0, 1, 3, 2))[written]
-        rvw = np.transpose(hv[l], (0, 1, 3, 2))[written]
+        np.testing.assert_array_equal(gv[~written], v0[~written])
+        gkw, rkw = gk[written], hk[written]
+        gvw, rvw = gv[written], hv[written]
         say(f"  layer {l}: appended k max diff {np.abs(gkw - rkw).max():.2e}, "
             f"v {np.abs(gvw - rvw).max():.2e}; equal {np.mean(gkw == rkw):.3f} / "
             f"{np.mean(gvw == rvw):.3f}")
@@ -116,7 +118,7 @@ def test_tiny_step_deterministic_and_resumable(S):
     say("tiny step determinism / resume")
 
     def run(steps_a, steps_b):
-        pop, model, kp, vp, d = _setup(S, w, extra=4)
+        pop, model, kvp, d = _setup(S, w, extra=4)
         toks = torch.from_numpy(pop.tokens).cuda()
         pos = d["lengths"].clone()
         out = []
@@ -125,14 +127,14 @@ def test_tiny_step_deterministic_and_resumable(S):
                 # resume: a fresh model handle over the same device state
                 model.close()
                 model = sevo.sevo_init_model(w.shape, model.tensors, max_position=1024)
-            ids, lps = sevo.sevo_decode_step(model, toks, pos, d["page_table"], kp, vp, d["uids"],
+            ids, lps = sevo.sevo_decode_step(model, toks, pos, d["page_table"], kvp, d["uids"],
                                              1234, 1.0)
             torch.cuda.synchronize()
             out.append((ids.cpu().numpy().copy(), lps.cpu().numpy().copy()))
             toks = ids.clone()
             pos += 1
         model.close()
-        return out, [bf16_bits(k) for k in kp]
+        return out, [bf16_bits(k) for k in kvp]
 
     a, ka = run(4, 0)
     b, kb = run(2, 2)
@@ -147,9 +149,9 @@ def test_step_rejects_small_workspace_and_bad_temperature(S):
     sevo, di = S
     import ctypes as C
     w = synth.WORKLOADS["tiny_step"]
-    pop, model, kp, vp, d = _setup(S, w, extra=1)
+    pop, model, kvp, d = _setup(S, w, extra=1)
     b = sevo.StepBuffers(model, torch.from_numpy(pop.tokens).cuda(), d["lengths"],
-                         d["page_table"], kp, vp, d["uids"], 1, 1.0)
+                         d["page_table"], kvp, d["uids"], 1, 1.0)
     b.args.workspace_bytes = 1024
     assert sevo.lib().sevo_decode_step(model.handle, C.byref(b.args), None) == \
         sevo.WORKSPACE_TOO_SMALL
@@ -161,24 +163,21 @@ def test_step_rejects_small_workspace_and_bad_temperature(S):
 
 
 def _subset_host_state(shape, seed, pop, idx, layers):
-    """Host K/V pools holding only the pages of candidates ``idx`` (the slot the
+    """Host KV pools holding only the pages of candidates ``idx`` (the slot the
     step appends included), compacted, with a matching page table."""
     need = (pop.lengths[idx].astype(np.int64) + pop.extra_tokens + 15) // 16
     pt = np.full((len(idx), int(need.max())), -1, np.int64)
-    kp = [np.empty((int(need.sum()), shape.n_kv_heads, shape.head_dim // 32, 16, 32))
-          for _ in range(layers)]
-    vp = [np.empty((int(need.sum()), shape.n_kv_heads, shape.head_dim, 16))
-          for _ in range(layers)]
+    kvp = [np.empty((int(need.sum()), shape.n_kv_heads, 2, 16 * shape.head_dim))
+           for _ in range(layers)]
     c = 0
     for j, i in enumerate(idx):
         pages = pop.page_table[i, :need[j]]
         for l in range(layers):
-            kspec, vspec = synth.kv_specs(shape, seed, l, pop.n_pages)
-            kp[l][c:c + need[j]] = synth.pool_pages(kspec, pages)
-            vp[l][c:c + need[j]] = synth.pool_pages(vspec, pages)
+            kvp[l][c:c + need[j]] = synth.pool_pages(synth.kv_spec(shape, seed, l, pop.n_pages),
+                                                      pages)
         pt[j, :need[j]] = np.arange(c, c + need[j])
         c += need[j]
-    return kp, vp, pt
+    return kvp, pt
 
 
 # Full-width tolerances.  bf16 storage turns any difference in the last fp32
@@ -208,10 +207,10 @@ def test_full_width_step_reduced_depth(S, workload, layers):
     w = synth.WORKLOADS[workload]
     shape = dataclasses.replace(w.shape, n_layers=layers)
     say(f"full-width step {workload} at {layers} layers")
-    pop, model, kp, vp, d = _setup(S, w, extra=1, shape=shape)
+    pop, model, kvp, d = _setup(S, w, extra=1, shape=shape)
     seed, temp = 77, 1.0
     ids, lps, logits = sevo.sevo_decode_step(model, d["tokens"], d["lengths"], d["page_table"],
-                                             kp, vp, d["uids"], seed, temp, keep_logits=True)
+                                             kvp, d["uids"], seed, temp, keep_logits=True)
     torch.cuda.synchronize()
     idx = sorted({int(np.argmin(pop.lengths)), int(np.argmax(pop.lengths)), 1})
     g_logits = logits.double().cpu().numpy()[idx]
@@ -219,13 +218,13 @@ def test_full_width_step_reduced_depth(S, workload, layers):
     g_lps = lps.cpu().numpy()[idx]
     assert np.isfinite(logits.cpu().numpy()).all()
     model.close()
-    del kp, vp
+    del kvp
     torch.cuda.empty_cache()
-    hk, hv, hpt = _subset_host_state(shape, w.seed, pop, idx, layers)
+    hkv, hpt = _subset_host_state(shape, w.seed, pop, idx, layers)
     hw = synth.host_weights(shape, w.seed, lazy=True)
     hw = {"embed": hw["embed"], "final_norm": hw["final_norm"], "layers": hw["layers"],
           "lm_head": hw["lm_head"][0:shape.vocab]}
-    ref = od.decode_step(shape, hw, hk, hv, hpt, pop.tokens[idx], pop.lengths[idx],
+    ref = od.decode_step(shape, hw, hkv, hpt, pop.tokens[idx], pop.lengths[idx],
                          pop.uids[idx], seed, temp)
     err = np.abs(g_logits - ref["logits"]).max()
     lp_err = np.abs(g_lps - ref["lps"]).max()
@@ -250,11 +249,11 @@ def test_step_kernel_timing_counts_every_launch(S):
     sevo, di = S
     w = synth.WORKLOADS["tiny_step"]
     say("step kernel timing")
-    pop, model, kp, vp, d = _setup(S, w, extra=2)
+    pop, model, kvp, d = _setup(S, w, extra=2)
     toks = torch.from_numpy(pop.tokens).cuda()
     L = w.shape.n_layers
     sevo.sevo_profile_begin(64, sevo.PROF_KINDS)
-    sevo.sevo_decode_step(model, toks, d["lengths"], d["page_table"], kp, vp, d["uids"], 5, 1.0)
+    sevo.sevo_decode_step(model, toks, d["lengths"], d["page_table"], kvp, d["uids"], 5, 1.0)
     prof = sevo.sevo_profile_end()
     want = {"attn_split": L, "attn_combine": L, "qkv": L, "attn_out": L, "gate_up": L, "down": L,
             "lm_head": 1, "norm": 2 * L + 1, "rope_append": L, "sample": 1, "embed": 1}
@@ -262,6 +261,6 @@ def test_step_kernel_timing_counts_every_launch(S):
     assert all(ms > 0 for ms, c in prof.values())
     # a recording of one kind times only that kind
     sevo.sevo_profile_begin(8, ["lm_head"])
-    sevo.sevo_decode_step(model, toks, d["lengths"], d["page_table"], kp, vp, d["uids"], 5, 1.0)
+    sevo.sevo_decode_step(model, toks, d["lengths"], d["page_table"], kvp, d["uids"], 5, 1.0)
     assert list(sevo.sevo_profile_end()) == ["lm_head"]
     model.close()

@@ -73,10 +73,8 @@ def _hf_model(shape, w):
 
 
 def _empty_pools(shape, n_pages):
-    kp = [np.zeros((n_pages, shape.n_kv_heads, shape.head_dim // 32, 16, 32))
-          for _ in range(shape.n_layers)]
-    vp = [np.zeros((n_pages, shape.n_kv_heads, shape.head_dim, 16)) for _ in range(shape.n_layers)]
-    return kp, vp
+    return [np.zeros((n_pages, shape.n_kv_heads, 2, 16 * shape.head_dim))
+            for _ in range(shape.n_layers)]
 
 
 def test_incremental_paged_decode_equals_transformers_causal_forward():
@@ -87,10 +85,10 @@ def test_incremental_paged_decode_equals_transformers_causal_forward():
     pages_per = (T + 15) // 16
     perm = rng.permutation(N * pages_per)
     pt = perm.reshape(N, pages_per)
-    kp, vp = _empty_pools(SHAPE, N * pages_per)
+    kvp = _empty_pools(SHAPE, N * pages_per)
     oracle_logits = np.empty((N, T, SHAPE.vocab))
     for t in range(T):
-        out = od.decode_step(SHAPE, w, kp, vp, pt, seqs[:, t], np.full(N, t), np.arange(N),
+        out = od.decode_step(SHAPE, w, kvp, pt, seqs[:, t], np.full(N, t), np.arange(N),
                              seed=1, temperature=1.0, mirror=False)
         oracle_logits[:, t] = out["logits"]
     m = _hf_model(SHAPE, w)
@@ -109,24 +107,22 @@ def test_whole_step_invariant_under_page_permutation_and_deterministic():
     lens = np.array([5, 33, 20])
     need = (lens + 1 + 15) // 16
     P = int(need.sum())
-    kp = [rng.standard_normal((P, 2, 1, 16, 32)) for _ in range(2)]
-    vp = [rng.standard_normal((P, 2, 32, 16)) for _ in range(2)]
+    kvp = [rng.standard_normal((P, 2, 2, 16 * 32)) for _ in range(2)]
     pt = np.full((N, need.max()), -1)
     c = 0
     for i in range(N):
         pt[i, :need[i]] = np.arange(c, c + need[i])
         c += need[i]
     perm = rng.permutation(P)
-    kp2, vp2 = [], []
+    kvp2 = []
     for l in range(2):
-        a = np.empty_like(kp[l]); a[perm] = kp[l]; kp2.append(a)
-        b = np.empty_like(vp[l]); b[perm] = vp[l]; vp2.append(b)
+        a = np.empty_like(kvp[l]); a[perm] = kvp[l]; kvp2.append(a)
     pt2 = np.where(pt >= 0, perm[np.maximum(pt, 0)], -1)
     toks = np.array([1, 50, 96])
     args = dict(tokens=toks, positions=lens, uids=np.array([10, 11, 12]), seed=3, temperature=1.0)
-    a = od.decode_step(SHAPE, w, [k.copy() for k in kp], [v.copy() for v in vp], pt, **args)
-    b = od.decode_step(SHAPE, w, kp2, vp2, pt2, **args)
-    c2 = od.decode_step(SHAPE, w, [k.copy() for k in kp], [v.copy() for v in vp], pt, **args)
+    a = od.decode_step(SHAPE, w, [k.copy() for k in kvp], pt, **args)
+    b = od.decode_step(SHAPE, w, kvp2, pt2, **args)
+    c2 = od.decode_step(SHAPE, w, [k.copy() for k in kvp], pt, **args)
     np.testing.assert_array_equal(a["logits"], b["logits"])
     np.testing.assert_array_equal(a["ids"], b["ids"])
     np.testing.assert_array_equal(a["logits"], c2["logits"])
@@ -140,12 +136,12 @@ def test_zero_blocks_reduce_to_embedding_head():
     for lw in w["layers"]:
         lw["w_o"] = np.zeros_like(lw["w_o"])
         lw["w_down"] = np.zeros_like(lw["w_down"])
-    kp, vp = _empty_pools(SHAPE, 4)
-    for k in kp + vp:
+    kvp = _empty_pools(SHAPE, 4)
+    for k in kvp:
         k[:] = rng.standard_normal(k.shape)
     pt = np.array([[0, 1], [2, 3]])
     toks = np.array([3, 40])
-    out = od.decode_step(SHAPE, w, kp, vp, pt, toks, np.array([20, 7]), np.array([0, 1]), 0, 1.0,
+    out = od.decode_step(SHAPE, w, kvp, pt, toks, np.array([20, 7]), np.array([0, 1]), 0, 1.0,
                          mirror=False)
     x = w["embed"][toks]
     hf = x / np.sqrt((x * x).mean(-1, keepdims=True) + SHAPE.rms_eps) * w["final_norm"]
@@ -157,15 +153,13 @@ def test_mirror_rounds_only_storage_points():
     small but non-zero relative change of the logits."""
     rng = np.random.default_rng(10)
     w = _weights(SHAPE, rng)
-    kp, vp = _empty_pools(SHAPE, 4)
-    for k in kp + vp:
+    kvp = _empty_pools(SHAPE, 4)
+    for k in kvp:
         k[:] = rng.standard_normal(k.shape)
     pt = np.array([[0, 1], [2, 3]])
     args = dict(tokens=np.array([3, 40]), positions=np.array([20, 7]), uids=np.array([0, 1]),
                 seed=0, temperature=1.0)
-    a = od.decode_step(SHAPE, w, [k.copy() for k in kp], [v.copy() for v in vp], pt,
-                       mirror=False, **args)
-    b = od.decode_step(SHAPE, w, [k.copy() for k in kp], [v.copy() for v in vp], pt,
-                       mirror=True, **args)
+    a = od.decode_step(SHAPE, w, [k.copy() for k in kvp], pt, mirror=False, **args)
+    b = od.decode_step(SHAPE, w, [k.copy() for k in kvp], pt, mirror=True, **args)
     rel = np.abs(a["logits"] - b["logits"]).max() / np.abs(a["logits"]).max()
     assert 1e-5 < rel < 5e-2, rel

@@ -313,23 +313,25 @@ def test_split_equals_unsplit(L, S):
 
 
 def _random_pool(n_pages, hkv, d):
-    return (RNG.standard_normal((n_pages, hkv, d // 32, 16, 32)),
-            RNG.standard_normal((n_pages, hkv, d, 16)))
+    return RNG.standard_normal((n_pages, hkv, 2, 16 * d))
 
 
 def test_gather_layout_by_hand():
-    kp, vp = _random_pool(5, 2, 64)
+    kvp = _random_pool(5, 2, 64)
     pages = np.array([3, 0, 4])
-    K, V = od.gather_kv(kp, vp, pages, 35)
-    assert K.shape == (2, 35, 64)
+    K, V = od.gather_kv(kvp, pages, 35)
+    assert K.shape == (2, 35, 64) and V.shape == (2, 35, 64)
     # key 20 lives in logical page 1 -> physical 0, slot 4; dim 40 is in dim
-    # block 1 at offset 8: flat tile position (1 * 16 + 4) * 32 + 8
-    flat = kp.reshape(5, 2, -1)
-    assert K[1, 20, 40] == flat[0, 1, (1 * 16 + 4) * 32 + 8]
-    np.testing.assert_array_equal(K[1, 20], np.concatenate([kp[0, 1, 0, 4], kp[0, 1, 1, 4]]))
-    np.testing.assert_array_equal(V[1, 20], vp[0, 1, :, 4])
-    assert K[0, 34, 3] == flat[4, 0, 2 * 32 + 3]
-    np.testing.assert_array_equal(V[0, 0], vp[3, 0, :, 0])
+    # block 1 at offset 8: K tile position (1 * 16 + 4) * 32 + 8
+    assert K[1, 20, 40] == kvp[0, 1, 0, (1 * 16 + 4) * 32 + 8]
+    # V tile is dim-major: dim 40, slot 4 at 40 * 16 + 4
+    assert V[1, 20, 40] == kvp[0, 1, 1, 40 * 16 + 4]
+    # key 34: logical page 2 -> physical 4, slot 2; dim 3 in block 0
+    assert K[0, 34, 3] == kvp[4, 0, 0, 2 * 32 + 3]
+    np.testing.assert_array_equal(V[0, 0], kvp[3, 0, 1, np.arange(64) * 16])
+    # one K row of a slot is two 32-dim runs of the tile
+    np.testing.assert_array_equal(K[1, 20], np.concatenate([kvp[0, 1, 0, 4 * 32:5 * 32],
+                                                           kvp[0, 1, 0, 20 * 32:21 * 32]]))
 
 
 def test_paging_invariant_under_physical_permutation():
@@ -337,38 +339,43 @@ def test_paging_invariant_under_physical_permutation():
     lens = np.array([16, 45, 70])
     need = (lens + 15) // 16
     P = int(need.sum())
-    kp, vp = _random_pool(P, hkv, d)
+    kvp = _random_pool(P, hkv, d)
     pt_id = np.full((N, need.max()), -1)
     c = 0
     for i in range(N):
         pt_id[i, : need[i]] = np.arange(c, c + need[i])
         c += need[i]
     perm = RNG.permutation(P)          # logical page L now lives at physical perm[L]
-    kp2 = np.empty_like(kp)
-    vp2 = np.empty_like(vp)
-    kp2[perm] = kp
-    vp2[perm] = vp
+    kvp2 = np.empty_like(kvp)
+    kvp2[perm] = kvp
     pt2 = np.where(pt_id >= 0, perm[np.maximum(pt_id, 0)], -1)
     q = RNG.standard_normal((N, hq, d))
-    a = od.paged_attention(q, kp, vp, pt_id, lens, 0.25)
-    b = od.paged_attention(q, kp2, vp2, pt2, lens, 0.25)
+    a = od.paged_attention(q, kvp, pt_id, lens, 0.25)
+    b = od.paged_attention(q, kvp2, pt2, lens, 0.25)
     np.testing.assert_array_equal(a, b)
 
 
 def test_append_writes_exactly_one_slot():
-    kp, vp = _random_pool(6, 2, 64)
-    k0, v0 = kp.copy(), vp.copy()
+    kvp = _random_pool(6, 2, 64)
+    kv0 = kvp.copy()
     pt = np.array([[5, 1], [0, 3]])
     pos = np.array([17, 9])
     k = RNG.standard_normal((2, 2, 64))
     v = RNG.standard_normal((2, 2, 64))
-    od.append_kv(kp, vp, pt, pos, k, v)
-    changed_k = np.argwhere((kp != k0).any(axis=(2, 4)))     # [page, head, slot]
-    assert sorted(map(tuple, changed_k.tolist())) == [(0, 0, 9), (0, 1, 9), (1, 0, 1), (1, 1, 1)]
-    assert int((kp != k0).sum()) == 4 * 64
-    np.testing.assert_array_equal(kp[1, :, :, 1, :].reshape(2, 64), k[0])
-    np.testing.assert_array_equal(vp[0, :, :, 9], v[1])
-    assert int(((vp != v0).any(axis=-2)).sum()) == 4
+    od.append_kv(kvp, pt, pos, k, v)
+    changed = np.argwhere(kvp != kv0)                 # [page, head, K|V, position]
+    assert int(len(changed)) == 2 * 2 * 2 * 64
+    assert sorted(set(map(tuple, changed[:, :2].tolist()))) == [(0, 0), (0, 1), (1, 0), (1, 1)]
+    K, V = od.gather_kv(kvp, pt[0], 18)               # candidate 0, key 17: page 1, slot 1
+    np.testing.assert_array_equal(K[:, 17], k[0])
+    np.testing.assert_array_equal(V[:, 17], v[0])
+    K, V = od.gather_kv(kvp, pt[1], 10)               # candidate 1, key 9: page 0, slot 9
+    np.testing.assert_array_equal(K[:, 9], k[1])
+    np.testing.assert_array_equal(V[:, 9], v[1])
+    # K values sit at the slot's tile positions, V values at the dim-major ones
+    np.testing.assert_array_equal(kvp[1, 0, 0, (np.arange(64) // 32 * 16 + 1) * 32 + np.arange(64) % 32],
+                                  k[0, 0])
+    np.testing.assert_array_equal(kvp[0, 1, 1, np.arange(64) * 16 + 9], v[1, 1])
 
 
 # ---------------------------------------------------------------- confidence (Eq. 1, 2)
