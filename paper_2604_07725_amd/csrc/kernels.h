@@ -79,6 +79,13 @@ hipError_t launch_linear(int m, int n_out, int k, int ldx, int x_tiled, int mode
 hipError_t launch_linear_partials(int m, int n_out, int k, int ldx, int x_tiled,
                                   const LinearPlan& plan, const bf16_t* x, const bf16_t* w,
                                   float* out, int accumulate, hipStream_t st);
+// ---- gemm_large.hip: one-pass Y = X W^T for large M (prefill token counts),
+// same operand layouts and epilogue modes as launch_linear (no workspace)
+constexpr int kLargeGemmMinM = 256;
+bool gemm_large_supported(int m, int n_out, int k);
+hipError_t launch_gemm_large(int m, int n_out, int k, int ldx, int x_tiled, int mode,
+                             const bf16_t* x, const bf16_t* w, void* out, int out_tiled,
+                             hipStream_t st);
 // row-major [n_out][k] -> packed weight layout; gate_up: rows 0..n_out/2-1 are
 // gate rows and the rest up rows, interleaved per superblock (32 + 32)
 hipError_t launch_pack_weight(const bf16_t* src, bf16_t* dst, int n_out, int k, int gate_up,

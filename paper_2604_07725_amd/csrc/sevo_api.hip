@@ -463,6 +463,13 @@ SEVO_API sevo_status sevo_linear(const sevo_linear_args* a, void* stream) {
   if (a->m == 0) return SEVO_OK;
   if (!a->x || !a->w || !a->out || !aligned16(a->x) || !aligned16(a->w) || !aligned16(a->out))
     return fail(SEVO_ERR_INVALID_ARGUMENT, "null or misaligned pointer");
+  if (a->m >= sevo::kLargeGemmMinM && sevo::gemm_large_supported(a->m, a->n_out, a->k)) {
+    hipError_t e = sevo::launch_gemm_large(
+        a->m, a->n_out, a->k, a->ldx, (a->flags & SEVO_LINEAR_X_TILED) ? 1 : 0, a->mode,
+        static_cast<const sevo::bf16_t*>(a->x), static_cast<const sevo::bf16_t*>(a->w), a->out,
+        (a->flags & SEVO_LINEAR_OUT_TILED) ? 1 : 0, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? SEVO_OK : hip_fail(e, "sevo_linear (large m)");
+  }
   const sevo::LinearPlan plan = sevo::plan_linear(a->m, a->n_out, a->k, a->k_splits, a->mode);
   const size_t need = sevo::linear_workspace_bytes(a->m, a->n_out, a->k, a->k_splits, a->mode);
   if (need > 0) {

@@ -348,6 +348,11 @@ LINEAR_CASES = [
     (64, 24576, 4096, 2, 0, 1), (16, 4096, 4096, 1, 0, 0), (100, 128, 256, 0, 2, 1),
     # k not a multiple of 128: per-wave step counts differ, short tails
     (5, 128, 96, 0, 0, 0), (20, 256, 160, 1, 0, 1), (3, 128, 32, 2, 0, 1), (40, 192, 352, 0, 2, 0),
+    # m >= 256 with k % 64 == 0: the large-M kernel (256 x 256 tiles, 64-k
+    # stages); one exact tile, ragged m and n tails, row-major X, prefill shapes
+    (256, 256, 64, 0, 0, 1), (300, 320, 128, 0, 0, 1), (777, 448, 192, 1, 0, 0),
+    (513, 640, 256, 2, 0, 1), (1024, 6144, 4096, 0, 0, 1), (1000, 4096, 12288, 1, 0, 1),
+    (600, 2048, 1024, 2, 0, 0), (255, 128, 64, 0, 0, 1),
 ]
 
 
@@ -414,12 +419,14 @@ def test_pack_weight_bit_exact(S, n_out, k, gate_up):
     np.testing.assert_array_equal(bf16_bits(wp).reshape(n_out, k), pack_weight_host(bits, gate_up))
 
 
-def test_swiglu_tiled_output_and_tiled_chain(S):
+@pytest.mark.parametrize("m", [37, 600])
+def test_swiglu_tiled_output_and_tiled_chain(S, m):
     """SwiGLU written in the tiled layout equals the row-major result, and feeds
-    the next projection as a tiled input (the decode step's FFN chain)."""
+    the next projection as a tiled input (the decode step's FFN chain; m = 600
+    takes the large-M kernel)."""
     sevo, _ = S
-    m, F2, H = 37, 512, 256
-    say("swiglu tiled chain")
+    F2, H = 512, 256
+    say(f"swiglu tiled chain m={m}")
     x, _, wp, _, _ = _linear_inputs(sevo, m, F2, H, 2)
     a_row = sevo.sevo_linear(x, wp, mode=2)
     a_til = sevo.sevo_linear(x, wp, mode=2, out_tiled=True)
