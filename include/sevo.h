@@ -170,6 +170,46 @@ int32_t sevo_attn_plan_splits(int32_t n, int32_t n_kv_heads, int32_t max_pages);
 size_t sevo_attn_workspace_bytes(int32_t n, int32_t n_q_heads, int32_t n_kv_heads,
                                  int32_t head_dim, int32_t max_pages, int32_t num_splits);
 
+/* ------------------------------------------------------------------ prefill */
+
+/* Causal GQA attention of a prefill: the forward pass the cross-model
+ * confidence engine runs over a whole prompt + trajectory (the "Confidence
+ * engine" paragraph of the System Implementation subsection; the prefill
+ * engine appendix), for a batch of sequences back to back.  Token t of
+ * sequence s sits at position pos(t) = start_pos[s] + (t - seq_starts[s]) and
+ * attends to every key up to its own position:
+ *   o[t][j] = softmax_{u <= pos(t)}(scale * q[t][j] . K_s[c][u]) V_s[c][u],
+ * c = j / (n_q_heads / n_kv_heads), keys read from the paged pool through row
+ * s of the page table.  The keys and values of positions 0..pos(t) must be in
+ * the pool already (sevo_qk_norm_rope_append writes a prefill's own keys).
+ *   q          bf16 [total_tokens][n_q_heads][head_dim]
+ *   kv_pool    paged layout above (bf16)
+ *   page_table int32 [n_seqs][max_pages]
+ *   seq_starts int32 [n_seqs + 1] (device): non-decreasing token offsets,
+ *              seq_starts[0] = 0, seq_starts[n_seqs] = total_tokens
+ *   start_pos  int32 [n_seqs] (device) or NULL (every sequence starts at 0)
+ *   out        bf16 [total_tokens][n_q_heads][head_dim]
+ *   max_seq_len (host) >= every sequence length: sizes the grid (rows of a
+ *              longer sequence past it are not computed)
+ * The probabilities are rounded to bf16 for the P V product (fp32
+ * accumulation; the softmax statistics stay fp32).  Page ids outside
+ * [0, num_pages) contribute zero keys and values (they are never read).
+ * Device arrays are not validated.  Errors: INVALID_ARGUMENT, UNSUPPORTED, HIP. */
+typedef struct {
+  int32_t n_seqs, total_tokens, max_seq_len;
+  int32_t n_q_heads, n_kv_heads, head_dim, page_size, max_pages;
+  int64_t num_pages;
+  const void* q;
+  const void* kv_pool;
+  const int32_t* page_table;
+  const int32_t* seq_starts;
+  const int32_t* start_pos;
+  float scale;
+  void* out;
+} sevo_prefill_attn_args;
+
+sevo_status sevo_attn_prefill(const sevo_prefill_attn_args* a, void* stream);
+
 /* ------------------------------------------------------------------ sampling */
 
 /* Full-vocabulary log-softmax and Gumbel-max sample, per candidate i:

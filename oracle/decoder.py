@@ -187,6 +187,25 @@ def paged_attention(q, kv_pool, page_table, seq_lens, scale):
     return out
 
 
+def prefill_attention(q, kv_pool, page_table, seq_starts, start_pos, scale):
+    """Causal attention of a prefill batch (the scoring pass of the confidence
+    engine): token t of sequence s sits at position start_pos[s] + t -
+    seq_starts[s] and attends to the keys 0..that position of the sequence
+    (page-table row s).  q [T, hq, d] -> [T, hq, d]."""
+    q = np.asarray(q, np.float64)
+    out = np.empty_like(q)
+    for s in range(len(seq_starts) - 1):
+        a, b = int(seq_starts[s]), int(seq_starts[s + 1])
+        if b <= a:
+            continue
+        p0 = 0 if start_pos is None else int(start_pos[s])
+        K, V = gather_kv(kv_pool, page_table[s], p0 + b - a)
+        for t in range(a, b):
+            n = p0 + (t - a) + 1
+            out[t] = attention_dense(q[t], K[:, :n], V[:, :n], scale)
+    return out
+
+
 def append_kv(kv_pool, page_table, positions, k, v):
     """Write key/value number p_i of every candidate into its page slot."""
     d = np.asarray(k).shape[-1]

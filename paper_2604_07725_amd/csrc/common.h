@@ -125,4 +125,36 @@ __device__ __forceinline__ float block_sum(float v, float* red) {
   return t;
 }
 
+// ---- wait counters and a fence-free barrier, for kernels that stream
+// through LDS with direct global -> LDS loads.
+// Waits until at most N vector-memory operations of this wave are
+// outstanding (gfx9 s_waitcnt: vmcnt split over bits 3:0 and 15:14, expcnt
+// and lgkmcnt left at their maxima).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+// Waits for all LDS reads of this wave (lgkmcnt 0, the others at maxima).
+__device__ __forceinline__ void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(0xC07F); }
+// Workgroup barrier without the release/acquire fences of __syncthreads:
+// those make the compiler wait for every outstanding direct load (vmcnt 0),
+// which would drain a multi-stage pipeline.  Each wave waits for exactly the
+// loads the next stage needs (wait_vmcnt) and for its own LDS reads
+// (wait_lgkm0) before arriving; the memory clobber keeps the compiler from
+// moving LDS accesses across the barrier.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_sched_barrier(0);
+  asm volatile("s_barrier" ::: "memory");
+  __builtin_amdgcn_sched_barrier(0);
+}
+// Direct global -> LDS load of 16 bytes per lane through a buffer descriptor:
+// lane i's bytes land at lds_wave_base + 16 i.  The descriptor's record count
+// bounds every access (offsets past it read zeros and touch no memory).
+template <typename T>
+__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, uint32_t voff, T* lds_wave_base) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(
+      r, (__attribute__((address_space(3))) void*)lds_wave_base, 16, (int)voff, 0, 0, 0);
+}
+
 }  // namespace sevo

@@ -35,37 +35,6 @@ constexpr int kLgBM = 256, kLgBN = 256, kLgBK = 32, kLgStages = 4;
 constexpr int kLgStageElems = 16 * 512 + 16 * 512;
 constexpr int kLgDmaPerStage = 8;  // direct loads per wave per stage
 
-// waits until at most N vector-memory operations of this wave are
-// outstanding (gfx9 s_waitcnt: vmcnt split over bits 3:0 and 15:14,
-// expcnt and lgkmcnt left at their maxima)
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
-}
-// waits for all LDS reads of this wave (lgkmcnt 0, the others at maxima)
-__device__ __forceinline__ void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(0xC07F); }
-
-// Workgroup barrier without the release/acquire fences of __syncthreads:
-// those make the compiler wait for every outstanding direct load (vmcnt 0),
-// which would drain the stage pipeline.  Each wave waits for exactly the
-// loads the next stage needs (wait_vmcnt) before arriving; the memory clobber
-// keeps the compiler from moving LDS reads across the barrier.
-__device__ __forceinline__ void lds_barrier() {
-  __builtin_amdgcn_sched_barrier(0);
-  asm volatile("s_barrier" ::: "memory");
-  __builtin_amdgcn_sched_barrier(0);
-}
-
-// Direct global -> LDS load of 16 bytes per lane through a buffer
-// descriptor: lane i's bytes land at lds_wave_base + 16 i.  The descriptor's
-// record count bounds every access (offsets past it read zeros and touch no
-// memory), so the ragged row tail of a row-major X needs no clamping.
-__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, uint32_t voff, bf16_t* lds_wave_base) {
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(
-      r, (__attribute__((address_space(3))) void*)lds_wave_base, 16, (int)voff, 0, 0, 0);
-}
-
 // EPI 0: out fp32 [M][ldo] = Y;  EPI 1: out += Y;  EPI 2: SwiGLU -> out_bf16
 // XT 1: X in the tiled activation layout, else row-major with stride ldx
 template <int EPI, int XT>

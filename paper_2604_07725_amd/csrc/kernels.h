@@ -35,6 +35,9 @@ struct RopeAppendArgs {
   float eps;
   bf16_t* q_out;
   bf16_t* kv_pool;  // [num_pages][hkv][2][16 d]: K tile, then V tile
+  // page-table row of token i (null: row i); a prefill's tokens share the row
+  // of their sequence
+  const int32_t* row_of_token = nullptr;
 };
 hipError_t launch_qk_norm_rope_append(const RopeAppendArgs& a, hipStream_t st);
 hipError_t launch_fill_bf16(bf16_t* dst, int64_t count, uint64_t key, int64_t offset, float mul,
@@ -59,6 +62,23 @@ struct AttnArgs {
   hipEvent_t ev_begin = nullptr, ev_mid = nullptr, ev_end = nullptr;
 };
 hipError_t launch_attn_decode(const AttnArgs& a, hipStream_t st);
+
+// ---- attn_prefill.hip: causal GQA attention of a prefill over the paged KV
+// cache (the keys of every sequence's tokens already appended)
+struct PrefillAttnArgs {
+  int n_seqs, hq, hkv, d, max_pages, max_seq_len;
+  int64_t num_pages;
+  const bf16_t* q;            // [T][hq][d], sequences back to back
+  const bf16_t* kv_pool;
+  const int32_t* page_table;  // [n_seqs][max_pages]
+  const int32_t* seq_starts;  // [n_seqs + 1] token offsets
+  const int32_t* start_pos;   // [n_seqs] position of each sequence's first token (null: 0)
+  float scale;
+  bf16_t* out;                // row-major [T][hq][d], or tiled [T][hq d] when out_tiled
+  int out_tiled;
+  int total_tokens;           // T (the tiled layout's row count)
+};
+hipError_t launch_attn_prefill(const PrefillAttnArgs& a, hipStream_t st);
 
 // ---- linear.hip
 struct LinearPlan {

@@ -76,6 +76,7 @@ __global__ __launch_bounds__(64) void qk_norm_rope_append_kernel(RopeAppendArgs 
   }
   const int p = a.positions[i];
   const bool pos_ok = p >= 0 && p < a.max_pos;
+  const int prow = a.row_of_token ? a.row_of_token[i] : i;
   if (hh < a.hq + a.hkv) {
     if (a.qk_norm) {
       const float ss = wave_sum(u0 * u0 + u1 * u1);
@@ -103,7 +104,7 @@ __global__ __launch_bounds__(64) void qk_norm_rope_append_kernel(RopeAppendArgs 
     if (!pos_ok) return;
     const int pg = p >> 4;
     if (pg >= a.max_pages) return;
-    const int page = a.page_table[(size_t)i * a.max_pages + pg];
+    const int page = a.page_table[(size_t)prow * a.max_pages + pg];
     if (page < 0 || (int64_t)page >= a.num_pages) return;
     const int kh = hh - a.hq;
     // K tile (first half of the (page, head) pair): dims in blocks of 32, each
@@ -117,7 +118,7 @@ __global__ __launch_bounds__(64) void qk_norm_rope_append_kernel(RopeAppendArgs 
     if (!act || !pos_ok) return;
     const int pg = p >> 4;
     if (pg >= a.max_pages) return;
-    const int page = a.page_table[(size_t)i * a.max_pages + pg];
+    const int page = a.page_table[(size_t)prow * a.max_pages + pg];
     if (page < 0 || (int64_t)page >= a.num_pages) return;
     const int vh = hh - a.hq - a.hkv;
     // V tile (second half): dim-major [dims][16 slots]

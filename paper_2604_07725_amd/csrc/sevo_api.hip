@@ -329,6 +329,34 @@ SEVO_API sevo_status sevo_attn_decode(const sevo_attn_args* a, void* stream) {
                    static_cast<hipStream_t>(stream));
 }
 
+// ------------------------------------------------------------------ prefill
+SEVO_API sevo_status sevo_attn_prefill(const sevo_prefill_attn_args* a, void* stream) {
+  if (!a) return fail(SEVO_ERR_INVALID_ARGUMENT, "null args");
+  sevo_status st = check_attn_shape(a->n_seqs, a->n_q_heads, a->n_kv_heads, a->head_dim,
+                                    a->page_size, a->max_pages);
+  if (st) return st;
+  if (a->total_tokens < 0 || a->max_seq_len < 0)
+    return fail(SEVO_ERR_INVALID_ARGUMENT, "total_tokens / max_seq_len < 0");
+  if (a->num_pages < 1) return fail(SEVO_ERR_INVALID_ARGUMENT, "num_pages < 1");
+  if (!(std::isfinite(a->scale)) || a->scale <= 0.f)
+    return fail(SEVO_ERR_INVALID_ARGUMENT, "scale must be finite and > 0");
+  if (a->n_seqs == 0 || a->total_tokens == 0) return SEVO_OK;
+  const void* ptrs[] = {a->q, a->kv_pool, a->page_table, a->seq_starts, a->out};
+  for (auto p : ptrs)
+    if (!p || !aligned16(p))
+      return fail(SEVO_ERR_INVALID_ARGUMENT, "null or non-16-byte-aligned pointer");
+  sevo::PrefillAttnArgs k;
+  k.n_seqs = a->n_seqs; k.hq = a->n_q_heads; k.hkv = a->n_kv_heads; k.d = a->head_dim;
+  k.max_pages = a->max_pages; k.max_seq_len = a->max_seq_len; k.num_pages = a->num_pages;
+  k.q = static_cast<const sevo::bf16_t*>(a->q);
+  k.kv_pool = static_cast<const sevo::bf16_t*>(a->kv_pool);
+  k.page_table = a->page_table; k.seq_starts = a->seq_starts; k.start_pos = a->start_pos;
+  k.scale = a->scale; k.out = static_cast<sevo::bf16_t*>(a->out); k.out_tiled = 0;
+  k.total_tokens = a->total_tokens;
+  hipError_t e = sevo::launch_attn_prefill(k, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? SEVO_OK : hip_fail(e, "sevo_attn_prefill");
+}
+
 // ------------------------------------------------------------------ sampling
 SEVO_API size_t sevo_sample_workspace_bytes(int32_t n, int32_t vocab) {
   if (n <= 0 || vocab <= 0) return 0;

@@ -57,6 +57,14 @@ class AttnArgs(C.Structure):
                 ("scale", f32), ("out", vp), ("workspace", vp), ("workspace_bytes", sz)]
 
 
+class PrefillAttnArgs(C.Structure):
+    _fields_ = [("n_seqs", i32), ("total_tokens", i32), ("max_seq_len", i32),
+                ("n_q_heads", i32), ("n_kv_heads", i32), ("head_dim", i32), ("page_size", i32),
+                ("max_pages", i32), ("num_pages", i64), ("q", vp), ("kv_pool", vp),
+                ("page_table", vp), ("seq_starts", vp), ("start_pos", vp), ("scale", f32),
+                ("out", vp)]
+
+
 class SampleArgs(C.Structure):
     _fields_ = [("logits", vp), ("n", i32), ("vocab", i32), ("ld", i64), ("temperature", f32),
                 ("seed", u64), ("cand_uid", vp), ("positions", vp), ("out_tokens", vp),
@@ -90,6 +98,7 @@ _SIGS = {
     "sevo_attn_decode": ([C.POINTER(AttnArgs), vp], i32),
     "sevo_attn_plan_splits": ([i32, i32, i32], i32),
     "sevo_attn_workspace_bytes": ([i32, i32, i32, i32, i32, i32], sz),
+    "sevo_attn_prefill": ([C.POINTER(PrefillAttnArgs), vp], i32),
     "sevo_logprob_sample": ([C.POINTER(SampleArgs), vp], i32),
     "sevo_sample_workspace_bytes": ([i32, i32], sz),
     "sevo_group_confidence": ([vp, vp, vp, i32, i32, vp, vp], i32),
@@ -188,6 +197,28 @@ def sevo_attn_decode(q, kv_pool, page_table, seq_lens, out=None, scale=None,
                  seq_lens=_p(seq_lens), scale=float(d ** -0.5 if scale is None else scale),
                  out=_p(out), workspace=_p(ws), workspace_bytes=ws.numel())
     _check(lib().sevo_attn_decode(C.byref(a), _stream(stream)))
+    return out
+
+
+# ------------------------------------------------------------------ prefill
+def sevo_attn_prefill(q, kv_pool, page_table, seq_starts, max_seq_len, start_pos=None, out=None,
+                      scale=None, stream=None):
+    """Causal GQA prefill attention.  q [T, hq, d] bf16 (sequences back to back);
+    kv_pool [P, hkv, 2, 16 d]; page_table int32 [n_seqs, max_pages]; seq_starts
+    int32 [n_seqs + 1] and start_pos int32 [n_seqs] (or None) on the device;
+    max_seq_len: host bound of the sequence lengths."""
+    T, hq, d = q.shape
+    hkv = kv_pool.shape[1]
+    n_seqs, max_pages = page_table.shape
+    if out is None:
+        out = torch.empty_like(q)
+    a = PrefillAttnArgs(n_seqs=n_seqs, total_tokens=T, max_seq_len=int(max_seq_len),
+                        n_q_heads=hq, n_kv_heads=hkv, head_dim=d, page_size=PAGE_SIZE,
+                        max_pages=max_pages, num_pages=kv_pool.shape[0], q=_p(q),
+                        kv_pool=_p(kv_pool), page_table=_p(page_table),
+                        seq_starts=_p(seq_starts), start_pos=_p(start_pos),
+                        scale=float(d ** -0.5 if scale is None else scale), out=_p(out))
+    _check(lib().sevo_attn_prefill(C.byref(a), _stream(stream)))
     return out
 
 

@@ -355,6 +355,58 @@ def test_paging_invariant_under_physical_permutation():
     np.testing.assert_array_equal(a, b)
 
 
+# ---------------------------------------------------------------- prefill attention
+def _seq_pool(lengths, hkv, d):
+    """Pool with the pages of each sequence (lengths = keys) randomly placed."""
+    need = [(n + 15) // 16 for n in lengths]
+    P = sum(need)
+    kvp = _random_pool(P, hkv, d)
+    perm = RNG.permutation(P)
+    pt = np.full((len(lengths), max(need)), -1)
+    c = 0
+    for i, n in enumerate(need):
+        pt[i, :n] = perm[c:c + n]
+        c += n
+    return kvp, pt
+
+
+@pytest.mark.parametrize("hq,hkv,d", [(4, 2, 32), (8, 8, 32), (8, 1, 64)])
+def test_prefill_attention_is_causal_sdpa(hq, hkv, d):
+    """Each sequence from position 0 equals torch's causal SDPA (float64) on its
+    gathered keys, GQA by repeat-interleave: the library special case."""
+    lens = [1, 17, 40]
+    kvp, pt = _seq_pool(lens, hkv, d)
+    starts = np.concatenate([[0], np.cumsum(lens)])
+    q = RNG.standard_normal((starts[-1], hq, d))
+    out = od.prefill_attention(q, kvp, pt, starts, None, 0.2)
+    for s, n in enumerate(lens):
+        K, V = od.gather_kv(kvp, pt[s], n)
+        g = hq // hkv
+        Kr = torch.from_numpy(K).repeat_interleave(g, dim=0)
+        Vr = torch.from_numpy(V).repeat_interleave(g, dim=0)
+        qs = torch.from_numpy(q[starts[s]:starts[s + 1]]).transpose(0, 1)   # [hq, n, d]
+        ref = torch.nn.functional.scaled_dot_product_attention(qs, Kr, Vr, is_causal=True,
+                                                               scale=0.2)
+        np.testing.assert_allclose(out[starts[s]:starts[s + 1]], ref.transpose(0, 1).numpy(),
+                                   atol=1e-12)
+
+
+def test_prefill_attention_rows_are_decode_steps_and_prefix_offsets():
+    """Row t of a prefill is the decode attention over keys 0..pos(t); a sequence
+    that starts at position p0 equals the tail rows of a prefill from 0 over the
+    same keys."""
+    hq, hkv, d = 4, 2, 32
+    n_all, p0 = 45, 29
+    kvp, pt = _seq_pool([n_all], hkv, d)
+    q = RNG.standard_normal((n_all, hq, d))
+    full = od.prefill_attention(q, kvp, pt, [0, n_all], None, 0.3)
+    for t in (0, 15, 16, 44):
+        dec = od.paged_attention(q[t:t + 1], kvp, pt, [t + 1], 0.3)
+        np.testing.assert_allclose(full[t], dec[0], atol=1e-13)
+    tail = od.prefill_attention(q[p0:], kvp, pt, [0, n_all - p0], [p0], 0.3)
+    np.testing.assert_allclose(tail, full[p0:], atol=1e-13)
+
+
 def test_append_writes_exactly_one_slot():
     kvp = _random_pool(6, 2, 64)
     kv0 = kvp.copy()
