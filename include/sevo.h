@@ -210,6 +210,56 @@ typedef struct {
 
 sevo_status sevo_attn_prefill(const sevo_prefill_attn_args* a, void* stream);
 
+/* The cross-model confidence engine: one prefill-only forward pass of the
+ * scoring model over every sequence of a batch (prompt + trajectory), reduced
+ * on the device to one confidence per sequence (Eq. 1 per position, Eq. 2's
+ * C(tau) per sequence; the "Confidence engine" paragraph of the System
+ * Implementation subsection and the prefill engine appendix).  Per layer the
+ * steps of sevo_decode_step run for all total_tokens tokens at once, with the
+ * causal prefill attention of sevo_attn_prefill; the keys and values of every
+ * token are written into the pools (a KV cache a decode can continue from).
+ * Then, for each scored row r -- a packed token index whose next-token
+ * distribution is scored --
+ *   c_r = logsumexp(logits_r) - mean of the conf_topk largest logits_r
+ * with logits_r = RMSNorm(x_r) g_final W_lm^T (fp32, T = 1), and
+ *   out_conf[s] = mean of c_r over the scored rows inside sequence s
+ *                 (C(tau) of Eq. 2; 0 for a sequence without scored rows).
+ * Only the scored rows go through the LM head (in chunks of 4096 rows).
+ *   tokens      int32 [total_tokens], sequences back to back
+ *   seq_starts  int32 [n_seqs + 1] (device), start_pos int32 [n_seqs] (device)
+ *               or NULL: as in sevo_attn_prefill; positions must be below the
+ *               model's max_position
+ *   page_table  int32 [n_seqs][max_pages]: pages for every key position
+ *   kv_pools    HOST array of n_layers pool pointers; a caller that does not
+ *               keep the cache may pass one pool for every layer (a layer's
+ *               keys are only read inside that layer)
+ *   max_seq_len host bound of the sequence lengths
+ *   conf_topk   K_l of Eq. 1, 1..32
+ *   scored_rows int32 [n_scored] (device): strictly increasing packed token
+ *               indices (not validated on the device)
+ *   out_conf    fp32 [n_seqs];  out_row_conf fp32 [n_scored] or NULL
+ * Errors: INVALID_ARGUMENT, UNSUPPORTED, WORKSPACE_TOO_SMALL, HIP. */
+typedef struct {
+  int32_t n_seqs, total_tokens, max_seq_len;
+  const int32_t* tokens;
+  const int32_t* seq_starts;
+  const int32_t* start_pos;
+  const int32_t* page_table;
+  int32_t max_pages;
+  int64_t num_pages;
+  void* const* kv_pools;
+  int32_t conf_topk;
+  int32_t n_scored;
+  const int32_t* scored_rows;
+  float* out_conf;
+  float* out_row_conf;
+  void* workspace;
+  size_t workspace_bytes;
+} sevo_prefill_args;
+
+sevo_status sevo_prefill_confidence(sevo_model* m, const sevo_prefill_args* a, void* stream);
+size_t sevo_prefill_workspace_bytes(const sevo_model* m, int32_t total_tokens, int32_t n_scored);
+
 /* ------------------------------------------------------------------ sampling */
 
 /* Full-vocabulary log-softmax and Gumbel-max sample, per candidate i:
@@ -409,9 +459,9 @@ sevo_status sevo_validate_paging(const int32_t* page_table, const int32_t* lengt
 
 /* ------------------------------------------------------------------ timing
  * Measurement aid: while a recording is open, the launches of the selected
- * kinds (inside sevo_decode_step; the attention kinds also in
- * sevo_attn_decode) are bracketed by HIP events on the stream they run on.
- * Process-wide; launches beyond max_launches are not timed; one recording at a
+ * kinds (inside sevo_decode_step and sevo_prefill_confidence; the attention
+ * kinds also in sevo_attn_decode and sevo_attn_prefill) are bracketed by HIP
+ * events on the stream they run on.  Process-wide; launches beyond max_launches are not timed; one recording at a
  * time.  kinds is a mask of (1u << SEVO_PROF_*).  sevo_profile_end waits for
  * the recorded events and returns, per kind, the summed milliseconds and the
  * number of timed launches (arrays of SEVO_PROF_NUM_KINDS entries; either may
@@ -427,7 +477,8 @@ sevo_status sevo_validate_paging(const int32_t* page_table, const int32_t* lengt
 #define SEVO_PROF_ROPE_APPEND 8   /* QK-norm + RoPE + KV append          */
 #define SEVO_PROF_SAMPLE 9        /* log-softmax + Gumbel-max (+ confidence) */
 #define SEVO_PROF_EMBED 10        /* embedding gather                    */
-#define SEVO_PROF_NUM_KINDS 11
+#define SEVO_PROF_ATTN_PREFILL 11 /* causal prefill attention            */
+#define SEVO_PROF_NUM_KINDS 12
 sevo_status sevo_profile_begin(int32_t max_launches, uint32_t kinds);
 sevo_status sevo_profile_end(float* total_ms, int32_t* launches);
 

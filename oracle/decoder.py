@@ -323,6 +323,58 @@ def decode_step(shape, weights, kv_pools, page_table, tokens, positions, uids,
     return {"ids": ids, "lps": lps, "gaps": gaps, "logits": logits, "x": x}
 
 
+# ------------------------------------------------------------------ prefill (scoring pass)
+def prefill_index(seq_starts, start_pos=None):
+    """Sequence (page-table row) and position of every packed token."""
+    seq_starts = np.asarray(seq_starts, np.int64)
+    T = int(seq_starts[-1])
+    row = np.empty(T, np.int64)
+    pos = np.empty(T, np.int64)
+    for s in range(len(seq_starts) - 1):
+        a, b = int(seq_starts[s]), int(seq_starts[s + 1])
+        p0 = 0 if start_pos is None else int(start_pos[s])
+        row[a:b] = s
+        pos[a:b] = p0 + np.arange(b - a)
+    return row, pos
+
+
+def prefill_forward(shape, weights, kv_pools, page_table, tokens, seq_starts, start_pos=None,
+                    mirror=True):
+    """Residual stream after the last layer for every token of a prefill batch.
+
+    Every token takes the decoder layer with its sequence's page-table row and
+    its own position: all keys of a layer are appended before its attention,
+    and token t attends keys 0..pos(t), which is causal attention over the
+    sequence (plus any cached prefix).  kv_pools are modified in place.
+    """
+    tokens = np.asarray(tokens, np.int64)
+    row, pos = prefill_index(seq_starts, start_pos)
+    pt_rows = np.asarray(page_table)[row]
+    x = np.asarray(weights["embed"][tokens], np.float64)
+    for l in range(shape.n_layers):
+        x = decoder_layer(shape, weights["layers"][l], x, pos, kv_pools[l], pt_rows, mirror)
+    return x
+
+
+def prefill_confidence(shape, weights, kv_pools, page_table, tokens, seq_starts, scored_rows,
+                       k_l, start_pos=None, mirror=True):
+    """The confidence engine: c (Eq. 1) of the next-token distribution at each
+    scored row, and per sequence C = mean of c over its scored rows (Eq. 2;
+    0 without any).  Returns (conf [n_seqs], row_conf [len(scored_rows)], logits)."""
+    x = prefill_forward(shape, weights, kv_pools, page_table, tokens, seq_starts, start_pos,
+                        mirror)
+    rows = np.asarray(scored_rows, np.int64)
+    logits = lm_logits(shape, weights["final_norm"], weights["lm_head"], x[rows], mirror)
+    c = token_confidence(logits, k_l)
+    seq_starts = np.asarray(seq_starts, np.int64)
+    conf = np.zeros(len(seq_starts) - 1)
+    for s in range(len(conf)):
+        sel = (rows >= seq_starts[s]) & (rows < seq_starts[s + 1])
+        if sel.any():
+            conf[s] = c[sel].mean()
+    return conf, c, logits
+
+
 # ------------------------------------------------------------------ fitness signal
 def token_confidence(logits, k_l):
     """Per-token confidence of Eq. 1 from the scoring model's logits.

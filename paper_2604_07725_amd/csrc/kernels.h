@@ -16,8 +16,14 @@ hipError_t launch_rmsnorm(const float* x, const bf16_t* gain, int rows, int cols
 // x += sum_s part[s] (split order; S == 0: nothing to add), then
 // out = bf16(RMSNorm(x) * gain) in the tiled activation layout (the GEMM
 // input).  part is [S][rows][cols] fp32.
+// row_idx (optional): output row r takes source row row_idx[r] of x and of
+// the partials (which then have part_rows rows); x is not written back.
 hipError_t launch_add_rmsnorm(float* x, const float* part, int S, const bf16_t* gain, int rows,
-                              int cols, float eps, bf16_t* out_tiled, hipStream_t st);
+                              int cols, float eps, bf16_t* out_tiled, hipStream_t st,
+                              const int32_t* row_idx = nullptr, int part_rows = 0);
+// per packed prefill token: page-table row (its sequence) and position
+hipError_t launch_prefill_index(const int32_t* seq_starts, const int32_t* start_pos, int n_seqs,
+                                int T, int32_t* row, int32_t* pos, hipStream_t st);
 struct RopeAppendArgs {
   const float* qkv;  // [qkv_splits][n][(hq + 2 hkv) d]: summed in split order
   int qkv_splits;
@@ -124,6 +130,12 @@ hipError_t launch_logprob_sample(const float* logits, int n, int vocab, int64_t 
                                  int top_k = 0, float top_p = 1.f, float min_p = 0.f);
 // a top-k / confidence list of list_len entries fits the chunk merge
 bool sample_conf_supported(int vocab, int list_len);
+// C of each sequence: the mean, in row order, of row_conf over the scored rows
+// (strictly increasing packed token indices) inside [seq_starts[s],
+// seq_starts[s + 1]); 0 for a sequence with none.
+hipError_t launch_seq_confidence(const float* row_conf, const int32_t* scored_rows, int n_scored,
+                                 const int32_t* seq_starts, int n_seqs, float* out,
+                                 hipStream_t st);
 hipError_t launch_group_confidence(const float* conf_sum, const int32_t* counts,
                                    const int32_t* groups, int n_groups, int K, float* out,
                                    hipStream_t st);

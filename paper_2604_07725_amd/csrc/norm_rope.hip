@@ -179,15 +179,19 @@ hipError_t launch_embed(const bf16_t* embed, const int32_t* tokens, int n, int h
 // stored in the tiled activation layout that the projections read.
 // 1024 threads per row, each owning 4 consecutive columns per 4096-column
 // pass with all split loads independent (latency, not bandwidth, is the cost).
+// With row_idx, output row r reads row row_idx[r] of x and the partials and
+// x is not written back (the final norm of a prefill's scored rows).
 __global__ __launch_bounds__(1024) void add_rmsnorm_kernel(float* __restrict__ x,
                                                            const float* __restrict__ part, int S,
                                                            size_t part_stride,
                                                            const bf16_t* __restrict__ gain,
                                                            int cols, float eps,
-                                                           bf16_t* __restrict__ out) {
+                                                           bf16_t* __restrict__ out,
+                                                           const int32_t* __restrict__ row_idx) {
   __shared__ float red[16];
-  float* xr = x + (size_t)blockIdx.x * cols;
-  const float* pr = part + (size_t)blockIdx.x * cols;
+  const size_t src = row_idx ? (size_t)row_idx[blockIdx.x] : (size_t)blockIdx.x;
+  float* xr = x + src * cols;
+  const float* pr = part + src * cols;
   float ss = 0.f;
   for (int c = threadIdx.x * 4; c < cols; c += 4096) {
     f32x4 v = *reinterpret_cast<const f32x4*>(xr + c);
@@ -199,14 +203,23 @@ __global__ __launch_bounds__(1024) void add_rmsnorm_kernel(float* __restrict__ x
 #pragma unroll
       for (int s = 0; s < 16; ++s)
         if (s < S) v += p[s];
-      *reinterpret_cast<f32x4*>(xr + c) = v;
+      if (!row_idx) *reinterpret_cast<f32x4*>(xr + c) = v;
     }
     ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
   }
   ss = block_sum<16>(ss, red);
   const float inv = 1.0f / sqrtf(ss / (float)cols + eps);
   for (int c = threadIdx.x * 4; c < cols; c += 4096) {
-    const f32x4 v = *reinterpret_cast<const f32x4*>(xr + c);
+    f32x4 v = *reinterpret_cast<const f32x4*>(xr + c);
+    if (row_idx) {  // x was not updated in place: add the partials again, same order
+      f32x4 p[16];
+#pragma unroll
+      for (int s = 0; s < 16; ++s)
+        if (s < S) p[s] = *reinterpret_cast<const f32x4*>(pr + s * part_stride + c);
+#pragma unroll
+      for (int s = 0; s < 16; ++s)
+        if (s < S) v += p[s];
+    }
     const uint2 g = *reinterpret_cast<const uint2*>(gain + c);
     uint2 o;
     o.x = pack_bf16x2(v.x * inv * bf16_lo(g.x), v.y * inv * bf16_hi(g.x));
@@ -217,11 +230,40 @@ __global__ __launch_bounds__(1024) void add_rmsnorm_kernel(float* __restrict__ x
 }
 
 hipError_t launch_add_rmsnorm(float* x, const float* part, int S, const bf16_t* gain, int rows,
-                              int cols, float eps, bf16_t* out_tiled, hipStream_t st) {
+                              int cols, float eps, bf16_t* out_tiled, hipStream_t st,
+                              const int32_t* row_idx, int part_rows) {
   if (rows == 0) return hipSuccess;
   if (S > 16) return hipErrorInvalidValue;
+  const size_t stride = (size_t)(row_idx ? part_rows : rows) * cols;
   hipLaunchKernelGGL(add_rmsnorm_kernel, dim3(rows), dim3(1024), 0, st, x, part, part ? S : 0,
-                     (size_t)rows * cols, gain, cols, eps, out_tiled);
+                     stride, gain, cols, eps, out_tiled, row_idx);
+  return hipGetLastError();
+}
+
+// Packed token t of a prefill batch -> its sequence s (the page-table row)
+// and position start_pos[s] + t - seq_starts[s].
+__global__ __launch_bounds__(256) void prefill_index_kernel(const int32_t* __restrict__ seq_starts,
+                                                            const int32_t* __restrict__ start_pos,
+                                                            int n_seqs, int T,
+                                                            int32_t* __restrict__ row,
+                                                            int32_t* __restrict__ pos) {
+  const int t = blockIdx.x * 256 + threadIdx.x;
+  if (t >= T) return;
+  int lo = 0, hi = n_seqs - 1;  // last s with seq_starts[s] <= t
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (seq_starts[mid] <= t) lo = mid;
+    else hi = mid - 1;
+  }
+  row[t] = lo;
+  pos[t] = (start_pos ? start_pos[lo] : 0) + t - seq_starts[lo];
+}
+
+hipError_t launch_prefill_index(const int32_t* seq_starts, const int32_t* start_pos, int n_seqs,
+                                int T, int32_t* row, int32_t* pos, hipStream_t st) {
+  if (T == 0) return hipSuccess;
+  hipLaunchKernelGGL(prefill_index_kernel, dim3((T + 255) / 256), dim3(256), 0, st, seq_starts,
+                     start_pos, n_seqs, T, row, pos);
   return hipGetLastError();
 }
 

@@ -148,8 +148,9 @@ __global__ __launch_bounds__(256) void sample_partial_kernel(
   const float* row = logits + (size_t)i * ld;
   const bool greedy = temp == 0.f;
   const bool unit_t = temp == 1.f;
-  const uint64_t cu = uid[i];
-  const uint32_t pos = (uint32_t)positions[i];
+  // greedy sampling draws no noise: uid and positions may be null then
+  const uint64_t cu = greedy ? 0 : uid[i];
+  const uint32_t pos = greedy ? 0u : (uint32_t)positions[i];
   const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
   float z[16], raw[16];
   float best = -INFINITY;
@@ -603,6 +604,49 @@ hipError_t launch_logprob_sample(const float* logits, int n, int vocab, int64_t 
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(sample_final_kernel, dim3(n), dim3(256), 0, st, part, nchunks, logits, ld,
                      temp, out_tokens, out_lp, conf_k, topk, out_conf, conf_sum);
+  return hipGetLastError();
+}
+
+// One workgroup per sequence: binary search of its scored rows, then each
+// thread sums a contiguous slice in order and the slices are added in thread
+// order (a fixed order: the result does not depend on scheduling).
+__global__ __launch_bounds__(256) void seq_confidence_kernel(const float* __restrict__ row_conf,
+                                                             const int32_t* __restrict__ rows,
+                                                             int n_scored,
+                                                             const int32_t* __restrict__ seq_starts,
+                                                             float* __restrict__ out) {
+  __shared__ float part[256];
+  const int s = blockIdx.x;
+  auto lower = [&](int key) {  // first r with rows[r] >= key
+    int lo = 0, hi = n_scored;
+    while (lo < hi) {
+      const int mid = (lo + hi) >> 1;
+      if (rows[mid] < key) lo = mid + 1;
+      else hi = mid;
+    }
+    return lo;
+  };
+  const int a = lower(seq_starts[s]), b = lower(seq_starts[s + 1]);
+  const int n = b - a;
+  const int per = (n + 255) / 256;
+  const int r0 = a + threadIdx.x * per, r1 = min(b, r0 + per);
+  float acc = 0.f;
+  for (int r = r0; r < r1; ++r) acc += row_conf[r];
+  part[threadIdx.x] = acc;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float t = 0.f;
+    for (int i = 0; i < 256; ++i) t += part[i];
+    out[s] = n > 0 ? t / (float)n : 0.f;
+  }
+}
+
+hipError_t launch_seq_confidence(const float* row_conf, const int32_t* scored_rows, int n_scored,
+                                 const int32_t* seq_starts, int n_seqs, float* out,
+                                 hipStream_t st) {
+  if (n_seqs == 0) return hipSuccess;
+  hipLaunchKernelGGL(seq_confidence_kernel, dim3(n_seqs), dim3(256), 0, st, row_conf, scored_rows,
+                     n_scored, seq_starts, out);
   return hipGetLastError();
 }
 

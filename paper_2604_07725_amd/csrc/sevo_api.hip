@@ -757,6 +757,206 @@ SEVO_API sevo_status sevo_decode_step(sevo_model* m, const sevo_step_args* a, vo
   return SEVO_OK;
 }
 
+// ------------------------------------------------------------------ confidence engine
+namespace {
+
+constexpr int kPrefillLogitRows = 4096;  // scored rows per LM-head chunk
+
+struct PrefillLayout {
+  size_t row, pos, x, h, qkv, q, o, a, part, hf, logits, sample, conf, ids, lps, total;
+  int rc;  // rows per LM-head chunk
+};
+
+PrefillLayout prefill_layout(const sevo_model_config& c, int T, int R) {
+  PrefillLayout L;
+  const size_t H = c.hidden, F = c.ffn, V = c.vocab;
+  const size_t qd = (size_t)c.n_q_heads * c.head_dim;
+  const size_t qkvd = (size_t)(c.n_q_heads + 2 * c.n_kv_heads) * c.head_dim;
+  L.rc = R < kPrefillLogitRows ? (R > 0 ? R : 1) : kPrefillLogitRows;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off += round_up(bytes, 256);
+    return o;
+  };
+  const size_t t = (size_t)T, t16 = round_up(t, 16), rc = (size_t)L.rc, rc16 = round_up(rc, 16);
+  L.row = take(t * 4);
+  L.pos = take(t * 4);
+  L.x = take(t * H * 4);
+  L.h = take(t16 * H * 2);
+  L.qkv = take(t * qkvd * 4);
+  L.q = take(t * qd * 2);
+  L.o = take(t16 * qd * 2);
+  L.a = take(t16 * F * 2);
+  L.part = take(t * H * 4);
+  L.hf = take(rc16 * H * 2);
+  L.logits = take(rc * V * 4);
+  L.sample = take(sevo::sample_workspace_bytes(L.rc, c.vocab));
+  L.conf = take((size_t)(R > 0 ? R : 1) * 4);
+  L.ids = take(rc * 4);
+  L.lps = take(rc * 4);
+  L.total = off;
+  return L;
+}
+
+// One projection of a prefill: the large-M kernel when it applies, else the
+// decode kernel in one K split (no workspace).  X in the tiled layout.
+hipError_t prefill_gemm(int m, int n_out, int k, int mode, const sevo::bf16_t* x,
+                        const void* w, void* out, int out_tiled, hipStream_t st) {
+  const sevo::bf16_t* wb = static_cast<const sevo::bf16_t*>(w);
+  if (m >= sevo::kLargeGemmMinM && sevo::gemm_large_supported(m, n_out, k))
+    return sevo::launch_gemm_large(m, n_out, k, k, 1, mode, x, wb, out, out_tiled, st);
+  const sevo::LinearPlan p = sevo::plan_linear(m, n_out, k, 1, mode);
+  return sevo::launch_linear(m, n_out, k, k, 1, mode, p, x, wb, out, out_tiled, nullptr, st);
+}
+
+}  // namespace
+
+SEVO_API size_t sevo_prefill_workspace_bytes(const sevo_model* m, int32_t total_tokens,
+                                             int32_t n_scored) {
+  if (!m || total_tokens <= 0 || n_scored < 0) return 0;
+  return prefill_layout(m->cfg, total_tokens, n_scored).total;
+}
+
+SEVO_API sevo_status sevo_prefill_confidence(sevo_model* m, const sevo_prefill_args* a,
+                                             void* stream) {
+  if (!m || !a) return fail(SEVO_ERR_INVALID_ARGUMENT, "null model or args");
+  const sevo_model_config& c = m->cfg;
+  if (a->n_seqs < 1 || a->total_tokens < 0 || a->max_seq_len < 0 || a->max_pages < 1 ||
+      a->num_pages < 1)
+    return fail(SEVO_ERR_INVALID_ARGUMENT,
+                "bad n_seqs / total_tokens / max_seq_len / max_pages / num_pages");
+  if (a->conf_topk < 1 || a->conf_topk > 32 || a->conf_topk > c.vocab)
+    return fail(SEVO_ERR_INVALID_ARGUMENT, "conf_topk %d outside [1, min(32, vocab)]",
+                a->conf_topk);
+  if (!sevo::sample_conf_supported(c.vocab, a->conf_topk))
+    return fail(SEVO_ERR_UNSUPPORTED, "confidence lists over a vocabulary of %d", c.vocab);
+  if (a->n_scored < 0 || a->n_scored > a->total_tokens)
+    return fail(SEVO_ERR_INVALID_ARGUMENT, "n_scored %d outside [0, total_tokens]", a->n_scored);
+  if (!a->seq_starts || !a->out_conf || !a->kv_pools || !a->workspace ||
+      !aligned16(a->workspace) || !aligned16(a->seq_starts))
+    return fail(SEVO_ERR_INVALID_ARGUMENT, "null or misaligned pointer");
+  const int T = a->total_tokens, R = a->n_scored;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  hipError_t e;
+  if (T == 0) {  // every sequence is empty: no scored rows, C = 0
+    e = sevo::launch_seq_confidence(nullptr, nullptr, 0, a->seq_starts, a->n_seqs, a->out_conf,
+                                    st);
+    return e == hipSuccess ? SEVO_OK : hip_fail(e, "prefill confidence");
+  }
+  if (!a->tokens || !a->page_table || (R > 0 && !a->scored_rows))
+    return fail(SEVO_ERR_INVALID_ARGUMENT, "null pointer");
+  for (int l = 0; l < c.n_layers; ++l)
+    if (!a->kv_pools[l] || !aligned16(a->kv_pools[l]))
+      return fail(SEVO_ERR_INVALID_ARGUMENT, "layer %d: null or misaligned KV pool", l);
+  const PrefillLayout L = prefill_layout(c, T, R);
+  if (a->workspace_bytes < L.total)
+    return fail(SEVO_ERR_WORKSPACE_TOO_SMALL, "prefill needs %zu workspace bytes, got %zu",
+                L.total, a->workspace_bytes);
+  char* ws = static_cast<char*>(a->workspace);
+  int32_t* row = reinterpret_cast<int32_t*>(ws + L.row);
+  int32_t* pos = reinterpret_cast<int32_t*>(ws + L.pos);
+  float* x = reinterpret_cast<float*>(ws + L.x);
+  sevo::bf16_t* h = reinterpret_cast<sevo::bf16_t*>(ws + L.h);
+  float* qkv = reinterpret_cast<float*>(ws + L.qkv);
+  sevo::bf16_t* q = reinterpret_cast<sevo::bf16_t*>(ws + L.q);
+  sevo::bf16_t* o = reinterpret_cast<sevo::bf16_t*>(ws + L.o);
+  sevo::bf16_t* act = reinterpret_cast<sevo::bf16_t*>(ws + L.a);
+  float* part = reinterpret_cast<float*>(ws + L.part);
+  sevo::bf16_t* hf = reinterpret_cast<sevo::bf16_t*>(ws + L.hf);
+  float* logits = reinterpret_cast<float*>(ws + L.logits);
+  float* smp = reinterpret_cast<float*>(ws + L.sample);
+  float* row_conf = a->out_row_conf ? a->out_row_conf : reinterpret_cast<float*>(ws + L.conf);
+  int32_t* ids = reinterpret_cast<int32_t*>(ws + L.ids);
+  float* lps = reinterpret_cast<float*>(ws + L.lps);
+
+  const int H = c.hidden, F = c.ffn, qd = c.n_q_heads * c.head_dim;
+  const int qkvd = (c.n_q_heads + 2 * c.n_kv_heads) * c.head_dim;
+  const float scale = 1.0f / std::sqrt((float)c.head_dim);
+
+  {
+    ProfScope ps(SEVO_PROF_EMBED, st);
+    e = sevo::launch_embed(static_cast<const sevo::bf16_t*>(m->embed), a->tokens, T, H, c.vocab,
+                           x, st);
+  }
+  if (e == hipSuccess)
+    e = sevo::launch_prefill_index(a->seq_starts, a->start_pos, a->n_seqs, T, row, pos, st);
+  if (e != hipSuccess) return hip_fail(e, "prefill (embed)");
+  // the output and down projections store their product in `part`; the next
+  // residual add + RMSNorm adds it to x
+  for (int l = 0; l < c.n_layers; ++l) {
+    {
+      ProfScope ps(SEVO_PROF_NORM, st);
+      e = sevo::launch_add_rmsnorm(x, l ? part : nullptr, l ? 1 : 0,
+                                   static_cast<const sevo::bf16_t*>(m->attn_norm[l]), T, H,
+                                   c.rms_eps, h, st);
+    }
+    if (e == hipSuccess) {
+      ProfScope ps(SEVO_PROF_QKV, st);
+      e = prefill_gemm(T, qkvd, H, SEVO_LINEAR_STORE, h, m->w_qkv[l], qkv, 0, st);
+    }
+    if (e == hipSuccess) {
+      ProfScope ps(SEVO_PROF_ROPE_APPEND, st);
+      sevo::RopeAppendArgs r;
+      fill_rope_args(m, l, qkv, 1, T, pos, a->page_table, a->max_pages, a->num_pages, q,
+                     a->kv_pools[l], r);
+      r.row_of_token = row;
+      e = sevo::launch_qk_norm_rope_append(r, st);
+    }
+    if (e == hipSuccess) {
+      ProfScope ps(SEVO_PROF_ATTN_PREFILL, st);
+      sevo::PrefillAttnArgs pa;
+      pa.n_seqs = a->n_seqs; pa.hq = c.n_q_heads; pa.hkv = c.n_kv_heads; pa.d = c.head_dim;
+      pa.max_pages = a->max_pages; pa.max_seq_len = a->max_seq_len; pa.num_pages = a->num_pages;
+      pa.q = q; pa.kv_pool = static_cast<const sevo::bf16_t*>(a->kv_pools[l]);
+      pa.page_table = a->page_table; pa.seq_starts = a->seq_starts; pa.start_pos = a->start_pos;
+      pa.scale = scale; pa.out = o; pa.out_tiled = 1; pa.total_tokens = T;
+      e = sevo::launch_attn_prefill(pa, st);
+    }
+    if (e == hipSuccess) {
+      ProfScope ps(SEVO_PROF_ATTN_OUT, st);
+      e = prefill_gemm(T, H, qd, SEVO_LINEAR_STORE, o, m->w_o[l], part, 0, st);
+    }
+    if (e == hipSuccess) {
+      ProfScope ps(SEVO_PROF_NORM, st);
+      e = sevo::launch_add_rmsnorm(x, part, 1, static_cast<const sevo::bf16_t*>(m->ffn_norm[l]),
+                                   T, H, c.rms_eps, h, st);
+    }
+    if (e == hipSuccess) {
+      ProfScope ps(SEVO_PROF_GATE_UP, st);
+      e = prefill_gemm(T, 2 * F, H, SEVO_LINEAR_SWIGLU, h, m->w_gate_up[l], act, 1, st);
+    }
+    if (e == hipSuccess) {
+      ProfScope ps(SEVO_PROF_DOWN, st);
+      e = prefill_gemm(T, H, F, SEVO_LINEAR_STORE, act, m->w_down[l], part, 0, st);
+    }
+    if (e != hipSuccess) return hip_fail(e, "prefill (layer)");
+  }
+  // scored rows, a chunk at a time: final norm of x + the last down product,
+  // LM head, per-row confidence (greedy pass of the sampler: no noise)
+  for (int r0 = 0; r0 < R; r0 += L.rc) {
+    const int nr = R - r0 < L.rc ? R - r0 : L.rc;
+    {
+      ProfScope ps(SEVO_PROF_NORM, st);
+      e = sevo::launch_add_rmsnorm(x, part, 1, static_cast<const sevo::bf16_t*>(m->final_norm),
+                                   nr, H, c.rms_eps, hf, st, a->scored_rows + r0, T);
+    }
+    if (e == hipSuccess) {
+      ProfScope ps(SEVO_PROF_LM_HEAD, st);
+      e = prefill_gemm(nr, c.vocab, H, SEVO_LINEAR_STORE, hf, m->lm_head, logits, 0, st);
+    }
+    if (e == hipSuccess) {
+      ProfScope ps(SEVO_PROF_SAMPLE, st);
+      e = sevo::launch_logprob_sample(logits, nr, c.vocab, c.vocab, 0.f, 0, nullptr, nullptr, ids,
+                                      lps, smp, a->conf_topk, row_conf + r0, nullptr, st);
+    }
+    if (e != hipSuccess) return hip_fail(e, "prefill (scored rows)");
+  }
+  e = sevo::launch_seq_confidence(row_conf, a->scored_rows, R, a->seq_starts, a->n_seqs,
+                                  a->out_conf, st);
+  return e == hipSuccess ? SEVO_OK : hip_fail(e, "prefill (sequence confidence)");
+}
+
 // ------------------------------------------------------------------ utilities
 SEVO_API sevo_status sevo_fill_normal_bf16(void* dst, int64_t count, uint64_t key, int64_t offset,
                                            float mul, float add, int32_t use_add, void* stream) {

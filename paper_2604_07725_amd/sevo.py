@@ -27,7 +27,7 @@ PACKED_WEIGHTS = {"w_qkv": PACK_PLAIN, "w_o": PACK_PLAIN, "w_gate_up": PACK_GATE
                   "w_down": PACK_PLAIN, "lm_head": PACK_PLAIN}
 PAGE_SIZE = 16
 PROF_KINDS = ["attn_split", "attn_combine", "qkv", "attn_out", "gate_up", "down", "lm_head",
-              "norm", "rope_append", "sample", "embed"]   # SEVO_PROF_* order
+              "norm", "rope_append", "sample", "embed", "attn_prefill"]   # SEVO_PROF_* order
 
 vp = C.c_void_p
 i32 = C.c_int32
@@ -63,6 +63,14 @@ class PrefillAttnArgs(C.Structure):
                 ("max_pages", i32), ("num_pages", i64), ("q", vp), ("kv_pool", vp),
                 ("page_table", vp), ("seq_starts", vp), ("start_pos", vp), ("scale", f32),
                 ("out", vp)]
+
+
+class PrefillArgs(C.Structure):
+    _fields_ = [("n_seqs", i32), ("total_tokens", i32), ("max_seq_len", i32), ("tokens", vp),
+                ("seq_starts", vp), ("start_pos", vp), ("page_table", vp), ("max_pages", i32),
+                ("num_pages", i64), ("kv_pools", C.POINTER(vp)), ("conf_topk", i32),
+                ("n_scored", i32), ("scored_rows", vp), ("out_conf", vp), ("out_row_conf", vp),
+                ("workspace", vp), ("workspace_bytes", sz)]
 
 
 class SampleArgs(C.Structure):
@@ -104,6 +112,8 @@ _SIGS = {
     "sevo_group_confidence": ([vp, vp, vp, i32, i32, vp, vp], i32),
     "sevo_decode_step": ([vp, C.POINTER(StepArgs), vp], i32),
     "sevo_step_workspace_bytes": ([vp, i32, i32, i32], sz),
+    "sevo_prefill_confidence": ([vp, C.POINTER(PrefillArgs), vp], i32),
+    "sevo_prefill_workspace_bytes": ([vp, i32, i32], sz),
     "sevo_embed": ([vp, vp, i32, i32, i32, vp, vp], i32),
     "sevo_rmsnorm": ([vp, vp, i32, i32, f32, vp, vp], i32),
     "sevo_linear": ([C.POINTER(LinearArgs), vp], i32),
@@ -470,3 +480,44 @@ def sevo_decode_step(model: Model, tokens, positions, page_table, kv_pools, cand
     out = (ids, lps) + ((b.out_logits,) if keep_logits else ()) + \
         ((b.out_conf,) if conf_topk else ())
     return out
+
+
+# ------------------------------------------------------------------ confidence engine
+def sevo_prefill_workspace_bytes(model: Model, total_tokens: int, n_scored: int) -> int:
+    return int(lib().sevo_prefill_workspace_bytes(model.handle, int(total_tokens), int(n_scored)))
+
+
+class PrefillBuffers:
+    """Argument struct and outputs of one confidence-engine call shape (the
+    workspace is allocated once; ``run`` only enqueues kernels)."""
+
+    def __init__(self, model: Model, tokens, seq_starts, page_table, kv_pools, scored_rows,
+                 conf_topk, max_seq_len, start_pos=None, keep_row_conf=True, workspace=None):
+        T = tokens.shape[0]
+        n_seqs = seq_starts.shape[0] - 1
+        dev = tokens.device
+        R = 0 if scored_rows is None else scored_rows.shape[0]
+        self.model = model
+        self.out_conf = torch.empty(n_seqs, dtype=torch.float32, device=dev)
+        self.out_row_conf = (torch.empty(max(R, 1), dtype=torch.float32, device=dev)
+                             if keep_row_conf else None)
+        need = sevo_prefill_workspace_bytes(model, max(T, 1), R)
+        self.workspace = _workspace(need, dev, workspace)
+        L = model.shape.n_layers
+        if not isinstance(kv_pools, (list, tuple)):
+            kv_pools = [kv_pools] * L
+        self._kv = (vp * L)(*[p.data_ptr() for p in kv_pools])
+        self.keep = (tokens, seq_starts, page_table, kv_pools, scored_rows, start_pos)
+        self.args = PrefillArgs(
+            n_seqs=n_seqs, total_tokens=T, max_seq_len=int(max_seq_len), tokens=_p(tokens),
+            seq_starts=_p(seq_starts), start_pos=_p(start_pos), page_table=_p(page_table),
+            max_pages=page_table.shape[1], num_pages=kv_pools[0].shape[0],
+            kv_pools=C.cast(self._kv, C.POINTER(vp)), conf_topk=int(conf_topk), n_scored=R,
+            scored_rows=_p(scored_rows), out_conf=_p(self.out_conf),
+            out_row_conf=_p(self.out_row_conf), workspace=_p(self.workspace),
+            workspace_bytes=self.workspace.numel())
+
+    def run(self, stream=None):
+        _check(lib().sevo_prefill_confidence(self.model.handle, C.byref(self.args),
+                                             _stream(stream)))
+        return self.out_conf

@@ -43,13 +43,21 @@ int main(void) {
   P(sevo_step_args, out_conf) P(sevo_step_args, workspace_bytes)
   S(sevo_linear_args) P(sevo_linear_args, flags) P(sevo_linear_args, x)
   P(sevo_linear_args, workspace_bytes)
+  S(sevo_prefill_attn_args) P(sevo_prefill_attn_args, num_pages) P(sevo_prefill_attn_args, q)
+  P(sevo_prefill_attn_args, start_pos) P(sevo_prefill_attn_args, scale)
+  P(sevo_prefill_attn_args, out)
+  S(sevo_prefill_args) P(sevo_prefill_args, tokens) P(sevo_prefill_args, max_pages)
+  P(sevo_prefill_args, num_pages) P(sevo_prefill_args, kv_pools) P(sevo_prefill_args, conf_topk)
+  P(sevo_prefill_args, scored_rows) P(sevo_prefill_args, out_row_conf)
+  P(sevo_prefill_args, workspace_bytes)
   return 0;
 }
 """
 
 _PY = {"sevo_model_config": sevo.ModelConfig, "sevo_weights": sevo.Weights,
        "sevo_attn_args": sevo.AttnArgs, "sevo_sample_args": sevo.SampleArgs,
-       "sevo_step_args": sevo.StepArgs, "sevo_linear_args": sevo.LinearArgs}
+       "sevo_step_args": sevo.StepArgs, "sevo_linear_args": sevo.LinearArgs,
+       "sevo_prefill_attn_args": sevo.PrefillAttnArgs, "sevo_prefill_args": sevo.PrefillArgs}
 
 
 def test_ctypes_structs_match_c_layout():
@@ -230,9 +238,9 @@ def test_profile_begin_rejects_bad_arguments():
     L = sevo.lib()
     assert L.sevo_profile_begin(0, 1) == sevo.INVALID_ARGUMENT
     assert L.sevo_profile_begin(8, 0) == sevo.INVALID_ARGUMENT
-    assert L.sevo_profile_begin(8, 1 << 11) == sevo.INVALID_ARGUMENT
+    assert L.sevo_profile_begin(8, 1 << len(sevo.PROF_KINDS)) == sevo.INVALID_ARGUMENT
     # ending without a recording returns empty totals
     import ctypes as CT
-    ms = (CT.c_float * 11)()
-    cnt = (CT.c_int32 * 11)()
+    ms = (CT.c_float * len(sevo.PROF_KINDS))()
+    cnt = (CT.c_int32 * len(sevo.PROF_KINDS))()
     assert L.sevo_profile_end(ms, cnt) == sevo.OK and sum(cnt) == 0

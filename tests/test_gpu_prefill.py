@@ -93,3 +93,114 @@ def test_attn_prefill_page_permutation_bit_exact(S):
     o2 = sevo.sevo_attn_prefill(q, kvp2, torch.from_numpy(pt2.astype(np.int32)).cuda(), ss, 150)
     torch.cuda.synchronize()
     assert torch.equal(o1.view(torch.int16), o2.view(torch.int16))
+
+
+# ------------------------------------------------------------------ confidence engine
+def _token_major(pool, d):
+    """K and V of every (page, head, slot) of a pool [P, hkv, 2, 16 d] as
+    [P, hkv, 16, d] arrays (tile offsets of the documented layout)."""
+    s = np.arange(16)[:, None]
+    e = np.arange(d)[None, :]
+    return (pool[:, :, 0, :][:, :, ((e // 32) * 16 + s) * 32 + e % 32],
+            pool[:, :, 1, :][:, :, e * 16 + s])
+
+
+def _engine_case(S, shape, seed, lens, scored, conf_k, starts=None):
+    """Run the confidence engine on the GPU; returns its outputs and the inputs
+    the oracle needs (host side)."""
+    sevo, di = S
+    lens = np.asarray(lens, np.int64)
+    starts = np.zeros(len(lens), np.int64) if starts is None else np.asarray(starts, np.int64)
+    pop = make_population(starts + lens, shuffle=True, seed=seed)
+    rng = np.random.default_rng(seed)
+    toks = rng.integers(0, shape.vocab, size=int(lens.sum())).astype(np.int32)
+    seq_starts = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    tensors = di.device_weights(shape, seed)
+    model = sevo.sevo_init_model(shape, tensors, max_position=int((starts + lens).max()) + 1)
+    kvp = di.device_pools(shape, seed, pop.n_pages)
+    buf = sevo.PrefillBuffers(model, torch.from_numpy(toks).cuda(),
+                              torch.from_numpy(seq_starts).cuda(),
+                              torch.from_numpy(pop.page_table.astype(np.int32)).cuda(), kvp,
+                              torch.from_numpy(np.asarray(scored, np.int32)).cuda(), conf_k,
+                              int(lens.max()),
+                              start_pos=torch.from_numpy(starts.astype(np.int32)).cuda())
+    conf = buf.run()
+    torch.cuda.synchronize()
+    out = (conf.cpu().numpy().astype(np.float64),
+           buf.out_row_conf[:len(scored)].cpu().numpy().astype(np.float64),
+           [p.double().cpu().numpy() for p in kvp])
+    model.close()
+    return out, pop, toks, seq_starts, starts
+
+
+def test_prefill_confidence_tiny_matches_oracle(S):
+    """Two sequences of the tiny model through the whole engine: per-row c
+    (Eq. 1), per-sequence C (Eq. 2) and every appended K/V slot against the
+    oracle's prefill."""
+    shape = synth.WORKLOADS["tiny_step"].shape
+    lens = [300, 170]
+    scored = list(range(40, 300)) + list(range(320, 470))
+    say("prefill confidence (tiny model)")
+    (g_conf, g_row, g_pools), pop, toks, seq_starts, starts = _engine_case(
+        S, shape, 3, lens, scored, 20)
+    hw = synth.host_weights(shape, 3)
+    hkv = [p.astype(np.float64) for p in synth.host_pools(shape, 3, pop.n_pages)]
+    conf, c, _ = od.prefill_confidence(shape, hw, hkv, pop.page_table, toks, seq_starts, scored,
+                                       20)
+    row_err = np.abs(g_row - c).max()
+    say(f"  row c max err {row_err:.2e} (c in [{c.min():.3f}, {c.max():.3f}]); C {g_conf} vs "
+        f"{conf}")
+    # logits of the tiny model hold to 1e-2 end to end (bf16 storage flips, as
+    # for the decode step); c = logsumexp - mean top-K follows them
+    assert row_err <= 2e-2
+    assert np.abs(g_conf - conf).max() <= 1e-2
+    # every key / value the prefill appended, within one bf16 rounding step
+    for l in range(shape.n_layers):
+        gk, gv = _token_major(g_pools[l], shape.head_dim)
+        hk, hv = _token_major(hkv[l], shape.head_dim)
+        written = np.zeros(gk.shape[:3], bool)
+        for s, n in enumerate(lens):
+            for p in range(n):
+                written[pop.page_table[s, p // 16], :, p % 16] = True
+        spec = synth.kv_spec(shape, 3, l, pop.n_pages)
+        k0, v0 = _token_major(synth.host_values(spec).reshape(spec.shape), shape.head_dim)
+        np.testing.assert_array_equal(gk[~written], k0[~written])
+        np.testing.assert_array_equal(gv[~written], v0[~written])
+        for name, g, h in (("k", gk[written], hk[written]), ("v", gv[written], hv[written])):
+            # g, h: [slots, d].  A value is one bf16 rounding step from the
+            # oracle's, except where an upstream bf16 storage point (the
+            # normed input h of the projection) rounded the other way: that
+            # moves a whole vector by about one step of its largest entry
+            d = np.abs(g - h)
+            step = 2.0 ** -7 * np.abs(h) + 1e-6
+            vec = 2.0 ** -7 * np.abs(h).max(axis=-1, keepdims=True)
+            frac = float(np.mean(d <= step))
+            say(f"  layer {l} {name}: {frac:.5f} within one rounding step, worst "
+                f"{(d / (step + vec)).max():.2f} of the vector-scale bound")
+            assert np.all(d <= step + vec)
+            assert frac >= 0.99
+
+
+def test_prefill_confidence_full_width_reduced_depth(S):
+    """The 8B-class widths (hidden 4096, 32/8 x 128 heads, FFN 12288, vocab
+    151936) at 2 layers, two sequences of 400 and 200 tokens (the large-M GEMM
+    and several query / key blocks), 32 scored rows spread over both."""
+    import dataclasses
+    shape = dataclasses.replace(synth.DENSE_8B, n_layers=2)
+    lens = [400, 200]
+    scored = sorted(set(np.linspace(0, 599, 32).astype(int).tolist()))
+    say("prefill confidence (8B widths, 2 layers)")
+    (g_conf, g_row, _), pop, toks, seq_starts, starts = _engine_case(S, shape, 4, lens, scored, 20)
+    torch.cuda.empty_cache()
+    hw = synth.host_weights(shape, 4, lazy=True)
+    hw = {"embed": hw["embed"], "final_norm": hw["final_norm"], "layers": hw["layers"],
+          "lm_head": hw["lm_head"][0:shape.vocab]}
+    hkv = [p.astype(np.float64) for p in synth.host_pools(shape, 4, pop.n_pages)]
+    conf, c, _ = od.prefill_confidence(shape, hw, hkv, pop.page_table, toks, seq_starts, scored,
+                                       20)
+    row_err = np.abs(g_row - c).max()
+    say(f"  row c max err {row_err:.2e} (c in [{c.min():.3f}, {c.max():.3f}]); C {g_conf} vs "
+        f"{conf}")
+    # the full-width end-to-end bar of the decode step (bf16 storage flips)
+    assert row_err <= 6e-2
+    assert np.abs(g_conf - conf).max() <= 3e-2

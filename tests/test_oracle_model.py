@@ -163,3 +163,75 @@ def test_mirror_rounds_only_storage_points():
     b = od.decode_step(SHAPE, w, [k.copy() for k in kvp], pt, mirror=True, **args)
     rel = np.abs(a["logits"] - b["logits"]).max() / np.abs(a["logits"]).max()
     assert 1e-5 < rel < 5e-2, rel
+
+
+# ------------------------------------------------------------------ prefill (confidence engine)
+def test_prefill_forward_equals_transformers_and_incremental_decode():
+    """The batched prefill (two sequences back to back, every token through the
+    layer at once) reproduces the transformers causal forward's logits of each
+    sequence, and the oracle's own token-by-token decode."""
+    rng = np.random.default_rng(11)
+    w = _weights(SHAPE, rng)
+    lens = [37, 20]
+    seqs = [rng.integers(0, SHAPE.vocab, size=n) for n in lens]
+    starts = np.array([0, lens[0], lens[0] + lens[1]])
+    need = [(n + 15) // 16 for n in lens]
+    perm = rng.permutation(sum(need))
+    pt = np.full((2, max(need)), -1)
+    pt[0, :need[0]] = perm[:need[0]]
+    pt[1, :need[1]] = perm[need[0]:]
+    kvp = _empty_pools(SHAPE, sum(need))
+    x = od.prefill_forward(SHAPE, w, kvp, pt, np.concatenate(seqs), starts, mirror=False)
+    logits = od.lm_logits(SHAPE, w["final_norm"], w["lm_head"], x, mirror=False)
+    m = _hf_model(SHAPE, w)
+    for s in range(2):
+        with torch.no_grad():
+            ref = m(input_ids=torch.from_numpy(seqs[s][None])).logits.numpy()[0]
+        err = np.abs(logits[starts[s]:starts[s + 1]] - ref).max()
+        assert err < 2e-5 * np.abs(ref).max(), err
+    # token-by-token decode of sequence 1 from an empty cache
+    kvp2 = _empty_pools(SHAPE, sum(need))
+    for t in range(lens[1]):
+        out = od.decode_step(SHAPE, w, kvp2, pt[1:2], seqs[1][t:t + 1], np.array([t]),
+                             np.array([0]), seed=1, temperature=1.0, mirror=False)
+        np.testing.assert_allclose(out["logits"][0], logits[starts[1] + t], rtol=0,
+                                   atol=1e-10 * np.abs(logits).max())
+
+
+def test_prefill_with_cached_prefix_equals_full_prefill():
+    """A sequence whose first p0 tokens are already cached (start_pos = p0)
+    gives the same hidden states for the rest as prefilling it whole."""
+    rng = np.random.default_rng(12)
+    w = _weights(SHAPE, rng)
+    n, p0 = 41, 18
+    toks = rng.integers(0, SHAPE.vocab, size=n)
+    pt = rng.permutation(3)[None]
+    kvp = _empty_pools(SHAPE, 3)
+    full = od.prefill_forward(SHAPE, w, kvp, pt, toks, [0, n], mirror=False)
+    kvp2 = _empty_pools(SHAPE, 3)
+    od.prefill_forward(SHAPE, w, kvp2, pt, toks[:p0], [0, p0], mirror=False)
+    tail = od.prefill_forward(SHAPE, w, kvp2, pt, toks[p0:], [0, n - p0], start_pos=[p0],
+                              mirror=False)
+    np.testing.assert_allclose(tail, full[p0:], rtol=0, atol=1e-12 * np.abs(full).max())
+
+
+def test_prefill_confidence_per_sequence_means_and_batch_independence():
+    """C of a sequence is the mean of Eq. 1's c over its scored rows, computed
+    the same whether the sequence is scored alone or in a batch; a sequence
+    without scored rows gets 0."""
+    rng = np.random.default_rng(13)
+    w = _weights(SHAPE, rng)
+    lens = [30, 25, 9]
+    toks = rng.integers(0, SHAPE.vocab, size=sum(lens))
+    starts = np.concatenate([[0], np.cumsum(lens)])
+    pt = np.arange(6).reshape(3, 2)
+    rows = np.array([3, 10, 29, 31, 40, 54])   # none in the third sequence
+    conf, c, logits = od.prefill_confidence(SHAPE, w, _empty_pools(SHAPE, 6), pt, toks, starts,
+                                            rows, 5, mirror=False)
+    np.testing.assert_allclose(c, od.token_confidence(logits, 5))
+    np.testing.assert_allclose(conf[:2], [c[:3].mean(), c[3:].mean()])
+    assert conf[2] == 0.0
+    alone, c1, _ = od.prefill_confidence(SHAPE, w, _empty_pools(SHAPE, 6), pt[1:2],
+                                         toks[starts[1]:starts[2]], [0, lens[1]],
+                                         rows[3:] - starts[1], 5, mirror=False)
+    np.testing.assert_allclose(alone[0], conf[1], rtol=1e-12)
