@@ -142,6 +142,149 @@ def cpu_baseline(w, pop, n_sample, budget_s=30.0):
     }
 
 
+PREFILL_GEMM_KINDS = ("qkv", "attn_out", "gate_up", "down")
+
+
+def prefill_flops(shape, T, R):
+    """Algorithmic flops of one request of T tokens from position 0 with R
+    scored rows: causal attention (2 flops per multiply-add, q.k and p.v over
+    keys 0..t for every token and head), the projections (2 M N K) and the LM
+    head on the scored rows."""
+    hq, d, H, F = shape.n_q_heads, shape.head_dim, shape.hidden, shape.ffn
+    attn = 4.0 * hq * d * T * (T + 1) / 2
+    per_layer = {"qkv": 2.0 * T * shape.qkv_dim * H, "attn_out": 2.0 * T * H * shape.q_dim,
+                 "gate_up": 2.0 * T * 2 * F * H, "down": 2.0 * T * H * F}
+    return attn, per_layer, 2.0 * R * shape.vocab * H
+
+
+def prefill_cpu_baseline(shape, seed, n_tokens=256):
+    """The oracle on a bounded sample: layer 0 of the prefill over one
+    n_tokens sequence, then final norm + LM head + confidence for its rows;
+    extrapolated to the model's depth (the per-layer time is for that length)."""
+    from oracle import decoder as od
+    from paper_2604_07725_amd import synth
+    from threadpoolctl import threadpool_info
+    hw = synth.host_weights(shape, seed, lazy=True)
+    lw = hw["layers"][0]
+    rng = np.random.default_rng(seed)
+    toks = rng.integers(0, shape.vocab, n_tokens)
+    pages = (n_tokens + 15) // 16
+    pool = np.zeros((pages, shape.n_kv_heads, 2, 16 * shape.head_dim))
+    pt = np.arange(pages)[None]
+    row, pos = od.prefill_index([0, n_tokens])
+    x = np.asarray(hw["embed"][toks], np.float64)
+    t0 = time.perf_counter()
+    x = od.decoder_layer(shape, lw, x, pos, pool, pt[row], mirror=True)
+    t1 = time.perf_counter()
+    logits = od.lm_logits(shape, hw["final_norm"], hw["lm_head"][0:shape.vocab], x, mirror=True)
+    od.token_confidence(logits, 20)
+    t2 = time.perf_counter()
+    per_req = shape.n_layers * (t1 - t0) + (t2 - t1)
+    blas = threadpool_info()
+    return {"value": n_tokens / per_req, "unit": "tokens/s", "cores":
+            int(max([b.get("num_threads", 1) for b in blas] or [1])), "kind": "oracle",
+            "sample": (f"oracle prefill of one {n_tokens}-token sequence: layer 0 "
+                       f"({t1 - t0:.2f} s) x {shape.n_layers} layers + LM head and confidence "
+                       f"of every row ({t2 - t1:.2f} s) = {per_req:.1f} s; extrapolated in "
+                       f"depth only, at this length")}
+
+
+def prefill_main(args):
+    """The confidence engine (prefill-only scoring pass) on the 8B-class model:
+    one request at a time of each length, every row scored (Eq. 1 c, K_l = 20),
+    one C per request returned; per-kernel times from HIP events."""
+    import torch
+    from paper_2604_07725_amd import device_inputs as di
+    from paper_2604_07725_amd import sevo, synth
+    shape = synth.DENSE_8B
+    seed = 2
+    lengths = [int(v) for v in args.prefill_tokens.split(",")]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    t = time.time()
+    tensors = di.device_weights(shape, seed, dev)
+    model = sevo.sevo_init_model(shape, tensors, max_position=max(lengths) + 1)
+    torch.cuda.synchronize()
+    log(f"prefill: weights resident in {time.time() - t:.1f} s")
+    results = []
+    for T in lengths:
+        pages = (T + 15) // 16
+        pool = torch.empty(pages, shape.n_kv_heads, 2, 16 * shape.head_dim, dtype=torch.bfloat16,
+                           device=dev)   # one pool for every layer: the cache is not kept
+        perm = np.random.default_rng(T).permutation(pages).astype(np.int32)
+        pt = torch.from_numpy(perm[None]).to(dev)
+        toks = torch.from_numpy(np.random.default_rng(T + 1).integers(
+            0, shape.vocab, T).astype(np.int32)).to(dev)
+        ss = torch.tensor([0, T], dtype=torch.int32, device=dev)
+        rows = torch.arange(T, dtype=torch.int32, device=dev)
+        buf = sevo.PrefillBuffers(model, toks, ss, pt, pool, rows, 20, T, keep_row_conf=False)
+        buf.run()                      # warm-up
+        torch.cuda.synchronize()
+        reps = args.steps if args.steps < 16 else 2
+        start = torch.cuda.Event(enable_timing=True)
+        stop = torch.cuda.Event(enable_timing=True)
+        start.record()
+        for _ in range(reps):
+            buf.run()
+        stop.record()
+        torch.cuda.synchronize()
+        sec = start.elapsed_time(stop) / reps / 1e3
+        # per-kernel times: one more request with every launch bracketed
+        sevo.sevo_profile_begin(4096, sevo.PROF_KINDS)
+        buf.run()
+        torch.cuda.synchronize()
+        kp = sevo.sevo_profile_end()
+        attn_f, gemm_f, head_f = prefill_flops(shape, T, T)
+        kern = {}
+        for k, (ms, cnt) in kp.items():
+            row = {"ms": ms, "launches": cnt}
+            f = None
+            if k == "attn_prefill":
+                f = attn_f * shape.n_layers
+            elif k in gemm_f:
+                f = gemm_f[k] * shape.n_layers
+            elif k == "lm_head":
+                f = head_f
+            if f:
+                row["TFLOP_s"] = f / (ms * 1e-3) / 1e12
+                row["mfma_frac"] = row["TFLOP_s"] / BF16_PEAK_TFLOPS
+            kern[k] = row
+        conf = float(buf.out_conf.cpu()[0])
+        log(f"prefill {T} tokens: {sec:.3f} s per request; C = {conf:.4f}")
+        results.append({"tokens": T, "s_per_request": sec, "tokens_per_s": T / sec,
+                        "confidence": conf, "kernels": kern})
+        del buf, pool
+        torch.cuda.empty_cache()
+    model.close()
+    big = results[-1]
+    tot_gemm = sum(big["kernels"][k]["ms"] for k in PREFILL_GEMM_KINDS if k in big["kernels"])
+    gemm_flops = sum(prefill_flops(shape, big["tokens"], big["tokens"])[1].values()) * shape.n_layers
+    out = {
+        "metric": "confidence-engine prefill latency per request (s)",
+        "value": big["s_per_request"], "unit": "s", "higher_is_better": False,
+        "n_gpus": 1, "steps": args.steps if args.steps < 16 else 2, "warmup": 1,
+        "dtype": "bf16", "data": "synthetic (seeded; random-init weights)",
+        "vs_baseline": None,
+        "config": {"workload": "confidence_engine_dense8b", "model": "dense 8B-class decoder",
+                   "layers": shape.n_layers, "hidden": shape.hidden, "heads": "32/8x128",
+                   "ffn": shape.ffn, "vocab": shape.vocab, "batch": 1,
+                   "tokens": [r["tokens"] for r in results], "scored_rows": "all",
+                   "conf_topk": 20},
+        "roofline": {"kernel": "attn_prefill_kernel<128> (causal GQA prefill attention)",
+                     "bound": "mfma", "achieved": big["kernels"]["attn_prefill"]["TFLOP_s"],
+                     "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": big["kernels"]["attn_prefill"]["mfma_frac"], "traffic": None},
+        "gemm_roofline": {"bound": "mfma", "achieved": gemm_flops / (tot_gemm * 1e-3) / 1e12,
+                          "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                          "frac": gemm_flops / (tot_gemm * 1e-3) / 1e12 / BF16_PEAK_TFLOPS},
+        "per_length": results,
+    }
+    if not args.no_cpu_baseline:
+        log("timing the oracle on a bounded prefill sample (host cores)")
+        out["cpu_baseline"] = prefill_cpu_baseline(shape, seed)
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -157,6 +300,11 @@ def main():
     ap.add_argument("--min-p", type=float, default=0.0)
     ap.add_argument("--conf-topk", type=int, default=0,
                     help="also compute the per-token self-confidence (top-K log-probs) each step")
+    ap.add_argument("--mode", choices=("decode", "prefill"), default="decode",
+                    help="decode: the population decode step (default); prefill: the "
+                         "cross-model confidence engine at the prefill-benchmark lengths")
+    ap.add_argument("--prefill-tokens", default="40960,81920,122880",
+                    help="prefill mode: request lengths (tokens), one request at a time")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device copy (3 times), to scale HBM counters")
     args = ap.parse_args()
@@ -174,6 +322,8 @@ def main():
         torch.cuda.synchronize()
         print(json.dumps({"copy_calibration_bytes": src.numel() * 4, "copies": 3}), flush=True)
         return
+    if args.mode == "prefill":
+        return prefill_main(args)
     from paper_2604_07725_amd import device_inputs as di
     from paper_2604_07725_amd import sevo, synth
 
