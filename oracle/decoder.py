@@ -217,13 +217,63 @@ def append_kv(kv_pool, page_table, positions, k, v):
         tiles[:, 1, v_tile_offset(p % PAGE, e)] = v[i]
 
 
+# ------------------------------------------------------------------ mixture of experts
+def moe_route(logits, top_k, decision_dtype=np.float32):
+    """Experts and weights of each token: the top_k largest router logits
+    (value descending, ties to the lower expert index; the choice is taken in
+    ``decision_dtype``, the kernel's fp32) and a softmax over the selected
+    logits -- the router's softmax probabilities of the selected experts,
+    renormalised to sum to one.  ``gap`` = the float64 k-th minus (k+1)-th
+    largest logit, so a caller can tell choices rounding may flip.
+    Returns sel int64 [N, k], w float64 [N, k], gap float64 [N]."""
+    logits = np.asarray(logits, np.float64)
+    N, E = logits.shape
+    dec = logits.astype(decision_dtype).astype(np.float64)
+    sel = np.empty((N, top_k), np.int64)
+    w = np.empty((N, top_k))
+    gap = np.empty(N)
+    for t in range(N):
+        order = np.lexsort((np.arange(E), -dec[t]))
+        sel[t] = order[:top_k]
+        z = logits[t, sel[t]]
+        e = np.exp(z - z.max())
+        w[t] = e / e.sum()
+        srt = np.sort(logits[t])[::-1]
+        gap[t] = srt[top_k - 1] - srt[top_k] if top_k < E else np.inf
+    return sel, w, gap
+
+
+def moe_ffn(shape, lw, h2, mirror=True):
+    """The mixture-of-experts FFN on normed inputs h2 [N, H]:
+    sum over the token's selected experts e of w_e * (silu(h2 W_g[e]^T) *
+    (h2 W_u[e]^T)) W_d[e]^T.  Returns (out [N, H], routing gap [N])."""
+    rb = round_bf16 if mirror else _ident
+    keep32 = _f32 if mirror else _ident
+    Fe = shape.expert_ffn
+    h2 = np.asarray(h2, np.float64)
+    logits = keep32(h2 @ np.asarray(lw["w_router"], np.float64).T)
+    sel, w, gap = moe_route(logits, shape.top_k)
+    out = np.zeros_like(h2)
+    wgu = lw["w_expert_gate_up"]
+    wd = lw["w_expert_down"]
+    for t in range(h2.shape[0]):
+        for j in range(shape.top_k):
+            e = int(sel[t, j])
+            gu = h2[t] @ np.asarray(wgu[e], np.float64).T
+            a = rb(silu(gu[:Fe]) * gu[Fe:])
+            out[t] += w[t, j] * (a @ np.asarray(wd[e], np.float64).T)
+    return out, gap
+
+
 # ------------------------------------------------------------------ decoder
-def decoder_layer(shape, lw, x, positions, kv_pool, page_table, mirror=True):
+def decoder_layer(shape, lw, x, positions, kv_pool, page_table, mirror=True, stats=None):
     """One pre-norm GQA decoder layer for the population (updates x, appends KV).
 
     x [N, H] residual stream.  Steps: RMSNorm, QKV projection, per-head
     QK-RMSNorm, RoPE at p_i, append k and v as key p_i, attention over keys
-    0..p_i, output projection + residual, RMSNorm, SwiGLU FFN + residual.
+    0..p_i, output projection + residual, RMSNorm, SwiGLU FFN (or the
+    mixture of experts) + residual.  ``stats`` (a dict) collects the smallest
+    routing gap of MoE layers under "route_gap".
     """
     rb = round_bf16 if mirror else _ident
     keep32 = _f32 if mirror else _ident
@@ -249,6 +299,11 @@ def decoder_layer(shape, lw, x, positions, kv_pool, page_table, mirror=True):
     o = rb(o).reshape(N, hq * D)
     x = keep32(x + o @ np.asarray(lw["w_o"], np.float64).T)
     h2 = rb(rms_norm(x, lw["ffn_norm"], eps))
+    if shape.is_moe:
+        y, gap = moe_ffn(shape, lw, h2, mirror)
+        if stats is not None:
+            stats["route_gap"] = min(stats.get("route_gap", np.inf), float(gap.min()))
+        return keep32(x + y)
     gu = h2 @ np.asarray(lw["w_gate_up"], np.float64).T
     a = rb(silu(gu[:, :F]) * gu[:, F:])
     x = keep32(x + a @ np.asarray(lw["w_down"], np.float64).T)
@@ -302,7 +357,7 @@ def logprob_sample(logits, temperature, seed, uids, positions, noise=None,
 
 
 def decode_step(shape, weights, kv_pools, page_table, tokens, positions, uids,
-                seed, temperature, mirror=True, layers=None):
+                seed, temperature, mirror=True, layers=None, stats=None):
     """One decode step for a population.
 
     weights: mapping with "embed" [V, H] (row-indexable), "lm_head" [V, H],
@@ -317,7 +372,7 @@ def decode_step(shape, weights, kv_pools, page_table, tokens, positions, uids,
     n_layers = shape.n_layers if layers is None else layers
     for l in range(n_layers):
         x = decoder_layer(shape, weights["layers"][l], x, positions, kv_pools[l], page_table,
-                          mirror)
+                          mirror, stats)
     logits = lm_logits(shape, weights["final_norm"], weights["lm_head"], x, mirror)
     ids, lps, gaps = logprob_sample(logits, temperature, seed, uids, positions)
     return {"ids": ids, "lps": lps, "gaps": gaps, "logits": logits, "x": x}

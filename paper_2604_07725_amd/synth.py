@@ -142,6 +142,14 @@ class ModelShape:
     rms_eps: float = 1.0e-6
     qk_norm: bool = True
     page_size: int = PAGE_SIZE
+    # mixture-of-experts FFN (0 experts = the dense SwiGLU FFN of size ffn)
+    n_experts: int = 0
+    top_k: int = 0
+    expert_ffn: int = 0
+
+    @property
+    def is_moe(self) -> bool:
+        return self.n_experts > 0
 
     @property
     def q_dim(self) -> int:
@@ -155,13 +163,24 @@ class ModelShape:
     def qkv_dim(self) -> int:
         return self.q_dim + 2 * self.kv_dim
 
-    def layer_weight_elems(self) -> int:
+    def layer_weight_elems(self, active_experts: float | None = None) -> int:
+        """bf16 weight elements of one layer a decode step reads; a MoE layer
+        reads the router and the experts its tokens select (all experts if
+        active_experts is None)."""
         H = self.hidden
-        return (self.qkv_dim * H + H * self.q_dim + 2 * self.ffn * H + H * self.ffn)
+        attn = self.qkv_dim * H + H * self.q_dim
+        if self.is_moe:
+            e = self.n_experts if active_experts is None else active_experts
+            return attn + self.n_experts * H + e * 3 * self.expert_ffn * H
+        return attn + 2 * self.ffn * H + H * self.ffn
 
-    def weight_bytes(self) -> int:
+    def weight_bytes(self, active_experts: float | None = None) -> int:
         """Bytes of bf16 weights one decode step streams (layers + LM head)."""
-        return 2 * (self.n_layers * self.layer_weight_elems() + self.vocab * self.hidden)
+        return int(2 * (self.n_layers * self.layer_weight_elems(active_experts)
+                        + self.vocab * self.hidden))
+
+    def stored_weight_bytes(self) -> int:
+        return self.weight_bytes(None)
 
 
 TINY = ModelShape(n_layers=1, hidden=256, n_q_heads=4, n_kv_heads=2, head_dim=64,
@@ -170,6 +189,12 @@ DENSE_8B = ModelShape(n_layers=36, hidden=4096, n_q_heads=32, n_kv_heads=8, head
                       ffn=12288, vocab=151936)
 DENSE_32B = ModelShape(n_layers=64, hidden=5120, n_q_heads=64, n_kv_heads=8, head_dim=128,
                        ffn=25600, vocab=151936)
+# mixture-of-experts decoders (Qwen3-MoE layout: router, top-k of the experts,
+# softmax over the selected logits, SwiGLU experts)
+TINY_MOE = ModelShape(n_layers=2, hidden=256, n_q_heads=4, n_kv_heads=2, head_dim=64, ffn=0,
+                      vocab=4096, n_experts=64, top_k=4, expert_ffn=64)
+MOE_30B_A3B = ModelShape(n_layers=48, hidden=2048, n_q_heads=32, n_kv_heads=4, head_dim=128,
+                         ffn=0, vocab=151936, n_experts=128, top_k=8, expert_ffn=768)
 
 
 # ---------------------------------------------------------------- workloads
@@ -198,6 +223,11 @@ WORKLOADS = {
         Workload("dense8b_pop16_agg8", DENSE_8B, 16, "agg8_8k_pm10", seed=3, steps=128),
         # 32B-class, N=16, p = 16384
         Workload("dense32b_pop16_agg4", DENSE_32B, 16, "const16384", seed=4, steps=64),
+        # tiny MoE decoder (2 layers, 64 experts, top-4), N=4, p ~ U{256..512}
+        Workload("tiny_moe_step", TINY_MOE, 4, "u256_512", seed=5),
+        # 30B-A3B-class MoE decoder (48 layers, 128 experts, top-8), N=64,
+        # p ~ U{16384..32768}
+        Workload("moe30b_pop64_agg4", MOE_30B_A3B, 64, "u16384_32768", seed=6, steps=16),
     ]
 }
 
@@ -282,6 +312,7 @@ def workload_population(w: Workload, extra_tokens: int = 0, shuffle: bool = True
 K_EMBED, K_LMHEAD, K_FINAL_NORM = 1, 2, 3
 K_ATTN_NORM, K_WQKV, K_QNORM, K_KNORM, K_WO, K_FFN_NORM, K_WGU, K_WDOWN = range(10, 18)
 K_KVPOOL, K_Q = 30, 32
+K_WROUTER, K_WEGU, K_WEDOWN = 18, 19, 20
 
 WEIGHT_STD = 0.02
 GAIN_STD = 0.02
@@ -303,16 +334,25 @@ class TensorSpec:
 def layer_specs(shape: ModelShape, seed: int, layer: int) -> dict:
     H, F, D = shape.hidden, shape.ffn, shape.head_dim
     k = lambda kind: tensor_key(seed, kind, layer)  # noqa: E731
-    return {
+    specs = {
         "attn_norm": TensorSpec((H,), k(K_ATTN_NORM), GAIN_STD, 1.0),
         "w_qkv": TensorSpec((shape.qkv_dim, H), k(K_WQKV), WEIGHT_STD),
         "q_norm": TensorSpec((D,), k(K_QNORM), GAIN_STD, 1.0),
         "k_norm": TensorSpec((D,), k(K_KNORM), GAIN_STD, 1.0),
         "w_o": TensorSpec((H, shape.q_dim), k(K_WO), WEIGHT_STD),
         "ffn_norm": TensorSpec((H,), k(K_FFN_NORM), GAIN_STD, 1.0),
-        "w_gate_up": TensorSpec((2 * F, H), k(K_WGU), WEIGHT_STD),
-        "w_down": TensorSpec((H, F), k(K_WDOWN), WEIGHT_STD),
     }
+    if shape.is_moe:
+        E, Fe = shape.n_experts, shape.expert_ffn
+        specs["w_router"] = TensorSpec((E, H), k(K_WROUTER), WEIGHT_STD)
+        # expert e's gate (rows 0..Fe-1) and up (rows Fe..2Fe-1) projections,
+        # then its down projection, each expert's matrix contiguous
+        specs["w_expert_gate_up"] = TensorSpec((E, 2 * Fe, H), k(K_WEGU), WEIGHT_STD)
+        specs["w_expert_down"] = TensorSpec((E, H, Fe), k(K_WEDOWN), WEIGHT_STD)
+    else:
+        specs["w_gate_up"] = TensorSpec((2 * F, H), k(K_WGU), WEIGHT_STD)
+        specs["w_down"] = TensorSpec((H, F), k(K_WDOWN), WEIGHT_STD)
+    return specs
 
 
 def global_specs(shape: ModelShape, seed: int) -> dict:
