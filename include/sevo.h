@@ -88,7 +88,14 @@ const char* sevo_version(void);
 /* Decoder shape.  Supported: head_dim in {64, 128}; n_q_heads % n_kv_heads == 0
  * with n_q_heads / n_kv_heads in {1, 2, 4, 8}; page_size == 16; hidden, ffn and
  * n_q_heads * head_dim multiples of 128; vocab a multiple of 64; qk_norm in
- * {0, 1}; rms_eps > 0. */
+ * {0, 1}; rms_eps > 0.
+ * Mixture of experts (n_experts > 0; the FFN of every layer; ffn is then
+ * unused): the Qwen3-MoE layer -- router logits h W_r^T, the n_experts_active
+ * largest (ties to the lower expert index), weights = softmax over the
+ * selected logits (the router probabilities of the selected experts,
+ * renormalised), FFN(h) = sum over them of w_e * SwiGLU expert e.  Supported:
+ * n_experts a multiple of 64 up to 256; 1 <= n_experts_active <= 16;
+ * expert_ffn a multiple of 32. */
 typedef struct {
   int32_t n_layers, hidden, n_q_heads, n_kv_heads, head_dim, ffn, vocab;
   int32_t page_size;    /* must be 16 */
@@ -96,6 +103,9 @@ typedef struct {
   int32_t qk_norm;      /* 1: per-head RMSNorm of q and k before RoPE (Qwen3 style) */
   float rope_theta;     /* rotate-half RoPE base, e.g. 1e6 */
   float rms_eps;        /* RMSNorm epsilon, e.g. 1e-6 */
+  int32_t n_experts;        /* 0 = dense SwiGLU FFN */
+  int32_t n_experts_active; /* experts per token (top-k) */
+  int32_t expert_ffn;       /* intermediate size of one expert */
 } sevo_model_config;
 
 /* Borrowed bf16 weight pointers (device); they must outlive the model.  The
@@ -109,7 +119,14 @@ typedef struct {
  *   w_o       [hidden][n_q_heads head_dim]
  *   w_gate_up [2 ffn][hidden]        rows 0..ffn-1 gate, ffn..2ffn-1 up, packed
  *                                    with kind SEVO_PACK_GATE_UP
- *   w_down    [hidden][ffn] */
+ *   w_down    [hidden][ffn]
+ * A mixture-of-experts model (n_experts > 0) leaves w_gate_up / w_down NULL and
+ * gives, per layer (Fe = expert_ffn, E = n_experts):
+ *   w_router         [E][hidden] (packed)
+ *   w_expert_gate_up [E][2 Fe][hidden]: expert e's matrix (gate rows, then up
+ *                    rows) at element offset e * 2 Fe * hidden, each packed
+ *                    with kind SEVO_PACK_GATE_UP
+ *   w_expert_down    [E][hidden][Fe]: expert e at e * hidden * Fe, packed */
 typedef struct {
   const void* embed;
   const void* lm_head;
@@ -122,6 +139,9 @@ typedef struct {
   const void* const* ffn_norm;
   const void* const* w_gate_up;
   const void* const* w_down;
+  const void* const* w_router;
+  const void* const* w_expert_gate_up;
+  const void* const* w_expert_down;
 } sevo_weights;
 
 typedef struct sevo_model sevo_model;
@@ -441,6 +461,22 @@ sevo_status sevo_qk_norm_rope_append(const sevo_model* m, int32_t layer, const f
                                      int64_t num_pages, void* q_out, void* kv_pool,
                                      void* stream);
 
+/* The mixture-of-experts FFN of one layer on normed inputs (the sub-step of a
+ * MoE decode step): h bf16 in the tiled activation layout, n rows (a buffer
+ * of ceil(n / 16) * 16 rows; padding rows are not read), device memory owned
+ * by the caller like every output.
+ *   out_experts int32 [n][k] (selected experts, largest logit first; always k
+ *   distinct experts, also when logits are not finite);
+ *   out_weights fp32 [n][k]; out_partials fp32 [k][n][hidden]:
+ *   partial j of token t = w_{t,j} * SwiGLU expert out_experts[t][j] (h_t), so
+ *   FFN(h_t) = the sum of the k partials in slot order.
+ * n <= 65536 / k.  Errors: INVALID_ARGUMENT, UNSUPPORTED (dense model),
+ * WORKSPACE_TOO_SMALL, HIP. */
+sevo_status sevo_moe_ffn(const sevo_model* m, int32_t layer, const void* h, int32_t n,
+                         int32_t* out_experts, float* out_weights, float* out_partials,
+                         void* workspace, size_t workspace_bytes, void* stream);
+size_t sevo_moe_workspace_bytes(const sevo_model* m, int32_t n);
+
 /* ------------------------------------------------------------------ utilities */
 
 /* Synthetic-input generator (device twin of the host generator): element e of
@@ -478,7 +514,9 @@ sevo_status sevo_validate_paging(const int32_t* page_table, const int32_t* lengt
 #define SEVO_PROF_SAMPLE 9        /* log-softmax + Gumbel-max (+ confidence) */
 #define SEVO_PROF_EMBED 10        /* embedding gather                    */
 #define SEVO_PROF_ATTN_PREFILL 11 /* causal prefill attention            */
-#define SEVO_PROF_NUM_KINDS 12
+#define SEVO_PROF_MOE_ROUTE 12    /* MoE router GEMM, top-k, expert lists */
+#define SEVO_PROF_MOE_EXPERTS 13  /* MoE expert gate/up + down GEMMs      */
+#define SEVO_PROF_NUM_KINDS 14
 sevo_status sevo_profile_begin(int32_t max_launches, uint32_t kinds);
 sevo_status sevo_profile_end(float* total_ms, int32_t* launches);
 

@@ -86,6 +86,27 @@ struct PrefillAttnArgs {
 };
 hipError_t launch_attn_prefill(const PrefillAttnArgs& a, hipStream_t st);
 
+// ---- moe.hip: mixture-of-experts FFN of a decode step
+struct MoeExpertArgs {
+  int n, hidden, ffn, n_experts, top_k;
+  const bf16_t* x;          // normed input, tiled [n][hidden]
+  const bf16_t* w_gate_up;  // [E][2 ffn][hidden], each expert packed (gate/up superblocks)
+  const bf16_t* w_down;     // [E][hidden][ffn], each expert packed
+  const int32_t* offsets;   // [E + 1] assignment offsets per expert
+  const int32_t* assign;    // [n k] assignments t * k + slot, expert-major
+  const float* weights;     // [n k] routing weights
+  bf16_t* act;              // [n k][ffn] SwiGLU products, row = assignment position
+  float* part;              // [k][n][hidden] weighted expert outputs per slot
+};
+bool moe_supported(int n_experts, int top_k, int expert_ffn, int hidden);
+// logits = sum of S split partials [S][n][E]; sel / w [n][k]
+hipError_t launch_moe_route(const float* part, int S, int n, int E, int k, int32_t* sel,
+                            float* w, hipStream_t st);
+hipError_t launch_moe_plan(const int32_t* sel, int nk, int E, int32_t* offsets, int32_t* assign,
+                           hipStream_t st);
+// gate/up + SwiGLU into act, then down into part
+hipError_t launch_moe_experts(const MoeExpertArgs& a, hipStream_t st);
+
 // ---- linear.hip
 struct LinearPlan {
   int k_splits;

@@ -1,0 +1,286 @@
+// Mixture-of-experts FFN of a decode step (Qwen3-MoE layout): router logits,
+// the top-k experts of each token with a softmax over the selected logits,
+// then SwiGLU experts.  At decode every token of the population routes to k
+// experts, so a step touches most experts once: the FFN is a stream of the
+// selected experts' weights, each multiplied by the few tokens routed to it.
+//
+//   * route: one wave per token sums the router GEMM's split-K partials (in
+//     split order), takes the k largest logits by repeated wave arg-max
+//     (value, then lower expert index) and the softmax over them;
+//   * plan: one workgroup counts tokens per expert and lays the (token, slot)
+//     assignments out expert-major, tokens in order (a fixed order: results do
+//     not depend on scheduling);
+//   * experts: a grouped skinny GEMM over (64-row weight superblock, expert,
+//     64-assignment tile), the same weight stream as the dense projections
+//     (packed fragment-major weights, four waves taking the 32-k steps round
+//     robin, four fragment buffers in flight); activation rows are gathered
+//     through the assignment list.  Gate/up writes silu(g) * u per assignment
+//     (bf16, row-major); down writes w * y into partial [slot][token][hidden]
+//     (fp32), which the next residual add + RMSNorm sums in slot order.
+#include "common.h"
+#include "kernels.h"
+
+namespace sevo {
+
+constexpr int kMoeMaxExperts = 256;
+constexpr int kMoeMaxTopK = 16;
+
+// ---- route: logits [S][n][E] (split partials) -> sel [n][k], w [n][k]
+__global__ __launch_bounds__(64) void moe_route_kernel(const float* __restrict__ part, int S,
+                                                       int n, int E, int k,
+                                                       int32_t* __restrict__ sel,
+                                                       float* __restrict__ w) {
+  const int t = blockIdx.x;
+  const int lane = threadIdx.x;
+  float v[kMoeMaxExperts / 64];
+#pragma unroll
+  for (int i = 0; i < kMoeMaxExperts / 64; ++i) {
+    const int e = lane + 64 * i;
+    float acc = -INFINITY;
+    if (e < E) {
+      acc = 0.f;
+      for (int s = 0; s < S; ++s) acc += part[((size_t)s * n + t) * E + e];
+    }
+    v[i] = acc;
+  }
+  // k rounds of a wave arg-max over the experts not taken yet (value
+  // descending, then lower index); an expert is eligible even when its logit
+  // is -inf or NaN, so the k experts are always distinct and valid
+  float z[kMoeMaxTopK];
+  int id[kMoeMaxTopK];
+  uint32_t taken = 0;  // bit i: expert lane + 64 i already selected
+#pragma unroll
+  for (int r = 0; r < kMoeMaxTopK; ++r) {
+    z[r] = -INFINITY;
+    id[r] = 0;
+    if (r >= k) continue;
+    // this lane's best (index ascending with i: strict > keeps the lowest)
+    float bv = -INFINITY;
+    int bi = 0x7FFFFFFF;
+#pragma unroll
+    for (int i = 0; i < kMoeMaxExperts / 64; ++i) {
+      const int e = lane + 64 * i;
+      if (e < E && !((taken >> i) & 1u) && (bi == 0x7FFFFFFF || v[i] > bv)) {
+        bv = v[i];
+        bi = e;
+      }
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      const float ov = __shfl_xor(bv, o, kWave);
+      const int oi = __shfl_xor(bi, o, kWave);
+      if (oi != 0x7FFFFFFF && (bi == 0x7FFFFFFF || ov > bv || (ov == bv && oi < bi))) {
+        bv = ov;
+        bi = oi;
+      }
+    }
+    // lane 0's choice for every lane (the order is total unless a NaN is
+    // involved; then lanes could disagree)
+    bi = __builtin_amdgcn_readfirstlane(bi);
+    bv = __shfl(bv, 0, kWave);
+#pragma unroll
+    for (int i = 0; i < kMoeMaxExperts / 64; ++i)
+      if (lane + 64 * i == bi) taken |= 1u << i;
+    z[r] = bv;
+    id[r] = bi;
+  }
+  if (lane == 0) {
+    float sum = 0.f;
+#pragma unroll
+    for (int r = 0; r < kMoeMaxTopK; ++r)
+      if (r < k) sum += expf(z[r] - z[0]);
+#pragma unroll
+    for (int r = 0; r < kMoeMaxTopK; ++r)
+      if (r < k) {
+        sel[t * k + r] = id[r];
+        w[t * k + r] = expf(z[r] - z[0]) / sum;
+      }
+  }
+}
+
+// ---- plan: offsets [E + 1] and assign [n k] (entries t * k + slot)
+__global__ __launch_bounds__(256) void moe_plan_kernel(const int32_t* __restrict__ sel, int nk,
+                                                       int E, int32_t* __restrict__ offsets,
+                                                       int32_t* __restrict__ assign) {
+  __shared__ int cnt[kMoeMaxExperts + 1];
+  for (int e = threadIdx.x; e < E; e += 256) {
+    int c = 0;
+    for (int r = 0; r < nk; ++r) c += sel[r] == e;
+    cnt[e] = c;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int acc = 0;
+    for (int e = 0; e < E; ++e) {
+      const int c = cnt[e];
+      cnt[e] = acc;
+      offsets[e] = acc;
+      acc += c;
+    }
+    offsets[E] = acc;
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < E; e += 256) {
+    int pos = cnt[e];
+    for (int r = 0; r < nk; ++r)
+      if (sel[r] == e) assign[pos++] = r;
+  }
+}
+
+struct MoeFrag {
+  bf16x8v a[4];
+  bf16x8v b[4];
+};
+
+// Grouped skinny GEMM over the selected experts.
+// EPI 0 (gate/up): X = the normed input, tiled [n][H], rows gathered by
+//   token; W = packed gate/up of each expert [2 Fe][H] (32 + 32 row
+//   superblocks); out act [n k][Fe] bf16 row-major, row = assignment position.
+// EPI 1 (down): X = act rows of the expert (contiguous positions); W = packed
+//   down [H][Fe]; out part [k][n][H] fp32 = routing weight * product.
+template <int EPI>
+__global__ __launch_bounds__(256, 2) void moe_expert_kernel(MoeExpertArgs a) {
+  __shared__ f32x4 red[4][4][4][64];
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int sb = blockIdx.x, e = blockIdx.y;
+  const int off = a.offsets[e];
+  const int ne = a.offsets[e + 1] - off;
+  const int m0 = blockIdx.z * 64;
+  if (m0 >= ne) return;  // uniform over the workgroup
+  const int K = EPI == 0 ? a.hidden : a.ffn;
+  const int N = EPI == 0 ? 2 * a.ffn : a.hidden;
+  const int KS = K >> 5;
+  const int r = lane & 15, q = lane >> 4;
+  const bf16_t* W = (EPI == 0 ? a.w_gate_up : a.w_down) + (size_t)e * N * K;
+  const bf16_t* wp = W + (size_t)sb * KS * 2048 + lane * 8;
+  // activation rows of this lane per 16-row block (rows past the expert's
+  // count read its last row: they only feed outputs that are never stored)
+  const bf16_t* xp[4];
+#pragma unroll
+  for (int b = 0; b < 4; ++b) {
+    const int i = min(m0 + 16 * b + r, ne - 1);
+    if constexpr (EPI == 0) {
+      const int t = a.assign[off + i] / a.top_k;
+      xp[b] = a.x + ((size_t)(t >> 4) * KS) * 512 + (16 * q + (t & 15)) * 8;
+    } else {
+      xp[b] = a.act + (size_t)(off + i) * a.ffn + 8 * q;
+    }
+  }
+  const int cnt = KS > wave ? (KS - wave + 3) >> 2 : 0;  // this wave's 32-k steps
+  f32x4 acc[4][4];
+#pragma unroll
+  for (int tt = 0; tt < 4; ++tt)
+#pragma unroll
+    for (int b = 0; b < 4; ++b) acc[tt][b] = f32x4{0.f, 0.f, 0.f, 0.f};
+  auto load = [&](MoeFrag& f, int j) {
+    const int st = wave + 4 * min(j, cnt - 1);
+#pragma unroll
+    for (int tt = 0; tt < 4; ++tt)
+      f.a[tt] = *reinterpret_cast<const bf16x8v*>(wp + (size_t)st * 2048 + tt * 512);
+#pragma unroll
+    for (int b = 0; b < 4; ++b)
+      f.b[b] = *reinterpret_cast<const bf16x8v*>(xp[b] + (EPI == 0 ? (size_t)st * 512 : (size_t)st * 32));
+  };
+  auto mma = [&](const MoeFrag& f) {
+#pragma unroll
+    for (int tt = 0; tt < 4; ++tt)
+#pragma unroll
+      for (int b = 0; b < 4; ++b)
+        acc[tt][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f.a[tt], f.b[b], acc[tt][b], 0, 0, 0);
+  };
+  if (cnt > 0) {
+    MoeFrag f0, f1, f2, f3;
+    load(f0, 0);
+    load(f1, 1);
+    load(f2, 2);
+    for (int j = 0; j < cnt; j += 4) {
+      load(f3, j + 3);
+      __builtin_amdgcn_sched_barrier(0);
+      mma(f0);
+      __builtin_amdgcn_sched_barrier(0);
+      load(f0, j + 4);
+      __builtin_amdgcn_sched_barrier(0);
+      if (j + 1 < cnt) mma(f1);
+      __builtin_amdgcn_sched_barrier(0);
+      load(f1, j + 5);
+      __builtin_amdgcn_sched_barrier(0);
+      if (j + 2 < cnt) mma(f2);
+      __builtin_amdgcn_sched_barrier(0);
+      load(f2, j + 6);
+      __builtin_amdgcn_sched_barrier(0);
+      if (j + 3 < cnt) mma(f3);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+#pragma unroll
+  for (int tt = 0; tt < 4; ++tt)
+#pragma unroll
+    for (int b = 0; b < 4; ++b) red[wave][tt][b][lane] = acc[tt][b];
+  __syncthreads();
+  // D of tile (tt, b): lane holds activation row 16 b + lane % 16 and weight
+  // rows 16 tt + 4 (lane / 16) + 0..3 (4 consecutive output columns)
+  if constexpr (EPI == 0) {
+    for (int idx = threadIdx.x; idx < 2 * 4 * 64; idx += 256) {
+      const int l = idx & 63, tb = idx >> 6;
+      const int tt = tb >> 2, b = tb & 3;  // tt in {0, 1}: gate rows
+      const f32x4 g = red[0][tt][b][l] + red[1][tt][b][l] + red[2][tt][b][l] + red[3][tt][b][l];
+      const f32x4 u = red[0][tt + 2][b][l] + red[1][tt + 2][b][l] + red[2][tt + 2][b][l] +
+                      red[3][tt + 2][b][l];
+      const int i = m0 + 16 * b + (l & 15);
+      const int col = sb * 32 + 16 * tt + 4 * (l >> 4);
+      if (i < ne) {
+        uint2 o;
+        o.x = pack_bf16x2(g.x / (1.f + __expf(-g.x)) * u.x, g.y / (1.f + __expf(-g.y)) * u.y);
+        o.y = pack_bf16x2(g.z / (1.f + __expf(-g.z)) * u.z, g.w / (1.f + __expf(-g.w)) * u.w);
+        *reinterpret_cast<uint2*>(a.act + (size_t)(off + i) * a.ffn + col) = o;
+      }
+    }
+  } else {
+    for (int idx = threadIdx.x; idx < 4 * 4 * 64; idx += 256) {
+      const int l = idx & 63, tb = idx >> 6;
+      const int tt = tb >> 2, b = tb & 3;
+      const f32x4 v = red[0][tt][b][l] + red[1][tt][b][l] + red[2][tt][b][l] + red[3][tt][b][l];
+      const int i = m0 + 16 * b + (l & 15);
+      if (i < ne) {
+        const int asg = a.assign[off + i];
+        const int t = asg / a.top_k, slot = asg - t * a.top_k;
+        const float wt = a.weights[asg];
+        const int col = sb * 64 + 16 * tt + 4 * (l >> 4);
+        *reinterpret_cast<f32x4*>(a.part + ((size_t)slot * a.n + t) * a.hidden + col) = v * wt;
+      }
+    }
+  }
+}
+
+bool moe_supported(int E, int top_k, int ffn, int hidden) {
+  return E >= 64 && E <= kMoeMaxExperts && E % 64 == 0 && top_k >= 1 && top_k <= kMoeMaxTopK &&
+         top_k <= E && ffn >= 32 && ffn % 32 == 0 && hidden % 64 == 0;
+}
+
+hipError_t launch_moe_route(const float* part, int S, int n, int E, int k, int32_t* sel,
+                            float* w, hipStream_t st) {
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(moe_route_kernel, dim3(n), dim3(64), 0, st, part, S, n, E, k, sel, w);
+  return hipGetLastError();
+}
+
+hipError_t launch_moe_plan(const int32_t* sel, int nk, int E, int32_t* offsets, int32_t* assign,
+                           hipStream_t st) {
+  hipLaunchKernelGGL(moe_plan_kernel, dim3(1), dim3(256), 0, st, sel, nk, E, offsets, assign);
+  return hipGetLastError();
+}
+
+hipError_t launch_moe_experts(const MoeExpertArgs& a, hipStream_t st) {
+  if (a.n == 0) return hipSuccess;
+  const int mt = (a.n + 63) / 64;  // an expert takes each token at most once
+  hipLaunchKernelGGL(moe_expert_kernel<0>, dim3(2 * a.ffn / 64, a.n_experts, mt), dim3(256), 0,
+                     st, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(moe_expert_kernel<1>, dim3(a.hidden / 64, a.n_experts, mt), dim3(256), 0,
+                     st, a);
+  return hipGetLastError();
+}
+
+}  // namespace sevo

@@ -156,6 +156,7 @@ struct sevo_model {
   const void* lm_head;
   const void* final_norm;
   std::vector<const void*> attn_norm, w_qkv, q_norm, k_norm, w_o, ffn_norm, w_gate_up, w_down;
+  std::vector<const void*> w_router, w_expert_gate_up, w_expert_down;  // MoE models
   float* rope_cos = nullptr;
   float* rope_sin = nullptr;
   int device = 0;
@@ -185,21 +186,31 @@ SEVO_API sevo_status sevo_init_model(const sevo_model_config* cfg, const sevo_we
     if (!cfg || !w || !out) return fail(SEVO_ERR_INVALID_ARGUMENT, "null argument");
     *out = nullptr;
     const sevo_model_config& c = *cfg;
-    if (c.n_layers < 1 || c.hidden < 1 || c.ffn < 1 || c.vocab < 1)
+    const bool moe = c.n_experts > 0;
+    if (c.n_layers < 1 || c.hidden < 1 || c.vocab < 1 || (!moe && c.ffn < 1) ||
+        c.n_experts < 0)
       return fail(SEVO_ERR_INVALID_ARGUMENT, "non-positive model size");
+    if (moe && !sevo::moe_supported(c.n_experts, c.n_experts_active, c.expert_ffn, c.hidden))
+      return fail(SEVO_ERR_UNSUPPORTED,
+                  "MoE: n_experts %d (multiple of 64, <= 256), n_experts_active %d (1..16), "
+                  "expert_ffn %d (multiple of 32)", c.n_experts, c.n_experts_active,
+                  c.expert_ffn);
     if (c.max_position < 1) return fail(SEVO_ERR_INVALID_ARGUMENT, "max_position < 1");
     if (!(c.rms_eps > 0.f) || !(c.rope_theta > 1.f))
       return fail(SEVO_ERR_INVALID_ARGUMENT, "rms_eps must be > 0 and rope_theta > 1");
     if (c.qk_norm != 0 && c.qk_norm != 1) return fail(SEVO_ERR_INVALID_ARGUMENT, "qk_norm");
     sevo_status st = check_attn_shape(1, c.n_q_heads, c.n_kv_heads, c.head_dim, c.page_size, 1);
     if (st) return st;
-    if (c.hidden % 128 || c.ffn % 128 || (c.n_q_heads * c.head_dim) % 128 || c.vocab % 64)
+    if (c.hidden % 128 || (!moe && c.ffn % 128) || (c.n_q_heads * c.head_dim) % 128 ||
+        c.vocab % 64)
       return fail(SEVO_ERR_UNSUPPORTED, "hidden, ffn and n_q_heads*head_dim must be multiples "
                                         "of 128 and vocab of 64");
     if (!w->embed || !w->lm_head || !w->final_norm)
       return fail(SEVO_ERR_INVALID_ARGUMENT, "null embed / lm_head / final_norm");
-    const void* const* tabs[] = {w->attn_norm, w->w_qkv, w->w_o, w->ffn_norm, w->w_gate_up,
-                                 w->w_down};
+    const void* const* tabs[] = {w->attn_norm, w->w_qkv, w->w_o, w->ffn_norm,
+                                 moe ? w->w_router : w->w_gate_up,
+                                 moe ? w->w_expert_gate_up : w->w_down,
+                                 moe ? w->w_expert_down : w->w_down};
     for (auto t : tabs)
       if (!t) return fail(SEVO_ERR_INVALID_ARGUMENT, "null per-layer weight table");
     if (c.qk_norm && (!w->q_norm || !w->k_norm))
@@ -220,10 +231,15 @@ SEVO_API sevo_status sevo_init_model(const sevo_model_config* cfg, const sevo_we
       m->k_norm.push_back(c.qk_norm ? w->k_norm[l] : nullptr);
       m->w_o.push_back(w->w_o[l]);
       m->ffn_norm.push_back(w->ffn_norm[l]);
-      m->w_gate_up.push_back(w->w_gate_up[l]);
-      m->w_down.push_back(w->w_down[l]);
+      m->w_gate_up.push_back(moe ? nullptr : w->w_gate_up[l]);
+      m->w_down.push_back(moe ? nullptr : w->w_down[l]);
+      m->w_router.push_back(moe ? w->w_router[l] : nullptr);
+      m->w_expert_gate_up.push_back(moe ? w->w_expert_gate_up[l] : nullptr);
+      m->w_expert_down.push_back(moe ? w->w_expert_down[l] : nullptr);
       const void* need[] = {m->attn_norm[l], m->w_qkv[l], m->w_o[l], m->ffn_norm[l],
-                            m->w_gate_up[l], m->w_down[l]};
+                            moe ? m->w_router[l] : m->w_gate_up[l],
+                            moe ? m->w_expert_gate_up[l] : m->w_down[l],
+                            moe ? m->w_expert_down[l] : m->w_down[l]};
       for (auto p : need)
         if (!p || !aligned16(p)) {
           delete m;
@@ -572,8 +588,9 @@ namespace {
 
 struct StepLayout {
   size_t x, h, part_qkv, q, o, a, logits, part_x, attn, sample, total;
+  size_t m_router, m_sel, m_w, m_off, m_assign, m_act;  // MoE buffers
   int S, chunk;
-  sevo::LinearPlan p_qkv, p_o, p_gu, p_d, p_lm;
+  sevo::LinearPlan p_qkv, p_o, p_gu, p_d, p_lm, p_router;
 };
 
 StepLayout step_layout(const sevo_model_config& c, int n, int max_pages, int num_splits) {
@@ -583,8 +600,15 @@ StepLayout step_layout(const sevo_model_config& c, int n, int max_pages, int num
   resolve_splits(n, c.n_kv_heads, max_pages, num_splits, &L.S, &L.chunk);
   L.p_qkv = sevo::plan_linear(n, qkvd, c.hidden, 0, SEVO_LINEAR_STORE);
   L.p_o = sevo::plan_linear(n, c.hidden, qd, 0, SEVO_LINEAR_STORE);
-  L.p_gu = sevo::plan_linear(n, 2 * c.ffn, c.hidden, 0, SEVO_LINEAR_SWIGLU);
-  L.p_d = sevo::plan_linear(n, c.hidden, c.ffn, 0, SEVO_LINEAR_STORE);
+  const bool moe = c.n_experts > 0;
+  const int kact = moe ? c.n_experts_active : 0;
+  if (!moe) {
+    L.p_gu = sevo::plan_linear(n, 2 * c.ffn, c.hidden, 0, SEVO_LINEAR_SWIGLU);
+    L.p_d = sevo::plan_linear(n, c.hidden, c.ffn, 0, SEVO_LINEAR_STORE);
+  } else {
+    L.p_gu = L.p_d = sevo::LinearPlan{1, c.hidden};
+    L.p_router = sevo::plan_linear(n, c.n_experts, c.hidden, 0, SEVO_LINEAR_STORE);
+  }
   L.p_lm = sevo::plan_linear(n, c.vocab, c.hidden, 1, SEVO_LINEAR_STORE);
   size_t off = 0;
   auto take = [&](size_t bytes) {
@@ -592,20 +616,64 @@ StepLayout step_layout(const sevo_model_config& c, int n, int max_pages, int num
     off += round_up(bytes, 256);
     return o;
   };
-  const int sx = L.p_o.k_splits > L.p_d.k_splits ? L.p_o.k_splits : L.p_d.k_splits;
+  int sx = L.p_o.k_splits > L.p_d.k_splits ? L.p_o.k_splits : L.p_d.k_splits;
+  if (kact > sx) sx = kact;  // MoE: one partial per selected expert slot
   const size_t n16 = round_up((size_t)n, 16);  // tiled activations: 16-row blocks
   L.x = take((size_t)n * c.hidden * 4);
   L.h = take(n16 * c.hidden * 2);
   L.part_qkv = take((size_t)L.p_qkv.k_splits * n * qkvd * 4);
   L.q = take((size_t)n * qd * 2);
   L.o = take(n16 * qd * 2);
-  L.a = take(n16 * c.ffn * 2);
+  L.a = take(n16 * (moe ? 0 : c.ffn) * 2);
   L.logits = take((size_t)n * c.vocab * 4);
   L.part_x = take((size_t)sx * n * c.hidden * 4);
   L.attn = take(attn_ws(n, c.n_q_heads, c.head_dim, L.S));
   L.sample = take(sevo::sample_workspace_bytes(n, c.vocab));
+  L.m_router = L.m_sel = L.m_w = L.m_off = L.m_assign = L.m_act = 0;
+  if (moe) {
+    L.m_router = take((size_t)L.p_router.k_splits * n * c.n_experts * 4);
+    L.m_sel = take((size_t)n * kact * 4);
+    L.m_w = take((size_t)n * kact * 4);
+    L.m_off = take((size_t)(c.n_experts + 1) * 4);
+    L.m_assign = take((size_t)n * kact * 4);
+    L.m_act = take((size_t)n * kact * c.expert_ffn * 2);
+  }
   L.total = off;
   return L;
+}
+
+// The MoE FFN of layer l on the tiled normed input h: router GEMM, top-k,
+// expert lists, expert gate/up + down into part [k][n][hidden].
+hipError_t run_moe(const sevo_model* m, int l, int n, const sevo::bf16_t* h, char* ws,
+                   const StepLayout& L, int32_t* sel, float* wts, float* part, hipStream_t st) {
+  const sevo_model_config& c = m->cfg;
+  hipError_t e;
+  {
+    ProfScope ps(SEVO_PROF_MOE_ROUTE, st);
+    float* rl = reinterpret_cast<float*>(ws + L.m_router);
+    int32_t* off = reinterpret_cast<int32_t*>(ws + L.m_off);
+    int32_t* asg = reinterpret_cast<int32_t*>(ws + L.m_assign);
+    e = sevo::launch_linear_partials(n, c.n_experts, c.hidden, c.hidden, 1, L.p_router, h,
+                                     static_cast<const sevo::bf16_t*>(m->w_router[l]), rl, 0, st);
+    if (e == hipSuccess)
+      e = sevo::launch_moe_route(rl, L.p_router.k_splits, n, c.n_experts, c.n_experts_active,
+                                 sel, wts, st);
+    if (e == hipSuccess)
+      e = sevo::launch_moe_plan(sel, n * c.n_experts_active, c.n_experts, off, asg, st);
+  }
+  if (e != hipSuccess) return e;
+  ProfScope ps(SEVO_PROF_MOE_EXPERTS, st);
+  sevo::MoeExpertArgs ma;
+  ma.n = n; ma.hidden = c.hidden; ma.ffn = c.expert_ffn; ma.n_experts = c.n_experts;
+  ma.top_k = c.n_experts_active; ma.x = h;
+  ma.w_gate_up = static_cast<const sevo::bf16_t*>(m->w_expert_gate_up[l]);
+  ma.w_down = static_cast<const sevo::bf16_t*>(m->w_expert_down[l]);
+  ma.offsets = reinterpret_cast<const int32_t*>(ws + L.m_off);
+  ma.assign = reinterpret_cast<const int32_t*>(ws + L.m_assign);
+  ma.weights = wts;
+  ma.act = reinterpret_cast<sevo::bf16_t*>(ws + L.m_act);
+  ma.part = part;
+  return sevo::launch_moe_experts(ma, st);
 }
 
 }  // namespace
@@ -720,19 +788,26 @@ SEVO_API sevo_status sevo_decode_step(sevo_model* m, const sevo_step_args* a, vo
                                    static_cast<const sevo::bf16_t*>(m->ffn_norm[l]), n, H,
                                    c.rms_eps, h, st);
     }
-    if (e == hipSuccess) {
-      ProfScope ps(SEVO_PROF_GATE_UP, st);
-      e = sevo::launch_linear(n, 2 * F, H, H, 1, SEVO_LINEAR_SWIGLU, L.p_gu, h,
-                              static_cast<const sevo::bf16_t*>(m->w_gate_up[l]), act, 1, nullptr,
-                              st);
+    if (c.n_experts > 0) {
+      if (e == hipSuccess)
+        e = run_moe(m, l, n, h, ws, L, reinterpret_cast<int32_t*>(ws + L.m_sel),
+                    reinterpret_cast<float*>(ws + L.m_w), part_x, st);
+      pending = c.n_experts_active;
+    } else {
+      if (e == hipSuccess) {
+        ProfScope ps(SEVO_PROF_GATE_UP, st);
+        e = sevo::launch_linear(n, 2 * F, H, H, 1, SEVO_LINEAR_SWIGLU, L.p_gu, h,
+                                static_cast<const sevo::bf16_t*>(m->w_gate_up[l]), act, 1,
+                                nullptr, st);
+      }
+      if (e == hipSuccess) {
+        ProfScope ps(SEVO_PROF_DOWN, st);
+        e = sevo::launch_linear_partials(n, H, F, F, 1, L.p_d, act,
+                                         static_cast<const sevo::bf16_t*>(m->w_down[l]), part_x,
+                                         0, st);
+      }
+      pending = L.p_d.k_splits;
     }
-    if (e == hipSuccess) {
-      ProfScope ps(SEVO_PROF_DOWN, st);
-      e = sevo::launch_linear_partials(n, H, F, F, 1, L.p_d, act,
-                                       static_cast<const sevo::bf16_t*>(m->w_down[l]), part_x, 0,
-                                       st);
-    }
-    pending = L.p_d.k_splits;
     if (e != hipSuccess) return hip_fail(e, "decode step (layer)");
   }
   {
@@ -755,6 +830,35 @@ SEVO_API sevo_status sevo_decode_step(sevo_model* m, const sevo_step_args* a, vo
   }
   if (e != hipSuccess) return hip_fail(e, "decode step (head / sampler)");
   return SEVO_OK;
+}
+
+// ------------------------------------------------------------------ MoE sub-step
+SEVO_API size_t sevo_moe_workspace_bytes(const sevo_model* m, int32_t n) {
+  if (!m || n <= 0 || m->cfg.n_experts <= 0) return 0;
+  return step_layout(m->cfg, n, 1, 1).total;
+}
+
+SEVO_API sevo_status sevo_moe_ffn(const sevo_model* m, int32_t layer, const void* h, int32_t n,
+                                  int32_t* out_experts, float* out_weights, float* out_partials,
+                                  void* workspace, size_t workspace_bytes, void* stream) {
+  if (!m) return fail(SEVO_ERR_INVALID_ARGUMENT, "null model");
+  const sevo_model_config& c = m->cfg;
+  if (c.n_experts <= 0) return fail(SEVO_ERR_UNSUPPORTED, "dense model: no experts");
+  if (layer < 0 || layer >= c.n_layers) return fail(SEVO_ERR_INVALID_ARGUMENT, "bad layer");
+  if (n < 0 || (int64_t)n * c.n_experts_active > 65536)
+    return fail(SEVO_ERR_INVALID_ARGUMENT, "n %d outside [0, 65536 / k]", n);
+  if (n == 0) return SEVO_OK;
+  if (!h || !out_experts || !out_weights || !out_partials || !workspace || !aligned16(h) ||
+      !aligned16(out_partials) || !aligned16(workspace))
+    return fail(SEVO_ERR_INVALID_ARGUMENT, "null or misaligned pointer");
+  const StepLayout L = step_layout(c, n, 1, 1);
+  if (workspace_bytes < L.total)
+    return fail(SEVO_ERR_WORKSPACE_TOO_SMALL, "MoE FFN needs %zu workspace bytes, got %zu",
+                L.total, workspace_bytes);
+  hipError_t e = run_moe(m, layer, n, static_cast<const sevo::bf16_t*>(h),
+                         static_cast<char*>(workspace), L, out_experts, out_weights, out_partials,
+                         static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? SEVO_OK : hip_fail(e, "sevo_moe_ffn");
 }
 
 // ------------------------------------------------------------------ confidence engine
@@ -822,6 +926,8 @@ SEVO_API sevo_status sevo_prefill_confidence(sevo_model* m, const sevo_prefill_a
                                              void* stream) {
   if (!m || !a) return fail(SEVO_ERR_INVALID_ARGUMENT, "null model or args");
   const sevo_model_config& c = m->cfg;
+  if (c.n_experts > 0)
+    return fail(SEVO_ERR_UNSUPPORTED, "the prefill path takes dense-FFN models only");
   if (a->n_seqs < 1 || a->total_tokens < 0 || a->max_seq_len < 0 || a->max_pages < 1 ||
       a->num_pages < 1)
     return fail(SEVO_ERR_INVALID_ARGUMENT,

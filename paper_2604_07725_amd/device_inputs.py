@@ -37,6 +37,11 @@ def device_weights(shape: synth.ModelShape, seed: int, device="cuda") -> dict:
             buf = scratch["buf"] = torch.empty(n, dtype=torch.bfloat16, device=device)
         src = buf[:n].view(spec.shape)
         sevo_fill_normal_bf16(src, spec.key, 0, spec.std, spec.mean)
+        if len(spec.shape) == 3:   # one matrix per expert, each packed on its own
+            dst = torch.empty(spec.shape, dtype=torch.bfloat16, device=device)
+            for e in range(spec.shape[0]):
+                sevo_pack_weight(src[e], PACKED_WEIGHTS[name], dst=dst[e])
+            return dst
         return sevo_pack_weight(src, PACKED_WEIGHTS[name])
 
     g = synth.global_specs(shape, seed)

@@ -24,10 +24,12 @@ LINEAR_X_TILED, LINEAR_OUT_TILED = 1, 2
 PACK_PLAIN, PACK_GATE_UP = 0, 1
 # projection weights held in the packed layout, and how each is packed
 PACKED_WEIGHTS = {"w_qkv": PACK_PLAIN, "w_o": PACK_PLAIN, "w_gate_up": PACK_GATE_UP,
-                  "w_down": PACK_PLAIN, "lm_head": PACK_PLAIN}
+                  "w_down": PACK_PLAIN, "lm_head": PACK_PLAIN, "w_router": PACK_PLAIN,
+                  "w_expert_gate_up": PACK_GATE_UP, "w_expert_down": PACK_PLAIN}
 PAGE_SIZE = 16
 PROF_KINDS = ["attn_split", "attn_combine", "qkv", "attn_out", "gate_up", "down", "lm_head",
-              "norm", "rope_append", "sample", "embed", "attn_prefill"]   # SEVO_PROF_* order
+              "norm", "rope_append", "sample", "embed", "attn_prefill", "moe_route",
+              "moe_experts"]   # SEVO_PROF_* order
 
 vp = C.c_void_p
 i32 = C.c_int32
@@ -40,14 +42,17 @@ sz = C.c_size_t
 class ModelConfig(C.Structure):
     _fields_ = [("n_layers", i32), ("hidden", i32), ("n_q_heads", i32), ("n_kv_heads", i32),
                 ("head_dim", i32), ("ffn", i32), ("vocab", i32), ("page_size", i32),
-                ("max_position", i32), ("qk_norm", i32), ("rope_theta", f32), ("rms_eps", f32)]
+                ("max_position", i32), ("qk_norm", i32), ("rope_theta", f32), ("rms_eps", f32),
+                ("n_experts", i32), ("n_experts_active", i32), ("expert_ffn", i32)]
 
 
 class Weights(C.Structure):
     _fields_ = [("embed", vp), ("lm_head", vp), ("final_norm", vp),
                 ("attn_norm", C.POINTER(vp)), ("w_qkv", C.POINTER(vp)), ("q_norm", C.POINTER(vp)),
                 ("k_norm", C.POINTER(vp)), ("w_o", C.POINTER(vp)), ("ffn_norm", C.POINTER(vp)),
-                ("w_gate_up", C.POINTER(vp)), ("w_down", C.POINTER(vp))]
+                ("w_gate_up", C.POINTER(vp)), ("w_down", C.POINTER(vp)),
+                ("w_router", C.POINTER(vp)), ("w_expert_gate_up", C.POINTER(vp)),
+                ("w_expert_down", C.POINTER(vp))]
 
 
 class AttnArgs(C.Structure):
@@ -113,6 +118,8 @@ _SIGS = {
     "sevo_decode_step": ([vp, C.POINTER(StepArgs), vp], i32),
     "sevo_step_workspace_bytes": ([vp, i32, i32, i32], sz),
     "sevo_prefill_confidence": ([vp, C.POINTER(PrefillArgs), vp], i32),
+    "sevo_moe_ffn": ([vp, i32, vp, i32, vp, vp, vp, vp, sz, vp], i32),
+    "sevo_moe_workspace_bytes": ([vp, i32], sz),
     "sevo_prefill_workspace_bytes": ([vp, i32, i32], sz),
     "sevo_embed": ([vp, vp, i32, i32, i32, vp, vp], i32),
     "sevo_rmsnorm": ([vp, vp, i32, i32, f32, vp, vp], i32),
@@ -398,14 +405,18 @@ class Model:
             n_kv_heads=shape.n_kv_heads, head_dim=shape.head_dim, ffn=shape.ffn,
             vocab=shape.vocab, page_size=PAGE_SIZE, max_position=int(max_position),
             qk_norm=1 if shape.qk_norm else 0, rope_theta=float(shape.rope_theta),
-            rms_eps=float(shape.rms_eps))
+            rms_eps=float(shape.rms_eps), n_experts=int(shape.n_experts),
+            n_experts_active=int(shape.top_k), expert_ffn=int(shape.expert_ffn))
 
         def table(name):
-            arr = (vp * L)(*[t[name].data_ptr() for t in tensors["layers"]])
+            arr = (vp * L)(*[t[name].data_ptr() if name in t else None
+                             for t in tensors["layers"]])
             return arr
 
+        ffn = (("w_router", "w_expert_gate_up", "w_expert_down") if shape.is_moe
+               else ("w_gate_up", "w_down"))
         self._tables = {k: table(k) for k in ("attn_norm", "w_qkv", "q_norm", "k_norm", "w_o",
-                                               "ffn_norm", "w_gate_up", "w_down")}
+                                               "ffn_norm") + ffn}
         self.weights = Weights(embed=_p(tensors["embed"]), lm_head=_p(tensors["lm_head"]),
                                final_norm=_p(tensors["final_norm"]),
                                **{k: C.cast(v, C.POINTER(vp)) for k, v in self._tables.items()})
@@ -480,6 +491,23 @@ def sevo_decode_step(model: Model, tokens, positions, page_table, kv_pools, cand
     out = (ids, lps) + ((b.out_logits,) if keep_logits else ()) + \
         ((b.out_conf,) if conf_topk else ())
     return out
+
+
+# ------------------------------------------------------------------ mixture of experts
+def sevo_moe_ffn(model: Model, layer: int, h_tiled, n: int, stream=None):
+    """The MoE FFN of one layer on normed inputs in the tiled activation layout
+    (n rows).  Returns (experts int32 [n, k], weights fp32 [n, k],
+    partials fp32 [k, n, hidden])."""
+    shape = model.shape
+    k = shape.top_k
+    dev = h_tiled.device
+    ex = torch.empty(n, k, dtype=torch.int32, device=dev)
+    wt = torch.empty(n, k, dtype=torch.float32, device=dev)
+    part = torch.empty(k, n, shape.hidden, dtype=torch.float32, device=dev)
+    ws = _workspace(int(lib().sevo_moe_workspace_bytes(model.handle, n)), dev)
+    _check(lib().sevo_moe_ffn(model.handle, int(layer), _p(h_tiled), int(n), _p(ex), _p(wt),
+                              _p(part), _p(ws), ws.numel(), _stream(stream)))
+    return ex, wt, part
 
 
 # ------------------------------------------------------------------ confidence engine

@@ -44,6 +44,24 @@ def host_candidate_kv(shape, seed, layer, pop, i, n_keys, n_pages_total):
     return od.gather_kv(pool, np.arange(len(pages)), n_keys)
 
 
+def subset_host_state(shape, seed, pop, idx, layers):
+    """Host KV pools holding only the pages of candidates ``idx`` (the slot the
+    step appends included), compacted, with a matching page table."""
+    need = (pop.lengths[idx].astype(np.int64) + pop.extra_tokens + 15) // 16
+    pt = np.full((len(idx), int(need.max())), -1, np.int64)
+    kvp = [np.empty((int(need.sum()), shape.n_kv_heads, 2, 16 * shape.head_dim))
+           for _ in range(layers)]
+    c = 0
+    for j, i in enumerate(idx):
+        pages = pop.page_table[i, :need[j]]
+        for l in range(layers):
+            kvp[l][c:c + need[j]] = synth.pool_pages(synth.kv_spec(shape, seed, l, pop.n_pages),
+                                                      pages)
+        pt[j, :need[j]] = np.arange(c, c + need[j])
+        c += need[j]
+    return kvp, pt
+
+
 def attn_rel_err(o, ref):
     return float(np.abs(o - ref).max() / max(np.abs(ref).max(), 1e-30))
 

@@ -29,7 +29,9 @@ _LAYOUT_C = r"""
 #define S(T) printf(#T " %zu\n", sizeof(T));
 int main(void) {
   S(sevo_model_config) P(sevo_model_config, rope_theta) P(sevo_model_config, rms_eps)
-  S(sevo_weights) P(sevo_weights, w_down)
+  P(sevo_model_config, n_experts) P(sevo_model_config, expert_ffn)
+  S(sevo_weights) P(sevo_weights, w_down) P(sevo_weights, w_router)
+  P(sevo_weights, w_expert_down)
   S(sevo_attn_args) P(sevo_attn_args, num_pages) P(sevo_attn_args, q) P(sevo_attn_args, scale)
   P(sevo_attn_args, out) P(sevo_attn_args, workspace_bytes)
   S(sevo_sample_args) P(sevo_sample_args, ld) P(sevo_sample_args, temperature)

@@ -1,0 +1,151 @@
+"""GPU parity of the mixture-of-experts decode path against the oracle,
+through the C ABI: the MoE FFN alone (routing, weights, expert outputs) and
+whole decode steps of MoE models.
+
+Routing decisions are taken on fp32 router logits on both sides; an expert
+choice is compared exactly wherever the oracle's float64 gap between the k-th
+and (k+1)-th logit exceeds ROUTE_GAP (a choice that close could flip on
+rounding), and the test inputs are checked to have no closer choice.
+"""
+import dataclasses
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import decoder as od
+from paper_2604_07725_amd import synth
+from tests.gpu_helpers import check_ids, say, subset_host_state, tile_activations_host
+
+pytestmark = pytest.mark.gpu
+
+ROUTE_GAP = 1e-5
+
+
+@pytest.fixture(scope="module")
+def S():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2604_07725_amd import device_inputs, sevo
+    sevo.lib()
+    return sevo, device_inputs
+
+
+def _model(S, shape, seed, max_position=1024):
+    sevo, di = S
+    tensors = di.device_weights(shape, seed)
+    return sevo.sevo_init_model(shape, tensors, max_position=max_position)
+
+
+@pytest.mark.parametrize("shape_name,n", [("tiny", 37), ("tiny", 100), ("moe30b", 64)])
+def test_moe_ffn_matches_oracle(S, shape_name, n):
+    """One layer's MoE FFN on random normed inputs: selected experts (exact),
+    routing weights, and the sum of the per-slot partials against the oracle
+    on the same bf16 inputs."""
+    sevo, _ = S
+    shape = synth.TINY_MOE if shape_name == "tiny" else dataclasses.replace(
+        synth.MOE_30B_A3B, n_layers=1)
+    seed = 41 + n
+    say(f"moe ffn {shape_name} n={n}")
+    model = _model(S, shape, seed)
+    key = synth.tensor_key(seed, 60, 0)
+    h_vals = synth.host_values(synth.TensorSpec((n, shape.hidden), key, 1.0)).reshape(
+        n, shape.hidden)
+    bits = (np.ascontiguousarray(h_vals, np.float32).view(np.uint32) >> 16).astype(np.uint16)
+    ht = torch.from_numpy(tile_activations_host(bits).view(np.int16)).cuda().view(torch.bfloat16)
+    ex, wt, part = sevo.sevo_moe_ffn(model, 0, ht, n)
+    torch.cuda.synchronize()
+    g_ex = ex.cpu().numpy().astype(np.int64)
+    g_wt = wt.cpu().numpy().astype(np.float64)
+    g_out = part.double().sum(0).cpu().numpy()   # slot order is the sum order on the GPU too
+    model.close()
+    lw = synth.host_weights(shape, seed, lazy=True)["layers"][0]
+    logits = od._f32(h_vals.astype(np.float64) @ np.asarray(lw["w_router"], np.float64).T)
+    sel, w, gap = od.moe_route(logits, shape.top_k)
+    say(f"  smallest routing gap {gap.min():.2e}")
+    assert gap.min() > ROUTE_GAP, "test input has a routing near-tie"
+    np.testing.assert_array_equal(g_ex, sel)
+    np.testing.assert_allclose(g_wt, w, rtol=2e-5, atol=1e-6)
+    ref, _ = od.moe_ffn(shape, lw, h_vals.astype(np.float64))
+    err = np.abs(g_out - ref).max() / np.abs(ref).max()
+    say(f"  expert output max rel err {err:.2e}")
+    # one bf16 rounding of the SwiGLU product (mirrored) and fp32 sums
+    assert err <= 2e-3
+
+
+def test_tiny_moe_step_sequence_matches_oracle(S):
+    """Three decode steps of the tiny MoE workload (2 layers, 64 experts,
+    top-4): logits, ids and log-probs against the oracle."""
+    sevo, di = S
+    w = synth.WORKLOADS["tiny_moe_step"]
+    shape = w.shape
+    steps = 3
+    say("tiny MoE step sequence")
+    pop = synth.workload_population(w, extra_tokens=steps)
+    model = _model(S, shape, w.seed, max_position=int(pop.lengths.max()) + steps + 1)
+    kvp = di.device_pools(shape, w.seed, pop.n_pages)
+    d = di.device_population(pop)
+    hw = synth.host_weights(shape, w.seed)
+    hkv = [p.astype(np.float64) for p in synth.host_pools(shape, w.seed, pop.n_pages)]
+    toks = pop.tokens.astype(np.int64)
+    pos = pop.lengths.astype(np.int64)
+    pos_d = d["lengths"].clone()
+    for step in range(steps):
+        ids, lps, logits = sevo.sevo_decode_step(
+            model, torch.from_numpy(toks.astype(np.int32)).cuda(), pos_d, d["page_table"], kvp,
+            d["uids"], 7, 1.0, keep_logits=True)
+        torch.cuda.synchronize()
+        stats = {}
+        ref = od.decode_step(shape, hw, hkv, pop.page_table, toks, pos, pop.uids, 7, 1.0,
+                             stats=stats)
+        assert stats["route_gap"] > ROUTE_GAP, "test input has a routing near-tie"
+        err = np.abs(logits.double().cpu().numpy() - ref["logits"]).max()
+        say(f"  step {step}: logit max abs err {err:.2e}; route gap {stats['route_gap']:.2e}")
+        assert err <= 1e-2       # the tiny-model end-to-end bar of the dense step
+        check_ids(ids.cpu().numpy(), lps.cpu().numpy(), ref["ids"], ref["lps"], ref["gaps"],
+                  label=f"step {step}")
+        toks = ref["ids"]
+        pos = pos + 1
+        pos_d += 1
+    model.close()
+
+
+def test_moe30b_step_reduced_depth(S):
+    """The 30B-A3B-class MoE model at its real widths (hidden 2048, 32/4 heads,
+    128 experts, top-8, expert FFN 768, vocab 151936), full population and
+    contexts of the benchmark, 2 layers: logits and log-probs of sampled
+    candidates against the oracle on those candidates alone."""
+    sevo, di = S
+    w = synth.WORKLOADS["moe30b_pop64_agg4"]
+    shape = dataclasses.replace(w.shape, n_layers=2)
+    say("MoE 30B-A3B widths at 2 layers")
+    pop = synth.workload_population(w, extra_tokens=1)
+    model = _model(S, shape, w.seed, max_position=int(pop.lengths.max()) + 2)
+    kvp = di.device_pools(shape, w.seed, pop.n_pages)
+    d = di.device_population(pop)
+    ids, lps, logits = sevo.sevo_decode_step(model, d["tokens"], d["lengths"], d["page_table"],
+                                             kvp, d["uids"], 77, 1.0, keep_logits=True)
+    torch.cuda.synchronize()
+    idx = sorted({int(np.argmin(pop.lengths)), int(np.argmax(pop.lengths)), 1})
+    g_logits = logits.double().cpu().numpy()[idx]
+    g_lps = lps.cpu().numpy()[idx]
+    model.close()
+    del kvp
+    torch.cuda.empty_cache()
+    # the oracle runs on the sampled candidates alone: candidates do not
+    # interact, routing included (each token routes on its own)
+    hkv, pt = subset_host_state(shape, w.seed, pop, idx, shape.n_layers)
+    hw = synth.host_weights(shape, w.seed, lazy=True)
+    hw = {"embed": hw["embed"], "final_norm": hw["final_norm"], "layers": hw["layers"],
+          "lm_head": hw["lm_head"][0:shape.vocab]}
+    stats = {}
+    ref = od.decode_step(shape, hw, hkv, pt, pop.tokens[idx], pop.lengths[idx], pop.uids[idx],
+                         77, 1.0, stats=stats)
+    err = np.abs(g_logits - ref["logits"]).max()
+    lp_err = np.abs(g_lps - ref["lps"]).max()
+    say(f"  candidates {idx}: logit err {err:.2e}, lp err {lp_err:.2e}, route gap "
+        f"{stats['route_gap']:.2e}")
+    assert stats["route_gap"] > ROUTE_GAP, "test input has a routing near-tie"
+    # the full-width end-to-end bars of the dense step (bf16 storage flips)
+    assert err <= 6e-2
+    assert lp_err <= 2.5e-2

@@ -5,7 +5,7 @@ import torch
 
 from oracle import decoder as od
 from paper_2604_07725_amd import synth
-from tests.gpu_helpers import LP_ABS_TOL, bf16_bits, check_ids, say
+from tests.gpu_helpers import LP_ABS_TOL, bf16_bits, check_ids, say, subset_host_state
 
 pytestmark = pytest.mark.gpu
 
@@ -162,24 +162,6 @@ def test_step_rejects_small_workspace_and_bad_temperature(S):
     model.close()
 
 
-def _subset_host_state(shape, seed, pop, idx, layers):
-    """Host KV pools holding only the pages of candidates ``idx`` (the slot the
-    step appends included), compacted, with a matching page table."""
-    need = (pop.lengths[idx].astype(np.int64) + pop.extra_tokens + 15) // 16
-    pt = np.full((len(idx), int(need.max())), -1, np.int64)
-    kvp = [np.empty((int(need.sum()), shape.n_kv_heads, 2, 16 * shape.head_dim))
-           for _ in range(layers)]
-    c = 0
-    for j, i in enumerate(idx):
-        pages = pop.page_table[i, :need[j]]
-        for l in range(layers):
-            kvp[l][c:c + need[j]] = synth.pool_pages(synth.kv_spec(shape, seed, l, pop.n_pages),
-                                                      pages)
-        pt[j, :need[j]] = np.arange(c, c + need[j])
-        c += need[j]
-    return kvp, pt
-
-
 # Full-width tolerances.  bf16 storage turns any difference in the last fp32
 # bits before a rounding point into occasional one-ulp flips, and each later
 # rounding point multiplies the number of flips: the oracle run against itself
@@ -220,7 +202,7 @@ def test_full_width_step_reduced_depth(S, workload, layers):
     model.close()
     del kvp
     torch.cuda.empty_cache()
-    hkv, hpt = _subset_host_state(shape, w.seed, pop, idx, layers)
+    hkv, hpt = subset_host_state(shape, w.seed, pop, idx, layers)
     hw = synth.host_weights(shape, w.seed, lazy=True)
     hw = {"embed": hw["embed"], "final_norm": hw["final_norm"], "layers": hw["layers"],
           "lm_head": hw["lm_head"][0:shape.vocab]}
