@@ -9,6 +9,11 @@ RMSNorm / QKV / QK-norm + RoPE + KV append / paged attention / O / SwiGLU FFN,
 final norm, LM head, log-softmax + Gumbel-max sampling) followed by the
 host-side bookkeeping done on device (next tokens, positions + 1).
 
+--workload moe30b_pop64_agg4 runs the same step on a 30B-A3B-class
+mixture-of-experts decoder (48 layers, hidden 2048, 32/4 heads x 128, 128
+experts of FFN 768, top-8 routing, vocab 151936) at the same population and
+contexts.
+
 Prints one JSON line: tokens/s of the population, the roofline of the dominant
 kernel (the split-KV attention kernel, HIP events around every launch inside
 the timed steps) and the oracle's throughput on a bounded sample of the same
@@ -48,10 +53,34 @@ def attention_bytes(lengths, hkv, hq, d):
     return kv + 2 * n * hq * d * 2 + pages * 4
 
 
+def expected_distinct_experts(shape, n):
+    """Experts a layer touches when n tokens each pick top_k of n_experts
+    uniformly at random: E (1 - (1 - k / E)^n)."""
+    E, k = shape.n_experts, shape.top_k
+    return E * (1.0 - (1.0 - k / E) ** n)
+
+
+def model_name(shape):
+    if shape.is_moe:
+        return (f"MoE decoder ({shape.n_experts} experts, top-{shape.top_k}, "
+                f"{shape.weight_bytes() / 2e9:.1f}B stored / "
+                f"{shape.weight_bytes(shape.top_k) / 2e9:.1f}B active parameters)")
+    return f"dense {shape.weight_bytes() / 2e9:.0f}B-class decoder"
+
+
+def ffn_config(shape):
+    if shape.is_moe:
+        return {"experts": shape.n_experts, "experts_per_token": shape.top_k,
+                "expert_ffn": shape.expert_ffn}
+    return {"ffn": shape.ffn}
+
+
 def kernel_table(shape, n, kprof, attn_bytes):
     """Average time per launch of each kernel kind of the step, with the
     projections' weight-streaming rate and matrix-core utilisation (algorithmic
-    bytes: weights + activations in + outputs out; flops 2 M N K)."""
+    bytes: weights + activations in + outputs out; flops 2 M N K).  The MoE
+    experts row counts the weights of the experts a layer is expected to touch
+    under uniform routing, each once."""
     H, F, V = shape.hidden, shape.ffn, shape.vocab
     qd = shape.n_q_heads * shape.head_dim
     qkvd = qd + 2 * shape.n_kv_heads * shape.head_dim
@@ -61,11 +90,21 @@ def kernel_table(shape, n, kprof, attn_bytes):
     for kind, (ms, cnt) in kprof.items():
         avg = ms / cnt
         row = {"avg_us": avg * 1e3, "launches": cnt}
+        byts = flops = None
         if kind in gemms:
             N, K, ob = gemms[kind]
             out_bytes = n * (F * 2 if ob is None else N * ob)
             byts = N * K * 2 + n * K * 2 + out_bytes
             flops = 2.0 * n * N * K
+        elif kind == "moe_experts" and shape.is_moe:
+            Fe, k = shape.expert_ffn, shape.top_k
+            ne = expected_distinct_experts(shape, n)
+            # gate/up: weights, gathered rows in, SwiGLU rows out (bf16);
+            # down: weights, SwiGLU rows in, weighted fp32 partials out
+            byts = (ne * 3 * Fe * H * 2 + n * k * (H * 2 + Fe * 2) + n * k * (Fe * 2 + H * 4))
+            flops = 2.0 * n * k * 3 * Fe * H
+            row["expected_distinct_experts"] = ne
+        if byts is not None:
             row.update({"GB_s": byts / (avg * 1e-3) / 1e9,
                         "hbm_frac": byts / (avg * 1e-3) / 1e9 / HBM_PEAK_GBS,
                         "TFLOP_s": flops / (avg * 1e-3) / 1e12,
@@ -402,7 +441,8 @@ def main():
     split_avg_ms = split_ms / max(launches, 1)
     attn_avg_ms = attn_ms / max(launches, 1)
     achieved = attn_bytes_per_launch / (split_avg_ms * 1e-3) / 1e9
-    step_bytes = shape.n_layers * attn_bytes_per_launch + shape.weight_bytes()
+    active = expected_distinct_experts(shape, pop.n) if shape.is_moe else None
+    step_bytes = shape.n_layers * attn_bytes_per_launch + shape.weight_bytes(active)
     tr = measured_traffic(w.name)
     out = {
         "metric": "population decode tokens/s/GPU",
@@ -412,9 +452,9 @@ def main():
         "ms_per_step": ms_per_step,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16", "data": "synthetic (seeded; random-init weights)",
-        "config": {"workload": w.name, "model": "dense 8B-class decoder", "layers": shape.n_layers,
+        "config": {"workload": w.name, "model": model_name(shape), "layers": shape.n_layers,
                    "hidden": shape.hidden, "heads": f"{shape.n_q_heads}/{shape.n_kv_heads}x"
-                   f"{shape.head_dim}", "ffn": shape.ffn, "vocab": shape.vocab,
+                   f"{shape.head_dim}", "vocab": shape.vocab, **ffn_config(shape),
                    "population": pop.n, "aggregation_k": 4,
                    "context_tokens": [int(pop.lengths.min()), int(pop.lengths.max())],
                    "page_size": 16, "parallelism": "none (1 GPU)",

@@ -331,6 +331,236 @@ __global__ __launch_bounds__(256, (G <= 4 ? 2 : 1)) void attn_split_kernel(
   }
 }
 
+// The same split attention for large groups (G >= 8 query heads per kv
+// head), on the matrix cores.  With G heads a page is a small dense product
+// (16 tokens x G heads x D dims) that the vector dot products above can no
+// longer keep up with at HBM speed; per page and wave:
+//   QK  S = K Q^T with v_mfma_f32_16x16x32_bf16 over the D/32 dim blocks
+//       (A = the K tile, rows = tokens; B = the q fragments, columns = heads,
+//       columns >= G are zero): lane (head l % 16, token group l / 16) gets
+//       the scores of tokens 4 (l / 16) + 0..3 of its head.
+//   softmax  page max per head over the 4 token groups (two permlane swaps),
+//       lazy running max: the accumulators are rescaled only when a page
+//       raises a head's max by more than 2^kLazyRescaleLog2, which after the
+//       first pages is rare; p = exp2(s - m) <= 2^kLazyRescaleLog2.
+//   P   p = hi + lo (bf16 each, ~2^-17 relative), written to a per-wave LDS
+//       strip [hi|lo][head][token] and read back as the B operand of PV.
+//   PV  O^T = V^T P^T with one 16x16x32 MFMA per 16-dim block whose 32-deep
+//       k axis is [tokens of P hi | tokens of P lo] against the V tile twice,
+//       so one instruction takes both halves; the output lane holds its own
+//       head (l % 16) and dims 16 b + 4 (l / 16) + 0..3, so the rescale needs
+//       no data from other lanes.
+// Loads of the wave's next two pages are in flight while a page is consumed.
+constexpr float kLazyRescaleLog2 = 8.f;
+
+template <int D, int G>
+__global__ __launch_bounds__(256, 2) void attn_split_mfma_kernel(
+    const bf16_t* __restrict__ q, const bf16_t* __restrict__ kvpool,
+    const int32_t* __restrict__ page_table, int max_pages,
+    int num_pages32, const int32_t* __restrict__ seq_lens, int len_add, int hkv, int chunk, int S,
+    float qk_scale_log2, float* __restrict__ part_ml, float* __restrict__ part_acc) {
+  static_assert(G >= 8 && G <= 16, "one 16-column MFMA tile of heads");
+  constexpr int NI = D / 32;  // 32-dim blocks of K
+  constexpr int NB = D / 16;  // 16-dim blocks of the output
+  const int c = blockIdx.x;
+  const int s = blockIdx.y;
+  const int i = blockIdx.z;
+  const int hq = hkv * G;
+  int len = seq_lens[i] + len_add;
+  len = len < 0 ? 0 : (len > max_pages * kPage ? max_pages * kPage : len);
+  const int npg = (len + kPage - 1) / kPage;
+  const int pbeg = s * chunk;
+  if (pbeg >= npg) return;  // empty split: the combine pass skips it
+  const int pend = min(npg, pbeg + chunk);
+
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int col = lane & 15;  // head (QK / PV columns), token (K rows), dim (V rows)
+  const int grp = lane >> 4;
+
+  __shared__ __align__(16) bf16_t p_lds[4][2][16][kPage];  // [wave][hi|lo][head][token]
+  __shared__ float w_m[4][G], w_l[4][G];
+  __shared__ float w_acc[4][G][D];
+
+  // B operand of QK: head `col`, dims 32 ii + 8 grp .. +7 (zero for col >= G)
+  bf16x8v qf[NI];
+#pragma unroll
+  for (int ii = 0; ii < NI; ++ii) {
+    u32x4 w = u32x4{0u, 0u, 0u, 0u};
+    if (col < G)
+      w = *reinterpret_cast<const u32x4*>(q + ((size_t)i * hq + (size_t)c * G + col) * D +
+                                          32 * ii + 8 * grp);
+    qf[ii] = __builtin_bit_cast(bf16x8v, w);
+  }
+  float m_run = -INFINITY, l_run = 0.f;
+  f32x4 acc[NB];
+#pragma unroll
+  for (int b = 0; b < NB; ++b) acc[b] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  const int32_t* ptr = page_table + (size_t)i * max_pages;
+  const int my_pages = (pend - (pbeg + wave) + 3) >> 2;
+  int idv0 = -1, idv1 = -1;
+  if (lane < my_pages) {
+    const int id = ptr[pbeg + wave + 4 * lane];
+    idv0 = (id >= 0 && id < num_pages32) ? id : -1;
+  }
+  if (lane + 64 < my_pages) {
+    const int id = ptr[pbeg + wave + 4 * (lane + 64)];
+    idv1 = (id >= 0 && id < num_pages32) ? id : -1;
+  }
+  auto page_id = [&](int k) -> int {
+    const int kk = k < my_pages ? k : my_pages - 1;
+    return kk < 64 ? __builtin_amdgcn_readlane(idv0, kk) : __builtin_amdgcn_readlane(idv1, kk - 64);
+  };
+  constexpr uint32_t kTileBytes = kPage * D * 2;
+  const char* kv8 = reinterpret_cast<const char*>(kvpool);
+  // K: block ii, token col, dims 8 grp..+7; V: dim 16 b + col, tokens 8 (grp & 1)..+7
+  const uint32_t koff = (uint32_t)(col * 64 + grp * 16);
+  const uint32_t voff = (uint32_t)(col * kPage * 2 + (grp & 1) * 16);
+  struct Regs {
+    u32x4 k[NI];
+    u32x4 v[NB];
+  };
+  auto load = [&](Regs& r, int k) {
+    const int id = page_id(k);
+    const size_t tb = id < 0 ? 0 : ((size_t)id * hkv + c) * 2 * kTileBytes;
+    const int nrec = id < 0 ? 0 : (int)kTileBytes;
+    const __amdgpu_buffer_rsrc_t rk =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(kv8 + tb), 0, nrec, 0x00020000);
+    const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<char*>(kv8 + tb + kTileBytes), 0, nrec, 0x00020000);
+#pragma unroll
+    for (int ii = 0; ii < NI; ++ii)
+      r.k[ii] = __builtin_amdgcn_raw_buffer_load_b128(rk, (int)koff, ii * 1024, 2);
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+      r.v[b] = __builtin_amdgcn_raw_buffer_load_b128(rv, (int)voff, b * 16 * kPage * 2, 2);
+  };
+
+  auto consume = [&](const Regs& r, int k) {
+    const int pg = pbeg + wave + 4 * k;
+    int valid = len - pg * kPage;
+    valid = valid > kPage ? kPage : valid;
+    if (page_id(k) < 0) valid = 0;
+    f32x4 sc = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ii = 0; ii < NI; ++ii)
+      sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8v, r.k[ii]), qf[ii],
+                                                   sc, 0, 0, 0);
+    float z[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      z[e] = (4 * grp + e < valid) ? sc[e] * qk_scale_log2 : -INFINITY;
+    float pm = fmaxf(fmaxf(z[0], z[1]), fmaxf(z[2], z[3]));
+    pm = xor32_max(xor16_max(pm));
+    // lazy running max (a wave-uniform branch, rarely taken after the first pages)
+    const bool raise = pm > m_run + kLazyRescaleLog2;
+    if (__builtin_amdgcn_ballot_w64(raise)) {
+      const float mn = raise ? pm : m_run;
+      const float alpha = raise ? __builtin_amdgcn_exp2f(m_run - mn) : 1.f;  // 0 on the first page
+      l_run *= alpha;
+#pragma unroll
+      for (int b = 0; b < NB; ++b) acc[b] *= alpha;
+      m_run = mn;
+    }
+    uint32_t hi[2], lo[2];
+#pragma unroll
+    for (int e = 0; e < 4; e += 2) {
+      const float p0 = m_run == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(z[e] - m_run);
+      const float p1 = m_run == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(z[e + 1] - m_run);
+      l_run += p0 + p1;
+      const __bf16 h0 = (__bf16)p0, h1 = (__bf16)p1;
+      const __bf16 q0 = (__bf16)(p0 - (float)h0), q1 = (__bf16)(p1 - (float)h1);
+      hi[e / 2] = (uint32_t)__builtin_bit_cast(uint16_t, h0) |
+                  ((uint32_t)__builtin_bit_cast(uint16_t, h1) << 16);
+      lo[e / 2] = (uint32_t)__builtin_bit_cast(uint16_t, q0) |
+                  ((uint32_t)__builtin_bit_cast(uint16_t, q1) << 16);
+    }
+    *reinterpret_cast<uint2*>(&p_lds[wave][0][col][4 * grp]) = uint2{hi[0], hi[1]};
+    *reinterpret_cast<uint2*>(&p_lds[wave][1][col][4 * grp]) = uint2{lo[0], lo[1]};
+    // lanes read p values written by other lanes of the wave: order the LDS
+    // stores before the loads for the compiler (the hardware keeps one wave's
+    // LDS operations in order)
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    const bf16x8v pb = __builtin_bit_cast(
+        bf16x8v, *reinterpret_cast<const u32x4*>(&p_lds[wave][grp >> 1][col][8 * (grp & 1)]));
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      u32x4 vv = r.v[b];
+      if (valid < kPage) {
+        // slots past the last key may hold anything (even NaN patterns): zero them
+        const int t0 = 8 * (grp & 1);
+        vv.x = (t0 + 0 >= valid) ? 0u : ((t0 + 1 >= valid) ? (vv.x & 0xFFFFu) : vv.x);
+        vv.y = (t0 + 2 >= valid) ? 0u : ((t0 + 3 >= valid) ? (vv.y & 0xFFFFu) : vv.y);
+        vv.z = (t0 + 4 >= valid) ? 0u : ((t0 + 5 >= valid) ? (vv.z & 0xFFFFu) : vv.z);
+        vv.w = (t0 + 6 >= valid) ? 0u : ((t0 + 7 >= valid) ? (vv.w & 0xFFFFu) : vv.w);
+      }
+      acc[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8v, vv), pb, acc[b],
+                                                       0, 0, 0);
+    }
+  };
+
+  if (my_pages > 0) {
+    int k = 0;  // this wave's page index: logical page pbeg + wave + 4k
+    Regs A, B, C;
+    load(A, 0);
+    load(B, 1);
+    while (true) {
+      load(C, k + 2);
+      consume(A, k);
+      if (++k >= my_pages) break;
+      load(A, k + 2);
+      consume(B, k);
+      if (++k >= my_pages) break;
+      load(B, k + 2);
+      consume(C, k);
+      if (++k >= my_pages) break;
+    }
+  }
+
+  // finish this wave: l over the 4 token groups; the accumulators already
+  // hold full sums over the tokens
+  l_run = xor32_sum(xor16_sum(l_run));
+  if (grp == 0 && col < G) {
+    w_m[wave][col] = m_run;
+    w_l[wave][col] = l_run;
+  }
+  if (col < G) {
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) w_acc[wave][col][16 * b + 4 * grp + e] = acc[b][e];
+  }
+  __syncthreads();
+
+  // merge the four waves (fixed order) and store this split's partial
+  for (int idx = threadIdx.x; idx < G * D; idx += 256) {
+    const int j = idx / D;
+    const int e = idx - j * D;
+    float M = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) M = fmaxf(M, w_m[w][j]);
+    float L = 0.f, Acc = 0.f;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const float mw = w_m[w][j];
+      if (mw != -INFINITY) {
+        const float f = exp2f(mw - M);
+        L += w_l[w][j] * f;
+        Acc += w_acc[w][j][e] * f;
+      }
+    }
+    const size_t slot = ((size_t)i * hq + (size_t)c * G + j) * S + s;
+    part_acc[slot * D + e] = Acc;
+    if (e == 0) {
+      part_ml[slot * 2] = M;
+      part_ml[slot * 2 + 1] = L;
+    }
+  }
+}
+
 // Merge the non-empty splits of one (candidate, query head), in split order.
 template <int D>
 __global__ __launch_bounds__(64) void attn_combine_kernel(const float* __restrict__ part_ml,
@@ -375,7 +605,13 @@ template <int D, int G>
 static hipError_t launch_attn_t(const AttnArgs& a, hipStream_t st) {
   const float log2e = 1.4426950408889634f;
   if (a.ev_begin) (void)hipEventRecord(a.ev_begin, st);
-  hipLaunchKernelGGL((attn_split_kernel<D, G>), dim3(a.hkv, a.num_splits, a.n), dim3(256), 0, st,
+  // G >= 8 heads per kv head: the matrix-core variant
+  using SplitFn = void (*)(const bf16_t*, const bf16_t*, const int32_t*, int, int, const int32_t*,
+                           int, int, int, int, float, float*, float*);
+  SplitFn fn;
+  if constexpr (G >= 8) fn = attn_split_mfma_kernel<D, G>;
+  else fn = attn_split_kernel<D, G>;
+  hipLaunchKernelGGL(fn, dim3(a.hkv, a.num_splits, a.n), dim3(256), 0, st,
                      a.q, a.kv_pool, a.page_table, a.max_pages,
                      (int)(a.num_pages < 0x7FFFFFFF ? a.num_pages : 0x7FFFFFFF), a.seq_lens,
                      a.len_add, a.hkv, a.chunk, a.num_splits, a.scale * log2e, a.part_ml, a.part_acc);

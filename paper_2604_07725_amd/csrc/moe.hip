@@ -8,8 +8,8 @@
 //     split order), takes the k largest logits by repeated wave arg-max
 //     (value, then lower expert index) and the softmax over them;
 //   * plan: one workgroup counts tokens per expert and lays the (token, slot)
-//     assignments out expert-major, tokens in order (a fixed order: results do
-//     not depend on scheduling);
+//     assignments out expert-major, tokens in order (ranks from per-expert
+//     bit rows: a fixed order, results do not depend on scheduling);
 //   * experts: a grouped skinny GEMM over (64-row weight superblock, expert,
 //     64-assignment tile), the same weight stream as the dense projections
 //     (packed fragment-major weights, four waves taking the 32-k steps round
@@ -98,32 +98,76 @@ __global__ __launch_bounds__(64) void moe_route_kernel(const float* __restrict__
   }
 }
 
-// ---- plan: offsets [E + 1] and assign [n k] (entries t * k + slot)
-__global__ __launch_bounds__(256) void moe_plan_kernel(const int32_t* __restrict__ sel, int nk,
-                                                       int E, int32_t* __restrict__ offsets,
-                                                       int32_t* __restrict__ assign) {
-  __shared__ int cnt[kMoeMaxExperts + 1];
-  for (int e = threadIdx.x; e < E; e += 256) {
-    int c = 0;
-    for (int r = 0; r < nk; ++r) c += sel[r] == e;
-    cnt[e] = c;
+// ---- plan: offsets [E + 1] and assign [n k] (entries t * k + slot), one
+// workgroup.  Counts by LDS atomics; then the entries, 1024 at a time, set
+// their bit in a per-expert bit row, and an entry's rank among the entries of
+// its expert is the number of set bits before it: the lists are in entry
+// (token, slot) order whatever the scheduling.
+constexpr int kPlanThreads = 1024;
+constexpr int kPlanWords = kPlanThreads / 32;
+
+__global__ __launch_bounds__(kPlanThreads) void moe_plan_kernel(const int32_t* __restrict__ sel,
+                                                                int nk, int E,
+                                                                int32_t* __restrict__ offsets,
+                                                                int32_t* __restrict__ assign) {
+  __shared__ int cnt[kMoeMaxExperts];
+  __shared__ int base[kMoeMaxExperts];
+  __shared__ uint32_t bits[kMoeMaxExperts][kPlanWords];
+  const int tid = threadIdx.x;
+  for (int e = tid; e < E; e += kPlanThreads) cnt[e] = 0;
+  __syncthreads();
+  for (int r = tid; r < nk; r += kPlanThreads) {
+    const int e = sel[r];
+    if (e >= 0 && e < E) atomicAdd(&cnt[e], 1);
   }
   __syncthreads();
-  if (threadIdx.x == 0) {
-    int acc = 0;
-    for (int e = 0; e < E; ++e) {
-      const int c = cnt[e];
-      cnt[e] = acc;
-      offsets[e] = acc;
-      acc += c;
+  if (tid < 64) {
+    // exclusive prefix over the experts: lane j scans experts 4j..4j+3 (E <= 256)
+    int v[4], sum = 0;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int e = 4 * tid + u;
+      v[u] = e < E ? cnt[e] : 0;
+      sum += v[u];
     }
-    offsets[E] = acc;
+    int incl = sum;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int y = __shfl_up(incl, o, kWave);
+      if (tid >= o) incl += y;
+    }
+    int run = incl - sum;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int e = 4 * tid + u;
+      if (e < E) {
+        base[e] = run;
+        offsets[e] = run;
+      }
+      run += v[u];
+    }
+    if (tid == 63) offsets[E] = incl;
   }
-  __syncthreads();
-  for (int e = threadIdx.x; e < E; e += 256) {
-    int pos = cnt[e];
-    for (int r = 0; r < nk; ++r)
-      if (sel[r] == e) assign[pos++] = r;
+  for (int c0 = 0; c0 < nk; c0 += kPlanThreads) {
+    for (int w = tid; w < E * kPlanWords; w += kPlanThreads) (&bits[0][0])[w] = 0u;
+    __syncthreads();  // orders the prefix (first chunk) before the reads of base
+    const int r = c0 + tid;
+    const int e = r < nk ? sel[r] : -1;
+    const bool ok = e >= 0 && e < E;
+    if (ok) atomicOr(&bits[e][tid >> 5], 1u << (tid & 31));
+    __syncthreads();
+    if (ok) {
+      int rank = __popc(bits[e][tid >> 5] & ((1u << (tid & 31)) - 1u));
+      for (int w = 0; w < (tid >> 5); ++w) rank += __popc(bits[e][w]);
+      assign[base[e] + rank] = r;
+    }
+    __syncthreads();
+    for (int x = tid; x < E; x += kPlanThreads) {
+      int tot = 0;
+      for (int w = 0; w < kPlanWords; ++w) tot += __popc(bits[x][w]);
+      base[x] += tot;
+    }
+    __syncthreads();  // the bit rows are read above before the next chunk clears them
   }
 }
 
@@ -267,7 +311,8 @@ hipError_t launch_moe_route(const float* part, int S, int n, int E, int k, int32
 
 hipError_t launch_moe_plan(const int32_t* sel, int nk, int E, int32_t* offsets, int32_t* assign,
                            hipStream_t st) {
-  hipLaunchKernelGGL(moe_plan_kernel, dim3(1), dim3(256), 0, st, sel, nk, E, offsets, assign);
+  hipLaunchKernelGGL(moe_plan_kernel, dim3(1), dim3(kPlanThreads), 0, st, sel, nk, E, offsets,
+                     assign);
   return hipGetLastError();
 }
 

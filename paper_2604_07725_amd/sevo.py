@@ -494,16 +494,20 @@ def sevo_decode_step(model: Model, tokens, positions, page_table, kv_pools, cand
 
 
 # ------------------------------------------------------------------ mixture of experts
-def sevo_moe_ffn(model: Model, layer: int, h_tiled, n: int, stream=None):
+def sevo_moe_ffn(model: Model, layer: int, h_tiled, n: int, stream=None, partials=None):
     """The MoE FFN of one layer on normed inputs in the tiled activation layout
     (n rows).  Returns (experts int32 [n, k], weights fp32 [n, k],
-    partials fp32 [k, n, hidden])."""
+    partials fp32 [k, n, hidden]); ``partials`` may be given (written in full)."""
     shape = model.shape
     k = shape.top_k
     dev = h_tiled.device
     ex = torch.empty(n, k, dtype=torch.int32, device=dev)
     wt = torch.empty(n, k, dtype=torch.float32, device=dev)
-    part = torch.empty(k, n, shape.hidden, dtype=torch.float32, device=dev)
+    part = (torch.empty(k, n, shape.hidden, dtype=torch.float32, device=dev)
+            if partials is None else partials)
+    if (part.shape != (k, n, shape.hidden) or part.dtype != torch.float32
+            or not part.is_contiguous()):
+        raise ValueError("partials must be a contiguous fp32 [k, n, hidden] tensor")
     ws = _workspace(int(lib().sevo_moe_workspace_bytes(model.handle, n)), dev)
     _check(lib().sevo_moe_ffn(model.handle, int(layer), _p(h_tiled), int(n), _p(ex), _p(wt),
                               _p(part), _p(ws), ws.numel(), _stream(stream)))

@@ -73,6 +73,12 @@ ATTN_SMALL = [
     (16, 8, 64, [90, 300], 3),
     (64, 8, 128, [500, 33], 0),
     (8, 1, 128, [1000, 5], 2),
+    # 8 query heads per kv head: the matrix-core variant (every partial-page
+    # count, split counts, both head sizes)
+    (32, 4, 128, [1, 15, 16, 17, 31, 33, 1000, 257], 0),
+    (32, 4, 128, [1, 15, 16, 17, 31, 33, 1000, 257], 1),
+    (32, 4, 128, [700, 2000, 64, 129], 7),
+    (16, 2, 64, [1, 2, 3, 4, 5, 6, 7, 8, 9, 10, 11, 12, 13, 14, 15, 16, 500], 0),
 ]
 
 
@@ -90,9 +96,10 @@ def test_attention_small_matches_oracle(S, hq, hkv, d, lengths, splits):
         assert e <= 8e-3, (i, e)
 
 
-def test_attention_page_permutation_and_determinism_bit_exact(S):
+@pytest.mark.parametrize("hq,hkv", [(32, 8), (32, 4)])
+def test_attention_page_permutation_and_determinism_bit_exact(S, hq, hkv):
     sevo, di = S
-    shape = synth.ModelShape(1, 256, 32, 8, 128, 256, 256)
+    shape = synth.ModelShape(1, 256, hq, hkv, 128, 256, 256)
     lengths = [900, 33, 1600, 17]
     say("attention permutation / determinism")
     pop, q, kvp, pt, lens, out1 = _attn_case(S, shape, lengths, seed=5, shuffle=False)
@@ -109,9 +116,37 @@ def test_attention_page_permutation_and_determinism_bit_exact(S):
     np.testing.assert_array_equal(bf16_bits(out1), bf16_bits(out3))
 
 
-def test_attention_split_count_changes_only_rounding(S):
+@pytest.mark.parametrize("hq,hkv", [(32, 8), (32, 4)])
+def test_attention_ignores_slots_past_the_last_key(S, hq, hkv):
+    """Slots of a candidate's last page past its last key may hold anything:
+    NaN patterns written there (K and V tiles, every kv head) leave the output
+    bit-identical."""
     sevo, di = S
-    shape = synth.ModelShape(1, 256, 32, 8, 128, 256, 256)
+    d = 128
+    shape = synth.ModelShape(1, 256, hq, hkv, d, 256, 256)
+    lengths = [17, 5, 300, 31, 64]
+    say(f"attention with NaN past the last key hq={hq} hkv={hkv}")
+    pop, q, kvp, pt, lens, out1 = _attn_case(S, shape, lengths, seed=13)
+    pool = kvp.view(torch.int16).cpu().numpy().copy()   # [P][hkv][2][16 d]
+    e = np.arange(d)
+    for i, n in enumerate(lengths):
+        if n % 16 == 0:
+            continue
+        page = pop.page_table[i, n // 16]
+        for slot in range(n % 16, 16):
+            pool[page, :, 0, ((e // 32) * 16 + slot) * 32 + e % 32] = np.int16(0x7FC0)  # K
+            pool[page, :, 1, e * 16 + slot] = np.int16(0x7FC0)                          # V
+    kvp_nan = torch.from_numpy(pool).cuda().view(torch.bfloat16)
+    out2 = sevo.sevo_attn_decode(q, kvp_nan, pt, lens)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(bf16_bits(out1), bf16_bits(out2))
+    assert np.isfinite(to_np(out2)).all()
+
+
+@pytest.mark.parametrize("hq,hkv", [(32, 8), (32, 4)])
+def test_attention_split_count_changes_only_rounding(S, hq, hkv):
+    sevo, di = S
+    shape = synth.ModelShape(1, 256, hq, hkv, 128, 256, 256)
     say("attention split counts")
     pop, q, kvp, pt, lens, out1 = _attn_case(S, shape, [3000, 2500, 100], seed=6,
                                              num_splits=1)
@@ -122,10 +157,11 @@ def test_attention_split_count_changes_only_rounding(S):
         assert d < 4e-3, (s, d)
 
 
-def test_attention_out_of_range_page_ids_are_skipped(S):
+@pytest.mark.parametrize("hq,hkv", [(16, 4), (32, 4)])
+def test_attention_out_of_range_page_ids_are_skipped(S, hq, hkv):
     """A page id outside the pool contributes no keys and is never read."""
     sevo, di = S
-    shape = synth.ModelShape(1, 256, 16, 4, 128, 256, 256)
+    shape = synth.ModelShape(1, 256, hq, hkv, 128, 256, 256)
     lengths = [200, 100]
     pop = make_population(lengths, seed=8)
     bad = pop.page_table.copy()
@@ -134,7 +170,7 @@ def test_attention_out_of_range_page_ids_are_skipped(S):
     say("attention bad page ids")
     _, q, kvp, pt, lens, out = _attn_case(S, shape, lengths, seed=8, pt_override=bad)
     o = to_np(out)
-    qh = synth.host_values(synth.q_spec(shape, 8, 2)).reshape(2, 16, 128)
+    qh = synth.host_values(synth.q_spec(shape, 8, 2)).reshape(2, hq, 128)
     for i, drop in ((0, range(48, 64)), (1, range(0, 16))):
         K, V = host_candidate_kv(shape, 8, 0, pop, i, int(pop.lengths[i]), pop.n_pages)
         keep = np.array([t for t in range(int(pop.lengths[i])) if t not in drop])
@@ -142,9 +178,10 @@ def test_attention_out_of_range_page_ids_are_skipped(S):
         assert attn_rel_err(o[i], ref) <= 8e-3
 
 
-def test_attention_zero_length_candidate_gives_zero(S):
+@pytest.mark.parametrize("hq,hkv", [(32, 8), (32, 4)])
+def test_attention_zero_length_candidate_gives_zero(S, hq, hkv):
     """A candidate with no cached keys yields o = 0 and never disturbs the others."""
-    shape = synth.ModelShape(1, 256, 32, 8, 128, 256, 256)
+    shape = synth.ModelShape(1, 256, hq, hkv, 128, 256, 256)
     say("attention with a zero-length candidate")
     pop, q, kvp, pt, lens, out = _attn_case(S, shape, [0, 40, 0, 300], seed=12)
     o = to_np(out)
@@ -155,7 +192,8 @@ def test_attention_zero_length_candidate_gives_zero(S):
 
 @pytest.mark.parametrize("workload,sample", [("attn_pop16_agg4", [0, 5, 11, 15]),
                                              ("dense8b_pop64_agg4", None),
-                                             ("dense8b_pop16_agg8", None)])
+                                             ("dense8b_pop16_agg8", None),
+                                             ("moe30b_pop64_agg4", None)])
 def test_attention_full_size_sampled(S, workload, sample):
     """Full-size pools and the benchmark's launch configuration (auto splits);
     the oracle checks sampled candidates (all heads), including the shortest

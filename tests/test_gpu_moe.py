@@ -5,7 +5,8 @@ whole decode steps of MoE models.
 Routing decisions are taken on fp32 router logits on both sides; an expert
 choice is compared exactly wherever the oracle's float64 gap between the k-th
 and (k+1)-th logit exceeds ROUTE_GAP (a choice that close could flip on
-rounding), and the test inputs are checked to have no closer choice.
+rounding).  The FFN test checks near-tie tokens for a valid choice instead;
+the step tests check that their inputs have none.
 """
 import dataclasses
 
@@ -37,11 +38,14 @@ def _model(S, shape, seed, max_position=1024):
     return sevo.sevo_init_model(shape, tensors, max_position=max_position)
 
 
-@pytest.mark.parametrize("shape_name,n", [("tiny", 37), ("tiny", 100), ("moe30b", 64)])
+@pytest.mark.parametrize("shape_name,n", [("tiny", 1), ("tiny", 37), ("tiny", 100), ("tiny", 2000),
+                                          ("moe30b", 64), ("moe30b", 300)])
 def test_moe_ffn_matches_oracle(S, shape_name, n):
     """One layer's MoE FFN on random normed inputs: selected experts (exact),
     routing weights, and the sum of the per-slot partials against the oracle
-    on the same bf16 inputs."""
+    on the same bf16 inputs.  The partials start as NaN, so a (token, slot)
+    the expert lists miss fails; n = 2000 spans several expert row tiles and
+    several chunks of the assignment planner."""
     sevo, _ = S
     shape = synth.TINY_MOE if shape_name == "tiny" else dataclasses.replace(
         synth.MOE_30B_A3B, n_layers=1)
@@ -53,21 +57,29 @@ def test_moe_ffn_matches_oracle(S, shape_name, n):
         n, shape.hidden)
     bits = (np.ascontiguousarray(h_vals, np.float32).view(np.uint32) >> 16).astype(np.uint16)
     ht = torch.from_numpy(tile_activations_host(bits).view(np.int16)).cuda().view(torch.bfloat16)
-    ex, wt, part = sevo.sevo_moe_ffn(model, 0, ht, n)
+    part = torch.full((shape.top_k, n, shape.hidden), float("nan"), device="cuda")
+    ex, wt, part = sevo.sevo_moe_ffn(model, 0, ht, n, partials=part)
     torch.cuda.synchronize()
     g_ex = ex.cpu().numpy().astype(np.int64)
     g_wt = wt.cpu().numpy().astype(np.float64)
     g_out = part.double().sum(0).cpu().numpy()   # slot order is the sum order on the GPU too
+    assert np.isfinite(g_out).all(), "a (token, slot) partial was never written"
     model.close()
     lw = synth.host_weights(shape, seed, lazy=True)["layers"][0]
     logits = od._f32(h_vals.astype(np.float64) @ np.asarray(lw["w_router"], np.float64).T)
     sel, w, gap = od.moe_route(logits, shape.top_k)
-    say(f"  smallest routing gap {gap.min():.2e}")
-    assert gap.min() > ROUTE_GAP, "test input has a routing near-tie"
-    np.testing.assert_array_equal(g_ex, sel)
-    np.testing.assert_allclose(g_wt, w, rtol=2e-5, atol=1e-6)
+    exact = gap > ROUTE_GAP
+    say(f"  smallest routing gap {gap.min():.2e}; {int((~exact).sum())} near-tie tokens")
+    assert exact.mean() > 0.9
+    np.testing.assert_array_equal(g_ex[exact], sel[exact])
+    np.testing.assert_allclose(g_wt[exact], w[exact], rtol=2e-5, atol=1e-6)
+    for t in np.nonzero(~exact)[0]:
+        # a near tie: k distinct experts, each within the gap of the k-th largest logit
+        assert len(set(g_ex[t].tolist())) == shape.top_k
+        kth = np.sort(logits[t])[::-1][shape.top_k - 1]
+        assert logits[t, g_ex[t]].min() >= kth - ROUTE_GAP
     ref, _ = od.moe_ffn(shape, lw, h_vals.astype(np.float64))
-    err = np.abs(g_out - ref).max() / np.abs(ref).max()
+    err = np.abs(g_out[exact] - ref[exact]).max() / np.abs(ref).max()
     say(f"  expert output max rel err {err:.2e}")
     # one bf16 rounding of the SwiGLU product (mirrored) and fp32 sums
     assert err <= 2e-3
