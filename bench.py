@@ -36,7 +36,7 @@ BF16_PEAK_TFLOPS = 2500.0
 # sources of the attention split kernel; the HBM-counter traffic recorded under
 # profiles/ is reported only while they are unchanged
 ATTN_SOURCES = ["paper_2604_07725_amd/csrc/attn_decode.hip", "paper_2604_07725_amd/csrc/common.h"]
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_split_kernel_traffic.json")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_split_mfma_kernel_traffic.json")
 
 
 def log(msg):
@@ -58,6 +58,12 @@ def expected_distinct_experts(shape, n):
     uniformly at random: E (1 - (1 - k / E)^n)."""
     E, k = shape.n_experts, shape.top_k
     return E * (1.0 - (1.0 - k / E) ** n)
+
+
+def attn_kernel_name(shape):
+    g = shape.n_q_heads // shape.n_kv_heads
+    kern = "attn_split_mfma_kernel" if g >= 4 else "attn_split_kernel"
+    return f"{kern}<{shape.head_dim},{g}>"
 
 
 def model_name(shape):
@@ -464,7 +470,7 @@ def main():
                    "sampling": ("full vocabulary" if args.top_k == 0 else
                                 f"top-k {args.top_k}, top-p {args.top_p}, min-p {args.min_p}"),
                    "self_confidence_topk": args.conf_topk},
-        "roofline": {"kernel": "attn_split_kernel<128,4> (paged split-KV GQA attention)",
+        "roofline": {"kernel": f"{attn_kernel_name(shape)} (paged split-KV GQA attention)",
                      "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
                      "traffic": None if tr is None else tr["traffic_bytes_per_launch"],

@@ -7,7 +7,8 @@
 // G = hq / hkv query heads that share the kv head, and merge through LDS at the
 // end.  The combine kernel merges the splits of a (candidate, head) in split
 // order, so results are deterministic and independent of the physical page
-// order.
+// order.  Groups of 4 or more heads run on the matrix cores (the second split
+// kernel below); groups of 1 or 2 heads use vector dot products:
 //
 // Per page and wave (tile = 16 tokens x D dims, 4 KB at D = 128; the K and V
 // tiles of a (page, kv head) are adjacent in the pool, so each page is one
@@ -331,10 +332,11 @@ __global__ __launch_bounds__(256, (G <= 4 ? 2 : 1)) void attn_split_kernel(
   }
 }
 
-// The same split attention for large groups (G >= 8 query heads per kv
-// head), on the matrix cores.  With G heads a page is a small dense product
-// (16 tokens x G heads x D dims) that the vector dot products above can no
-// longer keep up with at HBM speed; per page and wave:
+// The same split attention for groups of G >= 4 query heads per kv head, on
+// the matrix cores.  With G heads a page is a small dense product (16 tokens
+// x G heads x D dims): at G = 8 the vector dot products above cannot keep up
+// with HBM (measured 2.75 TB/s against 6.15 here), and at G = 4 this variant
+// is still a few percent faster; per page and wave:
 //   QK  S = K Q^T with v_mfma_f32_16x16x32_bf16 over the D/32 dim blocks
 //       (A = the K tile, rows = tokens; B = the q fragments, columns = heads,
 //       columns >= G are zero): lane (head l % 16, token group l / 16) gets
@@ -359,7 +361,7 @@ __global__ __launch_bounds__(256, 2) void attn_split_mfma_kernel(
     const int32_t* __restrict__ page_table, int max_pages,
     int num_pages32, const int32_t* __restrict__ seq_lens, int len_add, int hkv, int chunk, int S,
     float qk_scale_log2, float* __restrict__ part_ml, float* __restrict__ part_acc) {
-  static_assert(G >= 8 && G <= 16, "one 16-column MFMA tile of heads");
+  static_assert(G >= 4 && G <= 16, "one 16-column MFMA tile of heads");
   constexpr int NI = D / 32;  // 32-dim blocks of K
   constexpr int NB = D / 16;  // 16-dim blocks of the output
   const int c = blockIdx.x;
@@ -605,11 +607,11 @@ template <int D, int G>
 static hipError_t launch_attn_t(const AttnArgs& a, hipStream_t st) {
   const float log2e = 1.4426950408889634f;
   if (a.ev_begin) (void)hipEventRecord(a.ev_begin, st);
-  // G >= 8 heads per kv head: the matrix-core variant
+  // G >= 4 heads per kv head: the matrix-core variant
   using SplitFn = void (*)(const bf16_t*, const bf16_t*, const int32_t*, int, int, const int32_t*,
                            int, int, int, int, float, float*, float*);
   SplitFn fn;
-  if constexpr (G >= 8) fn = attn_split_mfma_kernel<D, G>;
+  if constexpr (G >= 4) fn = attn_split_mfma_kernel<D, G>;
   else fn = attn_split_kernel<D, G>;
   hipLaunchKernelGGL(fn, dim3(a.hkv, a.num_splits, a.n), dim3(256), 0, st,
                      a.q, a.kv_pool, a.page_table, a.max_pages,

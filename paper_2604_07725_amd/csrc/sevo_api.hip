@@ -48,17 +48,28 @@ constexpr int kMaxSplitPages = 512;
 
 int min_splits(int max_pages) { return (max_pages + kMaxSplitPages - 1) / kMaxSplitPages; }
 
-// Splits per candidate so that (n * hkv * S) workgroups fill the 256 CUs
-// about 16 times over (512 resident at 2 per CU), with at least 32 pages
-// (8 per wave) per split.
+// Splits per candidate.  About 512 split workgroups are resident at once (2
+// per CU); every split adds a fixed cost (its start-up, partial write and
+// combine share), while a count whose n * hkv * S leaves the last round of
+// resident workgroups part-empty idles CUs.  So: the fewest splits (at least
+// the kMaxSplitPages minimum) that fill one round, raised (up to doubling) to
+// the first count that fills whole rounds; at least 32 pages (8 per wave)
+// per split where the minimum allows.  Measured on the matrix-core kernel:
+// 64 x 8 pairs at 16k-32k -> 4, 16 x 8 pairs at 64k -> 12 (9 and 10 are 7%
+// slower), 16 x 8 at 8k-16k -> 4 (28 is 20% slower).
+constexpr int kResidentSplitGroups = 512;
+
 int plan_splits(int n, int hkv, int max_pages) {
-  const int pairs = n * hkv > 0 ? n * hkv : 1;
-  int s = (4096 + pairs - 1) / pairs;
-  const int cap = (max_pages + 31) / 32;
-  if (s > cap) s = cap;
-  if (s < 1) s = 1;
-  if (s < min_splits(max_pages)) s = min_splits(max_pages);
-  return s;
+  const long long pairs = (long long)(n > 0 ? n : 1) * (hkv > 0 ? hkv : 1);
+  const int smin = min_splits(max_pages);
+  int cap = (max_pages + 31) / 32;
+  if (cap < smin) cap = smin;
+  long long s = smin;
+  if (pairs * s < kResidentSplitGroups) s = (kResidentSplitGroups + pairs - 1) / pairs;
+  if (s > cap) return cap;
+  for (long long t = s; t <= 2 * s && t <= cap; ++t)
+    if ((pairs * t) % kResidentSplitGroups == 0) return (int)t;
+  return (int)s;
 }
 
 // The split count actually used: the requested (or planned) count, raised so

@@ -119,11 +119,17 @@ def test_split_planning():
     L = sevo.lib()
     # enough workgroups for 256 CUs, at least 32 pages per split, at least one
     # split, and no split longer than 512 pages
-    assert L.sevo_attn_plan_splits(64, 8, 2049) == 8
-    assert L.sevo_attn_plan_splits(64, 8, 1024) == 8
-    assert L.sevo_attn_plan_splits(16, 8, 1024) == 32
+    # fewest splits that fill whole rounds of 512 resident workgroups, at
+    # least the 512-pages-per-split minimum, at most max_pages / 32
+    assert L.sevo_attn_plan_splits(64, 8, 2037) == 4
+    assert L.sevo_attn_plan_splits(64, 8, 2049) == 5      # the minimum rises to 5
+    assert L.sevo_attn_plan_splits(64, 8, 1024) == 2
+    assert L.sevo_attn_plan_splits(16, 8, 1024) == 4      # 2 would leave half a round
+    assert L.sevo_attn_plan_splits(16, 8, 4470) == 12     # minimum 9, 12 fills 3 rounds
+    assert L.sevo_attn_plan_splits(64, 4, 2040) == 4
     assert L.sevo_attn_plan_splits(64, 8, 4100) == 9
-    assert L.sevo_attn_plan_splits(4, 2, 33) == 2
+    assert L.sevo_attn_plan_splits(3, 5, 4000) == 35      # no whole-round count up to 2x
+    assert L.sevo_attn_plan_splits(4, 2, 33) == 2         # capped: 32 pages per split
     assert L.sevo_attn_plan_splits(1, 1, 1) == 1
     ws = L.sevo_attn_workspace_bytes(64, 32, 8, 128, 2049, 0)
     assert ws >= 64 * 32 * 4 * 130 * 4
