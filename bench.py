@@ -60,6 +60,105 @@ def expected_distinct_experts(shape, n):
     return E * (1.0 - (1.0 - k / E) ** n)
 
 
+def peak_fracs(achieved, peak):
+    """achieved GB/s as fractions of the measured read ceilings (None if not measured)."""
+    if not peak:
+        return {"frac_of_measured_sequential": None, "frac_of_measured_pages": None}
+    return {"frac_of_measured_sequential": achieved / peak["sequential_GBs"],
+            "frac_of_measured_pages": achieved / peak["pages_8KB_GBs"]}
+
+
+def attention_main(args, w, peak):
+    """Attention-only workload (split-KV attention + combine of one layer):
+    `reps` timed calls rotating 4 independent KV pools (each larger than the
+    256 MB Infinity Cache), HIP events around every split launch."""
+    import torch
+    from paper_2604_07725_amd import device_inputs as di
+    from paper_2604_07725_amd import sevo, synth
+    shape = w.shape
+    reps = 100 if args.steps is None else args.steps
+    pop = synth.workload_population(w)
+    dev = torch.device("cuda:0")
+    pools = [di.device_pools(shape, w.seed + 1000 * r, pop.n_pages, dev, layers=[0])[0]
+             for r in range(4)]
+    q = di.device_q(shape, w.seed, pop.n, dev)
+    lens = torch.from_numpy(pop.lengths.astype(np.int32)).to(dev)
+    pt = torch.from_numpy(pop.page_table).to(dev)
+    S = args.num_splits or sevo.sevo_attn_plan_splits(pop.n, shape.n_kv_heads, pop.max_pages)
+    ws = torch.empty(sevo.sevo_attn_workspace_bytes(pop.n, shape.n_q_heads, shape.n_kv_heads,
+                                                    shape.head_dim, pop.max_pages, S),
+                     dtype=torch.uint8, device=dev)
+    out = torch.empty(pop.n, shape.n_q_heads, shape.head_dim, dtype=torch.bfloat16, device=dev)
+    call = lambda r: sevo.sevo_attn_decode(q, pools[r % 4], pt, lens, num_splits=S,  # noqa: E731
+                                           out=out, workspace=ws)
+    for r in range(args.warmup + 4):
+        call(r)
+    torch.cuda.synchronize()
+    sevo.sevo_profile_begin(reps, ("attn_split", "attn_combine"))
+    a = torch.cuda.Event(enable_timing=True)
+    b = torch.cuda.Event(enable_timing=True)
+    a.record()
+    for r in range(reps):
+        call(r)
+    b.record()
+    torch.cuda.synchronize()
+    prof = sevo.sevo_profile_end()
+    total_ms = a.elapsed_time(b)
+    byts = attention_bytes(pop.lengths, shape.n_kv_heads, shape.n_q_heads, shape.head_dim)
+    split_ms = prof["attn_split"][0] / max(prof["attn_split"][1], 1)
+    comb_ms = prof["attn_combine"][0] / max(prof["attn_combine"][1], 1)
+    achieved = byts / (split_ms * 1e-3) / 1e9
+    res = {
+        "metric": "attention HBM GB/s", "value": byts / ((split_ms + comb_ms) * 1e-3) / 1e9,
+        "unit": "GB/s", "n_gpus": 1, "steps": reps, "warmup": args.warmup,
+        "ms_per_step": total_ms / reps, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic (seeded)",
+        "config": {"workload": w.name, "heads": f"{shape.n_q_heads}/{shape.n_kv_heads}x"
+                   f"{shape.head_dim}", "population": pop.n, "aggregation_k": 4,
+                   "context_tokens": [int(pop.lengths.min()), int(pop.lengths.max())],
+                   "page_size": 16, "num_splits": S, "kv_pools_rotated": 4,
+                   "parallelism": "none (1 GPU)"},
+        "roofline": {"kernel": f"{attn_kernel_name(shape)} (paged split-KV GQA attention)",
+                     "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "bytes_per_launch": byts, "avg_launch_ms": split_ms,
+                     "combine_avg_ms": comb_ms, **peak_fracs(achieved, peak)},
+        "read_peak": peak,
+    }
+    if not args.no_cpu_baseline:
+        log("timing the oracle on a bounded sample (host cores)")
+        res["cpu_baseline"] = attention_cpu_baseline(shape, w.seed, pop)
+    print(json.dumps(res), flush=True)
+
+
+def attention_cpu_baseline(shape, seed, pop, n_sample=4):
+    """The oracle's dense float64 attention (all heads) for the first n_sample
+    candidates over their full contexts; GB/s of their algorithmic bytes."""
+    from oracle import decoder as od
+    from paper_2604_07725_amd import synth
+    from threadpoolctl import threadpool_info
+    qh = synth.host_values(synth.q_spec(shape, seed, pop.n)).reshape(pop.n, shape.n_q_heads,
+                                                                      shape.head_dim)
+    spec = synth.kv_spec(shape, seed, 0, pop.n_pages)
+    kv = []
+    for i in range(n_sample):
+        n = int(pop.lengths[i])
+        pool = synth.pool_pages(spec, pop.page_table[i, :(n + 15) // 16])
+        kv.append(od.gather_kv(pool, np.arange(pool.shape[0]), n))
+    t0 = time.perf_counter()
+    for i in range(n_sample):
+        od.attention_dense(qh[i], kv[i][0], kv[i][1], shape.head_dim ** -0.5)
+    dt = time.perf_counter() - t0
+    byts = attention_bytes(pop.lengths[:n_sample], shape.n_kv_heads, shape.n_q_heads,
+                           shape.head_dim)
+    blas = threadpool_info()
+    return {"value": byts / dt / 1e9, "unit": "GB/s", "kind": "oracle",
+            "cores": int(max([b.get("num_threads", 1) for b in blas] or [1])),
+            "sample": f"oracle float64 attention of {n_sample} of {pop.n} candidates "
+                      f"({int(pop.lengths[:n_sample].sum())} cached tokens), {dt:.2f} s",
+            "host_cpus": len(os.sched_getaffinity(0))}
+
+
 def attn_kernel_name(shape):
     g = shape.n_q_heads // shape.n_kv_heads
     kern = "attn_split_mfma_kernel" if g >= 4 else "attn_split_kernel"
@@ -119,6 +218,33 @@ def kernel_table(shape, n, kprof, attn_bytes):
             row["GB_s"] = attn_bytes / (avg * 1e-3) / 1e9
         table[kind] = row
     return table
+
+
+def measure_read_peak(dev, gib=8, grid=32768, reps=10):
+    """The measured HBM read ceiling on this machine (sevo_hbm_read_probe): a
+    sequential read and random whole 8 KB pages (the decode attention's
+    pattern) of a {gib} GiB buffer, GB/s by events over `reps` reads each."""
+    import torch
+    from paper_2604_07725_amd import sevo
+    buf = torch.empty(gib << 30, dtype=torch.uint8, device=dev)
+    order = torch.randperm((gib << 30) // 8192, device=dev, dtype=torch.int32)
+    sink = torch.empty(grid * 16, dtype=torch.uint8, device=dev)
+    out = {"buffer_bytes": buf.numel(), "grid": grid}
+    for name, po in (("sequential_GBs", None), ("pages_8KB_GBs", order)):
+        for _ in range(2):
+            sevo.sevo_hbm_read_probe(buf, po, grid, sink)
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        a.record()
+        for _ in range(reps):
+            sevo.sevo_hbm_read_probe(buf, po, grid, sink)
+        b.record()
+        torch.cuda.synchronize()
+        out[name] = buf.numel() * reps / (a.elapsed_time(b) * 1e-3) / 1e9
+    del buf, order, sink
+    torch.cuda.empty_cache()
+    return out
 
 
 def measured_traffic(workload):
@@ -333,12 +459,15 @@ def prefill_main(args):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=16)
+    ap.add_argument("--steps", type=int, default=None,
+                    help="timed steps (default: the workload's own count, 16 for the default)")
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="dense8b_pop64_agg4")
     ap.add_argument("--num-splits", type=int, default=0)
     ap.add_argument("--cpu-sample", type=int, default=8)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-read-peak", action="store_true",
+                    help="skip the streaming-read measurement of the HBM ceiling")
     ap.add_argument("--temperature", type=float, default=1.0)
     ap.add_argument("--top-k", type=int, default=0, help="0 = full-vocabulary sampling")
     ap.add_argument("--top-p", type=float, default=1.0)
@@ -368,18 +497,26 @@ def main():
         print(json.dumps({"copy_calibration_bytes": src.numel() * 4, "copies": 3}), flush=True)
         return
     if args.mode == "prefill":
+        if args.steps is None:
+            args.steps = 16
         return prefill_main(args)
     from paper_2604_07725_amd import device_inputs as di
     from paper_2604_07725_amd import sevo, synth
 
     w = synth.WORKLOADS[args.workload]
     shape = w.shape
-    if w.attention_only:
-        raise SystemExit("bench.py times the full decode step; pick a decoder workload")
-    extra = args.warmup + args.steps + 1
-    pop = synth.workload_population(w, extra_tokens=extra)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    peak = None if args.no_read_peak else measure_read_peak(dev)
+    if peak:
+        log(f"measured read ceiling: sequential {peak['sequential_GBs']:.0f} GB/s, random 8 KB "
+            f"pages {peak['pages_8KB_GBs']:.0f} GB/s")
+    if w.attention_only:
+        return attention_main(args, w, peak)
+    if args.steps is None:
+        args.steps = w.steps
+    extra = args.warmup + args.steps + 1
+    pop = synth.workload_population(w, extra_tokens=extra)
     kv_bytes_total = 2 * shape.n_layers * pop.n_pages * shape.n_kv_heads * 16 * shape.head_dim * 2
     free, total = torch.cuda.mem_get_info()
     need = kv_bytes_total + shape.weight_bytes() + 2 * shape.vocab * shape.hidden + (2 << 30)
@@ -478,7 +615,9 @@ def main():
                      tr["traffic_bytes_per_launch"] / tr["algorithmic_bytes_per_launch"],
                      "bytes_per_launch": attn_bytes_per_launch,
                      "avg_launch_ms": split_avg_ms,
-                     "with_combine_GBs": attn_bytes_per_launch / (attn_avg_ms * 1e-3) / 1e9},
+                     "with_combine_GBs": attn_bytes_per_launch / (attn_avg_ms * 1e-3) / 1e9,
+                     **peak_fracs(achieved, peak)},
+        "read_peak": peak,
         "step_roofline": {"bound": "hbm", "bytes_per_step": step_bytes,
                           "achieved": step_bytes / (ms_per_step * 1e-3) / 1e9,
                           "peak": HBM_PEAK_GBS, "unit": "GB/s",

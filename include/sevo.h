@@ -479,6 +479,20 @@ size_t sevo_moe_workspace_bytes(const sevo_model* m, int32_t n);
 
 /* ------------------------------------------------------------------ utilities */
 
+/* Streaming-read microbenchmark (measurement tooling, not part of the decode
+ * step): the measured HBM read ceiling the decode attention is compared with,
+ * next to the 8 TB/s specification.  Reads `bytes` of device memory at buf
+ * (16-byte aligned) once:
+ *   page_order NULL: a grid-stride sequential read of bytes / 16 16-byte words;
+ *   else whole 8 KB pages in the order page_order [bytes / 8192] (int32 page
+ *   indexes; an index outside [0, bytes / 8192) is skipped), one wave per page,
+ *   the decode attention's access pattern.
+ * grid = workgroups (256 threads), 1..2^20; sink receives one 16-byte word
+ * per workgroup (device memory of >= 16 * grid bytes, caller-owned).  Time it
+ * with events on `stream`.  Errors: INVALID_ARGUMENT, HIP. */
+sevo_status sevo_hbm_read_probe(const void* buf, size_t bytes, const int32_t* page_order,
+                                int32_t grid, void* sink, void* stream);
+
 /* Synthetic-input generator (device twin of the host generator): element e of
  * dst (e < count) = bf16_rne(fp32(s - 131070) * mul [+ add]) with s the sum of
  * the four 16-bit fields of SplitMix64(key + (offset + e + 1) 0x9E3779B97F4A7C15).

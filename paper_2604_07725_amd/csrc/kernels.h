@@ -154,6 +154,9 @@ bool sample_conf_supported(int vocab, int list_len);
 // C of each sequence: the mean, in row order, of row_conf over the scored rows
 // (strictly increasing packed token indices) inside [seq_starts[s],
 // seq_starts[s + 1]); 0 for a sequence with none.
+// streaming-read microbenchmark (measurement tooling, not the decode path)
+hipError_t launch_hbm_read_probe(const void* buf, size_t bytes, const int32_t* page_order,
+                                 int grid, void* sink, hipStream_t st);
 hipError_t launch_seq_confidence(const float* row_conf, const int32_t* scored_rows, int n_scored,
                                  const int32_t* seq_starts, int n_seqs, float* out,
                                  hipStream_t st);

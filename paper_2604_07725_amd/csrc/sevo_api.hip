@@ -843,6 +843,20 @@ SEVO_API sevo_status sevo_decode_step(sevo_model* m, const sevo_step_args* a, vo
   return SEVO_OK;
 }
 
+// ------------------------------------------------------------------ read probe
+SEVO_API sevo_status sevo_hbm_read_probe(const void* buf, size_t bytes,
+                                         const int32_t* page_order, int32_t grid, void* sink,
+                                         void* stream) {
+  if (!buf || !sink || !aligned16(buf) || !aligned16(sink))
+    return fail(SEVO_ERR_INVALID_ARGUMENT, "null or misaligned buffer");
+  if (grid < 1 || grid > (1 << 20)) return fail(SEVO_ERR_INVALID_ARGUMENT, "grid %d", grid);
+  if (bytes < 16 || (page_order && bytes < 8192))
+    return fail(SEVO_ERR_INVALID_ARGUMENT, "buffer of %zu bytes too small", bytes);
+  hipError_t e = sevo::launch_hbm_read_probe(buf, bytes, page_order, grid, sink,
+                                             static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? SEVO_OK : hip_fail(e, "sevo_hbm_read_probe");
+}
+
 // ------------------------------------------------------------------ MoE sub-step
 SEVO_API size_t sevo_moe_workspace_bytes(const sevo_model* m, int32_t n) {
   if (!m || n <= 0 || m->cfg.n_experts <= 0) return 0;

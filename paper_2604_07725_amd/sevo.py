@@ -120,6 +120,7 @@ _SIGS = {
     "sevo_prefill_confidence": ([vp, C.POINTER(PrefillArgs), vp], i32),
     "sevo_moe_ffn": ([vp, i32, vp, i32, vp, vp, vp, vp, sz, vp], i32),
     "sevo_moe_workspace_bytes": ([vp, i32], sz),
+    "sevo_hbm_read_probe": ([vp, sz, vp, i32, vp, vp], i32),
     "sevo_prefill_workspace_bytes": ([vp, i32, i32], sz),
     "sevo_embed": ([vp, vp, i32, i32, i32, vp, vp], i32),
     "sevo_rmsnorm": ([vp, vp, i32, i32, f32, vp, vp], i32),
@@ -512,6 +513,18 @@ def sevo_moe_ffn(model: Model, layer: int, h_tiled, n: int, stream=None, partial
     _check(lib().sevo_moe_ffn(model.handle, int(layer), _p(h_tiled), int(n), _p(ex), _p(wt),
                               _p(part), _p(ws), ws.numel(), _stream(stream)))
     return ex, wt, part
+
+
+# ------------------------------------------------------------------ read probe
+def sevo_hbm_read_probe(buf, page_order=None, grid=32768, sink=None, stream=None):
+    """Read every byte of the device tensor ``buf`` once (sequentially, or as
+    8 KB pages in the int32 order ``page_order``); returns the sink tensor."""
+    if sink is None:
+        sink = torch.empty(grid * 16, dtype=torch.uint8, device=buf.device)
+    nbytes = buf.numel() * buf.element_size()
+    _check(lib().sevo_hbm_read_probe(_p(buf), nbytes, _p(page_order), int(grid), _p(sink),
+                                     _stream(stream)))
+    return sink
 
 
 # ------------------------------------------------------------------ confidence engine

@@ -252,3 +252,16 @@ def test_profile_begin_rejects_bad_arguments():
     ms = (CT.c_float * len(sevo.PROF_KINDS))()
     cnt = (CT.c_int32 * len(sevo.PROF_KINDS))()
     assert L.sevo_profile_end(ms, cnt) == sevo.OK and sum(cnt) == 0
+
+
+def test_read_probe_rejects_bad_arguments():
+    L = sevo.lib()
+    f = 1 << 20
+    assert L.sevo_hbm_read_probe(None, 1 << 20, None, 64, f, None) == sevo.INVALID_ARGUMENT
+    assert L.sevo_hbm_read_probe(f + 4, 1 << 20, None, 64, f, None) == sevo.INVALID_ARGUMENT
+    assert L.sevo_hbm_read_probe(f, 1 << 20, None, 64, None, None) == sevo.INVALID_ARGUMENT
+    assert L.sevo_hbm_read_probe(f, 1 << 20, None, 0, f, None) == sevo.INVALID_ARGUMENT
+    assert L.sevo_hbm_read_probe(f, 1 << 20, None, (1 << 20) + 1, f, None) == \
+        sevo.INVALID_ARGUMENT
+    assert L.sevo_hbm_read_probe(f, 8, None, 64, f, None) == sevo.INVALID_ARGUMENT
+    assert L.sevo_hbm_read_probe(f, 4096, f, 64, f, None) == sevo.INVALID_ARGUMENT

@@ -509,3 +509,34 @@ def test_rmsnorm_and_embed_match_oracle(S):
     assert np.all(np.abs(got - ref) <= 2 ** -8 * np.abs(ref) + 1e-6)
     # mostly equal to the oracle's own bf16 rounding of the same value
     assert np.mean(got == round_bf16(ref)) > 0.99
+
+
+# ------------------------------------------------------------------ read probe
+@pytest.mark.parametrize("grid", [1, 7, 256, 4096])
+def test_read_probe_reads_every_byte_once(S, grid):
+    """The streaming-read microbenchmark reads each 16-byte word exactly once:
+    the XOR of its per-workgroup words equals the XOR of the whole buffer
+    (sequential), of all pages (a permutation) and of the listed pages only
+    (ids outside the buffer skipped)."""
+    sevo, di = S
+    n_pages = 77
+    rng = np.random.default_rng(grid)
+    host = rng.integers(0, 2 ** 32, size=(n_pages, 512, 4), dtype=np.uint32)
+    buf = torch.from_numpy(host.view(np.int32)).cuda()
+    sink = torch.zeros(grid * 16, dtype=torch.uint8, device="cuda")
+
+    def xor_sink():
+        torch.cuda.synchronize()
+        return np.bitwise_xor.reduce(sink.cpu().numpy().view(np.uint32).reshape(grid, 4), axis=0)
+
+    whole = np.bitwise_xor.reduce(host.reshape(-1, 4), axis=0)
+    sevo.sevo_hbm_read_probe(buf, None, grid, sink)
+    np.testing.assert_array_equal(xor_sink(), whole)
+    order = rng.permutation(n_pages).astype(np.int32)
+    sevo.sevo_hbm_read_probe(buf, torch.from_numpy(order).cuda(), grid, sink)
+    np.testing.assert_array_equal(xor_sink(), whole)
+    order[[3, 40]] = [-1, n_pages + 5]     # two pages skipped
+    sevo.sevo_hbm_read_probe(buf, torch.from_numpy(order).cuda(), grid, sink)
+    listed = order[(order >= 0) & (order < n_pages)]
+    np.testing.assert_array_equal(
+        xor_sink(), np.bitwise_xor.reduce(host[listed].reshape(-1, 4), axis=0))
