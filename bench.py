@@ -466,6 +466,8 @@ def main():
     ap.add_argument("--num-splits", type=int, default=0)
     ap.add_argument("--cpu-sample", type=int, default=8)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--graph", action="store_true",
+                    help="replay the step as one captured HIP graph (same kernels, same work)")
     ap.add_argument("--no-read-peak", action="store_true",
                     help="skip the streaming-read measurement of the HBM ceiling")
     ap.add_argument("--temperature", type=float, default=1.0)
@@ -515,7 +517,10 @@ def main():
         return attention_main(args, w, peak)
     if args.steps is None:
         args.steps = w.steps
-    extra = args.warmup + args.steps + 1
+    # key slots every step appends: warm-up, timed, (graph mode: as many eager
+    # steps again for the attention timing), the 2 kernel-table steps
+    n_steps_total = args.warmup + args.steps * (2 if args.graph else 1) + 2
+    extra = n_steps_total + 1
     pop = synth.workload_population(w, extra_tokens=extra)
     kv_bytes_total = 2 * shape.n_layers * pop.n_pages * shape.n_kv_heads * 16 * shape.head_dim * 2
     free, total = torch.cuda.mem_get_info()
@@ -551,8 +556,18 @@ def main():
         step()
     torch.cuda.synchronize()
     log("warmup done")
+    eager_step = step
+    if args.graph:
+        # one step captured as a graph (every launch of sevo_decode_step and the
+        # bookkeeping reads and writes the same device buffers each step)
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            step()
+        torch.cuda.synchronize()   # capture does not run the step
+        step = graph.replay
 
-    sevo.sevo_profile_begin(shape.n_layers * args.steps, ("attn_split", "attn_combine"))
+    if not args.graph:
+        sevo.sevo_profile_begin(shape.n_layers * args.steps, ("attn_split", "attn_combine"))
     start = torch.cuda.Event(enable_timing=True)
     stop = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -562,6 +577,13 @@ def main():
     stop.record()
     torch.cuda.synchronize()
     total_ms = start.elapsed_time(stop)
+    if args.graph:
+        # the replayed graph records no per-launch events: time the attention
+        # launches over as many eager steps
+        sevo.sevo_profile_begin(shape.n_layers * args.steps, ("attn_split", "attn_combine"))
+        for _ in range(args.steps):
+            eager_step()
+        torch.cuda.synchronize()
     prof = sevo.sevo_profile_end()
     split_ms, launches = prof["attn_split"]
     attn_ms = split_ms + prof["attn_combine"][0]
@@ -571,13 +593,13 @@ def main():
     # (outside the timed region: the extra event records cost a little time)
     sevo.sevo_profile_begin(400 * 2, sevo.PROF_KINDS)
     for _ in range(2):
-        step()
+        eager_step()
     torch.cuda.synchronize()
     kprof = sevo.sevo_profile_end()
     log(f"{args.steps} steps: {ms_per_step:.3f} ms/step; attention launches {launches}")
 
     # algorithmic bytes of the timed attention launches (lengths grow by one per step)
-    base = pop.lengths.astype(np.int64) + args.warmup + 1
+    base = pop.lengths.astype(np.int64) + args.warmup + 1 + (args.steps if args.graph else 0)
     per_step = [attention_bytes(base + s, shape.n_kv_heads, shape.n_q_heads, shape.head_dim)
                 for s in range(args.steps)]
     attn_bytes_per_launch = float(np.mean(per_step))
@@ -606,7 +628,8 @@ def main():
                    "temperature": args.temperature,
                    "sampling": ("full vocabulary" if args.top_k == 0 else
                                 f"top-k {args.top_k}, top-p {args.top_p}, min-p {args.min_p}"),
-                   "self_confidence_topk": args.conf_topk},
+                   "self_confidence_topk": args.conf_topk,
+                   "launch": "hip graph replay" if args.graph else "stream launches"},
         "roofline": {"kernel": f"{attn_kernel_name(shape)} (paged split-KV GQA attention)",
                      "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,

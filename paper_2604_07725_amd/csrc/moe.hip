@@ -10,11 +10,10 @@
 //   * plan: one workgroup counts tokens per expert and lays the (token, slot)
 //     assignments out expert-major, tokens in order (ranks from per-expert
 //     bit rows: a fixed order, results do not depend on scheduling);
-//   * experts: a grouped skinny GEMM over (64-row weight superblock, expert,
-//     64-assignment tile), the same weight stream as the dense projections
-//     (packed fragment-major weights, four waves taking the 32-k steps round
-//     robin, four fragment buffers in flight); activation rows are gathered
-//     through the assignment list.  Gate/up writes silu(g) * u per assignment
+//   * experts: a grouped skinny GEMM over (superblocks, expert): each wave
+//     streams 32 or 64 rows of one selected expert's packed weights over the
+//     whole K range (no cross-wave reduction), activation rows gathered
+//     through the expert's entry list.  Gate/up writes silu(g) * u per entry
 //     (bf16, row-major); down writes w * y into partial [slot][token][hidden]
 //     (fp32), which the next residual add + RMSNorm sums in slot order.
 #include "common.h"
@@ -171,127 +170,140 @@ __global__ __launch_bounds__(kPlanThreads) void moe_plan_kernel(const int32_t* _
   }
 }
 
+// Grouped skinny GEMM over the selected experts.  At decode an expert sees a
+// few tokens, so the kernel is a stream of the selected experts' weights.
+// A wave takes FPW of the four 16-row fragments of one 64-row weight
+// superblock over the whole K range, so no partial sum crosses waves (no LDS,
+// no barrier); a workgroup's four waves take 4 FPW / 4 superblocks:
+//   EPI 0 (gate/up): gate fragment f pairs with up fragment f + 2 (the 32 + 32
+//     superblock), SwiGLU in registers; X = the normed input, tiled [n][H],
+//     rows gathered by token; out act [n k][Fe] bf16, row = entry position;
+//   EPI 1 (down): X = the expert's act rows; out part [k][n][H] fp32 =
+//     routing weight * product.
+// FPW is chosen so the grid fits one round of resident waves.  The expert's
+// entries come in tiles of 16 NB rows (NB from the expected entries per
+// expert); an expert with more entries takes further tiles, re-reading its
+// weights.  Four fragment buffers keep three steps' loads in flight.
+template <int NB, int FPW>
 struct MoeFrag {
-  bf16x8v a[4];
-  bf16x8v b[4];
+  bf16x8v a[FPW];
+  bf16x8v b[NB];
 };
 
-// Grouped skinny GEMM over the selected experts.
-// EPI 0 (gate/up): X = the normed input, tiled [n][H], rows gathered by
-//   token; W = packed gate/up of each expert [2 Fe][H] (32 + 32 row
-//   superblocks); out act [n k][Fe] bf16 row-major, row = assignment position.
-// EPI 1 (down): X = act rows of the expert (contiguous positions); W = packed
-//   down [H][Fe]; out part [k][n][H] fp32 = routing weight * product.
-template <int EPI>
-__global__ __launch_bounds__(256, 2) void moe_expert_kernel(MoeExpertArgs a) {
-  __shared__ f32x4 red[4][4][4][64];
+template <int EPI, int NB, int FPW>
+__global__ __launch_bounds__(256) void moe_expert_kernel(MoeExpertArgs a) {
+  static_assert(FPW == 2 || FPW == 4, "two or four fragments per wave");
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int sb = blockIdx.x, e = blockIdx.y;
+  const int e = blockIdx.y;
   const int off = a.offsets[e];
   const int ne = a.offsets[e + 1] - off;
-  const int m0 = blockIdx.z * 64;
-  if (m0 >= ne) return;  // uniform over the workgroup
   const int K = EPI == 0 ? a.hidden : a.ffn;
   const int N = EPI == 0 ? 2 * a.ffn : a.hidden;
+  constexpr int kSbPerGroup = FPW;  // superblocks per workgroup (4 waves)
+  const int sb = kSbPerGroup * blockIdx.x + wave / (4 / FPW);
+  if (ne <= 0 || sb >= N / 64) return;  // wave-uniform; no barrier follows
   const int KS = K >> 5;
+  const int p = wave & 1;  // which half of the superblock (FPW = 2)
+  // the wave's fragments; for gate/up, pairs (gate, up) are adjacent
+  int fr[FPW];
+  if constexpr (FPW == 4) {
+    if constexpr (EPI == 0) { fr[0] = 0; fr[1] = 2; fr[2] = 1; fr[3] = 3; }
+    else { fr[0] = 0; fr[1] = 1; fr[2] = 2; fr[3] = 3; }
+  } else {
+    if constexpr (EPI == 0) { fr[0] = p; fr[1] = p + 2; }
+    else { fr[0] = 2 * p; fr[1] = 2 * p + 1; }
+  }
   const int r = lane & 15, q = lane >> 4;
-  const bf16_t* W = (EPI == 0 ? a.w_gate_up : a.w_down) + (size_t)e * N * K;
-  const bf16_t* wp = W + (size_t)sb * KS * 2048 + lane * 8;
-  // activation rows of this lane per 16-row block (rows past the expert's
-  // count read its last row: they only feed outputs that are never stored)
-  const bf16_t* xp[4];
+  const bf16_t* wp = (EPI == 0 ? a.w_gate_up : a.w_down) + (size_t)e * N * K +
+                     (size_t)sb * KS * 2048 + lane * 8;
+
+  for (int m0 = 0; m0 < ne; m0 += 16 * NB) {
+    // activation rows of this lane per 16-row block (rows past the expert's
+    // count read its last row: they only feed outputs that are never stored)
+    const bf16_t* xp[NB];
 #pragma unroll
-  for (int b = 0; b < 4; ++b) {
-    const int i = min(m0 + 16 * b + r, ne - 1);
-    if constexpr (EPI == 0) {
-      const int t = a.assign[off + i] / a.top_k;
-      xp[b] = a.x + ((size_t)(t >> 4) * KS) * 512 + (16 * q + (t & 15)) * 8;
-    } else {
-      xp[b] = a.act + (size_t)(off + i) * a.ffn + 8 * q;
-    }
-  }
-  const int cnt = KS > wave ? (KS - wave + 3) >> 2 : 0;  // this wave's 32-k steps
-  f32x4 acc[4][4];
-#pragma unroll
-  for (int tt = 0; tt < 4; ++tt)
-#pragma unroll
-    for (int b = 0; b < 4; ++b) acc[tt][b] = f32x4{0.f, 0.f, 0.f, 0.f};
-  auto load = [&](MoeFrag& f, int j) {
-    const int st = wave + 4 * min(j, cnt - 1);
-#pragma unroll
-    for (int tt = 0; tt < 4; ++tt)
-      f.a[tt] = *reinterpret_cast<const bf16x8v*>(wp + (size_t)st * 2048 + tt * 512);
-#pragma unroll
-    for (int b = 0; b < 4; ++b)
-      f.b[b] = *reinterpret_cast<const bf16x8v*>(xp[b] + (EPI == 0 ? (size_t)st * 512 : (size_t)st * 32));
-  };
-  auto mma = [&](const MoeFrag& f) {
-#pragma unroll
-    for (int tt = 0; tt < 4; ++tt)
-#pragma unroll
-      for (int b = 0; b < 4; ++b)
-        acc[tt][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f.a[tt], f.b[b], acc[tt][b], 0, 0, 0);
-  };
-  if (cnt > 0) {
-    MoeFrag f0, f1, f2, f3;
-    load(f0, 0);
-    load(f1, 1);
-    load(f2, 2);
-    for (int j = 0; j < cnt; j += 4) {
-      load(f3, j + 3);
-      __builtin_amdgcn_sched_barrier(0);
-      mma(f0);
-      __builtin_amdgcn_sched_barrier(0);
-      load(f0, j + 4);
-      __builtin_amdgcn_sched_barrier(0);
-      if (j + 1 < cnt) mma(f1);
-      __builtin_amdgcn_sched_barrier(0);
-      load(f1, j + 5);
-      __builtin_amdgcn_sched_barrier(0);
-      if (j + 2 < cnt) mma(f2);
-      __builtin_amdgcn_sched_barrier(0);
-      load(f2, j + 6);
-      __builtin_amdgcn_sched_barrier(0);
-      if (j + 3 < cnt) mma(f3);
-      __builtin_amdgcn_sched_barrier(0);
-    }
-  }
-#pragma unroll
-  for (int tt = 0; tt < 4; ++tt)
-#pragma unroll
-    for (int b = 0; b < 4; ++b) red[wave][tt][b][lane] = acc[tt][b];
-  __syncthreads();
-  // D of tile (tt, b): lane holds activation row 16 b + lane % 16 and weight
-  // rows 16 tt + 4 (lane / 16) + 0..3 (4 consecutive output columns)
-  if constexpr (EPI == 0) {
-    for (int idx = threadIdx.x; idx < 2 * 4 * 64; idx += 256) {
-      const int l = idx & 63, tb = idx >> 6;
-      const int tt = tb >> 2, b = tb & 3;  // tt in {0, 1}: gate rows
-      const f32x4 g = red[0][tt][b][l] + red[1][tt][b][l] + red[2][tt][b][l] + red[3][tt][b][l];
-      const f32x4 u = red[0][tt + 2][b][l] + red[1][tt + 2][b][l] + red[2][tt + 2][b][l] +
-                      red[3][tt + 2][b][l];
-      const int i = m0 + 16 * b + (l & 15);
-      const int col = sb * 32 + 16 * tt + 4 * (l >> 4);
-      if (i < ne) {
-        uint2 o;
-        o.x = pack_bf16x2(g.x / (1.f + __expf(-g.x)) * u.x, g.y / (1.f + __expf(-g.y)) * u.y);
-        o.y = pack_bf16x2(g.z / (1.f + __expf(-g.z)) * u.z, g.w / (1.f + __expf(-g.w)) * u.w);
-        *reinterpret_cast<uint2*>(a.act + (size_t)(off + i) * a.ffn + col) = o;
+    for (int b = 0; b < NB; ++b) {
+      const int i = min(m0 + 16 * b + r, ne - 1);
+      if constexpr (EPI == 0) {
+        const int t = a.assign[off + i] / a.top_k;
+        xp[b] = a.x + ((size_t)(t >> 4) * KS) * 512 + (16 * q + (t & 15)) * 8;
+      } else {
+        xp[b] = a.act + (size_t)(off + i) * a.ffn + 8 * q;
       }
     }
-  } else {
-    for (int idx = threadIdx.x; idx < 4 * 4 * 64; idx += 256) {
-      const int l = idx & 63, tb = idx >> 6;
-      const int tt = tb >> 2, b = tb & 3;
-      const f32x4 v = red[0][tt][b][l] + red[1][tt][b][l] + red[2][tt][b][l] + red[3][tt][b][l];
-      const int i = m0 + 16 * b + (l & 15);
-      if (i < ne) {
+    f32x4 acc[FPW][NB];
+#pragma unroll
+    for (int h = 0; h < FPW; ++h)
+#pragma unroll
+      for (int b = 0; b < NB; ++b) acc[h][b] = f32x4{0.f, 0.f, 0.f, 0.f};
+    // step j of K; past the end it re-reads the last one (cache hits, unused)
+    auto load = [&](MoeFrag<NB, FPW>& f, int j) {
+      const int st = min(j, KS - 1);
+#pragma unroll
+      for (int h = 0; h < FPW; ++h)
+        f.a[h] = *reinterpret_cast<const bf16x8v*>(wp + (size_t)st * 2048 + fr[h] * 512);
+#pragma unroll
+      for (int b = 0; b < NB; ++b)
+        f.b[b] = *reinterpret_cast<const bf16x8v*>(
+            xp[b] + (EPI == 0 ? (size_t)st * 512 : (size_t)st * 32));
+    };
+    auto mma = [&](const MoeFrag<NB, FPW>& f) {
+#pragma unroll
+      for (int h = 0; h < FPW; ++h)
+#pragma unroll
+        for (int b = 0; b < NB; ++b)
+          acc[h][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f.a[h], f.b[b], acc[h][b], 0, 0, 0);
+    };
+    {
+      MoeFrag<NB, FPW> f0, f1, f2, f3;
+      load(f0, 0);
+      load(f1, 1);
+      load(f2, 2);
+      for (int j = 0; j < KS; j += 4) {
+        load(f3, j + 3);
+        __builtin_amdgcn_sched_barrier(0);
+        mma(f0);
+        __builtin_amdgcn_sched_barrier(0);
+        load(f0, j + 4);
+        __builtin_amdgcn_sched_barrier(0);
+        if (j + 1 < KS) mma(f1);
+        __builtin_amdgcn_sched_barrier(0);
+        load(f1, j + 5);
+        __builtin_amdgcn_sched_barrier(0);
+        if (j + 2 < KS) mma(f2);
+        __builtin_amdgcn_sched_barrier(0);
+        load(f2, j + 6);
+        __builtin_amdgcn_sched_barrier(0);
+        if (j + 3 < KS) mma(f3);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+    // D of fragment h, token block b: lane holds entry row 16 b + lane % 16
+    // and weight rows 4 (lane / 16) + 0..3 of the fragment (4 consecutive
+    // output columns)
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      const int i = m0 + 16 * b + r;
+      if (i >= ne) continue;
+      if constexpr (EPI == 0) {
+#pragma unroll
+        for (int h = 0; h < FPW; h += 2) {
+          const f32x4 g = acc[h][b], u = acc[h + 1][b];
+          const int col = sb * 32 + 16 * fr[h] + 4 * q;
+          uint2 o;
+          o.x = pack_bf16x2(g.x / (1.f + __expf(-g.x)) * u.x, g.y / (1.f + __expf(-g.y)) * u.y);
+          o.y = pack_bf16x2(g.z / (1.f + __expf(-g.z)) * u.z, g.w / (1.f + __expf(-g.w)) * u.w);
+          *reinterpret_cast<uint2*>(a.act + (size_t)(off + i) * a.ffn + col) = o;
+        }
+      } else {
         const int asg = a.assign[off + i];
         const int t = asg / a.top_k, slot = asg - t * a.top_k;
         const float wt = a.weights[asg];
-        const int col = sb * 64 + 16 * tt + 4 * (l >> 4);
-        *reinterpret_cast<f32x4*>(a.part + ((size_t)slot * a.n + t) * a.hidden + col) = v * wt;
+        float* dst = a.part + ((size_t)slot * a.n + t) * a.hidden + sb * 64 + 4 * q;
+#pragma unroll
+        for (int h = 0; h < FPW; ++h)
+          *reinterpret_cast<f32x4*>(dst + 16 * fr[h]) = acc[h][b] * wt;
       }
     }
   }
@@ -318,13 +330,26 @@ hipError_t launch_moe_plan(const int32_t* sel, int nk, int E, int32_t* offsets, 
 
 hipError_t launch_moe_experts(const MoeExpertArgs& a, hipStream_t st) {
   if (a.n == 0) return hipSuccess;
-  const int mt = (a.n + 63) / 64;  // an expert takes each token at most once
-  hipLaunchKernelGGL(moe_expert_kernel<0>, dim3(2 * a.ffn / 64, a.n_experts, mt), dim3(256), 0,
-                     st, a);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(moe_expert_kernel<1>, dim3(a.hidden / 64, a.n_experts, mt), dim3(256), 0,
-                     st, a);
+  // token tile from the expected entries per expert (n k / E): one 16-row
+  // block at decode sizes, up to four for prefill-like batches
+  const long long per = ((long long)a.n * a.top_k + a.n_experts - 1) / a.n_experts;
+  const int nb = per <= 12 ? 1 : (per <= 24 ? 2 : 4);
+  // gate/up: 2 fragments per wave (2 superblocks per workgroup); down: the
+  // whole superblock per wave (4 per workgroup), so that at the 30B-A3B shape
+  // each grid is one round of resident waves
+  const dim3 g0((2 * a.ffn / 64 + 1) / 2, a.n_experts), g1((a.hidden / 64 + 3) / 4, a.n_experts);
+#define SEVO_MOE_LAUNCH(NB)                                                          \
+  hipLaunchKernelGGL((moe_expert_kernel<0, NB, 2>), g0, dim3(256), 0, st, a);      \
+  if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;                 \
+  hipLaunchKernelGGL((moe_expert_kernel<1, NB, 4>), g1, dim3(256), 0, st, a);
+  if (nb == 1) {
+    SEVO_MOE_LAUNCH(1)
+  } else if (nb == 2) {
+    SEVO_MOE_LAUNCH(2)
+  } else {
+    SEVO_MOE_LAUNCH(4)
+  }
+#undef SEVO_MOE_LAUNCH
   return hipGetLastError();
 }
 

@@ -225,6 +225,53 @@ def test_full_width_step_reduced_depth(S, workload, layers):
             assert z.max() - z[g_ids[j]] <= FULL_GAP_EXACT
 
 
+def test_step_graph_replay_matches_eager_bit_exact(S):
+    """The decode step captured as a HIP graph (launches of sevo_decode_step and
+    the on-device bookkeeping) replays bit-identically to eager steps on a copy
+    of the same state: ids, log-probs, logits after every replay (with eager
+    work and synchronisations between replays) and the KV pools at the end."""
+    sevo, di = S
+    w = synth.WORKLOADS["tiny_step"]
+    shape = w.shape
+    steps = 3
+    say("decode step graph replay vs eager")
+    pop, model, kvp_a, d = _setup(S, w, extra=steps + 1)
+    kvp_b = [p.clone() for p in kvp_a]
+
+    def buffers(kvp):
+        toks = d["tokens"].clone()
+        pos = d["lengths"].clone()
+        b = sevo.StepBuffers(model, toks, pos, d["page_table"], kvp, d["uids"], seed=5,
+                             temperature=1.0, keep_logits=True)
+        return b, toks, pos, b.out_logits
+
+    ba, ta, pa, la = buffers(kvp_a)
+    bb, tb, pb, lb = buffers(kvp_b)
+
+    def step(b, toks, pos):
+        ids, _ = b.run()
+        toks.copy_(ids)
+        pos.add_(1)
+
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step(bb, tb, pb)
+    torch.cuda.synchronize()
+    for r in range(steps):
+        step(ba, ta, pa)
+        graph.replay()
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(ta.cpu().numpy(), tb.cpu().numpy())
+        np.testing.assert_array_equal(pa.cpu().numpy(), pb.cpu().numpy())
+        np.testing.assert_array_equal(ba.out_logprobs.cpu().numpy(), bb.out_logprobs.cpu().numpy())
+        np.testing.assert_array_equal(la.cpu().numpy(), lb.cpu().numpy())
+        say(f"  replay {r}: ids {tb.cpu().numpy().tolist()} identical")
+    for l in range(shape.n_layers):
+        np.testing.assert_array_equal(bf16_bits(kvp_a[l]), bf16_bits(kvp_b[l]))
+    model.close()
+
+
 def test_step_kernel_timing_counts_every_launch(S):
     """The per-kind timing records one launch of each kind where the step makes
     one (per layer or per step) and positive times."""
