@@ -313,7 +313,7 @@ def cpu_baseline(w, pop, n_sample, budget_s=30.0):
     }
 
 
-PREFILL_GEMM_KINDS = ("qkv", "attn_out", "gate_up", "down")
+PREFILL_GEMM_KINDS = ("qkv", "attn_out", "gate_up", "down", "moe_route", "moe_experts")
 
 
 def prefill_flops(shape, T, R):
@@ -323,8 +323,14 @@ def prefill_flops(shape, T, R):
     head on the scored rows."""
     hq, d, H, F = shape.n_q_heads, shape.head_dim, shape.hidden, shape.ffn
     attn = 4.0 * hq * d * T * (T + 1) / 2
-    per_layer = {"qkv": 2.0 * T * shape.qkv_dim * H, "attn_out": 2.0 * T * H * shape.q_dim,
-                 "gate_up": 2.0 * T * 2 * F * H, "down": 2.0 * T * H * F}
+    per_layer = {"qkv": 2.0 * T * shape.qkv_dim * H, "attn_out": 2.0 * T * H * shape.q_dim}
+    if shape.is_moe:
+        # router GEMM; the selected experts' gate/up + down for every token
+        per_layer["moe_route"] = 2.0 * T * shape.n_experts * H
+        per_layer["moe_experts"] = 2.0 * T * shape.top_k * 3 * shape.expert_ffn * H
+    else:
+        per_layer["gate_up"] = 2.0 * T * 2 * F * H
+        per_layer["down"] = 2.0 * T * H * F
     return attn, per_layer, 2.0 * R * shape.vocab * H
 
 
@@ -361,14 +367,17 @@ def prefill_cpu_baseline(shape, seed, n_tokens=256):
 
 
 def prefill_main(args):
-    """The confidence engine (prefill-only scoring pass) on the 8B-class model:
-    one request at a time of each length, every row scored (Eq. 1 c, K_l = 20),
+    """The confidence engine (prefill-only scoring pass) on the 8B-class model,
+    or on the 30B-A3B-class MoE model with --workload moe30b_pop64_agg4: one
+    request at a time of each length, every row scored (Eq. 1 c, K_l = 20),
     one C per request returned; per-kernel times from HIP events."""
     import torch
     from paper_2604_07725_amd import device_inputs as di
     from paper_2604_07725_amd import sevo, synth
-    shape = synth.DENSE_8B
-    seed = 2
+    w = synth.WORKLOADS[args.workload]
+    moe = w.shape.is_moe
+    shape = w.shape if moe else synth.DENSE_8B
+    seed = w.seed if moe else 2
     lengths = [int(v) for v in args.prefill_tokens.split(",")]
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
@@ -436,12 +445,15 @@ def prefill_main(args):
         "n_gpus": 1, "steps": args.steps if args.steps < 16 else 2, "warmup": 1,
         "dtype": "bf16", "data": "synthetic (seeded; random-init weights)",
         "vs_baseline": None,
-        "config": {"workload": "confidence_engine_dense8b", "model": "dense 8B-class decoder",
-                   "layers": shape.n_layers, "hidden": shape.hidden, "heads": "32/8x128",
-                   "ffn": shape.ffn, "vocab": shape.vocab, "batch": 1,
+        "config": {"workload": "confidence_engine_" + ("moe30b" if moe else "dense8b"),
+                   "model": model_name(shape), "layers": shape.n_layers,
+                   "hidden": shape.hidden,
+                   "heads": f"{shape.n_q_heads}/{shape.n_kv_heads}x{shape.head_dim}",
+                   **ffn_config(shape), "vocab": shape.vocab, "batch": 1,
                    "tokens": [r["tokens"] for r in results], "scored_rows": "all",
                    "conf_topk": 20},
-        "roofline": {"kernel": "attn_prefill_kernel<128> (causal GQA prefill attention)",
+        "roofline": {"kernel": f"attn_prefill_kernel<{shape.head_dim}> (causal GQA prefill "
+                               "attention)",
                      "bound": "mfma", "achieved": big["kernels"]["attn_prefill"]["TFLOP_s"],
                      "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                      "frac": big["kernels"]["attn_prefill"]["mfma_frac"], "traffic": None},

@@ -238,6 +238,10 @@ sevo_status sevo_attn_prefill(const sevo_prefill_attn_args* a, void* stream);
  * steps of sevo_decode_step run for all total_tokens tokens at once, with the
  * causal prefill attention of sevo_attn_prefill; the keys and values of every
  * token are written into the pools (a KV cache a decode can continue from).
+ * A mixture-of-experts model runs its expert FFN on chunks of moe_chunk
+ * tokens (rounded up to 16; 0 or more than 16384 = 16384): routing, expert
+ * lists and the per-slot outputs of a chunk live in the workspace, and each
+ * token's k expert outputs are summed in slot order.
  * Then, for each scored row r -- a packed token index whose next-token
  * distribution is scored --
  *   c_r = logsumexp(logits_r) - mean of the conf_topk largest logits_r
@@ -275,6 +279,8 @@ typedef struct {
   float* out_row_conf;
   void* workspace;
   size_t workspace_bytes;
+  int32_t moe_chunk;  /* MoE models: tokens per expert-FFN chunk, 0 = 16384 (the
+                         largest; sevo_prefill_workspace_bytes sizes for it) */
 } sevo_prefill_args;
 
 sevo_status sevo_prefill_confidence(sevo_model* m, const sevo_prefill_args* a, void* stream);

@@ -253,15 +253,19 @@ def moe_ffn(shape, lw, h2, mirror=True):
     h2 = np.asarray(h2, np.float64)
     logits = keep32(h2 @ np.asarray(lw["w_router"], np.float64).T)
     sel, w, gap = moe_route(logits, shape.top_k)
-    out = np.zeros_like(h2)
     wgu = lw["w_expert_gate_up"]
     wd = lw["w_expert_down"]
-    for t in range(h2.shape[0]):
-        for j in range(shape.top_k):
-            e = int(sel[t, j])
-            gu = h2[t] @ np.asarray(wgu[e], np.float64).T
-            a = rb(silu(gu[:Fe]) * gu[Fe:])
-            out[t] += w[t, j] * (a @ np.asarray(wd[e], np.float64).T)
+    # y[t, j] = w_{t,j} * expert sel[t, j] applied to h2[t]; an expert's
+    # matrices are read once for all the rows routed to it
+    y = np.zeros((h2.shape[0], shape.top_k, h2.shape[1]))
+    for e in np.unique(sel):
+        t, j = np.nonzero(sel == e)
+        gu = h2[t] @ np.asarray(wgu[e], np.float64).T
+        a = rb(silu(gu[:, :Fe]) * gu[:, Fe:])
+        y[t, j] = w[t, j][:, None] * (a @ np.asarray(wd[e], np.float64).T)
+    out = np.zeros_like(h2)
+    for j in range(shape.top_k):      # the k slots, summed in slot order
+        out += y[:, j]
     return out, gap
 
 
@@ -394,30 +398,32 @@ def prefill_index(seq_starts, start_pos=None):
 
 
 def prefill_forward(shape, weights, kv_pools, page_table, tokens, seq_starts, start_pos=None,
-                    mirror=True):
+                    mirror=True, stats=None):
     """Residual stream after the last layer for every token of a prefill batch.
 
     Every token takes the decoder layer with its sequence's page-table row and
     its own position: all keys of a layer are appended before its attention,
     and token t attends keys 0..pos(t), which is causal attention over the
     sequence (plus any cached prefix).  kv_pools are modified in place.
+    ``stats`` as in decoder_layer (the smallest routing gap of MoE layers).
     """
     tokens = np.asarray(tokens, np.int64)
     row, pos = prefill_index(seq_starts, start_pos)
     pt_rows = np.asarray(page_table)[row]
     x = np.asarray(weights["embed"][tokens], np.float64)
     for l in range(shape.n_layers):
-        x = decoder_layer(shape, weights["layers"][l], x, pos, kv_pools[l], pt_rows, mirror)
+        x = decoder_layer(shape, weights["layers"][l], x, pos, kv_pools[l], pt_rows, mirror,
+                          stats)
     return x
 
 
 def prefill_confidence(shape, weights, kv_pools, page_table, tokens, seq_starts, scored_rows,
-                       k_l, start_pos=None, mirror=True):
+                       k_l, start_pos=None, mirror=True, stats=None):
     """The confidence engine: c (Eq. 1) of the next-token distribution at each
     scored row, and per sequence C = mean of c over its scored rows (Eq. 2;
     0 without any).  Returns (conf [n_seqs], row_conf [len(scored_rows)], logits)."""
     x = prefill_forward(shape, weights, kv_pools, page_table, tokens, seq_starts, start_pos,
-                        mirror)
+                        mirror, stats)
     rows = np.asarray(scored_rows, np.int64)
     logits = lm_logits(shape, weights["final_norm"], weights["lm_head"], x[rows], mirror)
     c = token_confidence(logits, k_l)

@@ -23,6 +23,14 @@
 // Epilogues: fp32 store, fp32 accumulate (residual update), and SwiGLU over a
 // gate/up matrix packed in 32 + 32 row superblocks (bf16 output, tiled or
 // row-major).
+//
+// Grouped form (the mixture of experts of a prefill): the m-tiles are 256-entry
+// tiles of the experts' entry lists (tile_off from the planner), a tile's
+// weights are its expert's, and its A rows are gathered per lane: the entry's
+// token row of the tiled normed input (gate/up), or the expert's SwiGLU rows
+// (down).  The gate/up epilogue writes SwiGLU rows at the entries' positions;
+// the down epilogue scatters routing weight * product into the per-slot
+// outputs [slot][token][hidden].
 #include "common.h"
 #include "kernels.h"
 
@@ -35,13 +43,15 @@ constexpr int kLgBM = 256, kLgBN = 256, kLgBK = 32, kLgStages = 4;
 constexpr int kLgStageElems = 16 * 512 + 16 * 512;
 constexpr int kLgDmaPerStage = 8;  // direct loads per wave per stage
 
-// EPI 0: out fp32 [M][ldo] = Y;  EPI 1: out += Y;  EPI 2: SwiGLU -> out_bf16
+// EPI 0: out fp32 [M][ldo] = Y;  EPI 1: out += Y;  EPI 2: SwiGLU -> out_bf16;
+// EPI 3 (grouped down): out [slot][token][N] = weight * Y
 // XT 1: X in the tiled activation layout, else row-major with stride ldx
-template <int EPI, int XT>
+// GR 1: grouped (M = the rows of X: tokens for gate/up, entries for down)
+template <int EPI, int XT, int GR>
 __global__ __launch_bounds__(256, 1) void gemm_large_kernel(
     const bf16_t* __restrict__ X, int ldx, int M, const bf16_t* __restrict__ W, int N, int K,
     float* __restrict__ out, int ldo, bf16_t* __restrict__ out_bf16, int out_tiled, int tiles_m,
-    int tiles_n) {
+    int tiles_n, GroupArgs g) {
   __shared__ __attribute__((aligned(1024))) bf16_t smem[kLgStages * kLgStageElems];
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -61,7 +71,25 @@ __global__ __launch_bounds__(256, 1) void gemm_large_kernel(
   const int in_group = t - group * GM * tiles_n;
   const int tm = first_m + in_group % gsize;
   const int tn = in_group / gsize;
-  const int m0 = tm * kLgBM, n0 = tn * kLgBN;
+  int m0 = tm * kLgBM;
+  const int n0 = tn * kLgBN;
+  // grouped: the expert of m-tile tm and the tile's first entry of that expert
+  int rows = M;      // rows of this tile's matrix (the expert's entries)
+  int ent0 = 0;      // first entry of the expert
+  if constexpr (GR) {
+    const int total_m = g.tile_off[g.E];
+    if (tm >= total_m) return;  // uniform over the workgroup, before any barrier
+    int lo = 0, hi = g.E;       // tile_off[lo] <= tm < tile_off[hi]
+    while (hi - lo > 1) {
+      const int mid = (lo + hi) >> 1;
+      if (g.tile_off[mid] <= tm) lo = mid;
+      else hi = mid;
+    }
+    ent0 = g.offsets[lo];
+    rows = g.offsets[lo + 1] - ent0;
+    m0 = (tm - g.tile_off[lo]) * kLgBM;
+    W += (size_t)lo * N * K;
+  }
 
   const int KS = K >> 5;  // 32-column steps = stages
   const int last_blk = (M - 1) >> 4;
@@ -72,8 +100,28 @@ __global__ __launch_bounds__(256, 1) void gemm_large_kernel(
   // over the region it streams (byte offsets stay far below 2^32)
   __amdgpu_buffer_rsrc_t ra[4];
   uint32_t a_voff;  // this lane's byte offset at step 0 (plus 1 KB or 64 B per step)
+  uint32_t g_voff[4];  // grouped: per-lane gathered row offsets (one descriptor)
+  if constexpr (GR) {
+    // one descriptor over the whole X; a row past the tile's entries gets an
+    // offset past the records (the direct load then writes zeros)
+    const uint32_t recs = XT ? (uint32_t)(((M + 15) >> 4) * 16) * K * 2 : (uint32_t)M * ldx * 2;
+    ra[0] = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(X), 0, recs, 0x00020000);
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < 4; ++i) {
+      const int j = m0 + 16 * (4 * wave + i) + (lane & 15);
+      g_voff[i] = 0x80000000u;
+      if (j < rows) {
+        if constexpr (XT) {
+          const int tok = g.assign[ent0 + j] / g.k;
+          g_voff[i] = (uint32_t)(((tok >> 4) * KS * 512 + (16 * (lane >> 4) + (tok & 15)) * 8) * 2);
+        } else {
+          g_voff[i] = (uint32_t)(((size_t)(ent0 + j) * ldx + 8 * (lane >> 4)) * 2);
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < 4 && !GR; ++i) {
     const int blk = min((m0 >> 4) + 4 * wave + i, last_blk);
     if constexpr (XT) {
       ra[i] = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(X + (size_t)blk * KS * 512), 0,
@@ -94,9 +142,15 @@ __global__ __launch_bounds__(256, 1) void gemm_large_kernel(
 
   auto issue_a = [&](int st) {
     bf16_t* so = smem + (st & (kLgStages - 1)) * kLgStageElems;
-    const uint32_t v = a_voff + (XT ? st * 1024u : st * 64u);
+    if constexpr (GR) {
+      const uint32_t dv = XT ? st * 1024u : st * 64u;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) dma16(ra[i], v, so + (4 * wave + i) * 512);
+      for (int i = 0; i < 4; ++i) dma16(ra[0], g_voff[i] + dv, so + (4 * wave + i) * 512);
+    } else {
+      const uint32_t v = a_voff + (XT ? st * 1024u : st * 64u);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) dma16(ra[i], v, so + (4 * wave + i) * 512);
+    }
   };
   auto issue_b = [&](int st) {
     bf16_t* so = smem + (st & (kLgStages - 1)) * kLgStageElems;
@@ -217,14 +271,33 @@ __global__ __launch_bounds__(256, 1) void gemm_large_kernel(
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
           const int row = row_of(mt, e);
-          if (row < M) {
-            const float g = acc[mt][2 * j][e], u = acc[mt][2 * j + 1][e];
-            const float v = g / (1.f + __expf(-g)) * u;
-            const size_t off = out_tiled ? act_tile_offset(row, f, F) : (size_t)row * F + f;
+          if (row < rows) {
+            const float gt = acc[mt][2 * j][e], u = acc[mt][2 * j + 1][e];
+            const float v = gt / (1.f + __expf(-gt)) * u;
+            const size_t off =
+                out_tiled ? act_tile_offset(row, f, F) : (size_t)(ent0 + row) * F + f;
             out_bf16[off] = f32_to_bf16(v);
           }
         }
     }
+  } else if constexpr (EPI == 3) {
+    // grouped down: row = entry ent0 + row of the expert -> (token, slot)
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int row = row_of(mt, e);
+        if (row >= rows) continue;
+        const int asg = g.assign[ent0 + row];
+        const int tok = asg / g.k, slot = asg - tok * g.k;
+        const float wt = g.weights[asg];
+        float* dst = out + ((size_t)slot * g.n + tok) * ldo;
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt) {
+          const int col = n0 + wn * 128 + nt * 32 + col_l;
+          if (col < N) dst[col] = acc[mt][nt][e] * wt;
+        }
+      }
   } else {
     // a whole 32-row m-tile inside M takes the unmasked path; for the update
     // form all 64 old values of an n-tile pair are loaded before any store so
@@ -275,9 +348,10 @@ hipError_t launch_gemm_large(int m, int n_out, int k, int ldx, int x_tiled, int 
   const dim3 grid(tiles_m * tiles_n), block(256);
   float* of = reinterpret_cast<float*>(out);
   bf16_t* ob = reinterpret_cast<bf16_t*>(out);
+  const GroupArgs none{};
 #define SEVO_LG(E, T) \
-  hipLaunchKernelGGL((gemm_large_kernel<E, T>), grid, block, 0, st, x, ldx, m, w, n_out, k, of, \
-                     n_out, ob, out_tiled, tiles_m, tiles_n)
+  hipLaunchKernelGGL((gemm_large_kernel<E, T, 0>), grid, block, 0, st, x, ldx, m, w, n_out, k, of, \
+                     n_out, ob, out_tiled, tiles_m, tiles_n, none)
   if (x_tiled) {
     if (mode == 0) SEVO_LG(0, 1);
     else if (mode == 1) SEVO_LG(1, 1);
@@ -288,6 +362,21 @@ hipError_t launch_gemm_large(int m, int n_out, int k, int ldx, int x_tiled, int 
     else SEVO_LG(2, 0);
   }
 #undef SEVO_LG
+  return hipGetLastError();
+}
+
+hipError_t launch_gemm_grouped(int down, int m, int n_out, int k, const bf16_t* x,
+                               const bf16_t* w, void* out, const GroupArgs& g, int max_tiles_m,
+                               hipStream_t st) {
+  if (m == 0 || max_tiles_m == 0) return hipSuccess;
+  const int tiles_n = (n_out + kLgBN - 1) / kLgBN;
+  const dim3 grid(max_tiles_m * tiles_n), block(256);
+  if (down)
+    hipLaunchKernelGGL((gemm_large_kernel<3, 0, 1>), grid, block, 0, st, x, k, m, w, n_out, k,
+                       static_cast<float*>(out), n_out, nullptr, 0, max_tiles_m, tiles_n, g);
+  else
+    hipLaunchKernelGGL((gemm_large_kernel<2, 1, 1>), grid, block, 0, st, x, k, m, w, n_out, k,
+                       nullptr, n_out, static_cast<bf16_t*>(out), 0, max_tiles_m, tiles_n, g);
   return hipGetLastError();
 }
 

@@ -87,6 +87,8 @@ struct PrefillAttnArgs {
 hipError_t launch_attn_prefill(const PrefillAttnArgs& a, hipStream_t st);
 
 // ---- moe.hip: mixture-of-experts FFN of a decode step
+constexpr int kMoeGroupRows = 256;  // rows per tile of the grouped large-M GEMM
+
 struct MoeExpertArgs {
   int n, hidden, ffn, n_experts, top_k;
   const bf16_t* x;          // normed input, tiled [n][hidden]
@@ -102,8 +104,13 @@ bool moe_supported(int n_experts, int top_k, int expert_ffn, int hidden);
 // logits = sum of S split partials [S][n][E]; sel / w [n][k]
 hipError_t launch_moe_route(const float* part, int S, int n, int E, int k, int32_t* sel,
                             float* w, hipStream_t st);
+// out [n][H] = sum of the k slot partials [k][n][H] in slot order
+hipError_t launch_moe_sum_slots(const float* part, int k, int n, int H, float* out,
+                                hipStream_t st);
+// offsets [E + 1], assign [nk] (entries expert-major, token order); with
+// tile_off [E + 1]: each expert's first 256-entry tile (grouped GEMM)
 hipError_t launch_moe_plan(const int32_t* sel, int nk, int E, int32_t* offsets, int32_t* assign,
-                           hipStream_t st);
+                           hipStream_t st, int32_t* tile_off = nullptr);
 // gate/up + SwiGLU into act, then down into part
 hipError_t launch_moe_experts(const MoeExpertArgs& a, hipStream_t st);
 
@@ -130,6 +137,23 @@ hipError_t launch_linear_partials(int m, int n_out, int k, int ldx, int x_tiled,
 // same operand layouts and epilogue modes as launch_linear (no workspace)
 constexpr int kLargeGemmMinM = 256;
 bool gemm_large_supported(int m, int n_out, int k);
+// grouped form (mixture of experts): m-tiles are 256-entry tiles of the
+// experts' entry lists; the expert's weights at w + e n_out k
+struct GroupArgs {
+  const int32_t* offsets = nullptr;   // [E + 1] entry offsets
+  const int32_t* assign = nullptr;    // [n k] entries t * k + slot
+  const int32_t* tile_off = nullptr;  // [E + 1] first tile of each expert
+  const float* weights = nullptr;     // [n k] routing weights (down)
+  int E = 0, k = 1, n = 0;            // experts, top-k, tokens
+};
+// down 0: gate/up of every entry, x = the tiled normed input (m = tokens),
+//   out bf16 act [n k][n_out / 2] at the entry positions (SwiGLU);
+// down 1: x = act [n k][k] row-major (m = n k entries), out fp32
+//   [k slots][n][n_out] = weight * product.  max_tiles_m >= sum of the
+//   experts' tile counts (n k / 256 + E).
+hipError_t launch_gemm_grouped(int down, int m, int n_out, int k, const bf16_t* x,
+                               const bf16_t* w, void* out, const GroupArgs& g, int max_tiles_m,
+                               hipStream_t st);
 hipError_t launch_gemm_large(int m, int n_out, int k, int ldx, int x_tiled, int mode,
                              const bf16_t* x, const bf16_t* w, void* out, int out_tiled,
                              hipStream_t st);

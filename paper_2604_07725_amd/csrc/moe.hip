@@ -16,6 +16,8 @@
 //     through the expert's entry list.  Gate/up writes silu(g) * u per entry
 //     (bf16, row-major); down writes w * y into partial [slot][token][hidden]
 //     (fp32), which the next residual add + RMSNorm sums in slot order.
+#include <algorithm>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -108,7 +110,8 @@ constexpr int kPlanWords = kPlanThreads / 32;
 __global__ __launch_bounds__(kPlanThreads) void moe_plan_kernel(const int32_t* __restrict__ sel,
                                                                 int nk, int E,
                                                                 int32_t* __restrict__ offsets,
-                                                                int32_t* __restrict__ assign) {
+                                                                int32_t* __restrict__ assign,
+                                                                int32_t* __restrict__ tile_off) {
   __shared__ int cnt[kMoeMaxExperts];
   __shared__ int base[kMoeMaxExperts];
   __shared__ uint32_t bits[kMoeMaxExperts][kPlanWords];
@@ -121,31 +124,44 @@ __global__ __launch_bounds__(kPlanThreads) void moe_plan_kernel(const int32_t* _
   }
   __syncthreads();
   if (tid < 64) {
-    // exclusive prefix over the experts: lane j scans experts 4j..4j+3 (E <= 256)
-    int v[4], sum = 0;
+    // exclusive prefixes over the experts (lane j scans experts 4j..4j+3,
+    // E <= 256): entry offsets, and (tile_off) the first 256-entry tile of
+    // each expert for the grouped large-M GEMM
+    int v[4], tv[4], sum = 0, tsum = 0;
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       const int e = 4 * tid + u;
       v[u] = e < E ? cnt[e] : 0;
+      tv[u] = (v[u] + kMoeGroupRows - 1) / kMoeGroupRows;
       sum += v[u];
+      tsum += tv[u];
     }
-    int incl = sum;
+    int incl = sum, tincl = tsum;
 #pragma unroll
     for (int o = 1; o < 64; o <<= 1) {
       const int y = __shfl_up(incl, o, kWave);
-      if (tid >= o) incl += y;
+      const int ty = __shfl_up(tincl, o, kWave);
+      if (tid >= o) {
+        incl += y;
+        tincl += ty;
+      }
     }
-    int run = incl - sum;
+    int run = incl - sum, trun = tincl - tsum;
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       const int e = 4 * tid + u;
       if (e < E) {
         base[e] = run;
         offsets[e] = run;
+        if (tile_off) tile_off[e] = trun;
       }
       run += v[u];
+      trun += tv[u];
     }
-    if (tid == 63) offsets[E] = incl;
+    if (tid == 63) {
+      offsets[E] = incl;
+      if (tile_off) tile_off[E] = tincl;
+    }
   }
   for (int c0 = 0; c0 < nk; c0 += kPlanThreads) {
     for (int w = tid; w < E * kPlanWords; w += kPlanThreads) (&bits[0][0])[w] = 0u;
@@ -309,6 +325,31 @@ __global__ __launch_bounds__(256) void moe_expert_kernel(MoeExpertArgs a) {
   }
 }
 
+// Sum of the k slot partials of each row, in slot order: out [n][H] (row
+// stride ldo) = sum over j of part [j][n][H].  The prefill's chunks write
+// their rows of the residual update this way.
+__global__ __launch_bounds__(256) void moe_sum_slots_kernel(const float* __restrict__ part,
+                                                            int k, int n, int H,
+                                                            float* __restrict__ out) {
+  const size_t total4 = (size_t)n * H / 4;
+  const size_t plane = (size_t)n * H;
+  for (size_t g = (size_t)blockIdx.x * blockDim.x + threadIdx.x; g < total4;
+       g += (size_t)gridDim.x * blockDim.x) {
+    f32x4 acc = *reinterpret_cast<const f32x4*>(part + g * 4);
+    for (int j = 1; j < k; ++j) acc += *reinterpret_cast<const f32x4*>(part + j * plane + g * 4);
+    *reinterpret_cast<f32x4*>(out + g * 4) = acc;
+  }
+}
+
+hipError_t launch_moe_sum_slots(const float* part, int k, int n, int H, float* out,
+                                hipStream_t st) {
+  if (n == 0) return hipSuccess;
+  const size_t total4 = (size_t)n * H / 4;
+  const int grid = (int)std::min<size_t>((total4 + 255) / 256, 4096);
+  hipLaunchKernelGGL(moe_sum_slots_kernel, dim3(grid), dim3(256), 0, st, part, k, n, H, out);
+  return hipGetLastError();
+}
+
 bool moe_supported(int E, int top_k, int ffn, int hidden) {
   return E >= 64 && E <= kMoeMaxExperts && E % 64 == 0 && top_k >= 1 && top_k <= kMoeMaxTopK &&
          top_k <= E && ffn >= 32 && ffn % 32 == 0 && hidden % 64 == 0;
@@ -322,9 +363,9 @@ hipError_t launch_moe_route(const float* part, int S, int n, int E, int k, int32
 }
 
 hipError_t launch_moe_plan(const int32_t* sel, int nk, int E, int32_t* offsets, int32_t* assign,
-                           hipStream_t st) {
+                           hipStream_t st, int32_t* tile_off) {
   hipLaunchKernelGGL(moe_plan_kernel, dim3(1), dim3(kPlanThreads), 0, st, sel, nk, E, offsets,
-                     assign);
+                     assign, tile_off);
   return hipGetLastError();
 }
 

@@ -891,12 +891,18 @@ namespace {
 
 constexpr int kPrefillLogitRows = 4096;  // scored rows per LM-head chunk
 
+constexpr int kPrefillMoeRows = 16384;  // tokens per MoE FFN chunk (a multiple of 16)
+
 struct PrefillLayout {
   size_t row, pos, x, h, qkv, q, o, a, part, hf, logits, sample, conf, ids, lps, total;
+  // MoE FFN, one token chunk at a time: router logits, routing, entry lists,
+  // SwiGLU rows, per-slot outputs
+  size_t m_router, m_sel, m_w, m_off, m_assign, m_act, m_slots, m_tiles;
   int rc;  // rows per LM-head chunk
+  int mc;  // tokens per MoE chunk
 };
 
-PrefillLayout prefill_layout(const sevo_model_config& c, int T, int R) {
+PrefillLayout prefill_layout(const sevo_model_config& c, int T, int R, int moe_chunk = 0) {
   PrefillLayout L;
   const size_t H = c.hidden, F = c.ffn, V = c.vocab;
   const size_t qd = (size_t)c.n_q_heads * c.head_dim;
@@ -918,6 +924,23 @@ PrefillLayout prefill_layout(const sevo_model_config& c, int T, int R) {
   L.o = take(t16 * qd * 2);
   L.a = take(t16 * F * 2);
   L.part = take(t * H * 4);
+  L.mc = 0;
+  L.m_router = L.m_sel = L.m_w = L.m_off = L.m_assign = L.m_act = L.m_slots = L.m_tiles = 0;
+  if (c.n_experts > 0) {
+    size_t mc = moe_chunk > 0 && moe_chunk < kPrefillMoeRows ? round_up(moe_chunk, 16)
+                                                              : (size_t)kPrefillMoeRows;
+    if (mc > t16) mc = t16;
+    const size_t kk = c.n_experts_active, E = c.n_experts;
+    L.mc = (int)mc;
+    L.m_router = take(mc * E * 4);
+    L.m_sel = take(mc * kk * 4);
+    L.m_w = take(mc * kk * 4);
+    L.m_off = take((E + 1) * 4);
+    L.m_assign = take(mc * kk * 4);
+    L.m_act = take(mc * kk * c.expert_ffn * 2);
+    L.m_slots = take(kk * mc * H * 4);
+    L.m_tiles = take((E + 1) * 4);
+  }
   L.hf = take(rc16 * H * 2);
   L.logits = take(rc * V * 4);
   L.sample = take(sevo::sample_workspace_bytes(L.rc, c.vocab));
@@ -939,6 +962,69 @@ hipError_t prefill_gemm(int m, int n_out, int k, int mode, const sevo::bf16_t* x
   return sevo::launch_linear(m, n_out, k, k, 1, mode, p, x, wb, out, out_tiled, nullptr, st);
 }
 
+// Entries per expert (n k / E on average) from which a prefill chunk's experts
+// run as grouped large-M GEMMs (256-entry tiles, each expert's weights read
+// once per tile) instead of the decode kernels (16-64-row tiles).
+constexpr int kPrefillGroupedMinPerExpert = 32;
+
+// The MoE FFN of prefill rows c0 .. c0 + nc (c0 a multiple of 16) on the tiled
+// normed input h: router GEMM, top-k, entry lists, expert gate/up + down into
+// per-slot outputs, then part[c0 + i] = their slot-order sum.
+hipError_t run_moe_prefill_chunk(const sevo_model* m, int l, int c0, int nc,
+                                 const sevo::bf16_t* h, char* ws, const PrefillLayout& L,
+                                 float* part, hipStream_t st) {
+  const sevo_model_config& c = m->cfg;
+  const int H = c.hidden, E = c.n_experts, k = c.n_experts_active;
+  const sevo::bf16_t* hc = h + (size_t)(c0 / 16) * (H / 32) * 512;  // 16-row blocks
+  float* rl = reinterpret_cast<float*>(ws + L.m_router);
+  int32_t* sel = reinterpret_cast<int32_t*>(ws + L.m_sel);
+  float* wts = reinterpret_cast<float*>(ws + L.m_w);
+  int32_t* off = reinterpret_cast<int32_t*>(ws + L.m_off);
+  int32_t* asg = reinterpret_cast<int32_t*>(ws + L.m_assign);
+  float* slots = reinterpret_cast<float*>(ws + L.m_slots);
+  int32_t* tiles = reinterpret_cast<int32_t*>(ws + L.m_tiles);
+  const bool grouped = (long long)nc * k >= (long long)kPrefillGroupedMinPerExpert * E;
+  hipError_t e;
+  {
+    ProfScope ps(SEVO_PROF_MOE_ROUTE, st);
+    e = prefill_gemm(nc, E, H, SEVO_LINEAR_STORE, hc, m->w_router[l], rl, 0, st);
+    if (e == hipSuccess) e = sevo::launch_moe_route(rl, 1, nc, E, k, sel, wts, st);
+    if (e == hipSuccess)
+      e = sevo::launch_moe_plan(sel, nc * k, E, off, asg, st, grouped ? tiles : nullptr);
+  }
+  if (e != hipSuccess) return e;
+  ProfScope ps(SEVO_PROF_MOE_EXPERTS, st);
+  if (grouped) {
+    sevo::GroupArgs g;
+    g.offsets = off; g.assign = asg; g.tile_off = tiles; g.weights = wts;
+    g.E = E; g.k = k; g.n = nc;
+    const int max_tiles = (nc * k + sevo::kMoeGroupRows - 1) / sevo::kMoeGroupRows + E;
+    sevo::bf16_t* act = reinterpret_cast<sevo::bf16_t*>(ws + L.m_act);
+    e = sevo::launch_gemm_grouped(0, nc, 2 * c.expert_ffn, H, hc,
+                                  static_cast<const sevo::bf16_t*>(m->w_expert_gate_up[l]), act,
+                                  g, max_tiles, st);
+    if (e == hipSuccess)
+      e = sevo::launch_gemm_grouped(1, nc * k, H, c.expert_ffn, act,
+                                    static_cast<const sevo::bf16_t*>(m->w_expert_down[l]), slots,
+                                    g, max_tiles, st);
+    if (e == hipSuccess)
+      e = sevo::launch_moe_sum_slots(slots, k, nc, H, part + (size_t)c0 * H, st);
+    return e;
+  }
+  sevo::MoeExpertArgs ma;
+  ma.n = nc; ma.hidden = H; ma.ffn = c.expert_ffn; ma.n_experts = E; ma.top_k = k; ma.x = hc;
+  ma.w_gate_up = static_cast<const sevo::bf16_t*>(m->w_expert_gate_up[l]);
+  ma.w_down = static_cast<const sevo::bf16_t*>(m->w_expert_down[l]);
+  ma.offsets = off;
+  ma.assign = asg;
+  ma.weights = wts;
+  ma.act = reinterpret_cast<sevo::bf16_t*>(ws + L.m_act);
+  ma.part = slots;
+  e = sevo::launch_moe_experts(ma, st);
+  if (e == hipSuccess) e = sevo::launch_moe_sum_slots(slots, k, nc, H, part + (size_t)c0 * H, st);
+  return e;
+}
+
 }  // namespace
 
 SEVO_API size_t sevo_prefill_workspace_bytes(const sevo_model* m, int32_t total_tokens,
@@ -951,8 +1037,6 @@ SEVO_API sevo_status sevo_prefill_confidence(sevo_model* m, const sevo_prefill_a
                                              void* stream) {
   if (!m || !a) return fail(SEVO_ERR_INVALID_ARGUMENT, "null model or args");
   const sevo_model_config& c = m->cfg;
-  if (c.n_experts > 0)
-    return fail(SEVO_ERR_UNSUPPORTED, "the prefill path takes dense-FFN models only");
   if (a->n_seqs < 1 || a->total_tokens < 0 || a->max_seq_len < 0 || a->max_pages < 1 ||
       a->num_pages < 1)
     return fail(SEVO_ERR_INVALID_ARGUMENT,
@@ -980,7 +1064,7 @@ SEVO_API sevo_status sevo_prefill_confidence(sevo_model* m, const sevo_prefill_a
   for (int l = 0; l < c.n_layers; ++l)
     if (!a->kv_pools[l] || !aligned16(a->kv_pools[l]))
       return fail(SEVO_ERR_INVALID_ARGUMENT, "layer %d: null or misaligned KV pool", l);
-  const PrefillLayout L = prefill_layout(c, T, R);
+  const PrefillLayout L = prefill_layout(c, T, R, a->moe_chunk);
   if (a->workspace_bytes < L.total)
     return fail(SEVO_ERR_WORKSPACE_TOO_SMALL, "prefill needs %zu workspace bytes, got %zu",
                 L.total, a->workspace_bytes);
@@ -1053,13 +1137,22 @@ SEVO_API sevo_status sevo_prefill_confidence(sevo_model* m, const sevo_prefill_a
       e = sevo::launch_add_rmsnorm(x, part, 1, static_cast<const sevo::bf16_t*>(m->ffn_norm[l]),
                                    T, H, c.rms_eps, h, st);
     }
-    if (e == hipSuccess) {
-      ProfScope ps(SEVO_PROF_GATE_UP, st);
-      e = prefill_gemm(T, 2 * F, H, SEVO_LINEAR_SWIGLU, h, m->w_gate_up[l], act, 1, st);
-    }
-    if (e == hipSuccess) {
-      ProfScope ps(SEVO_PROF_DOWN, st);
-      e = prefill_gemm(T, H, F, SEVO_LINEAR_STORE, act, m->w_down[l], part, 0, st);
+    if (c.n_experts > 0) {
+      // the mixture of experts, a chunk of tokens at a time: per-slot outputs
+      // of the chunk, then their slot-order sum into its rows of `part`
+      for (int c0 = 0; c0 < T && e == hipSuccess; c0 += L.mc) {
+        const int nc = T - c0 < L.mc ? T - c0 : L.mc;
+        e = run_moe_prefill_chunk(m, l, c0, nc, h, ws, L, part, st);
+      }
+    } else {
+      if (e == hipSuccess) {
+        ProfScope ps(SEVO_PROF_GATE_UP, st);
+        e = prefill_gemm(T, 2 * F, H, SEVO_LINEAR_SWIGLU, h, m->w_gate_up[l], act, 1, st);
+      }
+      if (e == hipSuccess) {
+        ProfScope ps(SEVO_PROF_DOWN, st);
+        e = prefill_gemm(T, H, F, SEVO_LINEAR_STORE, act, m->w_down[l], part, 0, st);
+      }
     }
     if (e != hipSuccess) return hip_fail(e, "prefill (layer)");
   }

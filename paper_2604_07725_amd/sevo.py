@@ -75,7 +75,7 @@ class PrefillArgs(C.Structure):
                 ("seq_starts", vp), ("start_pos", vp), ("page_table", vp), ("max_pages", i32),
                 ("num_pages", i64), ("kv_pools", C.POINTER(vp)), ("conf_topk", i32),
                 ("n_scored", i32), ("scored_rows", vp), ("out_conf", vp), ("out_row_conf", vp),
-                ("workspace", vp), ("workspace_bytes", sz)]
+                ("workspace", vp), ("workspace_bytes", sz), ("moe_chunk", i32)]
 
 
 class SampleArgs(C.Structure):
@@ -537,7 +537,8 @@ class PrefillBuffers:
     workspace is allocated once; ``run`` only enqueues kernels)."""
 
     def __init__(self, model: Model, tokens, seq_starts, page_table, kv_pools, scored_rows,
-                 conf_topk, max_seq_len, start_pos=None, keep_row_conf=True, workspace=None):
+                 conf_topk, max_seq_len, start_pos=None, keep_row_conf=True, workspace=None,
+                 moe_chunk=0):
         T = tokens.shape[0]
         n_seqs = seq_starts.shape[0] - 1
         dev = tokens.device
@@ -560,7 +561,7 @@ class PrefillBuffers:
             kv_pools=C.cast(self._kv, C.POINTER(vp)), conf_topk=int(conf_topk), n_scored=R,
             scored_rows=_p(scored_rows), out_conf=_p(self.out_conf),
             out_row_conf=_p(self.out_row_conf), workspace=_p(self.workspace),
-            workspace_bytes=self.workspace.numel())
+            workspace_bytes=self.workspace.numel(), moe_chunk=int(moe_chunk))
 
     def run(self, stream=None):
         _check(lib().sevo_prefill_confidence(self.model.handle, C.byref(self.args),

@@ -51,7 +51,7 @@ int main(void) {
   S(sevo_prefill_args) P(sevo_prefill_args, tokens) P(sevo_prefill_args, max_pages)
   P(sevo_prefill_args, num_pages) P(sevo_prefill_args, kv_pools) P(sevo_prefill_args, conf_topk)
   P(sevo_prefill_args, scored_rows) P(sevo_prefill_args, out_row_conf)
-  P(sevo_prefill_args, workspace_bytes)
+  P(sevo_prefill_args, workspace_bytes) P(sevo_prefill_args, moe_chunk)
   return 0;
 }
 """

@@ -105,7 +105,7 @@ def _token_major(pool, d):
             pool[:, :, 1, :][:, :, e * 16 + s])
 
 
-def _engine_case(S, shape, seed, lens, scored, conf_k, starts=None):
+def _engine_case(S, shape, seed, lens, scored, conf_k, starts=None, moe_chunk=0):
     """Run the confidence engine on the GPU; returns its outputs and the inputs
     the oracle needs (host side)."""
     sevo, di = S
@@ -123,7 +123,8 @@ def _engine_case(S, shape, seed, lens, scored, conf_k, starts=None):
                               torch.from_numpy(pop.page_table.astype(np.int32)).cuda(), kvp,
                               torch.from_numpy(np.asarray(scored, np.int32)).cuda(), conf_k,
                               int(lens.max()),
-                              start_pos=torch.from_numpy(starts.astype(np.int32)).cuda())
+                              start_pos=torch.from_numpy(starts.astype(np.int32)).cuda(),
+                              moe_chunk=moe_chunk)
     conf = buf.run()
     torch.cuda.synchronize()
     out = (conf.cpu().numpy().astype(np.float64),
@@ -202,5 +203,62 @@ def test_prefill_confidence_full_width_reduced_depth(S):
     say(f"  row c max err {row_err:.2e} (c in [{c.min():.3f}, {c.max():.3f}]); C {g_conf} vs "
         f"{conf}")
     # the full-width end-to-end bar of the decode step (bf16 storage flips)
+    assert row_err <= 6e-2
+    assert np.abs(g_conf - conf).max() <= 3e-2
+
+
+@pytest.mark.parametrize("lens,moe_chunk", [([300, 170], 0), ([300, 170], 64),
+                                            ([400, 300], 0), ([400, 300], 512)])
+def test_prefill_confidence_tiny_moe_matches_oracle(S, lens, moe_chunk):
+    """The tiny MoE model (2 layers, 64 experts of FFN 64, top-4) through the
+    whole engine: per-row c, per-sequence C against the oracle's prefill.  The
+    expert FFN runs in one chunk or in several (the last one partial); 470
+    tokens take the decode expert kernels, 700 tokens (>= 32 entries per
+    expert) the grouped large-M GEMMs, and 512 + 188 one of each.  The inputs
+    have no routing choice closer than 1e-5."""
+    shape = synth.TINY_MOE
+    seed = 9
+    T = sum(lens)
+    scored = list(range(40, lens[0])) + list(range(lens[0] + 20, T))
+    say(f"prefill confidence (tiny MoE, {lens}, chunk {moe_chunk})")
+    (g_conf, g_row, _), pop, toks, seq_starts, starts = _engine_case(
+        S, shape, seed, lens, scored, 20, moe_chunk=moe_chunk)
+    hw = synth.host_weights(shape, seed)
+    hkv = [p.astype(np.float64) for p in synth.host_pools(shape, seed, pop.n_pages)]
+    stats = {}
+    conf, c, _ = od.prefill_confidence(shape, hw, hkv, pop.page_table, toks, seq_starts, scored,
+                                       20, stats=stats)
+    row_err = np.abs(g_row - c).max()
+    say(f"  row c max err {row_err:.2e}; C {g_conf} vs {conf}; route gap {stats['route_gap']:.2e}")
+    assert stats["route_gap"] > 1e-5, "test input has a routing near-tie"
+    assert row_err <= 2e-2
+    assert np.abs(g_conf - conf).max() <= 1e-2
+
+
+@pytest.mark.parametrize("moe_chunk", [0, 256])
+def test_prefill_confidence_moe30b_reduced_depth(S, moe_chunk):
+    """The 30B-A3B-class MoE widths (hidden 2048, 32/4 heads, 128 experts of
+    FFN 768, top-8, vocab 151936) at 2 layers, two sequences of 400 and 200
+    tokens, 32 scored rows; the expert FFN in one chunk (37.5 entries per
+    expert: the grouped large-M GEMMs) or in 256-token chunks (the decode
+    expert kernels)."""
+    import dataclasses
+    shape = dataclasses.replace(synth.MOE_30B_A3B, n_layers=2)
+    lens = [400, 200]
+    scored = sorted(set(np.linspace(0, 599, 32).astype(int).tolist()))
+    say("prefill confidence (30B-A3B widths, 2 layers)")
+    (g_conf, g_row, _), pop, toks, seq_starts, starts = _engine_case(
+        S, shape, 10, lens, scored, 20, moe_chunk=moe_chunk)
+    torch.cuda.empty_cache()
+    hw = synth.host_weights(shape, 10, lazy=True)
+    hw = {"embed": hw["embed"], "final_norm": hw["final_norm"], "layers": hw["layers"],
+          "lm_head": hw["lm_head"][0:shape.vocab]}
+    hkv = [p.astype(np.float64) for p in synth.host_pools(shape, 10, pop.n_pages)]
+    stats = {}
+    conf, c, _ = od.prefill_confidence(shape, hw, hkv, pop.page_table, toks, seq_starts, scored,
+                                       20, stats=stats)
+    row_err = np.abs(g_row - c).max()
+    say(f"  row c max err {row_err:.2e}; C {g_conf} vs {conf}; route gap {stats['route_gap']:.2e}")
+    assert stats["route_gap"] > 1e-5, "test input has a routing near-tie"
     assert row_err <= 6e-2
     assert np.abs(g_conf - conf).max() <= 3e-2
