@@ -314,6 +314,9 @@ def cpu_baseline(w, pop, n_sample, budget_s=30.0):
 
 
 PREFILL_GEMM_KINDS = ("qkv", "attn_out", "gate_up", "down", "moe_route", "moe_experts")
+# the paper's confidence-engine latency for Qwen3-30B-A3B (the shapes of the MoE
+# stand-in), seconds per request at each length: another machine's figures
+PAPER_ENGINE_S_QWEN3_30B_A3B = {40960: 1.58, 81920: 4.42, 122880: 8.41}
 
 
 def prefill_flops(shape, T, R):
@@ -444,7 +447,8 @@ def prefill_main(args):
         "value": big["s_per_request"], "unit": "s", "higher_is_better": False,
         "n_gpus": 1, "steps": args.steps if args.steps < 16 else 2, "warmup": 1,
         "dtype": "bf16", "data": "synthetic (seeded; random-init weights)",
-        "vs_baseline": None,
+        "vs_baseline": (big["s_per_request"] / PAPER_ENGINE_S_QWEN3_30B_A3B[big["tokens"]]
+                        if moe and big["tokens"] in PAPER_ENGINE_S_QWEN3_30B_A3B else None),
         "config": {"workload": "confidence_engine_" + ("moe30b" if moe else "dense8b"),
                    "model": model_name(shape), "layers": shape.n_layers,
                    "hidden": shape.hidden,
