@@ -584,15 +584,16 @@ def main():
 
     if not args.graph:
         sevo.sevo_profile_begin(shape.n_layers * args.steps, ("attn_split", "attn_combine"))
-    start = torch.cuda.Event(enable_timing=True)
-    stop = torch.cuda.Event(enable_timing=True)
+    # one event per step boundary (median and spread of the step time)
+    marks = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     torch.cuda.synchronize()
-    start.record()
-    for _ in range(args.steps):
+    marks[0].record()
+    for i in range(args.steps):
         step()
-    stop.record()
+        marks[i + 1].record()
     torch.cuda.synchronize()
-    total_ms = start.elapsed_time(stop)
+    total_ms = marks[0].elapsed_time(marks[-1])
+    step_ms = np.array([marks[i].elapsed_time(marks[i + 1]) for i in range(args.steps)])
     if args.graph:
         # the replayed graph records no per-launch events: time the attention
         # launches over as many eager steps
@@ -631,6 +632,8 @@ def main():
         "unit": "tokens/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": ms_per_step,
+        "ms_per_step_median": float(np.median(step_ms)),
+        "ms_per_step_min_max": [float(step_ms.min()), float(step_ms.max())],
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16", "data": "synthetic (seeded; random-init weights)",
         "config": {"workload": w.name, "model": model_name(shape), "layers": shape.n_layers,

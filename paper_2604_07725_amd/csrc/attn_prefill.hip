@@ -5,10 +5,11 @@
 //
 //   * one workgroup of NW waves per (sequence, NW query units, kv head); a
 //     unit is one query head of the kv head's group over 32 NQT consecutive
-//     tokens, and each wave owns one unit.  The shipped shape is 8 waves of
-//     32 queries: 173 registers per wave, so two waves share each SIMD and one
-//     wave's MFMAs overlap the other's softmax (4 waves of 64 queries, one per
-//     SIMD, measured 16% slower and a hand-pipelined single wave spilled);
+//     tokens, and each wave owns one unit.  The shipped shape is 12 waves of
+//     32 queries: 162 registers per wave, so three waves share each SIMD and
+//     the MFMAs of one overlap the softmax of the others (8 waves, two per
+//     SIMD, measured 5% slower; 16 waves spill; 4 waves of 64 queries, one per
+//     SIMD, 16% slower than 8, and a hand-pipelined single wave spilled);
 //   * scores are computed transposed, S^T = K Q^T, with 32x32x16 bf16 MFMAs:
 //     a lane then holds one query (lane % 32) and 16 of each 32-key tile's
 //     scores, so the online-softmax max and sum are in-lane plus one
@@ -19,8 +20,8 @@
 //   * O^T = V^T P^T with the same instruction; P^T's B operand is made from
 //     the score accumulators by one permlane32 swap per 8 keys (no LDS);
 //   * keys stream in blocks of 64 (4 pages) straight into LDS with direct
-//     loads through a per-page buffer descriptor (two waves per page: one K
-//     tile, one V tile) -- a page id outside the pool, or a page past the
+//     loads through a per-page buffer descriptor (waves 0-7, two per page: one
+//     K tile, one V tile) -- a page id outside the pool, or a page past the
 //     workgroup's keys, gets zero records and reads zeros; four LDS stages
 //     hold the block being multiplied and up to three more in flight;
 //   * LDS holds the tiles with their 16-byte chunks XOR-swizzled (within each
@@ -40,7 +41,7 @@ namespace sevo {
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 constexpr int kPfStages = 4;
-constexpr int kPfWaves = 8;      // waves per workgroup
+constexpr int kPfWaves = 12;     // waves per workgroup
 constexpr int kPfQueryTiles = 1; // 32-query tiles per wave
 
 // K tile block (16 slots x 32 dims, 1 KB): chunk (slot s, dim quarter q) at
@@ -92,6 +93,7 @@ __global__ __launch_bounds__(64 * NW, 1) void attn_prefill_kernel(PrefillAttnArg
         const_cast<bf16_t*>(a.kv_pool + (ok ? ((size_t)page * a.hkv + c) * PAGE_ELEMS : 0)), 0,
         ok ? PAGE_ELEMS * 2 : 0, 0x00020000);
     bf16_t* dst = smem + (b % kPfStages) * STAGE_ELEMS + (NW == 4 ? wave : wave >> 1) * PAGE_ELEMS;
+    if (NW > 8 && wave >= 8) return;  // waves 8.. load nothing
     if (NW == 4 || (wave & 1) == 0) {
 #pragma unroll
       for (int kb = 0; kb < KB; ++kb) dma16(r, k_src + kb * 1024, dst + kb * 512);
