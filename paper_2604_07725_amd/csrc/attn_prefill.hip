@@ -32,7 +32,8 @@
 //     loads its part of the block and meets the barriers); workgroups are
 //     launched latest (longest) query blocks first.
 // P is rounded to bf16 for the P V product (fp32 accumulation); the softmax
-// statistics stay fp32.
+// statistics stay fp32.  The exponentials are the bare hardware exp2 (results
+// below 2^-126 flush to zero; a row's running max keeps its sum >= 2^-8).
 #include "common.h"
 #include "kernels.h"
 
@@ -178,7 +179,7 @@ __global__ __launch_bounds__(64 * NW, 1) void attn_prefill_kernel(PrefillAttnArg
         mx = xor32_max(mx) * sl2;
         if (__any(mx > m_run[qt] + 8.f)) {
           const float m_new = fmaxf(m_run[qt], mx);
-          const float alpha = exp2f(m_run[qt] - m_new);
+          const float alpha = __builtin_amdgcn_exp2f(m_run[qt] - m_new);
           m_run[qt] = m_new;
           l_run[qt] *= alpha;
 #pragma unroll
@@ -190,7 +191,7 @@ __global__ __launch_bounds__(64 * NW, 1) void attn_prefill_kernel(PrefillAttnArg
         for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
           for (int e = 0; e < 16; ++e) {
-            const float p = exp2f(__builtin_fmaf(acc_s[kt][qt][e], sl2, nm));
+            const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(acc_s[kt][qt][e], sl2, nm));
             acc_s[kt][qt][e] = p;
             sum += p;
           }
