@@ -161,12 +161,10 @@ __global__ __launch_bounds__(256, 1) void gemm_large_kernel(
   // wait until stage st has landed.  When it is waited for, stage st + 1 is
   // fully issued and stage st + 2 only its A half (issue_b of a stage follows
   // the barrier), so up to 8 + 4 younger loads may stay outstanding.
-  auto wait_stage = [&](int st) {
-    const int after = min(2, KS - 1 - st);  // < 0 past the last stage
-    if (after >= 2) wait_vmcnt<kLgDmaPerStage + kLgDmaPerStage / 2>();
-    else if (after == 1) wait_vmcnt<kLgDmaPerStage>();
-    else wait_vmcnt<0>();
-  };
+  // every iteration issues a full stage (stages past the last one load zeros
+  // or unused rows into a buffer nobody reads again), so when stage st is
+  // waited for, stage st + 1 is fully issued and st + 2 only its A half
+  auto wait_stage = [&](int) { wait_vmcnt<kLgDmaPerStage + kLgDmaPerStage / 2>(); };
 
   f32x16 acc[4][4];
 #pragma unroll
@@ -226,31 +224,28 @@ __global__ __launch_bounds__(256, 1) void gemm_large_kernel(
     __builtin_amdgcn_sched_group_barrier(0x8, 8, 0);
   };
   Frags f0, f1;
-  for (int st = 0; st < 3 && st < KS; ++st) {
+  for (int st = 0; st < 3; ++st) {
     issue_a(st);
     issue_b(st);
   }
-  if (KS >= 3) wait_vmcnt<2 * kLgDmaPerStage>();  // stage 0 landed
-  else if (KS == 2) wait_vmcnt<kLgDmaPerStage>();
-  else wait_vmcnt<0>();
+  wait_vmcnt<2 * kLgDmaPerStage>();  // stage 0 landed
   lds_barrier();
   read(f0, 0, 0);
   for (int kt = 0; kt < KS; ++kt) {
-    const bool more = kt + 3 < KS;
-    if (more) issue_a(kt + 3);
+    issue_a(kt + 3);
     read(f1, kt, 1);
     mma(f0);
-    interleave(more ? 4 : 0);
+    interleave(4);
     __builtin_amdgcn_sched_barrier(0);
     // (after the last stage this reads a stale buffer that is never used:
     // keeping the step unconditional keeps the LDS reads interleaved)
     wait_stage(kt + 1);
     wait_lgkm0();
     lds_barrier();
-    if (more) issue_b(kt + 3);
+    issue_b(kt + 3);
     read(f0, kt + 1, 0);
     mma(f1);
-    interleave(more ? 4 : 0);
+    interleave(4);
     __builtin_amdgcn_sched_barrier(0);
   }
   wait_vmcnt<0>();
