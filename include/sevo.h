@@ -280,7 +280,8 @@ typedef struct {
   void* workspace;
   size_t workspace_bytes;
   int32_t moe_chunk;  /* MoE models: tokens per expert-FFN chunk, 0 = 16384 (the
-                         largest; sevo_prefill_workspace_bytes sizes for it) */
+                         largest; sevo_prefill_workspace_bytes sizes for it);
+                         negative: INVALID_ARGUMENT */
 } sevo_prefill_args;
 
 sevo_status sevo_prefill_confidence(sevo_model* m, const sevo_prefill_args* a, void* stream);
@@ -476,7 +477,7 @@ sevo_status sevo_qk_norm_rope_append(const sevo_model* m, int32_t layer, const f
  *   out_weights fp32 [n][k]; out_partials fp32 [k][n][hidden]:
  *   partial j of token t = w_{t,j} * SwiGLU expert out_experts[t][j] (h_t), so
  *   FFN(h_t) = the sum of the k partials in slot order.
- * n <= 65536 / k.  Errors: INVALID_ARGUMENT, UNSUPPORTED (dense model),
+ * n k <= 2^30.  Errors: INVALID_ARGUMENT, UNSUPPORTED (dense model),
  * WORKSPACE_TOO_SMALL, HIP. */
 sevo_status sevo_moe_ffn(const sevo_model* m, int32_t layer, const void* h, int32_t n,
                          int32_t* out_experts, float* out_weights, float* out_partials,

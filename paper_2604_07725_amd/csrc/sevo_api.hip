@@ -597,6 +597,9 @@ SEVO_API sevo_status sevo_qk_norm_rope_append(const sevo_model* m, int32_t layer
 // ------------------------------------------------------------------ decode step
 namespace {
 
+// MoE: (token, slot) entries t * k + slot are int32
+constexpr int64_t kMoeMaxEntries = int64_t(1) << 30;
+
 struct StepLayout {
   size_t x, h, part_qkv, q, o, a, logits, part_x, attn, sample, total;
   size_t m_router, m_sel, m_w, m_off, m_assign, m_act;  // MoE buffers
@@ -705,6 +708,8 @@ SEVO_API sevo_status sevo_decode_step(sevo_model* m, const sevo_step_args* a, vo
   if (sevo_status cs = conf_check(a->conf_topk, c.vocab, a->out_conf, a->conf_sum, a->top_k,
                                   a->top_p, a->min_p))
     return cs;
+  if (c.n_experts > 0 && (int64_t)a->n * c.n_experts_active > kMoeMaxEntries)
+    return fail(SEVO_ERR_INVALID_ARGUMENT, "n %d: more than 2^30 expert entries", a->n);
   if (a->n == 0) return SEVO_OK;
   if (!a->tokens || !a->positions || !a->page_table || !a->kv_pools ||
       !a->cand_uid || !a->out_tokens || !a->out_logprobs || !a->workspace)
@@ -870,8 +875,8 @@ SEVO_API sevo_status sevo_moe_ffn(const sevo_model* m, int32_t layer, const void
   const sevo_model_config& c = m->cfg;
   if (c.n_experts <= 0) return fail(SEVO_ERR_UNSUPPORTED, "dense model: no experts");
   if (layer < 0 || layer >= c.n_layers) return fail(SEVO_ERR_INVALID_ARGUMENT, "bad layer");
-  if (n < 0 || (int64_t)n * c.n_experts_active > 65536)
-    return fail(SEVO_ERR_INVALID_ARGUMENT, "n %d outside [0, 65536 / k]", n);
+  if (n < 0 || (int64_t)n * c.n_experts_active > kMoeMaxEntries)
+    return fail(SEVO_ERR_INVALID_ARGUMENT, "n %d outside [0, 2^30 / k]", n);
   if (n == 0) return SEVO_OK;
   if (!h || !out_experts || !out_weights || !out_partials || !workspace || !aligned16(h) ||
       !aligned16(out_partials) || !aligned16(workspace))
@@ -1046,6 +1051,7 @@ SEVO_API sevo_status sevo_prefill_confidence(sevo_model* m, const sevo_prefill_a
                 a->conf_topk);
   if (!sevo::sample_conf_supported(c.vocab, a->conf_topk))
     return fail(SEVO_ERR_UNSUPPORTED, "confidence lists over a vocabulary of %d", c.vocab);
+  if (a->moe_chunk < 0) return fail(SEVO_ERR_INVALID_ARGUMENT, "moe_chunk %d < 0", a->moe_chunk);
   if (a->n_scored < 0 || a->n_scored > a->total_tokens)
     return fail(SEVO_ERR_INVALID_ARGUMENT, "n_scored %d outside [0, total_tokens]", a->n_scored);
   if (!a->seq_starts || !a->out_conf || !a->kv_pools || !a->workspace ||

@@ -161,3 +161,36 @@ def test_moe30b_step_reduced_depth(S):
     # the full-width end-to-end bars of the dense step (bf16 storage flips)
     assert err <= 6e-2
     assert lp_err <= 2.5e-2
+
+
+def test_moe_entry_points_reject_bad_arguments(S):
+    """Error paths: the MoE FFN of a dense model (UNSUPPORTED), a layer out of
+    range and more than 2^30 expert entries (INVALID_ARGUMENT), and the
+    confidence engine with a negative moe_chunk (INVALID_ARGUMENT)."""
+    import ctypes as C
+    sevo, di = S
+    dense = _model(S, synth.TINY, 1)
+    moe = _model(S, synth.TINY_MOE, 1)
+    L = sevo.lib()
+    buf = torch.zeros(1 << 20, dtype=torch.uint8, device="cuda")
+    p = C.c_void_p(buf.data_ptr())
+    args = lambda m, layer, n: (m.handle, layer, p, n, p, p, p, p, buf.numel(), None)  # noqa: E731
+    assert L.sevo_moe_ffn(*args(dense, 0, 4)) == sevo.UNSUPPORTED
+    assert L.sevo_moe_ffn(*args(moe, 2, 4)) == sevo.INVALID_ARGUMENT
+    assert L.sevo_moe_ffn(*args(moe, -1, 4)) == sevo.INVALID_ARGUMENT
+    assert L.sevo_moe_ffn(*args(moe, 0, (1 << 30) // 4 + 1)) == sevo.INVALID_ARGUMENT
+    assert L.sevo_moe_ffn(*args(moe, 0, 0)) == sevo.OK
+    # the engine on the MoE model with a negative chunk
+    toks = torch.zeros(32, dtype=torch.int32, device="cuda")
+    ss = torch.tensor([0, 32], dtype=torch.int32, device="cuda")
+    pt = torch.arange(2, dtype=torch.int32, device="cuda")[None]
+    pool = torch.zeros(2, 2, 2, 16 * 64, dtype=torch.bfloat16, device="cuda")
+    rows = torch.arange(32, dtype=torch.int32, device="cuda")
+    b = sevo.PrefillBuffers(moe, toks, ss, pt, pool, rows, 20, 32, moe_chunk=-1)
+    assert L.sevo_prefill_confidence(moe.handle, C.byref(b.args), None) == sevo.INVALID_ARGUMENT
+    b.args.moe_chunk = 16
+    assert L.sevo_prefill_confidence(moe.handle, C.byref(b.args), None) == sevo.OK
+    torch.cuda.synchronize()
+    assert np.isfinite(b.out_conf.cpu().numpy()).all()
+    dense.close()
+    moe.close()
