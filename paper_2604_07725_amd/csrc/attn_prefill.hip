@@ -30,7 +30,10 @@
 //     per-lane source offsets;
 //   * blocks entirely above a wave's queries skip their MFMAs (the wave still
 //     loads its part of the block and meets the barriers); workgroups are
-//     launched latest (longest) query blocks first.
+//     launched latest (longest) query blocks first;
+//   * the slots of a sequence's last page past its last key may hold anything
+//     (NaN included): in the block holding that key they are zeroed in the V
+//     tiles (the scores there are masked; K needs nothing).
 // P is rounded to bf16 for the P V product (fp32 accumulation); the softmax
 // statistics stay fp32.  The exponentials are the bare hardware exp2 (results
 // below 2^-126 flush to zero; a row's running max keeps its sum >= 2^-8).
@@ -139,7 +142,21 @@ __global__ __launch_bounds__(64 * NW, 1) void attn_prefill_kernel(PrefillAttnArg
   else if (nkb == 2) wait_vmcnt<DMA>();
   else wait_vmcnt<0>();
   lds_barrier();
+  const int nkeys = p0 + L;  // the sequence's keys; later slots may hold anything
   for (int b = 0; b < nkb; ++b) {
+    if (64 * b + 64 > nkeys) {
+      // the block with the sequence's last key: its V slots past that key
+      // are zeroed in LDS (P is 0 there, but 0 x NaN would not be); uniform
+      // over the workgroup
+      bf16_t* so = smem + (b % kPfStages) * STAGE_ELEMS + KT_ELEMS;
+      for (int idx = threadIdx.x; idx < 4 * D; idx += 64 * NW) {
+        const int j = idx / D, e = idx - (idx / D) * D;
+        for (int sl = 0; sl < kPage; ++sl)
+          if (64 * b + 16 * j + sl >= nkeys)
+            so[j * PAGE_ELEMS + (e * 2 + ((sl >> 3) ^ pf_vswz(e))) * 8 + (sl & 7)] = 0;
+      }
+      lds_barrier();
+    }
     if (active && b <= last_b) {
       const bf16_t* so = smem + (b % kPfStages) * STAGE_ELEMS;
       f32x16 acc_s[2][NQT];

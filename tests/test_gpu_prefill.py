@@ -95,6 +95,38 @@ def test_attn_prefill_page_permutation_bit_exact(S):
     assert torch.equal(o1.view(torch.int16), o2.view(torch.int16))
 
 
+@pytest.mark.parametrize("dims", [(32, 8, 128), (32, 4, 128), (8, 2, 64)])
+def test_attn_prefill_ignores_slots_past_the_last_key(S, dims):
+    """Slots of a sequence's last page past its last key may hold anything:
+    NaN patterns written there (K and V tiles, every kv head) leave the
+    output bit-identical."""
+    sevo, di = S
+    shape = _shape(*dims)
+    d = shape.head_dim
+    lens = np.array([37, 100, 16, 250])
+    say(f"attn prefill with NaN past the last key {dims}")
+    pop = make_population(lens, shuffle=True, seed=21)
+    kvp = di.device_pools(shape, 21, pop.n_pages, layers=[0])[0]
+    q = di.device_q(shape, 21, int(lens.sum()))
+    ss = torch.from_numpy(np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)).cuda()
+    pt = torch.from_numpy(pop.page_table.astype(np.int32)).cuda()
+    o1 = sevo.sevo_attn_prefill(q, kvp, pt, ss, int(lens.max()))
+    pool = kvp.view(torch.int16).cpu().numpy().copy()   # [P][hkv][2][16 d]
+    e = np.arange(d)
+    for i, n in enumerate(lens):
+        if n % 16 == 0:
+            continue
+        page = pop.page_table[i, n // 16]
+        for slot in range(n % 16, 16):
+            pool[page, :, 0, ((e // 32) * 16 + slot) * 32 + e % 32] = np.int16(0x7FC0)  # K
+            pool[page, :, 1, e * 16 + slot] = np.int16(0x7FC0)                          # V
+    kvp_nan = torch.from_numpy(pool).cuda().view(torch.bfloat16)
+    o2 = sevo.sevo_attn_prefill(q, kvp_nan, pt, ss, int(lens.max()))
+    torch.cuda.synchronize()
+    assert torch.isfinite(o2.float()).all()
+    assert torch.equal(o1.view(torch.int16), o2.view(torch.int16))
+
+
 # ------------------------------------------------------------------ confidence engine
 def _token_major(pool, d):
     """K and V of every (page, head, slot) of a pool [P, hkv, 2, 16 d] as
