@@ -1,10 +1,12 @@
 // Fused full-vocabulary log-softmax + Gumbel-max sampling.
 //
 // Pass 1: one 256-thread workgroup per (4096-entry vocab chunk, candidate).
-// Each thread owns four Philox4x32-10 counters = 16 consecutive vocab entries
-// read as four 16-byte loads, computes z = logit / T, the chunk-local max and
-// sum of exp(z - max) (wavefront shuffle reductions, then LDS), and the best
-// perturbed value z + G (ties -> lowest index).  Pass 2: one workgroup per
+// Thread t owns the 4-entry groups 1024 r + 4 t (r < 4) of the chunk, each one
+// Philox4x32-10 counter and one 16-byte load; it computes z = logit / T, the
+// chunk-local max and sum of exp(z - max) (wavefront shuffle reductions, then
+// LDS), and the best perturbed value z + G (ties -> lowest index).  The
+// temperature mode (T = 0, T = 1, other) is a template parameter, so greedy
+// sampling carries no noise or division code.  Pass 2: one workgroup per
 // candidate merges its chunks in a fixed order and writes the token id and
 // log-probability z_id - logsumexp(z).
 //
@@ -12,8 +14,9 @@
 // the group-confidence fitness signal (Eq. 1): c = logsumexp(x) - mean of the
 // conf_k largest logits x, i.e. minus the mean of the top-conf_k
 // log-probabilities under the model's own distribution (T = 1).  Pass 1 keeps
-// each chunk's conf_k largest logits (per-wave extraction, then a merge of the
-// four waves), pass 2 merges the chunks' lists.
+// each chunk's conf_k largest logits (per wave by a threshold and a bitonic
+// sort, then a bitonic merge of the four waves' lists), pass 2 merges the
+// chunks' lists the same way.
 //
 // Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11): 10 rounds; round r uses
 // key + r * (0x9E3779B9, 0xBB67AE85); multipliers 0xD2511F53, 0xCD9E8D57.
@@ -57,9 +60,16 @@ struct SamplePartial {
 constexpr int kConfMaxK = 32;     // largest supported top-K of the confidence
 constexpr int kConfMergeNV = 24;  // list entries per lane in the chunk merge
 
+constexpr float kLog2e = 1.4426950408889634f;
+
+// e^d for d <= 0 (or -inf) on the hardware exp2: one rounding of d log2(e),
+// then v_exp_f32 (results below 2^-126 may flush to zero; they only ever add
+// to sums whose largest term is 1)
+__device__ __forceinline__ float exp_le0(float d) { return __builtin_amdgcn_exp2f(d * kLog2e); }
+
 __device__ __forceinline__ void lse_merge(float& m, float& s, float om, float os) {
   const float M = fmaxf(m, om);
-  s = (m == -INFINITY ? 0.f : s * expf(m - M)) + (om == -INFINITY ? 0.f : os * expf(om - M));
+  s = (m == -INFINITY ? 0.f : s * exp_le0(m - M)) + (om == -INFINITY ? 0.f : os * exp_le0(om - M));
   m = M;
 }
 
@@ -98,11 +108,86 @@ __device__ __forceinline__ void wave_topk(float (&x)[NV], int K, float* out) {
   }
 }
 
+// Descending bitonic sort of one value per lane across the wave (21
+// compare-exchange steps; values only).
+__device__ __forceinline__ float wave_sort_desc(float v) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int k = 2; k <= 64; k <<= 1)
+#pragma unroll
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      const float o = __shfl_xor(v, j, kWave);
+      v = (((lane & k) == 0) == ((lane & j) == 0)) ? fmaxf(v, o) : fminf(v, o);
+    }
+  return v;
+}
+
+// Descending sort of a bitonic sequence held one value per lane (6 steps).
+__device__ __forceinline__ float wave_merge_desc(float v) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int j = 32; j > 0; j >>= 1) {
+    const float o = __shfl_xor(v, j, kWave);
+    v = (lane & j) == 0 ? fmaxf(v, o) : fminf(v, o);
+  }
+  return v;
+}
+
+// The same result as wave_topk (the K <= 32 largest values, descending, in
+// out[0..K)), written by lanes 0..K-1, found by thresholding: L = the K-th
+// largest of the 64 lane maxima is a lower bound of the K-th largest value
+// (the K largest lane maxima are K values >= L), so the values >= L contain
+// the top K.  When there are at most 64 of them (the common case), they are
+// compacted into cand (64 floats of LDS) with ballots and sorted across the
+// wave; otherwise (many equal values, or fewer than K finite ones) the wave
+// falls back to wave_topk.  NaN is never taken, as in wave_topk.
+template <int NV>
+__device__ __forceinline__ void wave_topk_fast(float (&x)[NV], int K, float* out, float* cand) {
+  const int lane = threadIdx.x & 63;
+  float lm = -INFINITY;
+#pragma unroll
+  for (int e = 0; e < NV; ++e) lm = fmaxf(lm, x[e]);
+  const float L = __shfl(wave_sort_desc(lm), K - 1, kWave);
+  const uint64_t below = (1ull << lane) - 1ull;
+  int n = 0;
+#pragma unroll
+  for (int e = 0; e < NV; ++e) {
+    const bool c = x[e] >= L;
+    const uint64_t m = __ballot(c);
+    const int pos = n + __popcll(m & below);
+    if (c && pos < kWave) cand[pos] = x[e];
+    n += __popcll(m);
+  }
+  if (n <= kWave) {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    const float v = wave_sort_desc(lane < n ? cand[lane] : -INFINITY);
+    if (lane < K) out[lane] = v;
+  } else {
+    wave_topk<NV>(x, K, out);
+  }
+}
+
+// Merges four descending lists of K <= 32 values (list w at lists[w * 32])
+// into their K largest, descending, returned in lanes 0..K-1 (one wave).
+__device__ __forceinline__ float merge4_desc(const float* lists, int K) {
+  const int lane = threadIdx.x & 63;
+  auto get = [&](int w, int r) { return r < K ? lists[w * kConfMaxK + r] : -INFINITY; };
+  // list 0 descending then list 1 ascending: a bitonic sequence
+  const float a = wave_merge_desc(lane < 32 ? get(0, lane) : get(1, 63 - lane));
+  const float b = wave_merge_desc(lane < 32 ? get(2, lane) : get(3, 63 - lane));
+  const float br = __shfl(b, 63 - lane, kWave);  // lanes 32..63: b[31..0], ascending
+  return wave_merge_desc(lane < 32 ? a : br);
+}
+
 __device__ __forceinline__ bool better(float a, int ia, float b, int ib) {
   return a > b || (a == b && ia < ib);
 }
 
-template <int NW>
+// RAW: the raw-logit statistics (m1, s1) differ from z's and are merged too;
+// otherwise they are set equal to the merged (m, s)
+template <int NW, bool RAW = true>
 __device__ __forceinline__ SamplePartial block_merge(SamplePartial p, SamplePartial* red) {
   // wave level
 #pragma unroll
@@ -111,10 +196,12 @@ __device__ __forceinline__ SamplePartial block_merge(SamplePartial p, SamplePart
     const float os = __shfl_xor(p.s, o, kWave);
     const float ob = __shfl_xor(p.best, o, kWave);
     const int oi = __shfl_xor(p.idx, o, kWave);
-    const float om1 = __shfl_xor(p.m1, o, kWave);
-    const float os1 = __shfl_xor(p.s1, o, kWave);
     lse_merge(p.m, p.s, om, os);
-    lse_merge(p.m1, p.s1, om1, os1);
+    if constexpr (RAW) {
+      const float om1 = __shfl_xor(p.m1, o, kWave);
+      const float os1 = __shfl_xor(p.s1, o, kWave);
+      lse_merge(p.m1, p.s1, om1, os1);
+    }
     if (better(ob, oi, p.best, p.idx)) {
       p.best = ob;
       p.idx = oi;
@@ -128,38 +215,36 @@ __device__ __forceinline__ SamplePartial block_merge(SamplePartial p, SamplePart
   for (int k = 1; k < NW; ++k) {
     const SamplePartial o = red[k];
     lse_merge(r.m, r.s, o.m, o.s);
-    lse_merge(r.m1, r.s1, o.m1, o.s1);
+    if constexpr (RAW) lse_merge(r.m1, r.s1, o.m1, o.s1);
     if (better(o.best, o.idx, r.best, r.idx)) {
       r.best = o.best;
       r.idx = o.idx;
     }
   }
+  if constexpr (!RAW) {
+    r.m1 = r.m;
+    r.s1 = r.s;
+  }
   return r;
 }
 
+// Pass 1.  MODE 0: T = 0 (greedy, no noise, z = x); 1: T = 1 (z = x); 2: any
+// other T (z = x / T).  CONF: also the chunk's conf_k largest raw logits.
+template <int MODE, bool CONF>
 __global__ __launch_bounds__(256) void sample_partial_kernel(
     const float* __restrict__ logits, int vocab, int64_t ld, float temp, uint64_t seed,
     const uint64_t* __restrict__ uid, const int32_t* __restrict__ positions,
     SamplePartial* __restrict__ part, int conf_k, float* __restrict__ topk) {
   __shared__ SamplePartial red[4];
   __shared__ float wtop[4][kConfMaxK];
+  __shared__ float cand[4][kWave];
   const int chunk = blockIdx.x;
   const int i = blockIdx.y;
   const float* row = logits + (size_t)i * ld;
-  const bool greedy = temp == 0.f;
-  const bool unit_t = temp == 1.f;
-  // greedy sampling draws no noise: uid and positions may be null then
-  const uint64_t cu = greedy ? 0 : uid[i];
-  const uint32_t pos = greedy ? 0u : (uint32_t)positions[i];
-  const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
-  float z[16], raw[16];
-  float best = -INFINITY;
-  int bidx = 0x7FFFFFFF;
-  float m = -INFINITY;
+  float raw[16];
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
-    const int q4 = chunk * (kSampleChunk / 4) + r * 256 + threadIdx.x;  // Philox counter word 0
-    const int v0 = q4 * 4;
+    const int v0 = (chunk * (kSampleChunk / 4) + r * 256 + threadIdx.x) * 4;
     float4 lv;
     if (v0 + 3 < vocab) {
       lv = *reinterpret_cast<const float4*>(row + v0);
@@ -169,75 +254,75 @@ __global__ __launch_bounds__(256) void sample_partial_kernel(
       lv.z = v0 + 2 < vocab ? row[v0 + 2] : -INFINITY;
       lv.w = v0 + 3 < vocab ? row[v0 + 3] : -INFINITY;
     }
-    float zz[4] = {lv.x, lv.y, lv.z, lv.w};
-    raw[r * 4 + 0] = lv.x;
-    raw[r * 4 + 1] = lv.y;
-    raw[r * 4 + 2] = lv.z;
-    raw[r * 4 + 3] = lv.w;
-    if (!greedy && !unit_t) {
+    raw[4 * r + 0] = lv.x;
+    raw[4 * r + 1] = lv.y;
+    raw[4 * r + 2] = lv.z;
+    raw[4 * r + 3] = lv.w;
+  }
+  float z[16];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) zz[e] = zz[e] / temp;
-    }
+  for (int e = 0; e < 16; ++e) z[e] = MODE == 2 ? raw[e] / temp : raw[e];
+  // the best perturbed value z + G (greedy: G = 0); v ascends within a
+  // thread, so the strict > keeps the lowest index of a tie
+  float best = -INFINITY;
+  int bidx = 0x7FFFFFFF;
+  uint64_t cu = 0;
+  uint32_t pos = 0;
+  if constexpr (MODE != 0) {
+    cu = uid[i];
+    pos = (uint32_t)positions[i];
+  }
+  const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int q4 = chunk * (kSampleChunk / 4) + r * 256 + threadIdx.x;  // Philox counter word 0
+    const int v0 = q4 * 4;
     float g[4] = {0.f, 0.f, 0.f, 0.f};
-    if (!greedy && v0 < vocab) {
-      const u32x4 w = philox4x32_10(u32x4{(uint32_t)q4, pos, (uint32_t)cu, (uint32_t)(cu >> 32)},
-                                    k0, k1);
-      g[0] = gumbel_from_bits(w.x);
-      g[1] = gumbel_from_bits(w.y);
-      g[2] = gumbel_from_bits(w.z);
-      g[3] = gumbel_from_bits(w.w);
+    if constexpr (MODE != 0) {
+      if (v0 < vocab) {
+        const u32x4 w = philox4x32_10(
+            u32x4{(uint32_t)q4, pos, (uint32_t)cu, (uint32_t)(cu >> 32)}, k0, k1);
+        g[0] = gumbel_from_bits(w.x);
+        g[1] = gumbel_from_bits(w.y);
+        g[2] = gumbel_from_bits(w.z);
+        g[3] = gumbel_from_bits(w.w);
+      }
     }
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      z[r * 4 + e] = zz[e];
-      m = fmaxf(m, zz[e]);
-      const int v = v0 + e;
-      if (v < vocab) {
-        const float pv = zz[e] + g[e];
-        if (pv > best) {  // ascending v within a thread: strict > keeps the lowest index
-          best = pv;
-          bidx = v;
-        }
+      const float pv = z[4 * r + e] + g[e];
+      if (v0 + e < vocab && pv > best) {
+        best = pv;
+        bidx = v0 + e;
       }
     }
   }
-  // greedy sampling reports log-probs under T = 1, and z = logits there
-  float s = 0.f;
-  if (m != -INFINITY) {
+  // max and sum of exp(z - max); for MODE 2 with the confidence also those
+  // of the raw logits (T = 1), else they are z's
+  auto lse16 = [](const float (&x)[16], float& m, float& s) {
+    m = -INFINITY;
 #pragma unroll
-    for (int e = 0; e < 16; ++e) s += (z[e] == -INFINITY) ? 0.f : expf(z[e] - m);
-  }
-  // statistics of the raw logits (T = 1) for the confidence; equal to the
-  // above when z is the raw logit
-  float m1 = m, s1 = s;
-  if (conf_k > 0 && !greedy && !unit_t) {
-    m1 = -INFINITY;
+    for (int e = 0; e < 16; ++e) m = fmaxf(m, x[e]);
+    s = 0.f;
+    if (m != -INFINITY) {
 #pragma unroll
-    for (int e = 0; e < 16; ++e) m1 = fmaxf(m1, raw[e]);
-    s1 = 0.f;
-    if (m1 != -INFINITY) {
-#pragma unroll
-      for (int e = 0; e < 16; ++e) s1 += (raw[e] == -INFINITY) ? 0.f : expf(raw[e] - m1);
+      for (int e = 0; e < 16; ++e) s += exp_le0(x[e] - m);  // exp(-inf) = 0
     }
-  }
-  SamplePartial p{m, s, best, bidx, m1, s1};
-  p = block_merge<4>(p, red);
+  };
+  constexpr bool kRaw = MODE == 2 && CONF;
+  SamplePartial p{-INFINITY, 0.f, best, bidx, -INFINITY, 0.f};
+  lse16(z, p.m, p.s);
+  if constexpr (kRaw) lse16(raw, p.m1, p.s1);
+  p = block_merge<4, kRaw>(p, red);
   if (threadIdx.x == 0) part[(size_t)i * gridDim.x + chunk] = p;
-  if (conf_k > 0) {
+  if constexpr (CONF) {
     // the chunk's conf_k largest raw logits: per wave, then merged by wave 0
-    const int wave = threadIdx.x >> 6;
-    wave_topk<16>(raw, conf_k, wtop[wave]);
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    wave_topk_fast<16>(raw, conf_k, wtop[wave], cand[wave]);
     __syncthreads();
     if (wave == 0) {
-      const int lane = threadIdx.x & 63;
-      float x2[2];
-#pragma unroll
-      for (int e = 0; e < 2; ++e) {
-        const int q = lane * 2 + e;  // entry q of the 4 lists of conf_k values
-        const int w = q / kConfMaxK, r = q - w * kConfMaxK;
-        x2[e] = (w < 4 && r < conf_k) ? wtop[w][r] : -INFINITY;
-      }
-      wave_topk<2>(x2, conf_k, topk + ((size_t)i * gridDim.x + chunk) * kConfMaxK);
+      const float v = merge4_desc(&wtop[0][0], conf_k);
+      if (lane < conf_k) topk[((size_t)i * gridDim.x + chunk) * kConfMaxK + lane] = v;
     }
   }
 }
@@ -269,8 +354,10 @@ __global__ __launch_bounds__(256) void sample_final_kernel(
     out_lp[i] = zid - (p.m + logf(p.s));
   }
   if (conf_k > 0) {
-    // merge the chunks' lists: wave w takes a contiguous quarter of them, then
-    // wave 0 merges the four results (host checks nchunks * conf_k fits)
+    // merge the chunks' lists: wave w takes a contiguous quarter of them (entry
+    // wave * per + 64 e + lane in lane, slot e), then wave 0 merges the four
+    // results (host checks nchunks * conf_k fits)
+    __shared__ float cand[4][kWave];
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     const int total = nchunks * conf_k;
     const int per = (total + 3) / 4;
@@ -278,23 +365,17 @@ __global__ __launch_bounds__(256) void sample_final_kernel(
     float x[kConfMergeNV];
 #pragma unroll
     for (int e = 0; e < kConfMergeNV; ++e) {
-      const int q = wave * per + lane * kConfMergeNV + e;  // entry of the flattened lists
-      const bool ok = lane * kConfMergeNV + e < per && q < total;
+      const int q = wave * per + e * kWave + lane;  // entry of the flattened lists
+      const bool ok = e * kWave + lane < per && q < total;
       const int c = ok ? q / conf_k : 0;
       x[e] = ok ? src[(size_t)c * kConfMaxK + (q - c * conf_k)] : -INFINITY;
     }
-    wave_topk<kConfMergeNV>(x, conf_k, wtop[wave]);
+    wave_topk_fast<kConfMergeNV>(x, conf_k, wtop[wave], cand[wave]);
     __syncthreads();
     if (wave == 0) {
-      float x2[2];
-#pragma unroll
-      for (int e = 0; e < 2; ++e) {
-        const int q = lane * 2 + e;
-        const int w = q / kConfMaxK, r = q - w * kConfMaxK;
-        x2[e] = (w < 4 && r < conf_k) ? wtop[w][r] : -INFINITY;
-      }
       __shared__ float top[kConfMaxK];
-      wave_topk<2>(x2, conf_k, top);
+      const float v = merge4_desc(&wtop[0][0], conf_k);
+      if (lane < conf_k) top[lane] = v;
       __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
       __builtin_amdgcn_wave_barrier();
       __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
@@ -598,8 +679,15 @@ hipError_t launch_logprob_sample(const float* logits, int n, int vocab, int64_t 
                        out_lp, conf_k, out_conf, conf_sum);
     return hipGetLastError();
   }
-  hipLaunchKernelGGL(sample_partial_kernel, dim3(nchunks, n), dim3(256), 0, st, logits, vocab, ld,
-                     temp, seed, uid, positions, part, conf_k, topk);
+  using PartialFn = void (*)(const float*, int, int64_t, float, uint64_t, const uint64_t*,
+                            const int32_t*, SamplePartial*, int, float*);
+  static constexpr PartialFn kPartial[3][2] = {
+      {sample_partial_kernel<0, false>, sample_partial_kernel<0, true>},
+      {sample_partial_kernel<1, false>, sample_partial_kernel<1, true>},
+      {sample_partial_kernel<2, false>, sample_partial_kernel<2, true>}};
+  const int mode = temp == 0.f ? 0 : temp == 1.f ? 1 : 2;
+  hipLaunchKernelGGL(kPartial[mode][conf_k > 0 ? 1 : 0], dim3(nchunks, n), dim3(256), 0, st,
+                     logits, vocab, ld, temp, seed, uid, positions, part, conf_k, topk);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(sample_final_kernel, dim3(n), dim3(256), 0, st, part, nchunks, logits, ld,
