@@ -418,6 +418,19 @@ sevo_status sevo_embed(const void* embed, const int32_t* tokens, int32_t n, int3
 sevo_status sevo_rmsnorm(const float* x, const void* gain, int32_t rows, int32_t cols,
                          float eps, void* out, void* stream);
 
+/* The residual update + RMSNorm that joins the sub-layers of a decoder layer:
+ *   x[r][:] += sum over s < n_partials of partials[s][r][:]   (in s order,
+ *              written back to x; x unchanged when n_partials = 0)
+ *   out[r][:] = bf16(x[r][:] / sqrt(mean(x[r]^2) + eps) * gain)
+ * x fp32 [rows][cols]; partials fp32 [n_partials][rows][cols] (the split-K
+ * partials of the projection before it; NULL when n_partials = 0); gain bf16
+ * [cols]; out bf16 in the tiled activation layout the projections read
+ * (16-row tiles, a buffer of ceil(rows / 16) * 16 rows; padding rows are not
+ * written).  cols % 4 == 0, 0 <= n_partials <= 16.  Errors: INVALID_ARGUMENT. */
+sevo_status sevo_add_rmsnorm(float* x, const float* partials, int32_t n_partials,
+                             const void* gain, int32_t rows, int32_t cols, float eps, void* out,
+                             void* stream);
+
 /* Y = X W^T with X bf16 [m][k], W bf16 [n_out][k] in the packed weight layout
  * (for SWIGLU packed with kind SEVO_PACK_GATE_UP), fp32 accumulation on the
  * matrix cores, then the epilogue:

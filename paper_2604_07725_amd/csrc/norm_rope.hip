@@ -53,11 +53,94 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const float* __restrict__ 
   }
 }
 
-// One wave per (candidate, head) of the QKV projection (given as the fp32
-// split-K partials of the GEMM, summed here in split order).  Lane m < d/2 owns
-// the rotate-half pair (m, m + d/2).  q heads -> q_out; k heads -> K pool slot
-// p_i; v heads -> V pool slot p_i (dim-major tile).  Positions outside the
-// RoPE table or page ids outside the pool skip the write (no fault).
+// What lane m needs of token i for every head: position, its K/V page (-1:
+// no append), the RoPE cos / sin of the pair (m, m + d/2) and the QK-norm
+// gains.  Positions outside the RoPE table or page ids outside the pool skip
+// the writes (no fault).
+struct RopeTok {
+  int p, page;
+  bool pos_ok;
+  float c, s, gq0, gq1, gk0, gk1;
+};
+
+__device__ __forceinline__ RopeTok rope_token(const RopeAppendArgs& a, int i, int m) {
+  const int half = a.d >> 1;
+  RopeTok t{};
+  t.p = a.positions[i];
+  t.pos_ok = t.p >= 0 && t.p < a.max_pos;
+  t.page = -1;
+  if (m < half) {
+    if (t.pos_ok) {
+      t.c = a.rope_cos[(size_t)t.p * half + m];
+      t.s = a.rope_sin[(size_t)t.p * half + m];
+      const int pg = t.p >> 4;
+      if (pg < a.max_pages) {
+        const int prow = a.row_of_token ? a.row_of_token[i] : i;
+        const int page = a.page_table[(size_t)prow * a.max_pages + pg];
+        if (page >= 0 && (int64_t)page < a.num_pages) t.page = page;
+      }
+    }
+    if (a.qk_norm) {
+      t.gq0 = bf16_to_f32(a.q_gain[m]);
+      t.gq1 = bf16_to_f32(a.q_gain[m + half]);
+      t.gk0 = bf16_to_f32(a.k_gain[m]);
+      t.gk1 = bf16_to_f32(a.k_gain[m + half]);
+    }
+  }
+  return t;
+}
+
+// QK-RMSNorm + RoPE + store of one (token i, head hh) of the QKV projection,
+// called by a whole wave with the summed values u0 = row[m], u1 = row[m + d/2]
+// in lane m < d/2 (lane m owns the rotate-half pair).  q heads -> q_out; k
+// heads -> K pool slot p_i; v heads -> V pool slot p_i (dim-major tile).
+__device__ __forceinline__ void rope_head(const RopeAppendArgs& a, const RopeTok& t, int i,
+                                          int hh, int m, float u0, float u1) {
+  const int half = a.d >> 1;
+  const bool act = m < half;
+  if (hh < a.hq + a.hkv) {
+    if (a.qk_norm) {
+      const float ss = wave_sum(u0 * u0 + u1 * u1);
+      const float inv = 1.0f / sqrtf(ss / (float)a.d + a.eps);
+      const bool q = hh < a.hq;
+      if (act) {
+        u0 = u0 * inv * (q ? t.gq0 : t.gk0);
+        u1 = u1 * inv * (q ? t.gq1 : t.gk1);
+      }
+    }
+    if (!act) return;
+    float r0 = 0.f, r1 = 0.f;
+    if (t.pos_ok) {
+      r0 = u0 * t.c - u1 * t.s;
+      r1 = u1 * t.c + u0 * t.s;
+    }
+    if (hh < a.hq) {
+      bf16_t* dst = a.q_out + ((size_t)i * a.hq + hh) * a.d;
+      dst[m] = f32_to_bf16(r0);
+      dst[m + half] = f32_to_bf16(r1);
+      return;
+    }
+    if (t.page < 0) return;
+    const int kh = hh - a.hq;
+    // K tile (first half of the (page, head) pair): dims in blocks of 32, each
+    // block [16 slots][32 dims]
+    bf16_t* tile = a.kv_pool + ((size_t)t.page * a.hkv + kh) * 2 * kPage * a.d;
+    const int s = t.p & 15;
+    const int e0 = m, e1 = m + half;
+    tile[((e0 >> 5) * kPage + s) * 32 + (e0 & 31)] = f32_to_bf16(r0);
+    tile[((e1 >> 5) * kPage + s) * 32 + (e1 & 31)] = f32_to_bf16(r1);
+  } else {
+    if (!act || t.page < 0) return;
+    const int vh = hh - a.hq - a.hkv;
+    // V tile (second half): dim-major [dims][16 slots]
+    bf16_t* dst = a.kv_pool + (((size_t)t.page * a.hkv + vh) * 2 + 1) * kPage * a.d + (t.p & 15);
+    dst[(size_t)m * kPage] = f32_to_bf16(u0);
+    dst[(size_t)(m + half) * kPage] = f32_to_bf16(u1);
+  }
+}
+
+// One wave per (candidate, head); the QKV projection given as the fp32
+// split-K partials of the GEMM, summed here in split order.
 __global__ __launch_bounds__(64) void qk_norm_rope_append_kernel(RopeAppendArgs a) {
   const int i = blockIdx.x;
   const int hh = blockIdx.y;
@@ -74,57 +157,47 @@ __global__ __launch_bounds__(64) void qk_norm_rope_append_kernel(RopeAppendArgs 
       u1 += src[sp * split_stride + m + half];
     }
   }
-  const int p = a.positions[i];
-  const bool pos_ok = p >= 0 && p < a.max_pos;
-  const int prow = a.row_of_token ? a.row_of_token[i] : i;
-  if (hh < a.hq + a.hkv) {
-    if (a.qk_norm) {
-      const float ss = wave_sum(u0 * u0 + u1 * u1);
-      const float inv = 1.0f / sqrtf(ss / (float)a.d + a.eps);
-      const bf16_t* g = hh < a.hq ? a.q_gain : a.k_gain;
-      if (act) {
-        u0 = u0 * inv * bf16_to_f32(g[m]);
-        u1 = u1 * inv * bf16_to_f32(g[m + half]);
+  rope_head(a, rope_token(a, i, m), i, hh, m, u0, u1);
+}
+
+// The same per token, for many tokens (a prefill): one 4-wave workgroup per
+// token, wave w taking heads w, w + 4, ...; the token's position, page, RoPE
+// row and gains are loaded once and every head's values before any
+// arithmetic (one wave per (token, head) left the launch of millions of
+// one-wave workgroups as the cost).  Identical output.
+constexpr int kRopeHeadsPerWave = 20;  // hq + 2 hkv <= 80
+__global__ __launch_bounds__(256) void qk_norm_rope_append_token_kernel(RopeAppendArgs a) {
+  const int i = blockIdx.x;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), m = threadIdx.x & 63;
+  const int half = a.d >> 1;
+  const bool act = m < half;
+  const int H = a.hq + 2 * a.hkv;
+  const int qkv_ld = H * a.d;
+  const size_t split_stride = (size_t)a.n * qkv_ld;
+  const RopeTok t = rope_token(a, i, m);
+  float u0[kRopeHeadsPerWave], u1[kRopeHeadsPerWave];
+#pragma unroll
+  for (int j = 0; j < kRopeHeadsPerWave; ++j) u0[j] = u1[j] = 0.f;
+  for (int sp = 0; sp < a.qkv_splits; ++sp) {  // split-K partials, in split order
+    // one descriptor over the token's row: the head offset is a scalar
+    // offset, the lane's 4 m bytes the only per-lane address
+    const __amdgpu_buffer_rsrc_t row = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<float*>(a.qkv + sp * split_stride + (size_t)i * qkv_ld), 0, qkv_ld * 4,
+        0x00020000);
+#pragma unroll
+    for (int j = 0; j < kRopeHeadsPerWave; ++j) {
+      const int hh = 4 * j + w;
+      if (act && hh < H) {
+        u0[j] += __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(row, m * 4, hh * a.d * 4, 0));
+        u1[j] += __uint_as_float(
+            __builtin_amdgcn_raw_buffer_load_b32(row, (m + half) * 4, hh * a.d * 4, 0));
       }
     }
-    if (!act) return;
-    float r0 = 0.f, r1 = 0.f;
-    if (pos_ok) {
-      const float c = a.rope_cos[(size_t)p * half + m];
-      const float s = a.rope_sin[(size_t)p * half + m];
-      r0 = u0 * c - u1 * s;
-      r1 = u1 * c + u0 * s;
-    }
-    if (hh < a.hq) {
-      bf16_t* dst = a.q_out + ((size_t)i * a.hq + hh) * a.d;
-      dst[m] = f32_to_bf16(r0);
-      dst[m + half] = f32_to_bf16(r1);
-      return;
-    }
-    if (!pos_ok) return;
-    const int pg = p >> 4;
-    if (pg >= a.max_pages) return;
-    const int page = a.page_table[(size_t)prow * a.max_pages + pg];
-    if (page < 0 || (int64_t)page >= a.num_pages) return;
-    const int kh = hh - a.hq;
-    // K tile (first half of the (page, head) pair): dims in blocks of 32, each
-    // block [16 slots][32 dims]
-    bf16_t* tile = a.kv_pool + ((size_t)page * a.hkv + kh) * 2 * kPage * a.d;
-    const int s = p & 15;
-    const int e0 = m, e1 = m + half;
-    tile[((e0 >> 5) * kPage + s) * 32 + (e0 & 31)] = f32_to_bf16(r0);
-    tile[((e1 >> 5) * kPage + s) * 32 + (e1 & 31)] = f32_to_bf16(r1);
-  } else {
-    if (!act || !pos_ok) return;
-    const int pg = p >> 4;
-    if (pg >= a.max_pages) return;
-    const int page = a.page_table[(size_t)prow * a.max_pages + pg];
-    if (page < 0 || (int64_t)page >= a.num_pages) return;
-    const int vh = hh - a.hq - a.hkv;
-    // V tile (second half): dim-major [dims][16 slots]
-    bf16_t* dst = a.kv_pool + (((size_t)page * a.hkv + vh) * 2 + 1) * kPage * a.d + (p & 15);
-    dst[(size_t)m * kPage] = f32_to_bf16(u0);
-    dst[(size_t)(m + half) * kPage] = f32_to_bf16(u1);
+  }
+#pragma unroll
+  for (int j = 0; j < kRopeHeadsPerWave; ++j) {
+    const int hh = 4 * j + w;
+    if (hh < H) rope_head(a, t, i, hh, m, u0[j], u1[j]);
   }
 }
 
@@ -229,14 +302,96 @@ __global__ __launch_bounds__(1024) void add_rmsnorm_kernel(float* __restrict__ x
   }
 }
 
+// The same for many rows with at most one partial (a prefill): 256 threads
+// per row, so eight rows per CU are in flight instead of two, and thread t
+// keeps the 4-column groups 1024 g + 4 t (g < NG) in registers across the
+// reduction.  The sum of squares is formed exactly as in the 1024-thread form:
+// the groups of its thread T = 256 (g % 4) + t in order, one wave sum per
+// wave of T, the 16 wave sums in order, so both forms give identical output.
+template <int NG>
+__global__ __launch_bounds__(256) void add_rmsnorm_rows_kernel(float* __restrict__ x,
+                                                               const float* __restrict__ part,
+                                                               int S, const bf16_t* __restrict__ gain,
+                                                               int cols, float eps,
+                                                               bf16_t* __restrict__ out,
+                                                               const int32_t* __restrict__ row_idx) {
+  __shared__ float red[16];
+  const size_t src = row_idx ? (size_t)row_idx[blockIdx.x] : (size_t)blockIdx.x;
+  float* xr = x + src * cols;
+  const float* pr = part + src * cols;
+  const int t = threadIdx.x;
+  f32x4 v[NG];
+#pragma unroll
+  for (int g = 0; g < NG; ++g) {
+    const int c = 1024 * g + 4 * t;
+    if (c < cols) v[g] = *reinterpret_cast<const f32x4*>(xr + c);
+  }
+  if (S > 0) {
+    f32x4 p[NG];
+#pragma unroll
+    for (int g = 0; g < NG; ++g) {
+      const int c = 1024 * g + 4 * t;
+      if (c < cols) p[g] = *reinterpret_cast<const f32x4*>(pr + c);
+    }
+#pragma unroll
+    for (int g = 0; g < NG; ++g) {
+      const int c = 1024 * g + 4 * t;
+      if (c < cols) {
+        v[g] += p[g];
+        if (!row_idx) *reinterpret_cast<f32x4*>(xr + c) = v[g];
+      }
+    }
+  }
+  float acc[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int g = 0; g < NG; ++g) {
+    const int c = 1024 * g + 4 * t;
+    if (c < cols) acc[g & 3] += v[g].x * v[g].x + v[g].y * v[g].y + v[g].z * v[g].z + v[g].w * v[g].w;
+  }
+  const int w = t >> 6;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const float sq = wave_sum(acc[q]);
+    if ((t & 63) == 0) red[4 * q + w] = sq;
+  }
+  __syncthreads();
+  float ss = 0.f;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) ss += red[i];
+  const float inv = 1.0f / sqrtf(ss / (float)cols + eps);
+#pragma unroll
+  for (int g = 0; g < NG; ++g) {
+    const int c = 1024 * g + 4 * t;
+    if (c < cols) {
+      const uint2 gn = *reinterpret_cast<const uint2*>(gain + c);
+      uint2 o;
+      o.x = pack_bf16x2(v[g].x * inv * bf16_lo(gn.x), v[g].y * inv * bf16_hi(gn.x));
+      o.y = pack_bf16x2(v[g].z * inv * bf16_lo(gn.y), v[g].w * inv * bf16_hi(gn.y));
+      *reinterpret_cast<uint2*>(out + act_tile_offset(blockIdx.x, c, cols)) = o;
+    }
+  }
+}
+
 hipError_t launch_add_rmsnorm(float* x, const float* part, int S, const bf16_t* gain, int rows,
                               int cols, float eps, bf16_t* out_tiled, hipStream_t st,
                               const int32_t* row_idx, int part_rows) {
   if (rows == 0) return hipSuccess;
   if (S > 16) return hipErrorInvalidValue;
   const size_t stride = (size_t)(row_idx ? part_rows : rows) * cols;
-  hipLaunchKernelGGL(add_rmsnorm_kernel, dim3(rows), dim3(1024), 0, st, x, part, part ? S : 0,
-                     stride, gain, cols, eps, out_tiled, row_idx);
+  const int s_eff = part ? S : 0;
+  if (rows >= 512 && s_eff <= 1 && cols <= 8192) {
+    const int ng = (cols + 1023) / 1024;
+    auto go = [&](auto kern) {
+      hipLaunchKernelGGL(kern, dim3(rows), dim3(256), 0, st, x, part, s_eff, gain, cols, eps,
+                         out_tiled, row_idx);
+    };
+    if (ng <= 2) go(add_rmsnorm_rows_kernel<2>);
+    else if (ng <= 4) go(add_rmsnorm_rows_kernel<4>);
+    else go(add_rmsnorm_rows_kernel<8>);
+    return hipGetLastError();
+  }
+  hipLaunchKernelGGL(add_rmsnorm_kernel, dim3(rows), dim3(1024), 0, st, x, part, s_eff, stride,
+                     gain, cols, eps, out_tiled, row_idx);
   return hipGetLastError();
 }
 
@@ -276,7 +431,10 @@ hipError_t launch_rmsnorm(const float* x, const bf16_t* gain, int rows, int cols
 
 hipError_t launch_qk_norm_rope_append(const RopeAppendArgs& a, hipStream_t st) {
   if (a.n == 0) return hipSuccess;
-  hipLaunchKernelGGL(qk_norm_rope_append_kernel, dim3(a.n, a.hq + 2 * a.hkv), dim3(64), 0, st, a);
+  if (a.n >= 256 && a.hq + 2 * a.hkv <= 4 * kRopeHeadsPerWave)
+    hipLaunchKernelGGL(qk_norm_rope_append_token_kernel, dim3(a.n), dim3(256), 0, st, a);
+  else
+    hipLaunchKernelGGL(qk_norm_rope_append_kernel, dim3(a.n, a.hq + 2 * a.hkv), dim3(64), 0, st, a);
   return hipGetLastError();
 }
 

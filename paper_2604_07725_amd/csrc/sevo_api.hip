@@ -488,6 +488,24 @@ SEVO_API sevo_status sevo_rmsnorm(const float* x, const void* gain, int32_t rows
   return e == hipSuccess ? SEVO_OK : hip_fail(e, "sevo_rmsnorm");
 }
 
+SEVO_API sevo_status sevo_add_rmsnorm(float* x, const float* partials, int32_t n_partials,
+                                      const void* gain, int32_t rows, int32_t cols, float eps,
+                                      void* out, void* stream) {
+  if (rows < 0 || cols < 4 || cols % 4) return fail(SEVO_ERR_INVALID_ARGUMENT, "bad rows / cols");
+  if (n_partials < 0 || n_partials > 16)
+    return fail(SEVO_ERR_INVALID_ARGUMENT, "n_partials %d outside 0..16", n_partials);
+  if (!(eps > 0.f)) return fail(SEVO_ERR_INVALID_ARGUMENT, "eps must be > 0");
+  if (rows == 0) return SEVO_OK;
+  if (!x || !gain || !out || !aligned16(x) || (n_partials > 0 && (!partials || !aligned16(partials))) ||
+      (reinterpret_cast<uintptr_t>(gain) & 7) || (reinterpret_cast<uintptr_t>(out) & 7))
+    return fail(SEVO_ERR_INVALID_ARGUMENT, "null or misaligned pointer");
+  hipError_t e = sevo::launch_add_rmsnorm(x, n_partials > 0 ? partials : nullptr, n_partials,
+                                          static_cast<const sevo::bf16_t*>(gain), rows, cols, eps,
+                                          static_cast<sevo::bf16_t*>(out),
+                                          static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? SEVO_OK : hip_fail(e, "sevo_add_rmsnorm");
+}
+
 static sevo_status linear_check(int m, int n_out, int k, int ldx, int mode, int k_splits,
                                 int flags) {
   if (m < 0 || n_out < 64 || k < 32) return fail(SEVO_ERR_INVALID_ARGUMENT, "bad m / n_out / k");
@@ -928,7 +946,7 @@ PrefillLayout prefill_layout(const sevo_model_config& c, int T, int R, int moe_c
   L.q = take(t * qd * 2);
   L.o = take(t16 * qd * 2);
   L.a = take(t16 * F * 2);
-  L.part = take(t * H * 4);
+  L.part = take(c.n_experts > 0 ? t * H * 4 : 0);  // the MoE FFN's output (dense: added in place)
   L.mc = 0;
   L.m_router = L.m_sel = L.m_w = L.m_off = L.m_assign = L.m_act = L.m_slots = L.m_tiles = 0;
   if (c.n_experts > 0) {
@@ -1103,12 +1121,16 @@ SEVO_API sevo_status sevo_prefill_confidence(sevo_model* m, const sevo_prefill_a
   if (e == hipSuccess)
     e = sevo::launch_prefill_index(a->seq_starts, a->start_pos, a->n_seqs, T, row, pos, st);
   if (e != hipSuccess) return hip_fail(e, "prefill (embed)");
-  // the output and down projections store their product in `part`; the next
-  // residual add + RMSNorm adds it to x
+  // the output and dense down projections add their product to x in the GEMM
+  // epilogue (the same single fp32 add as a separate residual update, without
+  // a round trip of the product through memory); a MoE FFN's slot-order sum
+  // goes to `part`, which the next residual add + RMSNorm adds to x
+  const bool moe = c.n_experts > 0;
   for (int l = 0; l < c.n_layers; ++l) {
     {
       ProfScope ps(SEVO_PROF_NORM, st);
-      e = sevo::launch_add_rmsnorm(x, l ? part : nullptr, l ? 1 : 0,
+      const bool add_part = l > 0 && moe;
+      e = sevo::launch_add_rmsnorm(x, add_part ? part : nullptr, add_part ? 1 : 0,
                                    static_cast<const sevo::bf16_t*>(m->attn_norm[l]), T, H,
                                    c.rms_eps, h, st);
     }
@@ -1136,14 +1158,14 @@ SEVO_API sevo_status sevo_prefill_confidence(sevo_model* m, const sevo_prefill_a
     }
     if (e == hipSuccess) {
       ProfScope ps(SEVO_PROF_ATTN_OUT, st);
-      e = prefill_gemm(T, H, qd, SEVO_LINEAR_STORE, o, m->w_o[l], part, 0, st);
+      e = prefill_gemm(T, H, qd, SEVO_LINEAR_ADD, o, m->w_o[l], x, 0, st);
     }
     if (e == hipSuccess) {
       ProfScope ps(SEVO_PROF_NORM, st);
-      e = sevo::launch_add_rmsnorm(x, part, 1, static_cast<const sevo::bf16_t*>(m->ffn_norm[l]),
+      e = sevo::launch_add_rmsnorm(x, nullptr, 0, static_cast<const sevo::bf16_t*>(m->ffn_norm[l]),
                                    T, H, c.rms_eps, h, st);
     }
-    if (c.n_experts > 0) {
+    if (moe) {
       // the mixture of experts, a chunk of tokens at a time: per-slot outputs
       // of the chunk, then their slot-order sum into its rows of `part`
       for (int c0 = 0; c0 < T && e == hipSuccess; c0 += L.mc) {
@@ -1157,19 +1179,20 @@ SEVO_API sevo_status sevo_prefill_confidence(sevo_model* m, const sevo_prefill_a
       }
       if (e == hipSuccess) {
         ProfScope ps(SEVO_PROF_DOWN, st);
-        e = prefill_gemm(T, H, F, SEVO_LINEAR_STORE, act, m->w_down[l], part, 0, st);
+        e = prefill_gemm(T, H, F, SEVO_LINEAR_ADD, act, m->w_down[l], x, 0, st);
       }
     }
     if (e != hipSuccess) return hip_fail(e, "prefill (layer)");
   }
-  // scored rows, a chunk at a time: final norm of x + the last down product,
-  // LM head, per-row confidence (greedy pass of the sampler: no noise)
+  // scored rows, a chunk at a time: final norm of x (+ the last MoE FFN
+  // output), LM head, per-row confidence (greedy pass of the sampler: no noise)
   for (int r0 = 0; r0 < R; r0 += L.rc) {
     const int nr = R - r0 < L.rc ? R - r0 : L.rc;
     {
       ProfScope ps(SEVO_PROF_NORM, st);
-      e = sevo::launch_add_rmsnorm(x, part, 1, static_cast<const sevo::bf16_t*>(m->final_norm),
-                                   nr, H, c.rms_eps, hf, st, a->scored_rows + r0, T);
+      e = sevo::launch_add_rmsnorm(x, moe ? part : nullptr, moe ? 1 : 0,
+                                   static_cast<const sevo::bf16_t*>(m->final_norm), nr, H,
+                                   c.rms_eps, hf, st, a->scored_rows + r0, T);
     }
     if (e == hipSuccess) {
       ProfScope ps(SEVO_PROF_LM_HEAD, st);

@@ -124,6 +124,7 @@ _SIGS = {
     "sevo_prefill_workspace_bytes": ([vp, i32, i32], sz),
     "sevo_embed": ([vp, vp, i32, i32, i32, vp, vp], i32),
     "sevo_rmsnorm": ([vp, vp, i32, i32, f32, vp, vp], i32),
+    "sevo_add_rmsnorm": ([vp, vp, i32, vp, i32, i32, f32, vp, vp], i32),
     "sevo_linear": ([C.POINTER(LinearArgs), vp], i32),
     "sevo_linear_workspace_bytes": ([i32, i32, i32, i32], sz),
     "sevo_pack_weight": ([vp, vp, i32, i32, i32, vp], i32),
@@ -302,6 +303,19 @@ def sevo_rmsnorm(x, gain, eps, out=None, stream=None):
     if out is None:
         out = torch.empty(rows, cols, dtype=torch.bfloat16, device=x.device)
     _check(lib().sevo_rmsnorm(_p(x), _p(gain), rows, cols, float(eps), _p(out), _stream(stream)))
+    return out
+
+
+def sevo_add_rmsnorm(x, partials, gain, eps, out=None, stream=None):
+    """x fp32 [rows, cols] += the partials fp32 [S, rows, cols] (in s order; None
+    for none), in place; returns RMSNorm(x) * gain as bf16 in the tiled
+    activation layout (a flat buffer of ceil(rows / 16) * 16 rows)."""
+    rows, cols = x.shape
+    S = 0 if partials is None else partials.shape[0]
+    if out is None:
+        out = torch.zeros(-(-rows // 16) * 16 * cols, dtype=torch.bfloat16, device=x.device)
+    _check(lib().sevo_add_rmsnorm(_p(x), _p(partials) if S else None, S, _p(gain), rows, cols,
+                                  float(eps), _p(out), _stream(stream)))
     return out
 
 

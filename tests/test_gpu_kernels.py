@@ -482,6 +482,79 @@ def test_swiglu_tiled_output_and_tiled_chain(S, m):
 
 
 # ------------------------------------------------------------------ norm / embed / rope
+@pytest.mark.parametrize("rows,cols,n_part", [(600, 4096, 1), (600, 2048, 1), (530, 5120, 1),
+                                                (600, 4096, 0), (100, 4096, 3), (37, 256, 16)])
+def test_add_rmsnorm_matches_oracle_and_forms_agree(S, rows, cols, n_part):
+    """Residual update + RMSNorm: x written back equal to the fp32 sum in
+    partial order, the normed rows against the oracle; from 512 rows with at
+    most one partial the many-row form runs, and the same rows in slices of
+    192 (the 1024-thread form) must give identical bits."""
+    sevo, _ = S
+    say(f"add_rmsnorm rows={rows} cols={cols} partials={n_part}")
+    g = torch.Generator(device="cuda")
+    g.manual_seed(rows * 7 + cols + n_part)
+    x0 = torch.randn(rows, cols, device="cuda", generator=g) * 2.0
+    parts = (torch.randn(n_part, rows, cols, device="cuda", generator=g) if n_part else None)
+    gain = (1.0 + 0.02 * torch.randn(cols, device="cuda", generator=g)).to(torch.bfloat16)
+    x = x0.clone()
+    out = sevo.sevo_add_rmsnorm(x, parts, gain, 1e-6)
+    torch.cuda.synchronize()
+    ref_x = x0.cpu().numpy()
+    for s_ in range(n_part):
+        ref_x = ref_x + parts[s_].cpu().numpy()        # float32, in partial order
+    np.testing.assert_array_equal(x.cpu().numpy(), ref_x)
+    got = untile_activations_host(to_np(out), rows, cols)
+    ref = od.rms_norm(ref_x.astype(np.float64), to_np(gain), 1e-6)
+    assert np.all(np.abs(got - ref) <= 2 ** -8 * np.abs(ref) + 1e-6)
+    if rows >= 512 and n_part <= 1:
+        xb = x0.clone()
+        outb = torch.zeros_like(out)
+        for a in range(0, rows, 192):
+            b = min(rows, a + 192)
+            pb = parts[:, a:b].contiguous() if n_part else None
+            nb = -(-(b - a) // 16) * 16 * cols
+            sevo.sevo_add_rmsnorm(xb[a:b], pb, gain, 1e-6, out=outb[a * cols:a * cols + nb])
+        torch.cuda.synchronize()
+        assert torch.equal(x, xb)
+        assert torch.equal(out.view(torch.int16), outb.view(torch.int16))
+
+
+@pytest.mark.parametrize("hq,hkv,d", [(32, 8, 128), (64, 8, 128), (4, 2, 64)])
+def test_qk_norm_rope_append_forms_agree(S, hq, hkv, d):
+    """The per-token form of QK-norm + RoPE + append (from 256 tokens) against
+    the per-(token, head) form (the same tokens in calls of 100): q and the
+    whole KV pool identical bit for bit, and every appended slot written."""
+    sevo, di = S
+    say(f"qk_norm_rope_append forms {hq}/{hkv}x{d}")
+    shape = synth.ModelShape(1, 512, hq, hkv, d, 256, 256)
+    n = 300
+    lens = np.random.default_rng(3).integers(1, 200, size=n)
+    pop = make_population(lens, shuffle=True, seed=4, extra=1)
+    model = sevo.sevo_init_model(shape, di.device_weights(shape, 5), max_position=256)
+    g = torch.Generator(device="cuda")
+    g.manual_seed(hq + d)
+    qkv = torch.randn(n, (hq + 2 * hkv) * d, device="cuda", generator=g)
+    pos = torch.from_numpy(pop.lengths.astype(np.int32)).cuda()
+    pt = torch.from_numpy(pop.page_table).cuda()
+    pool0 = torch.full((pop.n_pages, hkv, 2, 16 * d), float("nan"), dtype=torch.bfloat16,
+                       device="cuda")
+    pool_a = pool0.clone()
+    q_a = sevo.sevo_qk_norm_rope_append(model, 0, qkv, pos, pt, pool_a)
+    pool_b = pool0.clone()
+    q_b = torch.empty_like(q_a)
+    for a in range(0, n, 100):
+        b = min(n, a + 100)
+        sevo.sevo_qk_norm_rope_append(model, 0, qkv[a:b], pos[a:b], pt[a:b], pool_b, q_out=q_b[a:b])
+    torch.cuda.synchronize()
+    model.close()
+    assert torch.isfinite(q_a.float()).all()
+    assert torch.equal(q_a.view(torch.int16), q_b.view(torch.int16))
+    assert torch.equal(pool_a.view(torch.int16), pool_b.view(torch.int16))
+    # each token's slot: finite K and V in its page, the rest of the pool untouched
+    written = int(torch.isfinite(pool_a.float()).sum())
+    assert written == n * hkv * 2 * d
+
+
 def test_rmsnorm_and_embed_match_oracle(S):
     sevo, _ = S
     say("rmsnorm / embed")
