@@ -30,6 +30,15 @@ HIPCC_FLAGS = [
 ]
 
 
+# Per-source additions.  The causal prefill attention assumes no NaN in its
+# arithmetic: its masked scores are assigned -inf (which replaces a NaN score)
+# and the value slots past a sequence's last key are zeroed before use.  Under
+# IEEE NaN rules every fmaxf of the block max first canonicalised both MFMA
+# outputs, about 40 extra VALU instructions per 64-key block on a path the
+# vector ALU bounds.
+EXTRA_FLAGS = {"attn_prefill.hip": ["-fno-honor-nans"]}
+
+
 def _hipcc() -> str:
     for c in (os.environ.get("HIPCC"), "/opt/rocm/bin/hipcc", shutil.which("hipcc")):
         if c and os.path.exists(c):
@@ -62,7 +71,8 @@ def build_sevo(jobs: int = 8) -> str:
 
     def compile_one(src: str) -> str:
         obj = os.path.join(BUILD, src[:-4] + ".o")
-        _run([hipcc, *HIPCC_FLAGS, "-c", os.path.join(CSRC, src), "-o", obj])
+        _run([hipcc, *HIPCC_FLAGS, *EXTRA_FLAGS.get(src, []), "-c", os.path.join(CSRC, src), "-o",
+              obj])
         return obj
 
     with cf.ThreadPoolExecutor(max_workers=max(1, min(jobs, len(srcs)))) as ex:
