@@ -276,17 +276,33 @@ __global__ __launch_bounds__(256, 1) void gemm_large_kernel(
         }
     }
   } else if constexpr (EPI == 3) {
-    // grouped down: row = entry ent0 + row of the expert -> (token, slot)
+    // grouped down: row = entry ent0 + row of the expert -> (token, slot).
+    // The tile's 256 output rows and routing weights are staged in LDS first
+    // (read per row in the loop below, the dependent assign -> weight loads
+    // were 128 round trips per lane); every wave's direct loads have landed
+    // (wait above), so after the barrier the stage buffers are free.
+    lds_barrier();
+    int* t_row = reinterpret_cast<int*>(smem);
+    float* t_wt = reinterpret_cast<float*>(smem) + kLgBM;
+    {
+      const int row = m0 + threadIdx.x;  // 256 threads, one tile row each
+      if (row < rows) {
+        const int asg = g.assign[ent0 + row];
+        const int tok = asg / g.k, slot = asg - tok * g.k;
+        t_row[threadIdx.x] = slot * g.n + tok;
+        t_wt[threadIdx.x] = g.weights[asg];
+      }
+    }
+    lds_barrier();
 #pragma unroll
     for (int mt = 0; mt < 4; ++mt)
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
         const int row = row_of(mt, e);
         if (row >= rows) continue;
-        const int asg = g.assign[ent0 + row];
-        const int tok = asg / g.k, slot = asg - tok * g.k;
-        const float wt = g.weights[asg];
-        float* dst = out + ((size_t)slot * g.n + tok) * ldo;
+        const int lr = row - m0;
+        const float wt = t_wt[lr];
+        float* dst = out + (size_t)t_row[lr] * ldo;
 #pragma unroll
         for (int nt = 0; nt < 4; ++nt) {
           const int col = n0 + wn * 128 + nt * 32 + col_l;

@@ -109,8 +109,11 @@ hipError_t launch_moe_sum_slots(const float* part, int k, int n, int H, float* o
                                 hipStream_t st);
 // offsets [E + 1], assign [nk] (entries expert-major, token order); with
 // tile_off [E + 1]: each expert's first 256-entry tile (grouped GEMM)
+// scratch (optional, moe_plan_scratch_bytes): from 4097 entries the plan runs
+// as three launches over 1024-entry chunks instead of one workgroup
 hipError_t launch_moe_plan(const int32_t* sel, int nk, int E, int32_t* offsets, int32_t* assign,
-                           hipStream_t st, int32_t* tile_off = nullptr);
+                           hipStream_t st, int32_t* tile_off = nullptr, int32_t* scratch = nullptr);
+size_t moe_plan_scratch_bytes(int nk, int E);
 // gate/up + SwiGLU into act, then down into part
 hipError_t launch_moe_experts(const MoeExpertArgs& a, hipStream_t st);
 

@@ -186,6 +186,120 @@ __global__ __launch_bounds__(kPlanThreads) void moe_plan_kernel(const int32_t* _
   }
 }
 
+// ---- the same plan for many entries (a prefill chunk), in three launches
+// that give identical offsets, tiles and lists: (1) a workgroup per 1024-entry
+// chunk counts its entries per expert; (2) one workgroup turns the counts into
+// each (chunk, expert)'s first list position, plus offsets and tile_off;
+// (3) a workgroup per chunk ranks its entries by the same bit rows as above.
+__global__ __launch_bounds__(kPlanThreads) void moe_plan_count_kernel(
+    const int32_t* __restrict__ sel, int nk, int E, int32_t* __restrict__ ccnt) {
+  __shared__ int cnt[kMoeMaxExperts];
+  const int tid = threadIdx.x;
+  for (int e = tid; e < E; e += kPlanThreads) cnt[e] = 0;
+  __syncthreads();
+  const int r = blockIdx.x * kPlanThreads + tid;
+  if (r < nk) {
+    const int e = sel[r];
+    if (e >= 0 && e < E) atomicAdd(&cnt[e], 1);
+  }
+  __syncthreads();
+  for (int e = tid; e < E; e += kPlanThreads) ccnt[(size_t)blockIdx.x * E + e] = cnt[e];
+}
+
+// ccnt [chunks][E] counts in, first positions out.  Thread (part p, expert e)
+// walks a quarter of the chunks (E <= 256).
+__global__ __launch_bounds__(kPlanThreads) void moe_plan_scan_kernel(
+    int32_t* __restrict__ ccnt, int chunks, int E, int32_t* __restrict__ offsets,
+    int32_t* __restrict__ tile_off) {
+  constexpr int kParts = kPlanThreads / kMoeMaxExperts;
+  __shared__ int psum[kParts][kMoeMaxExperts];
+  __shared__ int ebase[kMoeMaxExperts];
+  const int tid = threadIdx.x;
+  const int p = tid / kMoeMaxExperts, e = tid % kMoeMaxExperts;
+  const int per = (chunks + kParts - 1) / kParts;
+  const int c0 = min(chunks, p * per), c1 = min(chunks, c0 + per);
+  int sum = 0;
+  if (e < E)
+    for (int c = c0; c < c1; ++c) sum += ccnt[(size_t)c * E + e];
+  psum[p][e] = sum;
+  __syncthreads();
+  if (tid < 64) {
+    // exclusive prefixes over the experts (lane j: experts 4j..4j+3): entry
+    // offsets and the first 256-entry tile of each expert
+    int v[4], tv[4], tot = 0, ttot = 0;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int x = 4 * tid + u;
+      v[u] = 0;
+      if (x < E)
+#pragma unroll
+        for (int q = 0; q < kParts; ++q) v[u] += psum[q][x];
+      tv[u] = (v[u] + kMoeGroupRows - 1) / kMoeGroupRows;
+      tot += v[u];
+      ttot += tv[u];
+    }
+    int incl = tot, tincl = ttot;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int y = __shfl_up(incl, o, kWave);
+      const int ty = __shfl_up(tincl, o, kWave);
+      if (tid >= o) {
+        incl += y;
+        tincl += ty;
+      }
+    }
+    int run = incl - tot, trun = tincl - ttot;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int x = 4 * tid + u;
+      if (x < E) {
+        ebase[x] = run;
+        offsets[x] = run;
+        if (tile_off) tile_off[x] = trun;
+      }
+      run += v[u];
+      trun += tv[u];
+    }
+    if (tid == 63) {
+      offsets[E] = incl;
+      if (tile_off) tile_off[E] = tincl;
+    }
+  }
+  __syncthreads();
+  if (e < E) {
+    int run = ebase[e];
+    for (int q = 0; q < p; ++q) run += psum[q][e];
+    for (int c = c0; c < c1; ++c) {
+      const int v = ccnt[(size_t)c * E + e];
+      ccnt[(size_t)c * E + e] = run;
+      run += v;
+    }
+  }
+}
+
+__global__ __launch_bounds__(kPlanThreads) void moe_plan_place_kernel(
+    const int32_t* __restrict__ sel, int nk, int E, const int32_t* __restrict__ cbase,
+    int32_t* __restrict__ assign) {
+  __shared__ uint32_t bits[kMoeMaxExperts][kPlanWords];
+  const int tid = threadIdx.x;
+  for (int w = tid; w < E * kPlanWords; w += kPlanThreads) (&bits[0][0])[w] = 0u;
+  __syncthreads();
+  const int r = blockIdx.x * kPlanThreads + tid;
+  const int e = r < nk ? sel[r] : -1;
+  const bool ok = e >= 0 && e < E;
+  if (ok) atomicOr(&bits[e][tid >> 5], 1u << (tid & 31));
+  __syncthreads();
+  if (ok) {
+    int rank = __popc(bits[e][tid >> 5] & ((1u << (tid & 31)) - 1u));
+    for (int w = 0; w < (tid >> 5); ++w) rank += __popc(bits[e][w]);
+    assign[cbase[(size_t)blockIdx.x * E + e] + rank] = r;
+  }
+}
+
+size_t moe_plan_scratch_bytes(int nk, int E) {
+  return (size_t)((nk + kPlanThreads - 1) / kPlanThreads) * E * 4;
+}
+
 // Grouped skinny GEMM over the selected experts.  At decode an expert sees a
 // few tokens, so the kernel is a stream of the selected experts' weights.
 // A wave takes FPW of the four 16-row fragments of one 64-row weight
@@ -363,7 +477,19 @@ hipError_t launch_moe_route(const float* part, int S, int n, int E, int k, int32
 }
 
 hipError_t launch_moe_plan(const int32_t* sel, int nk, int E, int32_t* offsets, int32_t* assign,
-                           hipStream_t st, int32_t* tile_off) {
+                           hipStream_t st, int32_t* tile_off, int32_t* scratch) {
+  if (scratch && nk > 4 * kPlanThreads) {
+    const int chunks = (nk + kPlanThreads - 1) / kPlanThreads;
+    hipLaunchKernelGGL(moe_plan_count_kernel, dim3(chunks), dim3(kPlanThreads), 0, st, sel, nk, E,
+                       scratch);
+    if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
+    hipLaunchKernelGGL(moe_plan_scan_kernel, dim3(1), dim3(kPlanThreads), 0, st, scratch, chunks,
+                       E, offsets, tile_off);
+    if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
+    hipLaunchKernelGGL(moe_plan_place_kernel, dim3(chunks), dim3(kPlanThreads), 0, st, sel, nk, E,
+                       scratch, assign);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL(moe_plan_kernel, dim3(1), dim3(kPlanThreads), 0, st, sel, nk, E, offsets,
                      assign, tile_off);
   return hipGetLastError();

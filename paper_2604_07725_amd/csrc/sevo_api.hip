@@ -920,7 +920,7 @@ struct PrefillLayout {
   size_t row, pos, x, h, qkv, q, o, a, part, hf, logits, sample, conf, ids, lps, total;
   // MoE FFN, one token chunk at a time: router logits, routing, entry lists,
   // SwiGLU rows, per-slot outputs
-  size_t m_router, m_sel, m_w, m_off, m_assign, m_act, m_slots, m_tiles;
+  size_t m_router, m_sel, m_w, m_off, m_assign, m_act, m_slots, m_tiles, m_plan;
   int rc;  // rows per LM-head chunk
   int mc;  // tokens per MoE chunk
 };
@@ -949,6 +949,7 @@ PrefillLayout prefill_layout(const sevo_model_config& c, int T, int R, int moe_c
   L.part = take(c.n_experts > 0 ? t * H * 4 : 0);  // the MoE FFN's output (dense: added in place)
   L.mc = 0;
   L.m_router = L.m_sel = L.m_w = L.m_off = L.m_assign = L.m_act = L.m_slots = L.m_tiles = 0;
+  L.m_plan = 0;
   if (c.n_experts > 0) {
     size_t mc = moe_chunk > 0 && moe_chunk < kPrefillMoeRows ? round_up(moe_chunk, 16)
                                                               : (size_t)kPrefillMoeRows;
@@ -963,6 +964,7 @@ PrefillLayout prefill_layout(const sevo_model_config& c, int T, int R, int moe_c
     L.m_act = take(mc * kk * c.expert_ffn * 2);
     L.m_slots = take(kk * mc * H * 4);
     L.m_tiles = take((E + 1) * 4);
+    L.m_plan = take(sevo::moe_plan_scratch_bytes((int)(mc * kk), (int)E));
   }
   L.hf = take(rc16 * H * 2);
   L.logits = take(rc * V * 4);
@@ -1013,7 +1015,8 @@ hipError_t run_moe_prefill_chunk(const sevo_model* m, int l, int c0, int nc,
     e = prefill_gemm(nc, E, H, SEVO_LINEAR_STORE, hc, m->w_router[l], rl, 0, st);
     if (e == hipSuccess) e = sevo::launch_moe_route(rl, 1, nc, E, k, sel, wts, st);
     if (e == hipSuccess)
-      e = sevo::launch_moe_plan(sel, nc * k, E, off, asg, st, grouped ? tiles : nullptr);
+      e = sevo::launch_moe_plan(sel, nc * k, E, off, asg, st, grouped ? tiles : nullptr,
+                                reinterpret_cast<int32_t*>(ws + L.m_plan));
   }
   if (e != hipSuccess) return e;
   ProfScope ps(SEVO_PROF_MOE_EXPERTS, st);

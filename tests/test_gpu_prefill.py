@@ -240,14 +240,16 @@ def test_prefill_confidence_full_width_reduced_depth(S):
 
 
 @pytest.mark.parametrize("lens,moe_chunk", [([300, 170], 0), ([300, 170], 64),
-                                            ([400, 300], 0), ([400, 300], 512)])
+                                            ([400, 300], 0), ([400, 300], 512),
+                                            ([1500, 700], 0)])
 def test_prefill_confidence_tiny_moe_matches_oracle(S, lens, moe_chunk):
     """The tiny MoE model (2 layers, 64 experts of FFN 64, top-4) through the
     whole engine: per-row c, per-sequence C against the oracle's prefill.  The
     expert FFN runs in one chunk or in several (the last one partial); 470
     tokens take the decode expert kernels, 700 tokens (>= 32 entries per
-    expert) the grouped large-M GEMMs, and 512 + 188 one of each.  The inputs
-    have no routing choice closer than 1e-5."""
+    expert) the grouped large-M GEMMs, and 512 + 188 one of each; 2200 tokens
+    (8800 entries) plan their lists in 1024-entry chunks (three launches).  The
+    inputs have no routing choice closer than 1e-5."""
     shape = synth.TINY_MOE
     seed = 9
     T = sum(lens)
