@@ -190,6 +190,27 @@ def test_pack_weight_rejects_bad_arguments(kw, status):
                                        None) == status
 
 
+@pytest.mark.parametrize("kw,status", [
+    (dict(rows=-1), sevo.INVALID_ARGUMENT),
+    (dict(cols=4094), sevo.INVALID_ARGUMENT),
+    (dict(n_partials=17), sevo.INVALID_ARGUMENT),
+    (dict(n_partials=-1), sevo.INVALID_ARGUMENT),
+    (dict(eps=0.0), sevo.INVALID_ARGUMENT),
+    (dict(x=0), sevo.INVALID_ARGUMENT),
+    (dict(x=(1 << 20) + 8), sevo.INVALID_ARGUMENT),                      # x not 16-byte aligned
+    (dict(partials=0), sevo.INVALID_ARGUMENT),                           # partials needed
+    (dict(gain=(1 << 22) + 2), sevo.INVALID_ARGUMENT),
+    (dict(rows=0), sevo.OK),                                             # nothing to do
+])
+def test_add_rmsnorm_rejects_bad_arguments(kw, status):
+    """Host-side validation of the residual add + RMSNorm sub-step (no launch)."""
+    a = dict(x=1 << 20, partials=1 << 21, n_partials=2, gain=1 << 22, rows=4, cols=4096,
+             eps=1e-6, out=1 << 23)
+    a.update(kw)
+    assert sevo.lib().sevo_add_rmsnorm(a["x"], a["partials"], a["n_partials"], a["gain"],
+                                       a["rows"], a["cols"], a["eps"], a["out"], None) == status
+
+
 def test_init_model_rejects_bad_config():
     cfg = sevo.ModelConfig(n_layers=1, hidden=256, n_q_heads=4, n_kv_heads=2, head_dim=64,
                            ffn=1024, vocab=4096, page_size=16, max_position=1024, qk_norm=1,
