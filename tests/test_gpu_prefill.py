@@ -73,6 +73,37 @@ def test_attn_prefill_matches_oracle(S, dims, lens, starts):
         assert err <= min(ATTN_REL_TOL, 8e-3), f"seq {s}: {err}"
 
 
+@pytest.mark.parametrize("hq,hkv", [(32, 8), (32, 4)])
+def test_attn_prefill_full_size_sampled(S, hq, hkv):
+    """The prefill attention at the engine benchmark's size and launch shape
+    (one 40960-token sequence, d = 128, the 8B and 30B-A3B head layouts) on
+    sampled query rows, each computed by the oracle over its keys 0..t."""
+    sevo, di = S
+    T, d = 40960, 128
+    shape = _shape(hq, hkv, d)
+    seed = 91 + hkv
+    say(f"attn prefill full size {hq}/{hkv} x {d}, {T} tokens")
+    pop = make_population([T], shuffle=True, seed=seed)
+    kvp = di.device_pools(shape, seed, pop.n_pages, layers=[0])[0]
+    q = di.device_q(shape, seed, T)
+    pt = torch.from_numpy(pop.page_table.astype(np.int32)).cuda()
+    ss = torch.tensor([0, T], dtype=torch.int32, device="cuda")
+    out = sevo.sevo_attn_prefill(q, kvp, pt, ss, T)
+    rows = [0, 1, 63, 64, 4095, 20011, 40958, 40959]
+    got = to_np(out[rows])
+    del kvp, q, out
+    torch.cuda.empty_cache()
+    pool = synth.pool_pages(synth.kv_spec(shape, seed, 0, pop.n_pages), np.arange(pop.n_pages))
+    K, V = od.gather_kv(pool, pop.page_table[0], T)
+    qspec = synth.q_spec(shape, seed, T)
+    for i, t in enumerate(rows):
+        qt = synth.host_values(qspec, offset=t * hq * d, count=hq * d).reshape(hq, d)
+        ref = od.attention_dense(qt, K[:, :t + 1], V[:, :t + 1], d ** -0.5)
+        err = attn_rel_err(got[i], ref)
+        say(f"  row {t}: rel err {err:.2e}")
+        assert err <= min(ATTN_REL_TOL, 8e-3), f"row {t}: {err}"
+
+
 def test_attn_prefill_page_permutation_bit_exact(S):
     """The result depends only on the logical key order: moving the pages to
     other physical slots gives identical bits."""
