@@ -406,6 +406,47 @@ def _linear_inputs(sevo, m, n_out, k, mode):
     return x, w, wp, xh, wh
 
 
+@pytest.mark.parametrize("n_out,k,mode,xt", [(24576, 4096, 2, 1), (6144, 4096, 0, 0)])
+def test_linear_large_m_full_size_sampled(S, n_out, k, mode, xt):
+    """The large-M GEMM at the confidence engine's size (M = 40960 tokens: the
+    whole tile grid and its XCD-aware order): gate/up + SwiGLU on tiled
+    activations and the QKV store on row-major ones, on sampled rows against
+    float64 products of those rows."""
+    sevo, _ = S
+    m = 40960
+    say(f"linear full size m={m} n={n_out} k={k} mode={mode} x_tiled={xt}")
+    x = torch.empty(m, k, dtype=torch.bfloat16, device="cuda")
+    w = torch.empty(n_out, k, dtype=torch.bfloat16, device="cuda")
+    kx, kw = synth.tensor_key(m, 53, k), synth.tensor_key(n_out, 54, k)
+    sevo.sevo_fill_normal_bf16(x, kx, 0, 1.0)
+    sevo.sevo_fill_normal_bf16(w, kw, 0, 0.02)
+    wp = sevo.sevo_pack_weight(w, sevo.PACK_GATE_UP if mode == 2 else sevo.PACK_PLAIN)
+    del w
+    if xt:
+        xb = tile_activations_host(bf16_bits(x).reshape(m, k))
+        x = torch.from_numpy(xb.view(np.int16)).cuda().view(torch.bfloat16)
+    out = sevo.sevo_linear(x, wp, mode=mode, x_tiled=bool(xt), m=m)
+    torch.cuda.synchronize()
+    rows = np.array([0, 1, 255, 256, 12345, 20479, 40703, 40959])
+    if mode == 2:
+        got = to_np(out)[rows]
+    else:
+        got = out[torch.from_numpy(rows).cuda()].double().cpu().numpy()
+    del x, wp, out
+    torch.cuda.empty_cache()
+    wh = synth.host_values(synth.TensorSpec((n_out, k), kw, 0.02)).reshape(n_out, k)
+    xspec = synth.TensorSpec((m, k), kx, 1.0)
+    xh = np.stack([synth.host_values(xspec, offset=int(r) * k, count=k) for r in rows])
+    y = xh.astype(np.float64) @ wh.astype(np.float64).T
+    if mode == 2:
+        F = n_out // 2
+        ref = od.silu(y[:, :F]) * y[:, F:]
+        assert np.all(np.abs(got - ref) <= 2 ** -8 * np.abs(ref) + 1e-4 * np.abs(ref).max())
+    else:
+        scale = np.sqrt(k) * 0.02
+        np.testing.assert_allclose(got, y, rtol=0, atol=2e-5 * scale + 1e-6 * np.abs(y).max())
+
+
 @pytest.mark.parametrize("m,n_out,k,mode,ks,xt", LINEAR_CASES)
 def test_linear_matches_float64_matmul(S, m, n_out, k, mode, ks, xt):
     sevo, _ = S
