@@ -197,6 +197,51 @@ def _engine_case(S, shape, seed, lens, scored, conf_k, starts=None, moe_chunk=0)
     return out, pop, toks, seq_starts, starts
 
 
+def test_prefill_confidence_full_size_batch_invariance(S):
+    """The dense 8B engine at the benchmark's size (36 layers, 40960 tokens as
+    sequences of 24576 and 16384, every row scored): each row's c equals, bit
+    for bit, its value with the sequence run alone, and so does each C (rows
+    of different sequences never interact; a property at any size), all
+    finite, and C is the mean of its sequence's c."""
+    sevo, di = S
+    shape = synth.DENSE_8B
+    lens = [24576, 16384]
+    seed = 17
+    say(f"prefill confidence full size, dense 8B, sequences {lens}")
+    pop = make_population(lens, shuffle=True, seed=seed)
+    rng = np.random.default_rng(seed)
+    toks = [rng.integers(0, shape.vocab, size=n).astype(np.int32) for n in lens]
+    model = sevo.sevo_init_model(shape, di.device_weights(shape, seed),
+                                 max_position=max(lens) + 1)
+    # every slot the prefill reads it writes first; later slots may hold anything
+    kvp = [torch.empty(pop.n_pages, shape.n_kv_heads, 2, 16 * shape.head_dim,
+                       dtype=torch.bfloat16, device="cuda") for _ in range(shape.n_layers)]
+
+    def run(seqs):
+        t = np.concatenate([toks[i] for i in seqs])
+        ss = np.concatenate([[0], np.cumsum([lens[i] for i in seqs])]).astype(np.int32)
+        pt = np.ascontiguousarray(pop.page_table[seqs]).astype(np.int32)
+        buf = sevo.PrefillBuffers(model, torch.from_numpy(t).cuda(), torch.from_numpy(ss).cuda(),
+                                  torch.from_numpy(pt).cuda(), kvp,
+                                  torch.arange(len(t), dtype=torch.int32, device="cuda"), 20,
+                                  max(lens[i] for i in seqs))
+        conf = buf.run()
+        torch.cuda.synchronize()
+        return conf.cpu().numpy(), buf.out_row_conf[:len(t)].cpu().numpy()
+
+    c01, r01 = run([0, 1])
+    c0, r0 = run([0])
+    c1, r1 = run([1])
+    model.close()
+    say(f"  C = {c01}, alone {c0} {c1}")
+    assert np.isfinite(r01).all() and np.isfinite(c01).all()
+    np.testing.assert_array_equal(r01[:lens[0]], r0)
+    np.testing.assert_array_equal(r01[lens[0]:], r1)
+    np.testing.assert_array_equal(c01, np.concatenate([c0, c1]))
+    np.testing.assert_allclose(c01, [r0.astype(np.float64).mean(), r1.astype(np.float64).mean()],
+                               rtol=1e-5)
+
+
 def test_prefill_confidence_tiny_matches_oracle(S):
     """Two sequences of the tiny model through the whole engine: per-row c
     (Eq. 1), per-sequence C (Eq. 2) and every appended K/V slot against the
