@@ -239,7 +239,7 @@ sevo_status sevo_attn_prefill(const sevo_prefill_attn_args* a, void* stream);
  * causal prefill attention of sevo_attn_prefill; the keys and values of every
  * token are written into the pools (a KV cache a decode can continue from).
  * A mixture-of-experts model runs its expert FFN on chunks of moe_chunk
- * tokens (rounded up to 16; 0 or more than 16384 = 16384): routing, expert
+ * tokens (rounded up to 16; 0 or more than 65536 = 65536): routing, expert
  * lists and the per-slot outputs of a chunk live in the workspace, and each
  * token's k expert outputs are summed in slot order.
  * Then, for each scored row r -- a packed token index whose next-token
@@ -279,7 +279,7 @@ typedef struct {
   float* out_row_conf;
   void* workspace;
   size_t workspace_bytes;
-  int32_t moe_chunk;  /* MoE models: tokens per expert-FFN chunk, 0 = 16384 (the
+  int32_t moe_chunk;  /* MoE models: tokens per expert-FFN chunk, 0 = 65536 (the
                          largest; sevo_prefill_workspace_bytes sizes for it);
                          negative: INVALID_ARGUMENT */
 } sevo_prefill_args;

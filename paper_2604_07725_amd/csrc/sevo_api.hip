@@ -914,7 +914,7 @@ namespace {
 
 constexpr int kPrefillLogitRows = 4096;  // scored rows per LM-head chunk
 
-constexpr int kPrefillMoeRows = 16384;  // tokens per MoE FFN chunk (a multiple of 16)
+constexpr int kPrefillMoeRows = 65536;  // tokens per MoE FFN chunk (a multiple of 16)
 
 struct PrefillLayout {
   size_t row, pos, x, h, qkv, q, o, a, part, hf, logits, sample, conf, ids, lps, total;
