@@ -30,7 +30,8 @@
 //     per-lane source offsets;
 //   * blocks entirely above a wave's queries skip their MFMAs (the wave still
 //     loads its part of the block and meets the barriers); workgroups are
-//     launched latest (longest) query blocks first;
+//     launched latest (longest) query blocks first, the kv head varying
+//     fastest so each head stays on the same XCDs;
 //   * the slots of a sequence's last page past its last key may hold anything
 //     (NaN included): in the block holding that key they are zeroed in the V
 //     tiles (the scores there are masked; K needs nothing).
@@ -62,13 +63,18 @@ __global__ __launch_bounds__(64 * NW, 1) void attn_prefill_kernel(PrefillAttnArg
   __shared__ __attribute__((aligned(1024))) bf16_t smem[kPfStages * STAGE_ELEMS];
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int sq = blockIdx.z, c = blockIdx.y;
+  // the kv head is the fastest-varying part of the launch order, so the
+  // round-robin placement of workgroups on the 8 XCDs keeps a head's keys and
+  // values in the L2 of the same XCD(s); query groups go latest first
+  const int sq = blockIdx.z;
+  const int lin = blockIdx.x + gridDim.x * blockIdx.y;  // gridDim.y == hkv
+  const int c = lin % a.hkv;
   const int g = a.hq / a.hkv;
   const int seq0 = a.seq_starts[sq];
   const int L = a.seq_starts[sq + 1] - seq0;
   const int p0 = a.start_pos ? a.start_pos[sq] : 0;
   const int units = ((L + UQ - 1) / UQ) * g;
-  const int ug = gridDim.x - 1 - blockIdx.x;
+  const int ug = gridDim.x - 1 - lin / a.hkv;
   if (L <= 0 || NW * ug >= units) return;
   const int u = NW * ug + wave;
   const bool active = u < units;
