@@ -146,7 +146,12 @@ typedef struct {
 
 typedef struct sevo_model sevo_model;
 
-/* Validates the shape, copies the pointer tables and builds the RoPE cos/sin
+/* Creates the model a population decodes with.  The paper serves its own
+ * trained models and states no layer details; the decoder here is the pre-norm
+ * GQA transformer of the Qwen3 family that the workloads are shaped after
+ * (dense SwiGLU or mixture-of-experts FFN; the models of the System
+ * Implementation subsection and the generation hyper-parameter table).
+ * Validates the shape, copies the pointer tables and builds the RoPE cos/sin
  * table (angles in double, stored fp32) on the current device.
  * Errors: INVALID_ARGUMENT, UNSUPPORTED, OUT_OF_MEMORY, HIP. */
 sevo_status sevo_init_model(const sevo_model_config* cfg, const sevo_weights* w,
@@ -155,7 +160,10 @@ void sevo_free_model(sevo_model* m);
 
 /* ------------------------------------------------------------------ attention */
 
-/* Paged GQA split-KV decode attention (one query token per candidate):
+/* Paged GQA split-KV decode attention (one query token per candidate): the
+ * attention of one decode step of LLM aggregation, where a candidate's context
+ * is the K concatenated candidates of its group (Recombination paragraph of the
+ * method section; Algorithm 1, aggregation line):
  *   o[i][j] = softmax_t(scale * q[i][j] . K_i[c][t]) V_i[c][t],  t < seq_lens[i],
  * c = j / (n_q_heads / n_kv_heads).  Each candidate's pages are cut into
  * splits of ceil(max_pages / S) logical pages, where S is num_splits raised as
@@ -297,7 +305,8 @@ size_t sevo_prefill_workspace_bytes(const sevo_model* m, int32_t total_tokens, i
  * (v >> 2, position_i, uid_i lo, uid_i hi) and key (seed lo, seed hi).  Noise
  * is keyed by candidate uid and position, never by call count, so a resumed or
  * re-ordered population draws the same tokens.  T == 0: greedy argmax, logprob
- * under T = 1.  T < 0 or non-finite: INVALID_ARGUMENT.
+ * under T = 1.  T < 0 or non-finite: INVALID_ARGUMENT.  A row with no
+ * comparable perturbed value (every logit NaN) gets id -1 and logprob NaN.
  *   logits fp32 [n][ld] (first vocab entries used); cand_uid uint64 [n];
  *   positions int32 [n];  out_tokens int32 [n];  out_logprobs fp32 [n].
  * Truncated sampling (the top-k / top-p / min-p rows of the generation
@@ -356,7 +365,10 @@ sevo_status sevo_group_confidence(const float* conf_sum, const int32_t* token_co
 
 /* ------------------------------------------------------------------ decode step */
 
-/* One decode step of the whole population through the model:
+/* One decode step of the whole population through the model (the step that
+ * LLM aggregation repeats for every candidate: the Recombination paragraph of
+ * the method section and Algorithm 1's aggregation line; the returned
+ * log-probabilities are the per-token terms of Eq. 1):
  *   x = embed[token];  per layer: h = RMSNorm(x) g_attn;  [q|k|v] = h W_qkv^T;
  *   (qk_norm) q, k <- per-head RMSNorm * g_q / g_k;  RoPE(q, k) at p_i;
  *   append k, v as key number p_i;  o = attention over keys 0..p_i;
@@ -371,7 +383,10 @@ sevo_status sevo_group_confidence(const float* conf_sum, const int32_t* token_co
  *   out_tokens int32 [n];  out_logprobs fp32 [n];
  *   out_logits fp32 [n][vocab] or NULL (then kept in the workspace);
  *   top_k, top_p, min_p: truncated sampling; conf_topk, out_conf, conf_sum:
- *   the sampler's self-confidence (both above).
+ *   the sampler's self-confidence (both above);
+ *   out_hidden fp32 [n_layers + 1][n][hidden] or NULL: the residual stream x
+ *   entering each layer (entry l) and after the last layer (entry n_layers),
+ *   for layer-by-layer verification; one device-to-device copy per entry.
  * The library never changes positions or page tables: the caller advances p_i
  * and allocates pages.  Errors: INVALID_ARGUMENT, UNSUPPORTED,
  * WORKSPACE_TOO_SMALL, HIP. */
@@ -398,6 +413,7 @@ typedef struct {
   float* conf_sum;
   void* workspace;
   size_t workspace_bytes;
+  float* out_hidden; /* nullable, see above */
 } sevo_step_args;
 
 sevo_status sevo_decode_step(sevo_model* m, const sevo_step_args* a, void* stream);

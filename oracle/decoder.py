@@ -160,20 +160,22 @@ def v_tile_offset(slot, dim):
 
 
 def gather_kv(kv_pool, pages, n_keys):
-    """Logical K, V [hkv, n_keys, d] of one candidate from its page list."""
+    """Logical K, V [hkv, n_keys, d] of one candidate from its page list.
+
+    Logical key t is slot t % 16 of physical page pages[t // 16].  The offsets
+    of the tile layout are read as index decompositions: a K tile element
+    (s, e) at ((e // 32) * 16 + s) * 32 + e % 32 is entry [e // 32][s][e % 32]
+    of the tile viewed as [d / 32][16][32]; a V tile element (s, e) at
+    e * 16 + s is entry [e][s] of the tile viewed as [d][16].
+    """
     kv = np.asarray(kv_pool)
     hkv, d = kv.shape[1], kv.shape[3] // PAGE
-    t = np.arange(n_keys)
-    pg = np.asarray(pages, np.int64)[t // PAGE]
-    sl = t % PAGE
-    e = np.arange(d)
-    K = np.empty((hkv, n_keys, d))
-    V = np.empty((hkv, n_keys, d))
-    for p in np.unique(pg):             # one physical page at a time
-        sel = np.nonzero(pg == p)[0]
-        s = sl[sel]
-        K[:, sel, :] = kv[p, :, 0][:, k_tile_offset(s[:, None], e[None, :])]
-        V[:, sel, :] = kv[p, :, 1][:, v_tile_offset(s[:, None], e[None, :])]
+    pg = np.asarray(pages, np.int64)[: -(-n_keys // PAGE)]
+    tiles = kv[pg]                      # [n_pages][hkv][2][16 d], logical page order
+    K = tiles[:, :, 0].reshape(len(pg), hkv, d // 32, PAGE, 32).transpose(1, 0, 3, 2, 4)
+    V = tiles[:, :, 1].reshape(len(pg), hkv, d, PAGE).transpose(1, 0, 3, 2)
+    K = K.reshape(hkv, len(pg) * PAGE, d)[:, :n_keys].astype(np.float64)
+    V = V.reshape(hkv, len(pg) * PAGE, d)[:, :n_keys].astype(np.float64)
     return K, V
 
 
@@ -326,7 +328,7 @@ def lm_logits(shape, final_norm, lm_head, x, mirror=True, chunk=16384):
 
 
 def logprob_sample(logits, temperature, seed, uids, positions, noise=None,
-                   decision_dtype=np.float32):
+                   decision_dtype=np.float32, details=None):
     """Gumbel-max sample and its log-probability, per candidate.
 
     z = logits / T;  id = argmax_v (z_v + G_v) with ties to the lowest v;
@@ -334,7 +336,9 @@ def logprob_sample(logits, temperature, seed, uids, positions, noise=None,
     from T = 1.  The argmax decision is taken in ``decision_dtype`` (the
     kernel's fp32); ``gap`` is the float64 top-1 minus top-2 perturbed value,
     so a caller can tell decisions that rounding may flip.
-    ``noise`` [N, V] overrides the Philox noise (for pins).
+    ``noise`` [N, V] overrides the Philox noise (for pins).  ``details`` (a
+    dict) receives "pert" [N, V], the float64 perturbed values the decision is
+    taken on, and "logp" [N, V], log_softmax(z) of every vocabulary entry.
     Returns ids int64 [N], lps float64 [N], gaps float64 [N].
     """
     logits = np.asarray(logits, np.float64)
@@ -342,6 +346,9 @@ def logprob_sample(logits, temperature, seed, uids, positions, noise=None,
     ids = np.empty(N, np.int64)
     lps = np.empty(N)
     gaps = np.empty(N)
+    if details is not None:
+        details["pert"] = np.empty((N, V))
+        details["logp"] = np.empty((N, V))
     for i in range(N):
         if temperature == 0:
             z = logits[i]
@@ -357,11 +364,14 @@ def logprob_sample(logits, temperature, seed, uids, positions, noise=None,
         top2 = np.partition(pert, V - 2)[V - 2:] if V > 1 else np.array([-np.inf, pert[0]])
         gaps[i] = float(top2.max() - top2.min())
         lps[i] = log_softmax(z)[ids[i]]
+        if details is not None:
+            details["pert"][i] = pert
+            details["logp"][i] = log_softmax(z)
     return ids, lps, gaps
 
 
 def decode_step(shape, weights, kv_pools, page_table, tokens, positions, uids,
-                seed, temperature, mirror=True, layers=None, stats=None):
+                seed, temperature, mirror=True, layers=None, stats=None, details=None):
     """One decode step for a population.
 
     weights: mapping with "embed" [V, H] (row-indexable), "lm_head" [V, H],
@@ -369,6 +379,7 @@ def decode_step(shape, weights, kv_pools, page_table, tokens, positions, uids,
     attn_norm, w_qkv, q_norm, k_norm, w_o, ffn_norm, w_gate_up, w_down).
     kv_pools: per-layer pools in the paged layout (float arrays, modified in
     place by the KV append).  positions p_i = keys already cached.
+    ``details`` is handed to ``logprob_sample``.
     Returns dict(ids, lps, gaps, logits, x).
     """
     tokens = np.asarray(tokens, np.int64)
@@ -378,7 +389,7 @@ def decode_step(shape, weights, kv_pools, page_table, tokens, positions, uids,
         x = decoder_layer(shape, weights["layers"][l], x, positions, kv_pools[l], page_table,
                           mirror, stats)
     logits = lm_logits(shape, weights["final_norm"], weights["lm_head"], x, mirror)
-    ids, lps, gaps = logprob_sample(logits, temperature, seed, uids, positions)
+    ids, lps, gaps = logprob_sample(logits, temperature, seed, uids, positions, details=details)
     return {"ids": ids, "lps": lps, "gaps": gaps, "logits": logits, "x": x}
 
 
@@ -463,7 +474,7 @@ def group_confidence(cand_conf, groups):
 
 
 def truncated_logprob_sample(logits, temperature, seed, uids, positions, top_k, top_p=1.0,
-                             min_p=0.0, decision_dtype=np.float32):
+                             min_p=0.0, decision_dtype=np.float32, details=None):
     """Top-k sampling with min-p and top-p applied inside the top-k set.
 
     The kept list is the top_k logits in (value desc, index asc) order -- a
@@ -475,7 +486,9 @@ def truncated_logprob_sample(logits, temperature, seed, uids, positions, top_k, 
     ``logprob_sample``; lp = z_id - logsumexp(kept z).  T == 0 takes the first
     entry and evaluates the truncation and lp at T = 1.  Decisions in
     ``decision_dtype``; ``gap`` = float64 top-1 minus top-2 perturbed value
-    among the kept entries (inf when one is kept).
+    among the kept entries (inf when one is kept).  ``details`` (a dict)
+    receives "pert" and "logp" [N, V] as in ``logprob_sample``, over the kept
+    entries (-inf at every other entry).
     Returns ids int64 [N], lps float64 [N], gaps float64 [N].
     """
     logits = np.asarray(logits, np.float64)
@@ -484,6 +497,9 @@ def truncated_logprob_sample(logits, temperature, seed, uids, positions, top_k, 
     ids = np.empty(N, np.int64)
     lps = np.empty(N)
     gaps = np.empty(N)
+    if details is not None:
+        details["pert"] = np.full((N, V), -np.inf)
+        details["logp"] = np.full((N, V), -np.inf)
     for i in range(N):
         order = np.lexsort((np.arange(V), -logits[i]))[:int(top_k)]
         z = logits[i][order] / tdiv
@@ -513,5 +529,9 @@ def truncated_logprob_sample(logits, temperature, seed, uids, positions, top_k, 
         ids[i] = int(kv[best])
         srt = np.sort(pert)[::-1]
         gaps[i] = float(srt[0] - srt[1]) if len(srt) > 1 else np.inf
-        lps[i] = kz[best] - (kz.max() + np.log(np.sum(np.exp(kz - kz.max()))))
+        lse = kz.max() + np.log(np.sum(np.exp(kz - kz.max())))
+        lps[i] = kz[best] - lse
+        if details is not None:
+            details["pert"][i, kv] = pert
+            details["logp"][i, kv] = kz - lse
     return ids, lps, gaps

@@ -329,7 +329,7 @@ __global__ __launch_bounds__(256) void sample_partial_kernel(
 
 __global__ __launch_bounds__(256) void sample_final_kernel(
     const SamplePartial* __restrict__ part, int nchunks, const float* __restrict__ logits,
-    int64_t ld, float temp, int32_t* __restrict__ out_tokens, float* __restrict__ out_lp,
+    int vocab, int64_t ld, float temp, int32_t* __restrict__ out_tokens, float* __restrict__ out_lp,
     int conf_k, const float* __restrict__ topk, float* __restrict__ out_conf,
     float* __restrict__ conf_sum) {
   __shared__ SamplePartial red[4];
@@ -348,10 +348,17 @@ __global__ __launch_bounds__(256) void sample_final_kernel(
   p = block_merge<4>(p, red);
   if (threadIdx.x == 0) {
     const int id = p.idx;
-    float zid = logits[(size_t)i * ld + id];
-    if (temp != 0.f && temp != 1.f) zid = zid / temp;
-    out_tokens[i] = id;
-    out_lp[i] = zid - (p.m + logf(p.s));
+    if (id < 0 || id >= vocab) {
+      // no perturbed value compared greater than -inf (every logit NaN): no
+      // token, and the logits are not read at the missing index
+      out_tokens[i] = -1;
+      out_lp[i] = __builtin_nanf("");
+    } else {
+      float zid = logits[(size_t)i * ld + id];
+      if (temp != 0.f && temp != 1.f) zid = zid / temp;
+      out_tokens[i] = id;
+      out_lp[i] = zid - (p.m + logf(p.s));
+    }
   }
   if (conf_k > 0) {
     // merge the chunks' lists: wave w takes a contiguous quarter of them (entry
@@ -626,8 +633,9 @@ __global__ __launch_bounds__(256) void sample_trunc_final_kernel(
     ez += __shfl_xor(ez, o, kWave);
   }
   if (lane == 0) {
-    out_tokens[i] = pid;
-    out_lp[i] = zme - (fv[0] / tdiv + logf(ez));
+    const bool found = pid >= 0 && pid != 0x7FFFFFFF;   // a kept entry won
+    out_tokens[i] = found ? pid : -1;
+    out_lp[i] = found ? zme - (fv[0] / tdiv + logf(ez)) : __builtin_nanf("");
     if (conf_k > 0) {
       float sum = 0.f;
       for (int r = 0; r < conf_k; ++r) sum += fv[r];
@@ -690,8 +698,8 @@ hipError_t launch_logprob_sample(const float* logits, int n, int vocab, int64_t 
                      logits, vocab, ld, temp, seed, uid, positions, part, conf_k, topk);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(sample_final_kernel, dim3(n), dim3(256), 0, st, part, nchunks, logits, ld,
-                     temp, out_tokens, out_lp, conf_k, topk, out_conf, conf_sum);
+  hipLaunchKernelGGL(sample_final_kernel, dim3(n), dim3(256), 0, st, part, nchunks, logits, vocab,
+                     ld, temp, out_tokens, out_lp, conf_k, topk, out_conf, conf_sum);
   return hipGetLastError();
 }
 

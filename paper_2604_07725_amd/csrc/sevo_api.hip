@@ -735,6 +735,8 @@ SEVO_API sevo_status sevo_decode_step(sevo_model* m, const sevo_step_args* a, vo
   if (!aligned16(a->workspace)) return fail(SEVO_ERR_INVALID_ARGUMENT, "misaligned workspace");
   if (a->out_logits && !aligned16(a->out_logits))
     return fail(SEVO_ERR_INVALID_ARGUMENT, "misaligned out_logits");
+  if (a->out_hidden && !aligned16(a->out_hidden))
+    return fail(SEVO_ERR_INVALID_ARGUMENT, "misaligned out_hidden");
   for (int l = 0; l < c.n_layers; ++l)
     if (!a->kv_pools[l] || !aligned16(a->kv_pools[l]))
       return fail(SEVO_ERR_INVALID_ARGUMENT, "layer %d: null or misaligned KV pool", l);
@@ -770,6 +772,14 @@ SEVO_API sevo_status sevo_decode_step(sevo_model* m, const sevo_step_args* a, vo
                            x, st);
   }
   if (e != hipSuccess) return hip_fail(e, "embed");
+  // x as it enters layer l (after the add that closes layer l - 1), or after
+  // the last layer: entry l of out_hidden
+  const size_t x_bytes = (size_t)n * H * sizeof(float);
+  auto keep_hidden = [&](int l) {
+    return a->out_hidden ? hipMemcpyAsync(a->out_hidden + (size_t)l * n * H, x, x_bytes,
+                                          hipMemcpyDeviceToDevice, st)
+                         : hipSuccess;
+  };
   int pending = 0;  // split partials of the last down projection, not yet in x
   for (int l = 0; l < c.n_layers; ++l) {
     {
@@ -778,6 +788,7 @@ SEVO_API sevo_status sevo_decode_step(sevo_model* m, const sevo_step_args* a, vo
                                    static_cast<const sevo::bf16_t*>(m->attn_norm[l]), n, H,
                                    c.rms_eps, h, st);
     }
+    if (e == hipSuccess) e = keep_hidden(l);
     if (e == hipSuccess) {
       ProfScope ps(SEVO_PROF_QKV, st);
       e = sevo::launch_linear_partials(n, qkvd, H, H, 1, L.p_qkv, h,
@@ -850,6 +861,7 @@ SEVO_API sevo_status sevo_decode_step(sevo_model* m, const sevo_step_args* a, vo
                                  static_cast<const sevo::bf16_t*>(m->final_norm), n, H, c.rms_eps,
                                  h, st);
   }
+  if (e == hipSuccess) e = keep_hidden(c.n_layers);
   if (e == hipSuccess) {
     ProfScope ps(SEVO_PROF_LM_HEAD, st);
     e = sevo::launch_linear_partials(n, c.vocab, H, H, 1, L.p_lm, h,

@@ -93,7 +93,7 @@ class StepArgs(C.Structure):
                 ("temperature", f32), ("num_splits", i32), ("out_tokens", vp),
                 ("out_logprobs", vp), ("out_logits", vp), ("top_k", i32), ("top_p", f32),
                 ("min_p", f32), ("conf_topk", i32), ("out_conf", vp), ("conf_sum", vp),
-                ("workspace", vp), ("workspace_bytes", sz)]
+                ("workspace", vp), ("workspace_bytes", sz), ("out_hidden", vp)]
 
 
 class LinearArgs(C.Structure):
@@ -464,10 +464,13 @@ class StepBuffers:
 
     def __init__(self, model: Model, tokens, positions, page_table, kv_pools, cand_uid,
                  seed, temperature, num_splits=0, keep_logits=False, workspace=None,
-                 conf_topk=0, conf_sum=None, top_k=0, top_p=1.0, min_p=0.0):
+                 conf_topk=0, conf_sum=None, top_k=0, top_p=1.0, min_p=0.0,
+                 keep_hidden=False):
         n = tokens.shape[0]
         dev = tokens.device
         self.model = model
+        self.out_hidden = (torch.empty(model.shape.n_layers + 1, n, model.shape.hidden,
+                                       dtype=torch.float32, device=dev) if keep_hidden else None)
         self.out_tokens = torch.empty(n, dtype=torch.int32, device=dev)
         self.out_logprobs = torch.empty(n, dtype=torch.float32, device=dev)
         self.out_logits = (torch.empty(n, model.shape.vocab, dtype=torch.float32, device=dev)
@@ -488,7 +491,8 @@ class StepBuffers:
             out_logprobs=_p(self.out_logprobs), out_logits=_p(self.out_logits),
             top_k=int(top_k), top_p=float(top_p), min_p=float(min_p),
             conf_topk=int(conf_topk), out_conf=_p(self.out_conf), conf_sum=_p(conf_sum),
-            workspace=_p(self.workspace), workspace_bytes=self.workspace.numel())
+            workspace=_p(self.workspace), workspace_bytes=self.workspace.numel(),
+            out_hidden=_p(self.out_hidden))
 
     def run(self, stream=None):
         _check(lib().sevo_decode_step(self.model.handle, C.byref(self.args), _stream(stream)))
@@ -497,14 +501,19 @@ class StepBuffers:
 
 def sevo_decode_step(model: Model, tokens, positions, page_table, kv_pools, cand_uid,
                      seed, temperature=1.0, num_splits=0, keep_logits=False, stream=None,
-                     conf_topk=0, conf_sum=None, top_k=0, top_p=1.0, min_p=0.0):
-    """One decode step of the population; returns (ids, logprobs[, logits][, conf])."""
+                     conf_topk=0, conf_sum=None, top_k=0, top_p=1.0, min_p=0.0,
+                     keep_hidden=False, workspace=None):
+    """One decode step of the population; returns (ids, logprobs[, logits][, conf]
+    [, hidden]), hidden = the residual stream entering each layer and after the
+    last [n_layers + 1, n, hidden].  ``workspace``: a caller's uint8 device
+    buffer of at least sevo_step_workspace_bytes (else one is allocated)."""
     b = StepBuffers(model, tokens, positions, page_table, kv_pools, cand_uid, seed,
                     temperature, num_splits, keep_logits, conf_topk=conf_topk, conf_sum=conf_sum,
-                    top_k=top_k, top_p=top_p, min_p=min_p)
+                    top_k=top_k, top_p=top_p, min_p=min_p, keep_hidden=keep_hidden,
+                    workspace=workspace)
     ids, lps = b.run(stream)
     out = (ids, lps) + ((b.out_logits,) if keep_logits else ()) + \
-        ((b.out_conf,) if conf_topk else ())
+        ((b.out_conf,) if conf_topk else ()) + ((b.out_hidden,) if keep_hidden else ())
     return out
 
 

@@ -77,6 +77,10 @@ def _lib():
             fn.argtypes = [ptr_t, ctypes.c_int64, ctypes.c_uint64, ctypes.c_int64,
                            ctypes.c_float, ctypes.c_float, ctypes.c_int]
             fn.restype = None
+        lib.synth_fill_pages_as_f32.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
+                                                ctypes.c_int64, ctypes.c_uint64, ctypes.c_float,
+                                                ctypes.c_float, ctypes.c_int]
+        lib.synth_fill_pages_as_f32.restype = None
         lib.synth_mix64.argtypes = [ctypes.c_uint64]
         lib.synth_mix64.restype = ctypes.c_uint64
         _LIB = lib
@@ -387,10 +391,15 @@ def host_bits(spec: TensorSpec) -> np.ndarray:
 def pool_pages(spec: TensorSpec, pages: np.ndarray) -> np.ndarray:
     """Values of selected physical pages of a KV pool spec -> [len(pages), ...]."""
     per_page = int(np.prod(spec.shape[1:]))
+    pages = np.ascontiguousarray(pages, np.int64)
+    if pages.size and (pages.min() < 0 or pages.max() >= spec.shape[0]):
+        raise IndexError("page id outside the pool")
     out = np.empty((len(pages),) + tuple(spec.shape[1:]), np.float32)
-    flat = out.reshape(len(pages), per_page)
-    for j, p in enumerate(np.asarray(pages, np.int64)):
-        flat[j] = fill_values(per_page, spec.key, int(p) * per_page, spec.std, spec.mean)
+    if len(pages):
+        _lib().synth_fill_pages_as_f32(out.ctypes.data, pages.ctypes.data, len(pages), per_page,
+                                       spec.key, float(ih_mul(spec.std)),
+                                       0.0 if spec.mean is None else float(spec.mean),
+                                       0 if spec.mean is None else 1)
     return out
 
 

@@ -60,3 +60,21 @@ void synth_fill_bf16_as_f32(float* out, int64_t count, uint64_t key, int64_t off
     memcpy(&out[i], &b, 4);
   }
 }
+
+/* Selected pages of a paged tensor: out[j * per_page + i] = the fp32 value of
+ * element pages[j] * per_page + i, for j < n_sel and i < per_page. */
+void synth_fill_pages_as_f32(float* out, const int64_t* pages, int64_t n_sel, int64_t per_page,
+                             uint64_t key, float mul, float add, int use_add) {
+#pragma omp parallel for schedule(static)
+  for (int64_t j = 0; j < n_sel; ++j)
+    for (int64_t i = 0; i < per_page; ++i) {
+      const int64_t el = pages[j] * per_page + i;
+      uint64_t r = mix64(key + (uint64_t)(el + 1) * 0x9E3779B97F4A7C15ULL);
+      int32_t s = (int32_t)(r & 0xFFFF) + (int32_t)((r >> 16) & 0xFFFF) +
+                  (int32_t)((r >> 32) & 0xFFFF) + (int32_t)(r >> 48);
+      volatile float v = (float)(s - 131070) * mul;
+      float w = use_add ? (float)(v + add) : (float)v;
+      uint32_t b = ((uint32_t)f32_to_bf16_rne(w)) << 16;
+      memcpy(&out[j * per_page + i], &b, 4);
+    }
+}

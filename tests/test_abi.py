@@ -42,7 +42,7 @@ int main(void) {
   P(sevo_step_args, kv_pools) P(sevo_step_args, seed) P(sevo_step_args, temperature)
   P(sevo_step_args, num_splits) P(sevo_step_args, out_logits) P(sevo_step_args, top_p)
   P(sevo_step_args, conf_topk)
-  P(sevo_step_args, out_conf) P(sevo_step_args, workspace_bytes)
+  P(sevo_step_args, out_conf) P(sevo_step_args, workspace_bytes) P(sevo_step_args, out_hidden)
   S(sevo_linear_args) P(sevo_linear_args, flags) P(sevo_linear_args, x)
   P(sevo_linear_args, workspace_bytes)
   S(sevo_prefill_attn_args) P(sevo_prefill_attn_args, num_pages) P(sevo_prefill_attn_args, q)

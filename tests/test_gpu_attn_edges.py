@@ -1,0 +1,204 @@
+"""GPU parity of the decode and prefill attention on the softmax's hard cases.
+
+Aggregation contexts concatenate K candidates (Recombination paragraph of the
+method section; Algorithm 1, aggregation line), so a long context can hold
+keys whose scores stand far above everything before them.  The kernels keep a
+running maximum per query head and raise it lazily, only when a score exceeds
+it by more than 2^8 (in the exp2 domain), rescaling the partial sums already
+accumulated; waves and splits are then merged from partials whose maxima
+differ widely.  The inputs here drive exactly those paths:
+
+* ``scale8`` / ``scale32``: q ~ N(0, 1) times 8 or 32 (scores with standard
+  deviation 8 or 32): the maximum rises many times along the keys;
+* ``rise``: small base scores (about N(0, 0.1^2)) and keys lifted by 7.5
+  (natural log units, 10.8 in log2) in the middle of split 0 and split 1, at
+  the first key of split 2, and twice inside split 3 (to 7.5, then 15), each
+  rise checked on the host to exceed every earlier score of its split by more
+  than 8 log2 units, after several pages the same wave has accumulated;
+* ``dominant``: one key in the middle split scoring 40 above the rest, so the
+  output is that key's value and every other split's partial is weighted by
+  about e^-37.
+
+Values are bf16 (rounded to nearest even by torch), the oracle computes in
+float64 on the same values, and the bar is the attention bar: max|o - o_ref| /
+max|o_ref| <= 2e-2 per candidate, tightened to 8e-3 as elsewhere.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import decoder as od
+from tests.gpu_helpers import ATTN_REL_TOL, attn_rel_err, make_population, say, to_np
+
+pytestmark = pytest.mark.gpu
+
+LEVEL = 7.5        # natural-log units; 10.8 in log2, above the kernels' 8
+LOG2E = 1.4426950408889634
+
+
+@pytest.fixture(scope="module")
+def S():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2604_07725_amd import sevo
+    sevo.lib()
+    return sevo
+
+
+def _bf16(a):
+    """Round to bf16 (torch, nearest even) and return float64 values."""
+    return torch.from_numpy(np.ascontiguousarray(a, np.float32)).to(torch.bfloat16).double().numpy()
+
+
+def _pool_from_logical(Ks, Vs, page_table, n_pages):
+    """Paged pool [P][hkv][2][16 d] holding candidate i's logical keys and values
+    Ks[i], Vs[i] [hkv, n_i, d] (the K and V tile offsets of the layout)."""
+    hkv, _, d = Ks[0].shape
+    pool = np.zeros((n_pages, hkv, 2, 16 * d), np.float32)
+    e = np.arange(d)
+    for i, (K, V) in enumerate(zip(Ks, Vs)):
+        for t0 in range(0, K.shape[1], 16):
+            s = np.arange(min(16, K.shape[1] - t0))
+            tiles = pool[page_table[i, t0 // 16]]
+            tiles[:, 0][:, od.k_tile_offset(s[:, None], e[None, :])] = K[:, t0:t0 + len(s)]
+            tiles[:, 1][:, od.v_tile_offset(s[:, None], e[None, :])] = V[:, t0:t0 + len(s)]
+    return torch.from_numpy(pool).to(torch.bfloat16).cuda()
+
+
+def _group_dirs(rng, hkv, d):
+    return rng.choice([-1.0, 1.0], size=(hkv, d))
+
+
+def _queries(mode, rng, rows, hq, hkv, d, w):
+    g = hq // hkv
+    if mode in ("scale8", "scale32"):
+        return _bf16(rng.standard_normal((rows, hq, d)) * (8.0 if mode == "scale8" else 32.0))
+    # every query head of kv group c points along w_c (plus noise), so a key
+    # lifted along w_c is lifted for the whole group
+    q = np.repeat(w, g, axis=0)[None] + 0.3 * rng.standard_normal((rows, hq, d))
+    return _bf16(q)
+
+
+def _keys(mode, rng, n, hkv, d, w, lifts):
+    """K, V [hkv, n, d]; lifts = {position: level} adds level / sqrt(d) * w_c."""
+    base = 0.1 if mode == "rise" else 1.0
+    K = base * rng.standard_normal((hkv, n, d))
+    for t, lvl in lifts.items():
+        if t < n:
+            K[:, t] += lvl / np.sqrt(d) * w
+    return _bf16(K), _bf16(rng.standard_normal((hkv, n, d)))
+
+
+def _lifts(mode, L, per_split):
+    """Positions and levels of the lifted keys, for splits (or key blocks) of
+    L keys.  per_split: each split's state starts afresh, so every split gets
+    its own rises (mid-split in splits 0 and 1, at the first key of split 2,
+    twice in split 3); otherwise (one split, or a causal prefill whose running
+    maximum spans all earlier keys) the levels climb as a staircase."""
+    if mode == "dominant":
+        return {2 * L + L // 2 + 3: 40.0}
+    if mode != "rise":
+        return {}
+    pos = [L // 2 + 7, L + L // 2, 2 * L, 3 * L + L // 3, 3 * L + 2 * L // 3]
+    if per_split:
+        return dict(zip(pos, [LEVEL, LEVEL, LEVEL, LEVEL, 2 * LEVEL]))
+    return {t: (k + 1) * LEVEL for k, t in enumerate(pos)}
+
+
+def _check_rises(q, K, lifts, split_keys, g):
+    """Each lifted key that is not the first key of its split scores more than
+    8 log2 units above every earlier key of its split, for every query head of
+    its group (a host check of the test input itself)."""
+    scale = K.shape[2] ** -0.5
+    for t in sorted(lifts):
+        lo = (t // split_keys) * split_keys
+        if t >= K.shape[1] or t == lo:
+            continue
+        for j in range(q.shape[0]):
+            s = (K[j // g, lo:t + 1] @ q[j]) * scale
+            assert (s[-1] - s[:-1].max()) * LOG2E > 8.0, (t, j, s[-1], s[:-1].max())
+
+
+DECODE_DIMS = [(8, 8, 128), (16, 8, 128), (32, 8, 128), (32, 4, 128),
+               (8, 8, 64), (16, 8, 64), (16, 4, 64), (16, 2, 64)]
+MODES = ["scale8", "scale32", "rise", "dominant"]
+
+
+@pytest.mark.parametrize("splits", [4, 1])
+@pytest.mark.parametrize("mode", MODES)
+@pytest.mark.parametrize("hq,hkv,d", DECODE_DIMS)
+def test_decode_attention_softmax_edges(S, hq, hkv, d, mode, splits):
+    sevo = S
+    if splits == 1 and mode != "rise":
+        pytest.skip("one split: the rise case covers the within-split rescale")
+    lengths = [1024, 700, 1000, 333]
+    pop = make_population(lengths, seed=hq * 131 + hkv * 7 + d)
+    rng = np.random.default_rng([hq, hkv, d, MODES.index(mode), splits])
+    w = _group_dirs(rng, hkv, d)
+    g = hq // hkv
+    # the library's split s covers logical pages [s c, (s + 1) c), c = ceil(max_pages / S)
+    split_keys = 16 * (-(-pop.max_pages // splits))
+    lifts = _lifts(mode, split_keys if splits > 1 else 256, per_split=splits > 1)
+    q = _queries(mode, rng, pop.n, hq, hkv, d, w)
+    KV = [_keys(mode, rng, n, hkv, d, w, lifts) for n in lengths]
+    if mode == "rise":
+        for i in range(pop.n):
+            _check_rises(q[i], KV[i][0], lifts, split_keys, g)
+    say(f"decode attention {mode} hq={hq} hkv={hkv} d={d} splits={splits}")
+    pool = _pool_from_logical([k for k, _ in KV], [v for _, v in KV], pop.page_table, pop.n_pages)
+    qd = torch.from_numpy(q.astype(np.float32)).to(torch.bfloat16).cuda()
+    out = sevo.sevo_attn_decode(qd, pool, torch.from_numpy(pop.page_table).cuda(),
+                                torch.from_numpy(pop.lengths).cuda(), num_splits=splits)
+    torch.cuda.synchronize()
+    o = to_np(out)
+    assert np.isfinite(o).all()
+    for i in range(pop.n):
+        ref = od.attention_dense(q[i], KV[i][0], KV[i][1], d ** -0.5)
+        e = attn_rel_err(o[i], ref)
+        say(f"  candidate {i} ({lengths[i]} keys): rel err {e:.2e}")
+        assert e <= ATTN_REL_TOL and e <= 8e-3, (i, e)
+
+
+PREFILL_DIMS = [(8, 8, 64), (4, 2, 64), (32, 8, 128), (32, 4, 128)]
+
+
+@pytest.mark.parametrize("mode", MODES)
+@pytest.mark.parametrize("hq,hkv,d", PREFILL_DIMS)
+def test_prefill_attention_softmax_edges(S, hq, hkv, d, mode):
+    """The causal prefill kernel (64-key blocks) on the same hard cases: lifts
+    in the middle of a key block, at a block start and twice within one block;
+    every query after a lift sees it."""
+    sevo = S
+    lens = np.array([300, 129])
+    pop = make_population(lens, seed=hq * 17 + d)
+    rng = np.random.default_rng([hq, hkv, d, MODES.index(mode), 99])
+    w = _group_dirs(rng, hkv, d)
+    g = hq // hkv
+    lifts = _lifts(mode, 64, per_split=False)      # 64-key blocks
+    T = int(lens.sum())
+    q = _queries(mode, rng, T, hq, hkv, d, w)
+    KV = [_keys(mode, rng, int(n), hkv, d, w, lifts) for n in lens]
+    if mode == "rise":
+        # against every earlier key of the sequence (a query block sees them all)
+        for s, n in enumerate(lens):
+            a = int(lens[:s].sum())
+            for t in sorted(x for x in lifts if x < n):
+                if t + a < T:
+                    _check_rises(q[a + t], KV[s][0], {t: lifts[t]}, 1 << 30, g)
+    say(f"prefill attention {mode} hq={hq} hkv={hkv} d={d}")
+    pool = _pool_from_logical([k for k, _ in KV], [v for _, v in KV], pop.page_table, pop.n_pages)
+    seq_starts = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    qd = torch.from_numpy(q.astype(np.float32)).to(torch.bfloat16).cuda()
+    out = sevo.sevo_attn_prefill(qd, pool, torch.from_numpy(pop.page_table).cuda(),
+                                 torch.from_numpy(seq_starts).cuda(), int(lens.max()))
+    torch.cuda.synchronize()
+    o = to_np(out)
+    assert np.isfinite(o).all()
+    for s in range(len(lens)):
+        a = seq_starts[s]
+        for t in range(int(lens[s])):
+            K, V = KV[s]
+            ref = od.attention_dense(q[a + t], K[:, :t + 1], V[:, :t + 1], d ** -0.5)
+            e = attn_rel_err(o[a + t], ref)
+            assert e <= ATTN_REL_TOL and e <= 8e-3, (s, t, e)
+    say(f"  {T} query rows within 8e-3")

@@ -1,0 +1,146 @@
+"""Full-depth parity of the decode step (sevo_decode_step) at the benchmark's
+widths, populations and contexts, teacher-forced layer by layer.
+
+The step runs once on the GPU for the whole population with every layer of
+the model (36 for the 8B-class decoder, 64 for the 32B-class one) and returns
+the residual stream entering each layer (``out_hidden``).  For three sampled
+candidates (shortest, longest, one more) the oracle then runs each layer l on
+the GPU's own x_l, with that layer's KV cache regenerated on the host, and its
+x_{l+1} is compared with the GPU's.  A layer's error therefore cannot hide in
+the amplification of bf16 rounding flips through the layers before it.  Last,
+the oracle takes the GPU's final x through the final norm, the LM head and
+the sampler, and the GPU's logits, ids and log-probabilities are held to the
+sampler's bars: log-probs within 3e-3, ids exact wherever the oracle's top-2
+perturbed-logit gap exceeds 1e-3 (Eq. 1 consumes these per-token
+log-probabilities).  The oracle's own chain through all layers (no teacher
+forcing) runs beside it, and its distance from the GPU is printed, not gated.
+"""
+import collections
+import concurrent.futures as cf
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import decoder as od
+from paper_2604_07725_amd import synth
+from tests.gpu_helpers import check_ids, poisoned, say
+
+pytestmark = pytest.mark.gpu
+
+# One layer, GPU vs oracle on the GPU's own input: max|x_gpu - x_ref| over the
+# three candidates, relative to the largest entry of the layer's update
+# max|x_ref - x_in|.  Inside one layer both sides round at the same bf16
+# storage points, so what remains is fp32 accumulation order and the rare
+# one-ulp rounding flip it causes (one flip of the SwiGLU product moves the
+# update by about 1e-4 of its largest entry).
+LAYER_REL_TOL = 2e-3
+# The oracle's own one-layer floor: the same layer with its input perturbed
+# by 1e-6 relative (fp32-level noise).  The GPU's error must stay within a
+# small multiple of the largest floor over the layers.
+FLOOR_FACTOR = 4.0
+FINAL_LOGIT_TOL = 1e-3    # logits from the GPU's final x (one matrix product)
+WINDOW = 4                # layers in flight on the host
+
+
+@pytest.fixture(scope="module")
+def S():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2604_07725_amd import device_inputs, sevo
+    sevo.lib()
+    return sevo, device_inputs
+
+
+def _subset_pool(shape, seed, pop, idx, layer, extra):
+    """Host KV pool of one layer holding only the pages of candidates idx, and a
+    matching page table."""
+    need = (pop.lengths[idx].astype(np.int64) + extra + 15) // 16
+    pt = np.full((len(idx), int(need.max())), -1, np.int64)
+    pages = np.concatenate([pop.page_table[i, :need[j]] for j, i in enumerate(idx)])
+    c = 0
+    for j in range(len(idx)):
+        pt[j, :need[j]] = np.arange(c, c + need[j])
+        c += need[j]
+    return synth.pool_pages(synth.kv_spec(shape, seed, layer, pop.n_pages), pages), pt
+
+
+@pytest.mark.timeout(1200)
+@pytest.mark.parametrize("workload", ["dense8b_pop64_agg4", "dense32b_pop16_agg4"])
+def test_full_depth_step_teacher_forced(S, workload):
+    from threadpoolctl import threadpool_limits
+    sevo, di = S
+    w = synth.WORKLOADS[workload]
+    shape = w.shape
+    L = shape.n_layers
+    extra = 1
+    torch.cuda.empty_cache()          # the pools of this test take most of the HBM
+    say(f"full-depth step {workload}: {L} layers, N = {w.n}")
+    pop = synth.workload_population(w, extra_tokens=extra)
+    tensors = di.device_weights(shape, w.seed)
+    model = sevo.sevo_init_model(shape, tensors, max_position=int(pop.lengths.max()) + extra + 1)
+    kvp = di.device_pools(shape, w.seed, pop.n_pages)
+    d = di.device_population(pop)
+    seed, temp = 77, 1.0
+    ws = poisoned(sevo.sevo_step_workspace_bytes(model, pop.n, pop.max_pages))   # all NaN
+    ids, lps, logits, hidden = sevo.sevo_decode_step(
+        model, d["tokens"], d["lengths"], d["page_table"], kvp, d["uids"], seed, temp,
+        keep_logits=True, keep_hidden=True, workspace=ws)
+    torch.cuda.synchronize()
+    assert torch.isfinite(logits).all() and torch.isfinite(hidden).all()
+    idx = sorted({int(np.argmin(pop.lengths)), int(np.argmax(pop.lengths)), 1})
+    gh = hidden[:, idx].double().cpu().numpy()           # [L + 1, 3, hidden]
+    g_logits = logits[idx].double().cpu().numpy()
+    g_ids = ids.cpu().numpy()[idx].astype(np.int64)
+    g_lps = lps.cpu().numpy()[idx].astype(np.float64)
+    model.close()
+    del kvp, tensors, model, hidden, logits, ws
+    torch.cuda.empty_cache()
+    # the step's input is the embedding row of each token (x_0, no arithmetic)
+    hw = synth.host_weights(shape, w.seed, lazy=True)
+    np.testing.assert_array_equal(gh[0], np.asarray(hw["embed"][pop.tokens[idx]], np.float64))
+    pos = pop.lengths[idx].astype(np.int64)
+    say(f"  candidates {idx}, contexts {pos.tolist()}")
+    rng = np.random.default_rng(1234)
+    noise = [1.0 + 1e-6 * rng.standard_normal(gh.shape[1:]) for _ in range(L)]
+
+    def layer_job(l):
+        lw = {k: np.asarray(v, np.float64) for k, v in hw["layers"][l].items()}
+        pool, pt = _subset_pool(shape, w.seed, pop, idx, l, extra)
+        x_tf = od.decoder_layer(shape, lw, gh[l], pos, pool.copy(), pt)
+        x_fl = od.decoder_layer(shape, lw, od._f32(gh[l] * noise[l]), pos, pool.copy(), pt)
+        return lw, pool, pt, x_tf, x_fl
+
+    errs, floors, own = [], [], gh[0].copy()
+    with threadpool_limits(1), cf.ThreadPoolExecutor(WINDOW) as ex:
+        futs = collections.deque(ex.submit(layer_job, l) for l in range(min(WINDOW, L)))
+        for l in range(L):
+            lw, pool, pt, x_tf, x_fl = futs.popleft().result()
+            if l + WINDOW < L:
+                futs.append(ex.submit(layer_job, l + WINDOW))
+            scale = np.abs(x_tf - gh[l]).max()
+            errs.append(np.abs(gh[l + 1] - x_tf).max() / scale)
+            floors.append(np.abs(x_fl - x_tf).max() / scale)
+            own = od.decoder_layer(shape, lw, own, pos, pool, pt)   # the oracle's own chain
+            say(f"  layer {l:2d}: rel err {errs[-1]:.2e} (floor {floors[-1]:.2e}), "
+                f"|update| {scale:.3f}, own-chain |x - x_gpu| {np.abs(own - gh[l + 1]).max():.2e}")
+        lm = hw["lm_head"][0:shape.vocab]
+        ref_logits = od.lm_logits(shape, hw["final_norm"], lm, gh[L])
+        own_logits = od.lm_logits(shape, hw["final_norm"], lm, own)
+    errs, floors = np.array(errs), np.array(floors)
+    say(f"  layers: max rel err {errs.max():.2e} at {int(errs.argmax())}, max floor "
+        f"{floors.max():.2e}; raw full depth (oracle's own chain): logits "
+        f"{np.abs(own_logits - g_logits).max():.2e}")
+    assert errs.max() <= LAYER_REL_TOL, errs
+    assert errs.max() <= FLOOR_FACTOR * floors.max(), (errs, floors)
+    # final norm -> LM head -> sampler on the GPU's final x
+    lerr = np.abs(g_logits - ref_logits).max()
+    det = {}
+    ref_ids, ref_lps, gaps = od.logprob_sample(ref_logits, temp, seed, pop.uids[idx], pos,
+                                               details=det)
+    lp_err, n_exact = check_ids(g_ids, g_lps, ref_ids, ref_lps, gaps, det,
+                                label=f"{workload} full depth")
+    say(f"  final: logits err {lerr:.2e} (max |logit| {np.abs(ref_logits).max():.2f}), lp err "
+        f"{lp_err:.2e}, ids {g_ids.tolist()} vs {ref_ids.tolist()} gaps "
+        f"{np.round(gaps, 4).tolist()} ({n_exact} exact)")
+    assert lerr <= FINAL_LOGIT_TOL

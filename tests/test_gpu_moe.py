@@ -16,7 +16,8 @@ import torch
 
 from oracle import decoder as od
 from paper_2604_07725_amd import synth
-from tests.gpu_helpers import check_ids, say, subset_host_state, tile_activations_host
+from tests.gpu_helpers import (check_ids, poisoned, say, subset_host_state,
+                               tile_activations_host)
 
 pytestmark = pytest.mark.gpu
 
@@ -102,20 +103,21 @@ def test_tiny_moe_step_sequence_matches_oracle(S):
     toks = pop.tokens.astype(np.int64)
     pos = pop.lengths.astype(np.int64)
     pos_d = d["lengths"].clone()
+    ws_bytes = sevo.sevo_step_workspace_bytes(model, pop.n, pop.max_pages)
     for step in range(steps):
         ids, lps, logits = sevo.sevo_decode_step(
             model, torch.from_numpy(toks.astype(np.int32)).cuda(), pos_d, d["page_table"], kvp,
-            d["uids"], 7, 1.0, keep_logits=True)
+            d["uids"], 7, 1.0, keep_logits=True, workspace=poisoned(ws_bytes))  # NaN scratch
         torch.cuda.synchronize()
-        stats = {}
+        stats, det = {}, {}
         ref = od.decode_step(shape, hw, hkv, pop.page_table, toks, pos, pop.uids, 7, 1.0,
-                             stats=stats)
+                             stats=stats, details=det)
         assert stats["route_gap"] > ROUTE_GAP, "test input has a routing near-tie"
         err = np.abs(logits.double().cpu().numpy() - ref["logits"]).max()
         say(f"  step {step}: logit max abs err {err:.2e}; route gap {stats['route_gap']:.2e}")
         assert err <= 1e-2       # the tiny-model end-to-end bar of the dense step
         check_ids(ids.cpu().numpy(), lps.cpu().numpy(), ref["ids"], ref["lps"], ref["gaps"],
-                  label=f"step {step}")
+                  det, label=f"step {step}")
         toks = ref["ids"]
         pos = pos + 1
         pos_d += 1

@@ -5,7 +5,8 @@ import torch
 
 from oracle import decoder as od
 from paper_2604_07725_amd import synth
-from tests.gpu_helpers import LP_ABS_TOL, bf16_bits, check_ids, say, subset_host_state
+from tests.gpu_helpers import (LP_ABS_TOL, bf16_bits, check_ids, poisoned, say,
+                               subset_host_state)
 
 pytestmark = pytest.mark.gpu
 
@@ -58,12 +59,18 @@ def test_tiny_step_sequence_matches_oracle(S):
     pos_d = d["lengths"].clone()
     conf_sum = torch.zeros(pop.n, dtype=torch.float32, device="cuda")
     ref_conf_sum = np.zeros(pop.n)
+    # every byte of the workspace NaN before each step: no kernel may read
+    # scratch it has not written
+    ws_bytes = sevo.sevo_step_workspace_bytes(model, pop.n, pop.max_pages)
     for step in range(steps):
         ids, lps, logits, conf = sevo.sevo_decode_step(
             model, torch.from_numpy(toks.astype(np.int32)).cuda(), pos_d, d["page_table"], kvp,
-            d["uids"], seed, temp, keep_logits=True, conf_topk=20, conf_sum=conf_sum)
+            d["uids"], seed, temp, keep_logits=True, conf_topk=20, conf_sum=conf_sum,
+            workspace=poisoned(ws_bytes))
         torch.cuda.synchronize()
-        ref = od.decode_step(shape, hw, hkv, pop.page_table, toks, pos, pop.uids, seed, temp)
+        det = {}
+        ref = od.decode_step(shape, hw, hkv, pop.page_table, toks, pos, pop.uids, seed, temp,
+                             details=det)
         # the step's self-confidence (Eq. 1) follows the logits it came from
         rc = od.token_confidence(ref["logits"], 20)
         ref_conf_sum += rc
@@ -80,7 +87,7 @@ def test_tiny_step_sequence_matches_oracle(S):
         # values are perturbed by 1e-6 relative, so logits are held to 1e-2.
         assert err <= TINY_LOGIT_TOL
         check_ids(ids.cpu().numpy(), lps.cpu().numpy(), ref["ids"], ref["lps"], ref["gaps"],
-                  label=f"step {step}")
+                  det, label=f"step {step}")
         toks = ref["ids"]
         pos = pos + 1
         pos_d += 1
@@ -191,8 +198,10 @@ def test_full_width_step_reduced_depth(S, workload, layers):
     say(f"full-width step {workload} at {layers} layers")
     pop, model, kvp, d = _setup(S, w, extra=1, shape=shape)
     seed, temp = 77, 1.0
+    ws = poisoned(sevo.sevo_step_workspace_bytes(model, pop.n, pop.max_pages))
     ids, lps, logits = sevo.sevo_decode_step(model, d["tokens"], d["lengths"], d["page_table"],
-                                             kvp, d["uids"], seed, temp, keep_logits=True)
+                                             kvp, d["uids"], seed, temp, keep_logits=True,
+                                             workspace=ws)
     torch.cuda.synchronize()
     idx = sorted({int(np.argmin(pop.lengths)), int(np.argmax(pop.lengths)), 1})
     g_logits = logits.double().cpu().numpy()[idx]

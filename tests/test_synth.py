@@ -58,3 +58,16 @@ def test_lazy_weights_match_eager():
     np.testing.assert_array_equal(eager["embed"][[5, 77]], lazy["embed"][[5, 77]])
     np.testing.assert_array_equal(eager["lm_head"][100:300], lazy["lm_head"][100:300])
     np.testing.assert_array_equal(eager["layers"][0]["w_qkv"], lazy["layers"][0]["w_qkv"])
+
+
+def test_pool_pages_equal_the_pool_slices():
+    """The batched page generator gives each selected page's elements of the
+    whole pool (and rejects page ids outside it)."""
+    import pytest
+    spec = synth.kv_spec(synth.TINY, 3, 1, 40)
+    full = synth.host_values(spec).reshape(spec.shape)
+    pages = np.array([7, 0, 39, 7, 12])
+    np.testing.assert_array_equal(synth.pool_pages(spec, pages), full[pages])
+    assert synth.pool_pages(spec, np.array([], np.int64)).shape == (0,) + spec.shape[1:]
+    with pytest.raises(IndexError):
+        synth.pool_pages(spec, np.array([40]))
