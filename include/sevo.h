@@ -218,10 +218,12 @@ size_t sevo_attn_workspace_bytes(int32_t n, int32_t n_q_heads, int32_t n_kv_head
  *   start_pos  int32 [n_seqs] (device) or NULL (every sequence starts at 0)
  *   out        bf16 [total_tokens][n_q_heads][head_dim]
  *   max_seq_len (host) >= every sequence length: sizes the grid (rows of a
- *              longer sequence past it are not computed)
+ *              longer sequence past it are not computed); a value below the
+ *              mean length total_tokens / n_seqs is rejected (INVALID_ARGUMENT)
  * The probabilities are rounded to bf16 for the P V product (fp32
- * accumulation; the softmax statistics stay fp32).  Page ids outside
- * [0, num_pages) contribute zero keys and values (they are never read).
+ * accumulation; the softmax statistics stay fp32).  A page id outside
+ * [0, num_pages) contributes no keys, as in sevo_attn_decode (it is never
+ * read; a row that sees no key at all gets o = 0).
  * Device arrays are not validated.  Errors: INVALID_ARGUMENT, UNSUPPORTED, HIP. */
 typedef struct {
   int32_t n_seqs, total_tokens, max_seq_len;
@@ -247,9 +249,11 @@ sevo_status sevo_attn_prefill(const sevo_prefill_attn_args* a, void* stream);
  * causal prefill attention of sevo_attn_prefill; the keys and values of every
  * token are written into the pools (a KV cache a decode can continue from).
  * A mixture-of-experts model runs its expert FFN on chunks of moe_chunk
- * tokens (rounded up to 16; 0 or more than 65536 = 65536): routing, expert
- * lists and the per-slot outputs of a chunk live in the workspace, and each
- * token's k expert outputs are summed in slot order.
+ * tokens (rounded up to 16; 0 or more than 65536 = 65536; lowered, to a
+ * multiple of 16, as needed to keep chunk * max(hidden, n_experts_active *
+ * expert_ffn) * 2 below 2^31 bytes): routing, expert lists and the per-slot
+ * outputs of a chunk live in the workspace, and each token's k expert outputs
+ * are summed in slot order.
  * Then, for each scored row r -- a packed token index whose next-token
  * distribution is scored --
  *   c_r = logsumexp(logits_r) - mean of the conf_topk largest logits_r
@@ -265,7 +269,8 @@ sevo_status sevo_attn_prefill(const sevo_prefill_attn_args* a, void* stream);
  *   kv_pools    HOST array of n_layers pool pointers; a caller that does not
  *               keep the cache may pass one pool for every layer (a layer's
  *               keys are only read inside that layer)
- *   max_seq_len host bound of the sequence lengths
+ *   max_seq_len host bound of the sequence lengths (at least the mean length
+ *               total_tokens / n_seqs, else INVALID_ARGUMENT)
  *   conf_topk   K_l of Eq. 1, 1..32
  *   scored_rows int32 [n_scored] (device): strictly increasing packed token
  *               indices (not validated on the device)

@@ -24,6 +24,12 @@
 //     K tile, one V tile) -- a page id outside the pool, or a page past the
 //     workgroup's keys, gets zero records and reads zeros; four LDS stages
 //     hold the block being multiplied and up to three more in flight;
+//   * the keys of a page whose id lies outside the pool are left out, as in
+//     decode: every wave learns the block's absent pages when it issues the
+//     block (scalar loads of its four page ids, kept as 4 bits per stage) and,
+//     only in a block that has one, sets their scores to kAbsentKey, a finite
+//     value so far below any real score that its weight is exactly 0 once a
+//     real key is seen (a row that sees none gets o = 0, its values being 0);
 //   * LDS holds the tiles with their 16-byte chunks XOR-swizzled (within each
 //     1 KB) so every MFMA operand read is free of bank conflicts for 8- and
 //     16-lane groups; the direct loads apply the swizzle through their
@@ -48,6 +54,7 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 constexpr int kPfStages = 4;
 constexpr int kPfWaves = 12;     // waves per workgroup
 constexpr int kPfQueryTiles = 1; // 32-query tiles per wave
+constexpr float kAbsentKey = -1e30f;  // score of a key on a page outside the pool
 
 // K tile block (16 slots x 32 dims, 1 KB): chunk (slot s, dim quarter q) at
 // s * 4 + (q ^ pf_kswz(s)).  V tile (dims x 16 slots): chunk (dim e, key half
@@ -94,10 +101,21 @@ __global__ __launch_bounds__(64 * NW, 1) void attn_prefill_kernel(PrefillAttnArg
   // 32 vb + lane/2, half (lane%2) ^ swz)
   const uint32_t k_src = (lane >> 2) * 64 + (((lane & 3) ^ pf_kswz(lane >> 2)) * 16);
   const uint32_t v_src = KT_ELEMS * 2 + (lane >> 1) * 32 + (((lane & 1) ^ pf_vswz(lane >> 1)) * 16);
+  uint32_t absent = 0;  // bit 4 (b % kPfStages) + j: page j of that stage's block is absent
   auto issue = [&](int b) {
-    const int pi = 4 * b + (NW == 4 ? wave : wave >> 1);
+    const int own = NW == 4 ? wave : wave >> 1;
     int page = -1;
-    if (pi < npages && pi < a.max_pages) page = a.page_table[(size_t)sq * a.max_pages + pi];
+    uint32_t bad = 0;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int pj = 4 * b + j;
+      if (pj >= npages) continue;  // past the workgroup's keys: causally masked
+      const int pg = pj < a.max_pages ? a.page_table[(size_t)sq * a.max_pages + pj] : -1;
+      if (pg < 0 || (int64_t)pg >= a.num_pages) bad |= 1u << j;
+      if (j == own) page = pg;
+    }
+    const int sh = 4 * (b % kPfStages);
+    absent = (absent & ~(0xFu << sh)) | (bad << sh);
     const bool ok = page >= 0 && (int64_t)page < a.num_pages;
     const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<bf16_t*>(a.kv_pool + (ok ? ((size_t)page * a.hkv + c) * PAGE_ELEMS : 0)), 0,
@@ -193,6 +211,16 @@ __global__ __launch_bounds__(64 * NW, 1) void attn_prefill_kernel(PrefillAttnArg
               const int key = 64 * b + 32 * kt + 8 * (e >> 2) + 4 * khi + (e & 3);
               if (key > qpos[qt]) acc_s[kt][qt][e] = -INFINITY;
             }
+        }
+        const uint32_t bad = (absent >> (4 * (b % kPfStages))) & 0xFu;
+        if (bad) {
+          // element e of tile kt holds a key of page 2 kt + e / 8 of the block
+#pragma unroll
+          for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+            for (int e = 0; e < 16; ++e)
+              if ((bad >> (2 * kt + (e >> 3))) & 1u)
+                acc_s[kt][qt][e] = fminf(acc_s[kt][qt][e], kAbsentKey);
         }
         float mx = -INFINITY;
 #pragma unroll

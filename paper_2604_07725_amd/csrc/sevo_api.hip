@@ -1,6 +1,7 @@
 // Host side of the libsevo C ABI: argument validation, split / workspace
 // planning, the model handle (RoPE table) and the decode-step composition.
 // Every entry point catches everything and reports through sevo_status.
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -364,6 +365,10 @@ SEVO_API sevo_status sevo_attn_prefill(const sevo_prefill_attn_args* a, void* st
   if (st) return st;
   if (a->total_tokens < 0 || a->max_seq_len < 0)
     return fail(SEVO_ERR_INVALID_ARGUMENT, "total_tokens / max_seq_len < 0");
+  if (a->n_seqs > 0 && (int64_t)a->max_seq_len * a->n_seqs < a->total_tokens)
+    return fail(SEVO_ERR_INVALID_ARGUMENT,
+                "max_seq_len %d below the mean sequence length (%d tokens in %d sequences)",
+                a->max_seq_len, a->total_tokens, a->n_seqs);
   if (a->num_pages < 1) return fail(SEVO_ERR_INVALID_ARGUMENT, "num_pages < 1");
   if (!(std::isfinite(a->scale)) || a->scale <= 0.f)
     return fail(SEVO_ERR_INVALID_ARGUMENT, "scale must be finite and > 0");
@@ -967,6 +972,13 @@ PrefillLayout prefill_layout(const sevo_model_config& c, int T, int R, int moe_c
                                                               : (size_t)kPrefillMoeRows;
     if (mc > t16) mc = t16;
     const size_t kk = c.n_experts_active, E = c.n_experts;
+    // the grouped expert GEMMs address a chunk's gathered rows (mc tokens of
+    // the normed input, mc k SwiGLU rows of expert_ffn) through one buffer
+    // descriptor with 32-bit byte offsets, and mark an unused row by offset
+    // 2^31: a chunk's rows must stay below 2^31 bytes
+    const size_t row_bytes = 2 * std::max((size_t)H, kk * (size_t)c.expert_ffn);
+    const size_t mc_cap = ((((size_t)1 << 31) - 1) / row_bytes) / 16 * 16;
+    if (mc > mc_cap) mc = mc_cap;
     L.mc = (int)mc;
     L.m_router = take(mc * E * 4);
     L.m_sel = take(mc * kk * 4);
@@ -1079,6 +1091,10 @@ SEVO_API sevo_status sevo_prefill_confidence(sevo_model* m, const sevo_prefill_a
       a->num_pages < 1)
     return fail(SEVO_ERR_INVALID_ARGUMENT,
                 "bad n_seqs / total_tokens / max_seq_len / max_pages / num_pages");
+  if ((int64_t)a->max_seq_len * a->n_seqs < a->total_tokens)
+    return fail(SEVO_ERR_INVALID_ARGUMENT,
+                "max_seq_len %d below the mean sequence length (%d tokens in %d sequences)",
+                a->max_seq_len, a->total_tokens, a->n_seqs);
   if (a->conf_topk < 1 || a->conf_topk > 32 || a->conf_topk > c.vocab)
     return fail(SEVO_ERR_INVALID_ARGUMENT, "conf_topk %d outside [1, min(32, vocab)]",
                 a->conf_topk);

@@ -286,3 +286,22 @@ def test_read_probe_rejects_bad_arguments():
         sevo.INVALID_ARGUMENT
     assert L.sevo_hbm_read_probe(f, 8, None, 64, f, None) == sevo.INVALID_ARGUMENT
     assert L.sevo_hbm_read_probe(f, 4096, f, 64, f, None) == sevo.INVALID_ARGUMENT
+
+
+@pytest.mark.parametrize("kw,ok", [
+    (dict(max_seq_len=0), False),                              # tokens but no length bound
+    (dict(max_seq_len=49), False),                             # below the mean (100 / 2)
+    (dict(max_seq_len=-1), False),
+    (dict(max_seq_len=50), True),                              # passes this check
+])
+def test_attn_prefill_rejects_a_short_max_seq_len(kw, ok):
+    """max_seq_len sizes the grid: a bound below the mean sequence length
+    would leave rows uncomputed, so it is rejected before any launch."""
+    base = dict(n_seqs=2, total_tokens=100, max_seq_len=60, n_q_heads=4, n_kv_heads=2,
+                head_dim=64, page_size=16, max_pages=8, num_pages=16, scale=0.125)
+    base.update(kw)
+    a = sevo.PrefillAttnArgs(**base)           # null pointers: the next check fails
+    st = sevo.lib().sevo_attn_prefill(C.byref(a), None)
+    assert st == sevo.INVALID_ARGUMENT
+    msg = sevo.lib().sevo_last_error().decode()
+    assert ("max_seq_len" in msg) != ok, msg

@@ -372,3 +372,100 @@ def test_prefill_confidence_moe30b_reduced_depth(S, moe_chunk):
     assert stats["route_gap"] > 1e-5, "test input has a routing near-tie"
     assert row_err <= 6e-2
     assert np.abs(g_conf - conf).max() <= 3e-2
+
+
+@pytest.mark.parametrize("dims", [(32, 8, 128), (8, 2, 64)])
+def test_attn_prefill_absent_pages_contribute_no_keys(S, dims):
+    """A page id outside the pool contributes no keys, as in decode: keys
+    48..63 of sequence 0 (an id past the pool) and keys 0..15 of sequence 1 (a
+    negative id) are left out of every row's softmax; rows 0..15 of sequence 1
+    then see no key at all and give o = 0."""
+    sevo, di = S
+    shape = _shape(*dims)
+    hq, d = shape.n_q_heads, shape.head_dim
+    lens = np.array([150, 70])
+    say(f"attn prefill with absent pages {dims}")
+    pop = make_population(lens, shuffle=True, seed=23)
+    bad = pop.page_table.copy()
+    bad[0, 3] = pop.n_pages + 1000
+    bad[1, 0] = -5
+    kvp = di.device_pools(shape, 23, pop.n_pages, layers=[0])[0]
+    T = int(lens.sum())
+    q = di.device_q(shape, 23, T)
+    ss = np.array([0, 150, 220], np.int32)
+    out = sevo.sevo_attn_prefill(q, kvp, torch.from_numpy(bad.astype(np.int32)).cuda(),
+                                 torch.from_numpy(ss).cuda(), int(lens.max()))
+    torch.cuda.synchronize()
+    got = to_np(out)
+    assert np.isfinite(got).all()
+    qh = synth.host_values(synth.q_spec(shape, 23, T)).reshape(T, hq, d)
+    pool = synth.pool_pages(synth.kv_spec(shape, 23, 0, pop.n_pages), np.arange(pop.n_pages))
+    worst = 0.0
+    for s, drop in ((0, range(48, 64)), (1, range(0, 16))):
+        K, V = od.gather_kv(pool, pop.page_table[s], int(lens[s]))
+        for t in range(int(lens[s])):
+            keep = np.array([u for u in range(t + 1) if u not in drop], np.int64)
+            row = got[ss[s] + t]
+            if keep.size == 0:
+                assert np.all(row == 0), (s, t)
+                continue
+            ref = od.attention_dense(qh[ss[s] + t], K[:, keep], V[:, keep], d ** -0.5)
+            worst = max(worst, attn_rel_err(row, ref))
+    say(f"  worst rel err {worst:.2e}")
+    assert worst <= min(ATTN_REL_TOL, 8e-3)
+
+
+def test_prefill_confidence_rejects_a_short_max_seq_len(S):
+    """max_seq_len below the mean sequence length (0 with tokens present
+    included) is rejected before any launch."""
+    sevo, di = S
+    shape = synth.WORKLOADS["tiny_step"].shape
+    pop = make_population([40, 30], seed=1)
+    model = sevo.sevo_init_model(shape, di.device_weights(shape, 1), max_position=64)
+    kvp = di.device_pools(shape, 1, pop.n_pages)
+    toks = torch.zeros(70, dtype=torch.int32, device="cuda")
+    ss = torch.tensor([0, 40, 70], dtype=torch.int32, device="cuda")
+    pt = torch.from_numpy(pop.page_table.astype(np.int32)).cuda()
+    rows = torch.arange(70, dtype=torch.int32, device="cuda")
+    for bound in (0, 34):
+        buf = sevo.PrefillBuffers(model, toks, ss, pt, kvp, rows, 20, bound)
+        with pytest.raises(sevo.SevoError) as e:
+            buf.run()
+        assert e.value.status == sevo.INVALID_ARGUMENT and "max_seq_len" in str(e.value)
+    sevo.PrefillBuffers(model, toks, ss, pt, kvp, rows, 20, 40).run()
+    torch.cuda.synchronize()
+    model.close()
+
+
+def test_prefill_confidence_moe_chunk_keeps_gathered_rows_below_2gib(S):
+    """A MoE model whose expert rows are wide (top-16 of 64 experts with FFN
+    4096: 128 KB of SwiGLU rows per token) at 40000 tokens: the default chunk
+    (65536 tokens, which would put 5.2 GB of gathered rows behind one 32-bit
+    buffer descriptor) is lowered to 16368 tokens; every row's c and each C
+    equal, bit for bit, the run in 4096-token chunks, and all are finite."""
+    sevo, di = S
+    shape = synth.ModelShape(n_layers=1, hidden=256, n_q_heads=4, n_kv_heads=2, head_dim=64,
+                             ffn=0, vocab=4096, n_experts=64, top_k=16, expert_ffn=4096)
+    T = 40000
+    say(f"prefill confidence MoE chunk bound: {T} tokens, top-16 of 64 experts x 4096")
+    pop = make_population([T], seed=31)
+    rng = np.random.default_rng(31)
+    toks = torch.from_numpy(rng.integers(0, shape.vocab, size=T).astype(np.int32)).cuda()
+    model = sevo.sevo_init_model(shape, di.device_weights(shape, 31), max_position=T + 1)
+    kvp = di.device_pools(shape, 31, pop.n_pages)
+    ss = torch.tensor([0, T], dtype=torch.int32, device="cuda")
+    pt = torch.from_numpy(pop.page_table.astype(np.int32)).cuda()
+    rows = torch.arange(T, dtype=torch.int32, device="cuda")
+    out = []
+    for chunk in (0, 4096):
+        buf = sevo.PrefillBuffers(model, toks, ss, pt, kvp, rows, 20, T, moe_chunk=chunk)
+        conf = buf.run()
+        torch.cuda.synchronize()
+        out.append((conf.cpu().numpy(), buf.out_row_conf[:T].cpu().numpy()))
+        del buf
+        torch.cuda.empty_cache()
+    model.close()
+    say(f"  C {out[0][0]} vs {out[1][0]}")
+    assert np.isfinite(out[0][1]).all()
+    np.testing.assert_array_equal(out[0][0], out[1][0])
+    np.testing.assert_array_equal(out[0][1], out[1][1])
