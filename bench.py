@@ -114,7 +114,7 @@ def attention_main(args, w, peak):
         "ms_per_step": total_ms / reps, "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "bf16", "data": "synthetic (seeded)",
         "config": {"workload": w.name, "heads": f"{shape.n_q_heads}/{shape.n_kv_heads}x"
-                   f"{shape.head_dim}", "population": pop.n, "aggregation_k": 4,
+                   f"{shape.head_dim}", "population": pop.n, "aggregation_k": w.aggregation_k,
                    "context_tokens": [int(pop.lengths.min()), int(pop.lengths.max())],
                    "page_size": 16, "num_splits": S, "kv_pools_rotated": 4,
                    "parallelism": "none (1 GPU)"},
@@ -639,7 +639,7 @@ def main():
         "config": {"workload": w.name, "model": model_name(shape), "layers": shape.n_layers,
                    "hidden": shape.hidden, "heads": f"{shape.n_q_heads}/{shape.n_kv_heads}x"
                    f"{shape.head_dim}", "vocab": shape.vocab, **ffn_config(shape),
-                   "population": pop.n, "aggregation_k": 4,
+                   "population": pop.n, "aggregation_k": w.aggregation_k,
                    "context_tokens": [int(pop.lengths.min()), int(pop.lengths.max())],
                    "page_size": 16, "parallelism": "none (1 GPU)",
                    "num_splits": int(buf.args.num_splits) or

@@ -63,23 +63,51 @@ def build_synth() -> str:
     return SYNTH_LIB
 
 
-def build_sevo(jobs: int = 8) -> str:
+# Host-side sanitizers for the checking build: AddressSanitizer and
+# UndefinedBehaviorSanitizer on the host code only (argument validation,
+# planning, layouts), each flag scoped to the host pass; device code is built
+# as in the product library.
+SANITIZE_HOST_FLAGS = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+                       "-Xarch_host", "-fno-sanitize-recover=undefined",
+                       "-Xarch_host", "-fno-omit-frame-pointer"]
+SANITIZED_LIB = os.path.join(PKG, "_build_sanitized", "libsevo_sanitized.so")
+
+
+def build_sevo(jobs: int = 8, sanitize: bool = False) -> str:
+    """Compile every csrc/*.hip for gfx950 and link libsevo.so (or, with
+    ``sanitize``, the host-sanitized checking build at SANITIZED_LIB)."""
     hipcc = _hipcc()
-    os.makedirs(BUILD, exist_ok=True)
+    out_dir = os.path.dirname(SANITIZED_LIB) if sanitize else BUILD
+    lib = SANITIZED_LIB if sanitize else LIB
+    extra = SANITIZE_HOST_FLAGS if sanitize else []
+    os.makedirs(out_dir, exist_ok=True)
     srcs = sorted(f for f in os.listdir(CSRC) if f.endswith(".hip"))
     objs = []
 
     def compile_one(src: str) -> str:
-        obj = os.path.join(BUILD, src[:-4] + ".o")
-        _run([hipcc, *HIPCC_FLAGS, *EXTRA_FLAGS.get(src, []), "-c", os.path.join(CSRC, src), "-o",
-              obj])
+        obj = os.path.join(out_dir, src[:-4] + ".o")
+        _run([hipcc, *HIPCC_FLAGS, *EXTRA_FLAGS.get(src, []), *extra, "-c",
+              os.path.join(CSRC, src), "-o", obj])
         return obj
 
     with cf.ThreadPoolExecutor(max_workers=max(1, min(jobs, len(srcs)))) as ex:
         objs = list(ex.map(compile_one, srcs))
-    _run([hipcc, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", LIB + ".tmp"])
-    os.replace(LIB + ".tmp", LIB)
-    return LIB
+    _run([hipcc, f"--offload-arch={ARCH}", "-shared", "-fPIC", *extra, *objs, "-o",
+          lib + ".tmp"])
+    os.replace(lib + ".tmp", lib)
+    return lib
+
+
+def asan_runtime() -> str:
+    """The clang AddressSanitizer runtime the sanitized build needs preloaded
+    into a host process that was not itself built with it."""
+    import glob
+    root = os.path.dirname(os.path.dirname(_hipcc()))
+    hits = sorted(glob.glob(os.path.join(root, "llvm", "lib", "clang", "*", "lib", "linux",
+                                         "libclang_rt.asan-x86_64.so")))
+    if not hits:
+        raise RuntimeError("clang AddressSanitizer runtime not found under " + root)
+    return hits[-1]
 
 
 def build(jobs: int = 8) -> None:

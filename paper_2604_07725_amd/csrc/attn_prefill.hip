@@ -25,11 +25,13 @@
 //     workgroup's keys, gets zero records and reads zeros; four LDS stages
 //     hold the block being multiplied and up to three more in flight;
 //   * the keys of a page whose id lies outside the pool are left out, as in
-//     decode: every wave learns the block's absent pages when it issues the
-//     block (scalar loads of its four page ids, kept as 4 bits per stage) and,
-//     only in a block that has one, sets their scores to kAbsentKey, a finite
-//     value so far below any real score that its weight is exactly 0 once a
-//     real key is seen (a row that sees none gets o = 0, its values being 0);
+//     decode.  Such ids are a caller's error, so the hot loop stays as it is
+//     unless the workgroup finds one among its pages in a pre-pass; then each
+//     wave learns a block's absent pages when it issues the block (scalar
+//     loads of its four page ids, kept as 4 bits per stage) and sets their
+//     scores to kAbsentKey, a finite value so far below any real score that
+//     its weight is exactly 0 once a real key is seen (a row that sees none
+//     gets o = 0, its values being 0);
 //   * LDS holds the tiles with their 16-byte chunks XOR-swizzled (within each
 //     1 KB) so every MFMA operand read is free of bank conflicts for 8- and
 //     16-lane groups; the direct loads apply the swizzle through their
@@ -54,7 +56,13 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 constexpr int kPfStages = 4;
 constexpr int kPfWaves = 12;     // waves per workgroup
 constexpr int kPfQueryTiles = 1; // 32-query tiles per wave
-constexpr float kAbsentKey = -1e30f;  // score of a key on a page outside the pool
+// Score given to a key on a page outside the pool.  Far below any real score
+// (|q . k| of ordinary bf16 inputs is many orders smaller), yet small enough
+// that its product with the scale, rounded to fp32, is off by well under 1 in
+// the exp2 argument fma(s, scale log2 e, -max): a row that has seen only such
+// keys gets weights near 1 on zero values (o = 0), never exp2(+huge) = inf
+// (-1e30 would leave an error of ~1e21 there).
+constexpr float kAbsentKey = -1e6f;
 
 // K tile block (16 slots x 32 dims, 1 KB): chunk (slot s, dim quarter q) at
 // s * 4 + (q ^ pf_kswz(s)).  V tile (dims x 16 slots): chunk (dim e, key half
@@ -101,21 +109,29 @@ __global__ __launch_bounds__(64 * NW, 1) void attn_prefill_kernel(PrefillAttnArg
   // 32 vb + lane/2, half (lane%2) ^ swz)
   const uint32_t k_src = (lane >> 2) * 64 + (((lane & 3) ^ pf_kswz(lane >> 2)) * 16);
   const uint32_t v_src = KT_ELEMS * 2 + (lane >> 1) * 32 + (((lane & 1) ^ pf_vswz(lane >> 1)) * 16);
+  // any page of the workgroup's key range outside the pool?  (workgroup-uniform)
+  int any_absent = 0;
+  for (int p = threadIdx.x; p < npages; p += 64 * NW) {
+    const int pg = p < a.max_pages ? a.page_table[(size_t)sq * a.max_pages + p] : -1;
+    any_absent |= pg < 0 || (int64_t)pg >= a.num_pages;
+  }
+  any_absent = __syncthreads_or(any_absent);
   uint32_t absent = 0;  // bit 4 (b % kPfStages) + j: page j of that stage's block is absent
   auto issue = [&](int b) {
-    const int own = NW == 4 ? wave : wave >> 1;
+    const int pi = 4 * b + (NW == 4 ? wave : wave >> 1);
     int page = -1;
-    uint32_t bad = 0;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int pj = 4 * b + j;
-      if (pj >= npages) continue;  // past the workgroup's keys: causally masked
-      const int pg = pj < a.max_pages ? a.page_table[(size_t)sq * a.max_pages + pj] : -1;
-      if (pg < 0 || (int64_t)pg >= a.num_pages) bad |= 1u << j;
-      if (j == own) page = pg;
+    if (pi < npages && pi < a.max_pages) page = a.page_table[(size_t)sq * a.max_pages + pi];
+    if (any_absent) {
+      uint32_t bad = 0;
+      for (int j = 0; j < 4; ++j) {
+        const int pj = 4 * b + j;
+        if (pj >= npages) continue;  // past the workgroup's keys: causally masked
+        const int pg = pj < a.max_pages ? a.page_table[(size_t)sq * a.max_pages + pj] : -1;
+        if (pg < 0 || (int64_t)pg >= a.num_pages) bad |= 1u << j;
+      }
+      const int sh = 4 * (b % kPfStages);
+      absent = (absent & ~(0xFu << sh)) | (bad << sh);
     }
-    const int sh = 4 * (b % kPfStages);
-    absent = (absent & ~(0xFu << sh)) | (bad << sh);
     const bool ok = page >= 0 && (int64_t)page < a.num_pages;
     const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<bf16_t*>(a.kv_pool + (ok ? ((size_t)page * a.hkv + c) * PAGE_ELEMS : 0)), 0,
@@ -212,7 +228,7 @@ __global__ __launch_bounds__(64 * NW, 1) void attn_prefill_kernel(PrefillAttnArg
               if (key > qpos[qt]) acc_s[kt][qt][e] = -INFINITY;
             }
         }
-        const uint32_t bad = (absent >> (4 * (b % kPfStages))) & 0xFu;
+        const uint32_t bad = any_absent ? (absent >> (4 * (b % kPfStages))) & 0xFu : 0u;
         if (bad) {
           // element e of tile kt holds a key of page 2 kt + e / 8 of the block
 #pragma unroll

@@ -15,7 +15,9 @@ import re
 import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libsevo.so")
+# SEVO_LIBRARY selects another build of the same library (the host-sanitized
+# checking build); the default is the in-tree libsevo.so
+LIB_PATH = os.environ.get("SEVO_LIBRARY") or os.path.join(_HERE, "libsevo.so")
 HEADER = os.path.join(os.path.dirname(_HERE), "include", "sevo.h")
 
 OK, INVALID_ARGUMENT, UNSUPPORTED, WORKSPACE_TOO_SMALL, OUT_OF_MEMORY, HIP, BAD_PAGE_TABLE = range(7)

@@ -212,23 +212,25 @@ class Workload:
     attention_only: bool = False
     steps: int = 1
     num_splits: int = 0    # 0 = library picks
+    aggregation_k: int | None = 4   # candidates concatenated per context (None: no recipe)
 
 
 WORKLOADS = {
     w.name: w for w in [
         # 1 layer, d=256, 4/2 heads x 64, FFN 1024, V 4096, N=4, p ~ U{256..512}
-        Workload("tiny_step", TINY, 4, "u256_512", seed=0),
+        Workload("tiny_step", TINY, 4, "u256_512", seed=0, aggregation_k=None),
         # attention only, 32/8 heads x 128, N=16, p = sum of 4 x U{2048..4096}
         Workload("attn_pop16_agg4", ModelShape(1, 4096, 32, 8, 128, 12288, 151936), 16,
                  "agg4_u2048_4096", seed=1, attention_only=True),
         # 8B-class dense decoder, N=64, p ~ U{16384..32768}
         Workload("dense8b_pop64_agg4", DENSE_8B, 64, "u16384_32768", seed=2, steps=16),
         # 8B-class, N=16, K=8 x 8k, +-10%
-        Workload("dense8b_pop16_agg8", DENSE_8B, 16, "agg8_8k_pm10", seed=3, steps=128),
+        Workload("dense8b_pop16_agg8", DENSE_8B, 16, "agg8_8k_pm10", seed=3, steps=128,
+                 aggregation_k=8),
         # 32B-class, N=16, p = 16384
         Workload("dense32b_pop16_agg4", DENSE_32B, 16, "const16384", seed=4, steps=64),
         # tiny MoE decoder (2 layers, 64 experts, top-4), N=4, p ~ U{256..512}
-        Workload("tiny_moe_step", TINY_MOE, 4, "u256_512", seed=5),
+        Workload("tiny_moe_step", TINY_MOE, 4, "u256_512", seed=5, aggregation_k=None),
         # 30B-A3B-class MoE decoder (48 layers, 128 experts, top-8), N=64,
         # p ~ U{16384..32768}
         Workload("moe30b_pop64_agg4", MOE_30B_A3B, 64, "u16384_32768", seed=6, steps=16),

@@ -30,14 +30,15 @@ pytestmark = pytest.mark.gpu
 
 # One layer, GPU vs oracle on the GPU's own input: max|x_gpu - x_ref| over the
 # three candidates, relative to the largest entry of the layer's update
-# max|x_ref - x_in|.  Inside one layer both sides round at the same bf16
-# storage points, so what remains is fp32 accumulation order and the rare
-# one-ulp rounding flip it causes (one flip of the SwiGLU product moves the
-# update by about 1e-4 of its largest entry).
-LAYER_REL_TOL = 2e-3
-# The oracle's own one-layer floor: the same layer with its input perturbed
-# by 1e-6 relative (fp32-level noise).  The GPU's error must stay within a
-# small multiple of the largest floor over the layers.
+# max|x_ref - x_in| (about 9 at the 8B widths, 17 at the 32B widths).  Inside
+# one layer both sides round at the same bf16 storage points, so what remains
+# is fp32 accumulation order and the one-ulp rounding flips it causes.  The
+# oracle's own one-layer floor -- the same layer with its input perturbed by
+# 1e-6 relative, fp32-level noise -- reaches 3.0e-3 of the update at these
+# widths (measured over the 36 and 64 layers); a wrong term, sign or index
+# moves the update by O(1).
+LAYER_REL_TOL = 5e-3
+# ... and the GPU's worst layer stays within a small multiple of the worst floor
 FLOOR_FACTOR = 4.0
 FINAL_LOGIT_TOL = 1e-3    # logits from the GPU's final x (one matrix product)
 WINDOW = 4                # layers in flight on the host
@@ -88,7 +89,9 @@ def test_full_depth_step_teacher_forced(S, workload):
         keep_logits=True, keep_hidden=True, workspace=ws)
     torch.cuda.synchronize()
     assert torch.isfinite(logits).all() and torch.isfinite(hidden).all()
-    idx = sorted({int(np.argmin(pop.lengths)), int(np.argmax(pop.lengths)), 1})
+    # the shortest and longest contexts and others, three distinct candidates
+    pick = [int(np.argmin(pop.lengths)), int(np.argmax(pop.lengths)), 1, w.n // 2, w.n - 1]
+    idx = sorted(list(dict.fromkeys(pick))[:3])
     gh = hidden[:, idx].double().cpu().numpy()           # [L + 1, 3, hidden]
     g_logits = logits[idx].double().cpu().numpy()
     g_ids = ids.cpu().numpy()[idx].astype(np.int64)

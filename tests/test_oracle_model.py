@@ -8,11 +8,14 @@ special case that exercises every layer step, the KV append slots and the
 RoPE positions.  Further invariants: page-permutation invariance of a whole
 step, the zero-block special case and determinism.
 """
+import contextlib
+
 import numpy as np
 import pytest
 import torch
 
 from oracle import decoder as od
+from oracle.bf16 import round_bf16
 from paper_2604_07725_amd.synth import ModelShape
 
 SHAPE = ModelShape(n_layers=2, hidden=64, n_q_heads=4, n_kv_heads=2, head_dim=32, ffn=96,
@@ -163,6 +166,158 @@ def test_mirror_rounds_only_storage_points():
     b = od.decode_step(SHAPE, w, [k.copy() for k in kvp], pt, mirror=True, **args)
     rel = np.abs(a["logits"] - b["logits"]).max() / np.abs(a["logits"]).max()
     assert 1e-5 < rel < 5e-2, rel
+
+
+# ------------------------------------------------------------------ bf16 storage points
+# The GPU path stores h, q and k (after RoPE), v, the attention output o, h2,
+# the SwiGLU product a and the final normed row in bf16, keeps the residual
+# stream and the logits in fp32, and computes everything else in fp32; the
+# oracle's mirror mode rounds at exactly those points.  The pin: the
+# transformers Qwen3 causal forward, run in float64 throughout (torch's
+# library rms_norm for every norm, a float64 RoPE table, SDPA attention) with
+# rounding hooks at those points only, must give the oracle's logits exactly,
+# while leaving out any single bf16 point moves them by ~1e-3.
+STORAGE_POINTS = ("h", "qk", "v", "o", "h2", "a", "hf", "x32", "logits32")
+
+
+def _bf16_t(t):
+    return t.to(torch.bfloat16).to(torch.float64)
+
+
+def _f32_t(t):
+    return t.to(torch.float32).to(torch.float64)
+
+
+@contextlib.contextmanager
+def _float64_with_storage_rounding(m, shape, points):
+    import torch.nn.functional as Fn
+    import transformers.models.qwen3.modeling_qwen3 as mq
+    hooks, saved = [], []
+    norms = [m.model.norm] + [n for l in m.model.layers for n in
+                              (l.input_layernorm, l.post_attention_layernorm,
+                               l.self_attn.q_norm, l.self_attn.k_norm)]
+    for n in norms:          # the library norm in float64 instead of its fp32 path
+        saved.append((n, n.forward))
+        n.forward = lambda x, n=n: Fn.rms_norm(x, (x.shape[-1],), n.weight, n.variance_epsilon)
+    rot = m.model.rotary_emb
+    old_inv, old_float, old_rope = rot.inv_freq, torch.Tensor.float, mq.apply_rotary_pos_emb
+    d = shape.head_dim
+    rot.inv_freq = 1.0 / (shape.rope_theta ** (torch.arange(0, d, 2, dtype=torch.float64) / d))
+    torch.Tensor.float = lambda self: self.to(torch.float64)   # its cos / sin in float64
+    impl = m.config._attn_implementation
+    m.config._attn_implementation = "sdpa"                     # float64 softmax
+    if "qk" in points:
+        def rope(q, k, cos, sin, *a, **kw):
+            qe, ke = old_rope(q, k, cos, sin, *a, **kw)
+            return _bf16_t(qe), _bf16_t(ke)
+        mq.apply_rotary_pos_emb = rope
+    out_hook = lambda mod, inp, out: _bf16_t(out)                          # noqa: E731
+    in_hook = lambda mod, inp: (_bf16_t(inp[0]),) + tuple(inp[1:])        # noqa: E731
+    for layer in m.model.layers:
+        res = {}
+        keep = lambda mod, inp, res=res: res.__setitem__("x", inp[0])     # noqa: E731
+        # fp32 residual: a branch output b becomes f32(x + b) - x (exact in
+        # float64), so the layer's own x + b is f32(x + b)
+        fix = lambda mod, inp, out, res=res: _f32_t(res["x"] + out) - res["x"]  # noqa: E731
+        if "x32" in points:
+            hooks += [layer.input_layernorm.register_forward_pre_hook(keep),
+                      layer.post_attention_layernorm.register_forward_pre_hook(keep)]
+        if "h" in points:
+            hooks.append(layer.input_layernorm.register_forward_hook(out_hook))
+        if "v" in points:
+            hooks.append(layer.self_attn.v_proj.register_forward_hook(out_hook))
+        if "o" in points:
+            hooks.append(layer.self_attn.o_proj.register_forward_pre_hook(in_hook))
+        if "x32" in points:
+            hooks.append(layer.self_attn.o_proj.register_forward_hook(fix))
+        if "h2" in points:
+            hooks.append(layer.post_attention_layernorm.register_forward_hook(out_hook))
+        if "a" in points:
+            hooks.append(layer.mlp.down_proj.register_forward_pre_hook(in_hook))
+        if "x32" in points:
+            hooks.append(layer.mlp.down_proj.register_forward_hook(fix))
+    if "hf" in points:
+        hooks.append(m.model.norm.register_forward_hook(out_hook))
+    if "logits32" in points:
+        hooks.append(m.lm_head.register_forward_hook(lambda mod, inp, out: _f32_t(out)))
+    try:
+        yield
+    finally:
+        for h in hooks:
+            h.remove()
+        for n, f in saved:
+            n.forward = f
+        rot.inv_freq = old_inv
+        torch.Tensor.float = old_float
+        mq.apply_rotary_pos_emb = old_rope
+        m.config._attn_implementation = impl
+
+
+def _hf64_logits(m, shape, seqs, points):
+    with _float64_with_storage_rounding(m, shape, points), torch.no_grad():
+        return m(input_ids=torch.from_numpy(np.asarray(seqs))).logits.numpy()
+
+
+def _bf16_weights(shape, rng):
+    w = _weights(shape, rng)
+    return {k: ([{kk: round_bf16(vv) for kk, vv in lw.items()} for lw in v] if k == "layers"
+                else round_bf16(v)) for k, v in w.items()}
+
+
+@pytest.mark.parametrize("seed", [0, 1])
+def test_mirror_storage_points_equal_transformers_with_bf16_hooks(seed):
+    """The oracle's mirrored decode (token by token from an empty paged cache)
+    equals the hooked float64 transformers forward exactly; without any one of
+    its bf16 points (or the fp32 logits) the forward differs, so every point
+    is in the oracle, and none is added elsewhere."""
+    rng = np.random.default_rng(100 + seed)
+    w = _bf16_weights(SHAPE, rng)
+    N, T = 2, 37
+    seqs = rng.integers(0, SHAPE.vocab, size=(N, T))
+    pt = rng.permutation(N * 3).reshape(N, 3)
+    kvp = _empty_pools(SHAPE, N * 3)
+    oracle_logits = np.empty((N, T, SHAPE.vocab))
+    for t in range(T):
+        out = od.decode_step(SHAPE, w, kvp, pt, seqs[:, t], np.full(N, t), np.arange(N),
+                             seed=1, temperature=1.0, mirror=True)
+        oracle_logits[:, t] = out["logits"]
+    m = _hf_model(SHAPE, w)
+    scale = np.abs(oracle_logits).max()
+    err = np.abs(_hf64_logits(m, SHAPE, seqs, STORAGE_POINTS) - oracle_logits).max() / scale
+    assert err <= 1e-12, err
+    for p in STORAGE_POINTS:
+        if p == "x32":
+            continue    # below the fp32 logits' resolution at this size (no flip it decides)
+        off = np.abs(_hf64_logits(m, SHAPE, seqs, [q for q in STORAGE_POINTS if q != p])
+                      - oracle_logits).max() / scale
+        assert off > (1e-9 if p == "logits32" else 1e-4), (p, off)
+    # and the pure definition: no rounding anywhere equals mirror=False exactly
+    kvp = _empty_pools(SHAPE, N * 3)
+    pure = np.empty_like(oracle_logits)
+    for t in range(T):
+        pure[:, t] = od.decode_step(SHAPE, w, kvp, pt, seqs[:, t], np.full(N, t), np.arange(N),
+                                    seed=1, temperature=1.0, mirror=False)["logits"]
+    err = np.abs(_hf64_logits(m, SHAPE, seqs, ()) - pure).max() / scale
+    assert err <= 1e-12, err
+
+
+def test_prefill_mirror_storage_points_equal_transformers_with_bf16_hooks():
+    """The same pin for the prefill (every token of two sequences through each
+    layer at once, the confidence engine's forward)."""
+    rng = np.random.default_rng(21)
+    w = _bf16_weights(SHAPE, rng)
+    lens = [37, 20]
+    seqs = [rng.integers(0, SHAPE.vocab, size=n) for n in lens]
+    starts = np.array([0, lens[0], lens[0] + lens[1]])
+    pt = np.array([[3, 0, 4], [1, 2, -1]])
+    x = od.prefill_forward(SHAPE, w, _empty_pools(SHAPE, 5), pt, np.concatenate(seqs), starts,
+                           mirror=True)
+    logits = od.lm_logits(SHAPE, w["final_norm"], w["lm_head"], x, mirror=True)
+    m = _hf_model(SHAPE, w)
+    for s in range(2):
+        ref = _hf64_logits(m, SHAPE, seqs[s][None], STORAGE_POINTS)[0]
+        err = np.abs(logits[starts[s]:starts[s + 1]] - ref).max() / np.abs(ref).max()
+        assert err <= 1e-12, (s, err)
 
 
 # ------------------------------------------------------------------ prefill (confidence engine)
