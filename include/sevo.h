@@ -198,6 +198,24 @@ int32_t sevo_attn_plan_splits(int32_t n, int32_t n_kv_heads, int32_t max_pages);
 size_t sevo_attn_workspace_bytes(int32_t n, int32_t n_q_heads, int32_t n_kv_heads,
                                  int32_t head_dim, int32_t max_pages, int32_t num_splits);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): the same
+ * attention as sevo_attn_decode, identical bits, with the split partials in a
+ * fixed device array of the library instead of a caller workspace (the
+ * workspace and workspace_bytes fields are ignored).  The array holds
+ * SEVO_NOALLOC_SCRATCH_BYTES (32 MiB) on each GPU the library runs on, until
+ * the process ends; a call whose partials need more
+ * (n_q_heads * n * splits * (head_dim + 2) * 4 bytes, rounded to 256-byte
+ * blocks) returns WORKSPACE_TOO_SMALL before launching anything.  Every call
+ * on one GPU shares that GPU's array: calls that overlap in time on one GPU
+ * (other streams, other threads) race and must be ordered by the caller.
+ * The stream must belong to the current device.  Nothing here calls
+ * hipMalloc or hipFree; the first call on a device looks up the array's
+ * address (hipGetSymbolAddress), so make it outside any graph capture.
+ * Errors: as sevo_attn_decode. */
+#define SEVO_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)
+sevo_status sevo_attn_decode_noalloc(const sevo_attn_args* a, void* stream);
+
 /* ------------------------------------------------------------------ prefill */
 
 /* Causal GQA attention of a prefill: the forward pass the cross-model

@@ -357,6 +357,69 @@ SEVO_API sevo_status sevo_attn_decode(const sevo_attn_args* a, void* stream) {
                    static_cast<hipStream_t>(stream));
 }
 
+// ------------------------------------------------------------------ attention, no allocation
+// The split partials of sevo_attn_decode_noalloc live in this fixed array:
+// each GPU the library runs on holds its own copy until the process ends.  In
+// host code the name `scratch` is a host-side stand-in, not a device address:
+// host code uses only the address hipGetSymbolAddress returns for the
+// current device, taken once per device and kept in g_scratch_ptr.
+constexpr size_t kNoAllocScratchBytes = SEVO_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) char scratch[kNoAllocScratchBytes];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices];  // device address of `scratch` per device; null = not taken yet
+
+sevo_status scratch_address(void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(SEVO_ERR_UNSUPPORTED, "device %d beyond the %d the scratch table covers", dev,
+                kMaxDevices);
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+    if (!p || !aligned16(p)) return fail(SEVO_ERR_HIP, "bad scratch address %p", p);
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return SEVO_OK;
+}
+}  // namespace
+
+SEVO_API sevo_status sevo_attn_decode_noalloc(const sevo_attn_args* a, void* stream) {
+  if (!a) return fail(SEVO_ERR_INVALID_ARGUMENT, "null args");
+  sevo_status st = check_attn_shape(a->n, a->n_q_heads, a->n_kv_heads, a->head_dim,
+                                    a->page_size, a->max_pages);
+  if (st) return st;
+  if (a->num_splits < 0) return fail(SEVO_ERR_INVALID_ARGUMENT, "num_splits < 0");
+  if (a->num_pages < 1) return fail(SEVO_ERR_INVALID_ARGUMENT, "num_pages < 1");
+  if (!(std::isfinite(a->scale)) || a->scale <= 0.f)
+    return fail(SEVO_ERR_INVALID_ARGUMENT, "scale must be finite and > 0");
+  if (a->n == 0) return SEVO_OK;
+  const void* ptrs[] = {a->q, a->kv_pool, a->page_table, a->seq_lens, a->out};
+  for (auto p : ptrs)
+    if (!p || !aligned16(p))
+      return fail(SEVO_ERR_INVALID_ARGUMENT, "null or non-16-byte-aligned pointer");
+  int S, chunk;
+  resolve_splits(a->n, a->n_kv_heads, a->max_pages, a->num_splits, &S, &chunk);
+  const size_t need = attn_ws(a->n, a->n_q_heads, a->head_dim, S);
+  if (need > kNoAllocScratchBytes)
+    return fail(SEVO_ERR_WORKSPACE_TOO_SMALL,
+                "attention needs %zu scratch bytes; the fixed scratch holds %zu (use "
+                "sevo_attn_decode with a workspace)",
+                need, kNoAllocScratchBytes);
+  void* ws = nullptr;
+  if ((st = scratch_address(&ws))) return st;
+  return attn_core(a->n, a->n_q_heads, a->n_kv_heads, a->head_dim, a->max_pages, a->num_splits,
+                   a->num_pages, a->q, a->kv_pool, a->page_table, a->seq_lens, a->scale, a->out,
+                   ws, kNoAllocScratchBytes, static_cast<hipStream_t>(stream));
+}
+
 // ------------------------------------------------------------------ prefill
 SEVO_API sevo_status sevo_attn_prefill(const sevo_prefill_attn_args* a, void* stream) {
   if (!a) return fail(SEVO_ERR_INVALID_ARGUMENT, "null args");

@@ -29,6 +29,7 @@ PACKED_WEIGHTS = {"w_qkv": PACK_PLAIN, "w_o": PACK_PLAIN, "w_gate_up": PACK_GATE
                   "w_down": PACK_PLAIN, "lm_head": PACK_PLAIN, "w_router": PACK_PLAIN,
                   "w_expert_gate_up": PACK_GATE_UP, "w_expert_down": PACK_PLAIN}
 PAGE_SIZE = 16
+NOALLOC_SCRATCH_BYTES = 32 << 20   # SEVO_NOALLOC_SCRATCH_BYTES
 PROF_KINDS = ["attn_split", "attn_combine", "qkv", "attn_out", "gate_up", "down", "lm_head",
               "norm", "rope_append", "sample", "embed", "attn_prefill", "moe_route",
               "moe_experts"]   # SEVO_PROF_* order
@@ -111,6 +112,7 @@ _SIGS = {
     "sevo_init_model": ([C.POINTER(ModelConfig), C.POINTER(Weights), C.POINTER(vp)], i32),
     "sevo_free_model": ([vp], None),
     "sevo_attn_decode": ([C.POINTER(AttnArgs), vp], i32),
+    "sevo_attn_decode_noalloc": ([C.POINTER(AttnArgs), vp], i32),
     "sevo_attn_plan_splits": ([i32, i32, i32], i32),
     "sevo_attn_workspace_bytes": ([i32, i32, i32, i32, i32, i32], sz),
     "sevo_attn_prefill": ([C.POINTER(PrefillAttnArgs), vp], i32),
@@ -218,6 +220,21 @@ def sevo_attn_decode(q, kv_pool, page_table, seq_lens, out=None, scale=None,
                  seq_lens=_p(seq_lens), scale=float(d ** -0.5 if scale is None else scale),
                  out=_p(out), workspace=_p(ws), workspace_bytes=ws.numel())
     _check(lib().sevo_attn_decode(C.byref(a), _stream(stream)))
+    return out
+
+
+def sevo_attn_decode_noalloc(q, kv_pool, page_table, seq_lens, out, scale=None, num_splits=0,
+                             stream=None):
+    """The same attention with the split partials in the library's fixed device
+    scratch (no workspace; ``out`` must be given, so nothing is allocated)."""
+    n, hq, d = q.shape
+    a = AttnArgs(n=n, n_q_heads=hq, n_kv_heads=kv_pool.shape[1], head_dim=d,
+                 page_size=PAGE_SIZE, max_pages=page_table.shape[1], num_splits=num_splits,
+                 num_pages=kv_pool.shape[0], q=_p(q), kv_pool=_p(kv_pool),
+                 page_table=_p(page_table), seq_lens=_p(seq_lens),
+                 scale=float(d ** -0.5 if scale is None else scale), out=_p(out), workspace=None,
+                 workspace_bytes=0)
+    _check(lib().sevo_attn_decode_noalloc(C.byref(a), _stream(stream)))
     return out
 
 
