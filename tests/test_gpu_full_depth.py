@@ -2,7 +2,8 @@
 widths, populations and contexts, teacher-forced layer by layer.
 
 The step runs once on the GPU for the whole population with every layer of
-the model (36 for the 8B-class decoder, 64 for the 32B-class one) and returns
+the model (36 for the 8B-class decoder, 64 for the 32B-class one, 48 for the
+30B-A3B-class mixture of experts) and returns
 the residual stream entering each layer (``out_hidden``).  For three sampled
 candidates (shortest, longest, one more) the oracle then runs each layer l on
 the GPU's own x_l, with that layer's KV cache regenerated on the host, and its
@@ -66,8 +67,20 @@ def _subset_pool(shape, seed, pop, idx, layer, extra):
     return synth.pool_pages(synth.kv_spec(shape, seed, layer, pop.n_pages), pages), pt
 
 
+# MoE: the GPU and the oracle each round h2 to bf16 on their own, which moves
+# router logits by ~1e-4, so a layer whose k-th and (k+1)-th router logits of a
+# sampled token are closer than ROUTE_GAP may select another expert on either
+# side (both valid; the oracle's own 1e-6-perturbed run does so too).  Such
+# layers are held to 4x their own floor or, failing that, to the change one
+# swapped expert can make (NEAR_TIE_TOL of the update), and reported; at most
+# a tenth of the layers may be in that class.
+ROUTE_GAP = 1e-3
+NEAR_TIE_TOL = 0.5
+
+
 @pytest.mark.timeout(1200)
-@pytest.mark.parametrize("workload", ["dense8b_pop64_agg4", "dense32b_pop16_agg4"])
+@pytest.mark.parametrize("workload", ["dense8b_pop64_agg4", "dense32b_pop16_agg4",
+                                      "moe30b_pop64_agg4"])
 def test_full_depth_step_teacher_forced(S, workload):
     from threadpoolctl import threadpool_limits
     sevo, di = S
@@ -108,42 +121,57 @@ def test_full_depth_step_teacher_forced(S, workload):
     noise = [1.0 + 1e-6 * rng.standard_normal(gh.shape[1:]) for _ in range(L)]
 
     def layer_job(l):
-        lw = {k: np.asarray(v, np.float64) for k, v in hw["layers"][l].items()}
+        # whole matrices in float64 once; a MoE layer's expert tensors stay as
+        # they are (the oracle converts the experts its tokens select)
+        lw = {k: (np.asarray(v, np.float64) if np.ndim(v) < 3 else v)
+              for k, v in hw["layers"][l].items()}
         pool, pt = _subset_pool(shape, w.seed, pop, idx, l, extra)
-        x_tf = od.decoder_layer(shape, lw, gh[l], pos, pool.copy(), pt)
+        st = {}
+        x_tf = od.decoder_layer(shape, lw, gh[l], pos, pool.copy(), pt, stats=st)
         x_fl = od.decoder_layer(shape, lw, od._f32(gh[l] * noise[l]), pos, pool.copy(), pt)
-        return lw, pool, pt, x_tf, x_fl
+        return lw, pool, pt, x_tf, x_fl, st.get("route_gap", np.inf)
 
-    errs, floors, own = [], [], gh[0].copy()
+    errs, floors, gaps, own = [], [], [], gh[0].copy()
     with threadpool_limits(1), cf.ThreadPoolExecutor(WINDOW) as ex:
         futs = collections.deque(ex.submit(layer_job, l) for l in range(min(WINDOW, L)))
         for l in range(L):
-            lw, pool, pt, x_tf, x_fl = futs.popleft().result()
+            lw, pool, pt, x_tf, x_fl, gap = futs.popleft().result()
             if l + WINDOW < L:
                 futs.append(ex.submit(layer_job, l + WINDOW))
             scale = np.abs(x_tf - gh[l]).max()
             errs.append(np.abs(gh[l + 1] - x_tf).max() / scale)
             floors.append(np.abs(x_fl - x_tf).max() / scale)
+            gaps.append(gap)
             own = od.decoder_layer(shape, lw, own, pos, pool, pt)   # the oracle's own chain
             say(f"  layer {l:2d}: rel err {errs[-1]:.2e} (floor {floors[-1]:.2e}), "
-                f"|update| {scale:.3f}, own-chain |x - x_gpu| {np.abs(own - gh[l + 1]).max():.2e}")
+                f"|update| {scale:.3f}, own-chain |x - x_gpu| {np.abs(own - gh[l + 1]).max():.2e}"
+                + (f", route gap {gap:.1e}" if shape.is_moe else ""))
         lm = hw["lm_head"][0:shape.vocab]
         ref_logits = od.lm_logits(shape, hw["final_norm"], lm, gh[L])
         own_logits = od.lm_logits(shape, hw["final_norm"], lm, own)
-    errs, floors = np.array(errs), np.array(floors)
-    say(f"  layers: max rel err {errs.max():.2e} at {int(errs.argmax())}, max floor "
-        f"{floors.max():.2e}; raw full depth (oracle's own chain): logits "
-        f"{np.abs(own_logits - g_logits).max():.2e}")
-    assert errs.max() <= LAYER_REL_TOL, errs
-    assert errs.max() <= FLOOR_FACTOR * floors.max(), (errs, floors)
+    errs, floors, gaps = np.array(errs), np.array(floors), np.array(gaps)
+    gated = gaps > ROUTE_GAP
+    near = np.nonzero(~gated)[0]
+    say(f"  layers: max rel err {errs[gated].max():.2e} over {int(gated.sum())} gated layers, "
+        f"max floor {floors[gated].max():.2e}; raw full depth (oracle's own chain): logits "
+        f"{np.abs(own_logits - g_logits).max():.2e}"
+        + ("" if gated.all() else f"; routing near-tie layers {near.tolist()}: errors "
+           f"{errs[near].round(5).tolist()}, floors {floors[near].round(5).tolist()}, gaps "
+           f"{[float(f'{g:.1e}') for g in gaps[near]]}"))
     # final norm -> LM head -> sampler on the GPU's final x
     lerr = np.abs(g_logits - ref_logits).max()
     det = {}
-    ref_ids, ref_lps, gaps = od.logprob_sample(ref_logits, temp, seed, pop.uids[idx], pos,
-                                               details=det)
-    lp_err, n_exact = check_ids(g_ids, g_lps, ref_ids, ref_lps, gaps, det,
+    ref_ids, ref_lps, sgaps = od.logprob_sample(ref_logits, temp, seed, pop.uids[idx], pos,
+                                                details=det)
+    lp_err, n_exact = check_ids(g_ids, g_lps, ref_ids, ref_lps, sgaps, det,
                                 label=f"{workload} full depth")
     say(f"  final: logits err {lerr:.2e} (max |logit| {np.abs(ref_logits).max():.2f}), lp err "
         f"{lp_err:.2e}, ids {g_ids.tolist()} vs {ref_ids.tolist()} gaps "
-        f"{np.round(gaps, 4).tolist()} ({n_exact} exact)")
+        f"{np.round(sgaps, 4).tolist()} ({n_exact} exact)")
     assert lerr <= FINAL_LOGIT_TOL
+    assert errs[gated].max() <= LAYER_REL_TOL, errs
+    assert errs[gated].max() <= FLOOR_FACTOR * floors[gated].max(), (errs, floors)
+    assert len(near) <= L // 10, f"{len(near)} layers with routing near-ties"
+    for l in near:
+        assert (errs[l] <= max(LAYER_REL_TOL, FLOOR_FACTOR * floors[l])
+                or errs[l] <= NEAR_TIE_TOL), (l, errs[l], floors[l], gaps[l])
