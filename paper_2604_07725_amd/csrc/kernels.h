@@ -121,6 +121,7 @@ hipError_t launch_moe_experts(const MoeExpertArgs& a, hipStream_t st);
 struct LinearPlan {
   int k_splits;
   int k_chunk;
+  int rb = 4;  // 16-row weight blocks per workgroup (SwiGLU: gate + up blocks)
 };
 LinearPlan plan_linear(int m, int n_out, int k, int k_splits, int mode);
 size_t linear_workspace_bytes(int m, int n_out, int k, int k_splits, int mode);

@@ -168,11 +168,17 @@ def test_linear_rejects_bad_shapes(kw, status):
 
 def test_linear_plan_and_workspace():
     L = sevo.lib()
-    # split K while fewer than 192 workgroups and each split keeps >= 1024 k
+    # the fewest splits (each >= 1024 k) whose row-block count fits the
+    # projection in one round of 256 workgroups: QKV 3 row blocks x 2 splits,
+    # output / down 4 x 4; at M = 16 QKV 5 x 2, output / down 5 x 4
     assert L.sevo_linear_workspace_bytes(64, 6144, 4096, 0) == 2 * 64 * 6144 * 4
     assert L.sevo_linear_workspace_bytes(64, 4096, 4096, 0) == 4 * 64 * 4096 * 4
     assert L.sevo_linear_workspace_bytes(64, 4096, 12288, 0) == 4 * 64 * 4096 * 4
-    assert L.sevo_linear_workspace_bytes(64, 151936, 4096, 0) == 0      # one split: no partials
+    assert L.sevo_linear_workspace_bytes(16, 10240, 5120, 0) == 2 * 16 * 10240 * 4
+    assert L.sevo_linear_workspace_bytes(16, 5120, 8192, 0) == 4 * 16 * 5120 * 4
+    assert L.sevo_linear_workspace_bytes(16, 5120, 25600, 0) == 4 * 16 * 5120 * 4
+    # several rounds whatever the split: one split, no partials
+    assert L.sevo_linear_workspace_bytes(64, 151936, 4096, 0) == 0
     assert L.sevo_linear_workspace_bytes(4, 512, 256, 0) == 0           # short k: one split
 
 
