@@ -367,12 +367,16 @@ __global__ __launch_bounds__(256) void moe_expert_kernel(MoeExpertArgs a) {
     for (int h = 0; h < FPW; ++h)
 #pragma unroll
       for (int b = 0; b < NB; ++b) acc[h][b] = f32x4{0.f, 0.f, 0.f, 0.f};
-    // step j of K; past the end it re-reads the last one (cache hits, unused)
+    // step j of K; past the end it re-reads the last one (cache hits, unused).
+    // Expert weights are read once: non-temporal loads keep their stream from
+    // evicting the gathered activation rows from L2 (experts 211 -> 200 us
+    // per layer at the 30B-A3B shape)
     auto load = [&](MoeFrag<NB, FPW>& f, int j) {
       const int st = min(j, KS - 1);
 #pragma unroll
       for (int h = 0; h < FPW; ++h)
-        f.a[h] = *reinterpret_cast<const bf16x8v*>(wp + (size_t)st * 2048 + fr[h] * 512);
+        f.a[h] = __builtin_nontemporal_load(
+            reinterpret_cast<const bf16x8v*>(wp + (size_t)st * 2048 + fr[h] * 512));
 #pragma unroll
       for (int b = 0; b < NB; ++b)
         f.b[b] = *reinterpret_cast<const bf16x8v*>(
