@@ -57,7 +57,8 @@ int min_splits(int max_pages) { return (max_pages + kMaxSplitPages - 1) / kMaxSp
 // the first count that fills whole rounds; at least 32 pages (8 per wave)
 // per split where the minimum allows.  Measured on the matrix-core kernel:
 // 64 x 8 pairs at 16k-32k -> 4, 16 x 8 pairs at 64k -> 12 (9 and 10 are 7%
-// slower), 16 x 8 at 8k-16k -> 4 (28 is 20% slower).
+// slower), 16 x 8 at 8k-16k -> 4 (28 is 20% slower), 64 x 4 pairs at
+// 16k-32k -> 8 (4: 525 against 510 us).
 constexpr int kResidentSplitGroups = 512;
 
 int plan_splits(int n, int hkv, int max_pages) {
@@ -69,7 +70,16 @@ int plan_splits(int n, int hkv, int max_pages) {
   if (pairs * s < kResidentSplitGroups) s = (kResidentSplitGroups + pairs - 1) / pairs;
   if (s > cap) return cap;
   for (long long t = s; t <= 2 * s && t <= cap; ++t)
-    if ((pairs * t) % kResidentSplitGroups == 0) return (int)t;
+    if ((pairs * t) % kResidentSplitGroups == 0) {
+      s = t;
+      break;
+    }
+  // fewer than three rounds of long splits leave a ragged last round (short
+  // candidates have empty or partial last splits): twice the splits, while
+  // each still spans at least 192 pages
+  if (pairs * s < 3 * kResidentSplitGroups && 2 * s <= cap &&
+      (max_pages + 2 * s - 1) / (2 * s) >= 192)
+    s *= 2;
   return (int)s;
 }
 

@@ -123,10 +123,10 @@ def test_split_planning():
     # least the 512-pages-per-split minimum, at most max_pages / 32
     assert L.sevo_attn_plan_splits(64, 8, 2037) == 4
     assert L.sevo_attn_plan_splits(64, 8, 2049) == 5      # the minimum rises to 5
-    assert L.sevo_attn_plan_splits(64, 8, 1024) == 2
+    assert L.sevo_attn_plan_splits(64, 8, 1024) == 4      # 2 would be two ragged rounds
     assert L.sevo_attn_plan_splits(16, 8, 1024) == 4      # 2 would leave half a round
     assert L.sevo_attn_plan_splits(16, 8, 4470) == 12     # minimum 9, 12 fills 3 rounds
-    assert L.sevo_attn_plan_splits(64, 4, 2040) == 4
+    assert L.sevo_attn_plan_splits(64, 4, 2040) == 8      # 4 would be two ragged rounds
     assert L.sevo_attn_plan_splits(64, 8, 4100) == 9
     assert L.sevo_attn_plan_splits(3, 5, 4000) == 35      # no whole-round count up to 2x
     assert L.sevo_attn_plan_splits(4, 2, 33) == 2         # capped: 32 pages per split
