@@ -497,6 +497,15 @@ typedef struct {
 
 sevo_status sevo_linear(const sevo_linear_args* a, void* stream);
 size_t sevo_linear_workspace_bytes(int32_t m, int32_t n_out, int32_t k, int32_t k_splits);
+/* The plan of the skinny kernel that sevo_linear runs for m < 256 (and the
+ * decode step for its projections): plan[0] = K splits, plan[1] = k per split,
+ * plan[2] = 16-row weight blocks per workgroup (for SWIGLU gate and up blocks,
+ * an even count).  The planner aims at one round of 256 equal workgroups (one
+ * per CU).  Writes plan[0..2] (caller-owned host memory) and returns SEVO_OK;
+ * INVALID_ARGUMENT for a null plan or a shape outside m in [1, 255],
+ * n_out % 64 == 0, k % 32 == 0, mode in {STORE, ADD, SWIGLU}. */
+sevo_status sevo_linear_plan(int32_t m, int32_t n_out, int32_t k, int32_t k_splits, int32_t mode,
+                             int32_t* plan);
 
 /* Row-major bf16 [n_out][k] (src) -> packed weight layout (dst, a separate
  * buffer of the same size).  SEVO_PACK_GATE_UP treats rows 0..n_out/2-1 as

@@ -607,6 +607,20 @@ SEVO_API size_t sevo_linear_workspace_bytes(int32_t m, int32_t n_out, int32_t k,
   return round_up(sevo::linear_workspace_bytes(m, n_out, k, k_splits, SEVO_LINEAR_STORE), 256);
 }
 
+SEVO_API sevo_status sevo_linear_plan(int32_t m, int32_t n_out, int32_t k, int32_t k_splits,
+                                      int32_t mode, int32_t* plan) {
+  if (!plan) return fail(SEVO_ERR_INVALID_ARGUMENT, "null plan");
+  if (m < 1 || m >= sevo::kLargeGemmMinM || n_out < 64 || n_out % 64 || k < 32 || k % 32 ||
+      k_splits < 0 || mode < SEVO_LINEAR_STORE || mode > SEVO_LINEAR_SWIGLU)
+    return fail(SEVO_ERR_INVALID_ARGUMENT, "bad shape m %d n_out %d k %d k_splits %d mode %d", m,
+                n_out, k, k_splits, mode);
+  const sevo::LinearPlan p = sevo::plan_linear(m, n_out, k, k_splits, mode);
+  plan[0] = p.k_splits;
+  plan[1] = p.k_chunk;
+  plan[2] = p.rb;
+  return SEVO_OK;
+}
+
 SEVO_API sevo_status sevo_linear(const sevo_linear_args* a, void* stream) {
   if (!a) return fail(SEVO_ERR_INVALID_ARGUMENT, "null args");
   sevo_status st = linear_check(a->m, a->n_out, a->k, a->ldx, a->mode, a->k_splits, a->flags);

@@ -131,6 +131,7 @@ _SIGS = {
     "sevo_add_rmsnorm": ([vp, vp, i32, vp, i32, i32, f32, vp, vp], i32),
     "sevo_linear": ([C.POINTER(LinearArgs), vp], i32),
     "sevo_linear_workspace_bytes": ([i32, i32, i32, i32], sz),
+    "sevo_linear_plan": ([i32, i32, i32, i32, i32, C.POINTER(i32)], i32),
     "sevo_pack_weight": ([vp, vp, i32, i32, i32, vp], i32),
     "sevo_qk_norm_rope_append": ([vp, i32, vp, i32, vp, vp, i32, i64, vp, vp, vp], i32),
     "sevo_fill_normal_bf16": ([vp, i64, u64, i64, f32, f32, i32, vp], i32),
@@ -340,6 +341,13 @@ def sevo_add_rmsnorm(x, partials, gain, eps, out=None, stream=None):
 
 def sevo_linear_workspace_bytes(m, n_out, k, k_splits=0) -> int:
     return int(lib().sevo_linear_workspace_bytes(m, n_out, k, k_splits))
+
+
+def sevo_linear_plan(m, n_out, k, k_splits=0, mode=LINEAR_STORE):
+    """(k splits, k per split, 16-row weight blocks per workgroup) of the skinny kernel."""
+    plan = (C.c_int32 * 3)()
+    _check(lib().sevo_linear_plan(m, n_out, k, k_splits, mode, plan))
+    return tuple(int(v) for v in plan)
 
 
 def sevo_linear(x, w, mode=LINEAR_STORE, out=None, k_splits=0, workspace=None, stream=None,

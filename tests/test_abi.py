@@ -182,6 +182,34 @@ def test_linear_plan_and_workspace():
     assert L.sevo_linear_workspace_bytes(4, 512, 256, 0) == 0           # short k: one split
 
 
+def test_linear_plans_of_the_decode_projections():
+    """(splits, k per split, row blocks per workgroup) of the decode shapes:
+    about one round of 256 workgroups each, the LM head many rounds."""
+    plan = sevo.sevo_linear_plan
+    # 8B-class, 64 candidates: QKV, output, gate/up (3 gate/up pairs), down, LM head
+    assert plan(64, 6144, 4096) == (2, 2048, 3)
+    assert plan(64, 4096, 4096) == (4, 1024, 4)
+    assert plan(64, 24576, 4096, mode=sevo.LINEAR_SWIGLU) == (1, 4096, 6)
+    assert plan(64, 4096, 12288) == (4, 3072, 4)
+    assert plan(64, 151936, 4096, k_splits=1) == (1, 4096, 8)
+    # 32B-class, 16 candidates (7 gate/up pairs: 229 workgroups)
+    assert plan(16, 10240, 5120) == (2, 2560, 5)
+    assert plan(16, 5120, 8192) == (4, 2048, 5)
+    assert plan(16, 51200, 5120, mode=sevo.LINEAR_SWIGLU) == (1, 5120, 14)
+    assert plan(16, 5120, 25600) == (4, 6400, 5)
+    assert plan(16, 151936, 5120, k_splits=1) == (1, 5120, 10)
+    # the caller's split count is kept
+    assert plan(64, 6144, 4096, k_splits=3)[0] == 3
+
+
+@pytest.mark.parametrize("args", [(0, 128, 256, 0, 0), (256, 128, 256, 0, 0), (4, 96, 256, 0, 0),
+                                  (4, 128, 48, 0, 0), (4, 128, 256, -1, 0), (4, 128, 256, 0, 3)])
+def test_linear_plan_rejects_bad_shapes(args):
+    out = (C.c_int32 * 3)()
+    assert sevo.lib().sevo_linear_plan(*args, out) == sevo.INVALID_ARGUMENT
+    assert sevo.lib().sevo_linear_plan(4, 128, 256, 0, 0, None) == sevo.INVALID_ARGUMENT
+
+
 @pytest.mark.parametrize("kw,status", [
     (dict(n_out=96), sevo.UNSUPPORTED),
     (dict(k=48), sevo.UNSUPPORTED),

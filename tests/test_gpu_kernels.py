@@ -488,6 +488,52 @@ def test_linear_matches_float64_matmul(S, m, n_out, k, mode, ks, xt):
     np.testing.assert_allclose(got, ref, rtol=0, atol=2e-5 * scale + 1e-6 * np.abs(ref).max())
 
 
+# one shape per instantiated skinny kernel: (M tile rows, 16-row weight blocks
+# per workgroup, SwiGLU pairs or not), found by running the planner over n_out;
+# every one leaves a ragged last workgroup (row blocks past the matrix)
+ROW_BLOCK_CASES = [
+    # m, n_out, mode, row blocks the plan must pick
+    (16, 128, 0, 2), (16, 128, 2, 2), (16, 8256, 0, 3), (16, 12352, 0, 4), (16, 8320, 2, 4),
+    (16, 16448, 0, 5), (16, 20544, 0, 6), (16, 16512, 2, 6), (16, 24640, 0, 8),
+    (16, 24704, 2, 8), (16, 32832, 0, 10), (16, 32896, 2, 10), (16, 41024, 0, 12),
+    (16, 41088, 2, 12), (16, 49216, 0, 14), (16, 49280, 2, 14), (16, 57408, 0, 16),
+    (16, 57472, 2, 16),
+    (24, 128, 0, 2), (24, 128, 2, 2), (24, 8256, 0, 3), (24, 12352, 0, 4), (24, 8320, 2, 4),
+    (24, 16448, 0, 5), (24, 20544, 0, 6), (24, 16512, 2, 6), (24, 24640, 0, 8),
+    (24, 24704, 2, 8), (24, 32832, 0, 10), (24, 32896, 2, 10), (24, 41024, 0, 12),
+    (24, 41088, 2, 12),
+    (64, 128, 0, 3), (64, 12352, 0, 4), (64, 128, 2, 4), (64, 16448, 0, 5), (64, 20544, 0, 6),
+    (64, 16512, 2, 6), (64, 24640, 0, 8), (64, 24704, 2, 8),
+]
+
+
+@pytest.mark.parametrize("m,n_out,mode,rb", ROW_BLOCK_CASES)
+def test_linear_every_row_block_kernel(S, m, n_out, mode, rb):
+    """Each (M tile, row blocks, epilogue) instance of the skinny kernel against
+    a float64 product, every output column (k = 256, one split); every third
+    case takes a row-major X."""
+    sevo, _ = S
+    k = 256
+    assert sevo.sevo_linear_plan(m, n_out, k, 0, mode)[2] == rb
+    xt = ROW_BLOCK_CASES.index((m, n_out, mode, rb)) % 3 != 0
+    say(f"linear row blocks {rb} m={m} n={n_out} mode={mode} x_tiled={xt}")
+    x, _, wp, xh, wh = _linear_inputs(sevo, m, n_out, k, mode)
+    if xt:
+        xb = tile_activations_host(bf16_bits(x).reshape(m, k))
+        x = torch.from_numpy(xb.view(np.int16)).cuda().view(torch.bfloat16)
+    out = sevo.sevo_linear(x, wp, mode=mode, x_tiled=xt, m=m)
+    torch.cuda.synchronize()
+    y = xh.astype(np.float64) @ wh.astype(np.float64).T
+    if mode == 2:
+        F = n_out // 2
+        ref = od.silu(y[:, :F]) * y[:, F:]
+        got = to_np(out)
+        assert np.all(np.abs(got - ref) <= 2 ** -8 * np.abs(ref) + 1e-4 * np.abs(ref).max())
+    else:
+        got = out.double().cpu().numpy()
+        np.testing.assert_allclose(got, y, rtol=0, atol=2e-5 * np.sqrt(k) * 0.02 + 1e-6 * np.abs(y).max())
+
+
 @pytest.mark.parametrize("n_out,k,gate_up", [(64, 32, False), (192, 160, False),
                                              (4096, 4096, False), (256, 96, True),
                                              (24576, 4096, True)])
