@@ -300,12 +300,17 @@ LinearPlan plan_linear(int m, int n_out, int k, int k_splits, int mode) {
   // streams 8 steps or more) whose plan fills 95% of its last round or needs
   // more than one round, else the fullest.  Split partials cost M x n_out x 8 bytes each (written and
   // read back), so more splits must fill the rounds clearly better (by 2%).
+  // A projection too small for 64 workgroups even at 1024 k per split (a MoE
+  // router: 128 experts) may split down to 256 k; its partials are tiny.
   int cands[5], nc = 0;
+  const int upw_min = (rb_min(mb) + per_unit - 1) / per_unit;
+  const long wgs_1024 = (long)((units + upw_min - 1) / upw_min) * mt * (k >= 2048 ? k / 1024 : 1);
+  const int min_chunk = wgs_1024 < 64 ? 256 : 1024;
   if (swiglu) cands[nc++] = 1;
   else if (k_splits > 0) cands[nc++] = k_splits;
   else
     for (int s = 1; s <= 16; s *= 2)
-      if (s == 1 || chunk_of(s) >= 1024) cands[nc++] = s;
+      if (s == 1 || chunk_of(s) >= min_chunk) cands[nc++] = s;
   double best_eff = -1.0;
   for (int i = 0; i < nc; ++i) {
     const int chunk = chunk_of(cands[i]);
