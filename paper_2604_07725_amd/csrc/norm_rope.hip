@@ -265,8 +265,8 @@ __global__ __launch_bounds__(1024) void add_rmsnorm_kernel(float* __restrict__ x
   const size_t src = row_idx ? (size_t)row_idx[blockIdx.x] : (size_t)blockIdx.x;
   float* xr = x + src * cols;
   const float* pr = part + src * cols;
-  float ss = 0.f;
-  for (int c = threadIdx.x * 4; c < cols; c += 4096) {
+  // x plus the partials (split order) at column c, written back to x
+  auto load_sum = [&](int c) {
     f32x4 v = *reinterpret_cast<const f32x4*>(xr + c);
     if (S > 0) {
       f32x4 p[16];
@@ -278,11 +278,38 @@ __global__ __launch_bounds__(1024) void add_rmsnorm_kernel(float* __restrict__ x
         if (s < S) v += p[s];
       if (!row_idx) *reinterpret_cast<f32x4*>(xr + c) = v;
     }
+    return v;
+  };
+  auto store_out = [&](int c, f32x4 v, float inv) {
+    const uint2 g = *reinterpret_cast<const uint2*>(gain + c);
+    uint2 o;
+    o.x = pack_bf16x2(v.x * inv * bf16_lo(g.x), v.y * inv * bf16_hi(g.x));
+    o.y = pack_bf16x2(v.z * inv * bf16_lo(g.y), v.w * inv * bf16_hi(g.y));
+    // 4 consecutive columns are contiguous in the tiled activation layout
+    *reinterpret_cast<uint2*>(out + act_tile_offset(blockIdx.x, c, cols)) = o;
+  };
+  // the first two 4-column groups of a thread (every row up to 8192 columns)
+  // stay in registers across the reduction instead of being read back from x
+  const int c0 = threadIdx.x * 4, c1 = c0 + 4096;
+  f32x4 v0 = f32x4{0.f, 0.f, 0.f, 0.f}, v1 = v0;
+  float ss = 0.f;
+  if (c0 < cols) {
+    v0 = load_sum(c0);
+    ss += v0.x * v0.x + v0.y * v0.y + v0.z * v0.z + v0.w * v0.w;
+  }
+  if (c1 < cols) {
+    v1 = load_sum(c1);
+    ss += v1.x * v1.x + v1.y * v1.y + v1.z * v1.z + v1.w * v1.w;
+  }
+  for (int c = c0 + 8192; c < cols; c += 4096) {
+    const f32x4 v = load_sum(c);
     ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
   }
   ss = block_sum<16>(ss, red);
   const float inv = 1.0f / sqrtf(ss / (float)cols + eps);
-  for (int c = threadIdx.x * 4; c < cols; c += 4096) {
+  if (c0 < cols) store_out(c0, v0, inv);
+  if (c1 < cols) store_out(c1, v1, inv);
+  for (int c = c0 + 8192; c < cols; c += 4096) {
     f32x4 v = *reinterpret_cast<const f32x4*>(xr + c);
     if (row_idx) {  // x was not updated in place: add the partials again, same order
       f32x4 p[16];
@@ -293,12 +320,7 @@ __global__ __launch_bounds__(1024) void add_rmsnorm_kernel(float* __restrict__ x
       for (int s = 0; s < 16; ++s)
         if (s < S) v += p[s];
     }
-    const uint2 g = *reinterpret_cast<const uint2*>(gain + c);
-    uint2 o;
-    o.x = pack_bf16x2(v.x * inv * bf16_lo(g.x), v.y * inv * bf16_hi(g.x));
-    o.y = pack_bf16x2(v.z * inv * bf16_lo(g.y), v.w * inv * bf16_hi(g.y));
-    // 4 consecutive columns are contiguous in the tiled activation layout
-    *reinterpret_cast<uint2*>(out + act_tile_offset(blockIdx.x, c, cols)) = o;
+    store_out(c, v, inv);
   }
 }
 
