@@ -18,9 +18,9 @@ the kernels rather than the storage format.  ``mirror=False`` gives the pure
 definition.
 
 Pins (checked by ``tests/test_oracle_*.py`` on the CPU): see each module.
-Parity unpinned by the paper: the paper prints no worked numeric example for
-this path, so every pin is a closed form, invariant, library special case or
-brute force, never a value printed in the paper.
+Every function is pinned.  The paper prints no worked numeric example for
+this path, so each pin is a closed form, an invariant, a library special
+case or a brute force rather than a value printed in the paper.
 """
 from .bf16 import round_bf16, bf16_bits_to_f32
 from .philox import philox4x32_10, uniform01, gumbel_noise
