@@ -3,9 +3,12 @@
 // in the thousands and the product is compute-bound (intensity ~ M flop per
 // weight byte, far above the ~315 flop/byte ridge of the chip).
 //
-//   * workgroup tile 256 (m) x 256 (n), 4 waves in a 2 x 2 grid, each wave a
-//     128 x 128 sub-tile held as 4 x 4 accumulators of the 32x32x16 bf16 MFMA
-//     (256 fp32 per lane, in the accumulation registers);
+//   * workgroup tile 256 (m) x 256 (n), 8 waves in a 2 x 4 grid, each wave a
+//     128 x 64 sub-tile held as 4 x 2 accumulators of the 32x32x16 bf16 MFMA
+//     (128 fp32 per lane, 180 registers in all), so two waves share each SIMD
+//     and one issues MFMAs while the other waits on its LDS reads or a
+//     barrier (2-3% faster than 4 waves of 128 x 128 sub-tiles, one per
+//     SIMD, on every 8B-class shape at M = 16K and 40K);
 //   * K is consumed in stages of 32: the 16 KB X slice and the 16 KB W slice
 //     of a stage go straight from global memory into LDS with the gfx950
 //     direct-to-LDS loads (16 bytes per lane, no register staging); four LDS
@@ -42,21 +45,22 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 constexpr int kLgBM = 256, kLgBN = 256, kLgBK = 32, kLgStages = 4;
 // one stage = one 32-column step: A 16 row blocks + B 4 superblocks x 4 fragments
 constexpr int kLgStageElems = 16 * 512 + 16 * 512;
-constexpr int kLgDmaPerStage = 8;  // direct loads per wave per stage
+constexpr int kLgDmaPerStage = 4;  // direct loads per wave per stage
+constexpr int kLgWaves = 8;
 
 // EPI 0: out fp32 [M][ldo] = Y;  EPI 1: out += Y;  EPI 2: SwiGLU -> out_bf16;
 // EPI 3 (grouped down): out [slot][token][N] = weight * Y
 // XT 1: X in the tiled activation layout, else row-major with stride ldx
 // GR 1: grouped (M = the rows of X: tokens for gate/up, entries for down)
 template <int EPI, int XT, int GR>
-__global__ __launch_bounds__(256, 1) void gemm_large_kernel(
+__global__ __launch_bounds__(64 * kLgWaves, 1) void gemm_large_kernel(
     const bf16_t* __restrict__ X, int ldx, int M, const bf16_t* __restrict__ W, int N, int K,
     float* __restrict__ out, int ldo, bf16_t* __restrict__ out_bf16, int out_tiled, int tiles_m,
     int tiles_n, GroupArgs g) {
   __shared__ __attribute__((aligned(1024))) bf16_t smem[kLgStages * kLgStageElems];
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave >> 2, wn = wave & 3;
 
   // ---- tile order: XCD-contiguous ranges, groups of GM m-tiles
   const int total = tiles_m * tiles_n;
@@ -96,20 +100,20 @@ __global__ __launch_bounds__(256, 1) void gemm_large_kernel(
   const int last_blk = (M - 1) >> 4;
   const int last_sb = (N >> 6) - 1;
 
-  // ---- this wave's direct loads per stage: A row blocks 4w..4w+3 and the
-  // four fragments of B superblock w, each through a wave-uniform descriptor
+  // ---- this wave's direct loads per stage: A row blocks 2w, 2w + 1 and
+  // fragments 2 (w % 2), + 1 of B superblock w / 2, each through a wave-uniform descriptor
   // over the region it streams (byte offsets stay far below 2^32)
-  __amdgpu_buffer_rsrc_t ra[4];
+  __amdgpu_buffer_rsrc_t ra[2];
   uint32_t a_voff;  // this lane's byte offset at step 0 (plus 1 KB or 64 B per step)
-  uint32_t g_voff[4];  // grouped: per-lane gathered row offsets (one descriptor)
+  uint32_t g_voff[2];  // grouped: per-lane gathered row offsets (one descriptor)
   if constexpr (GR) {
     // one descriptor over the whole X; a row past the tile's entries gets an
     // offset past the records (the direct load then writes zeros)
     const uint32_t recs = XT ? (uint32_t)(((M + 15) >> 4) * 16) * K * 2 : (uint32_t)M * ldx * 2;
     ra[0] = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(X), 0, recs, 0x00020000);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int j = m0 + 16 * (4 * wave + i) + (lane & 15);
+    for (int i = 0; i < 2; ++i) {
+      const int j = m0 + 16 * (2 * wave + i) + (lane & 15);
       g_voff[i] = 0x80000000u;
       if (j < rows) {
         if constexpr (XT) {
@@ -122,8 +126,8 @@ __global__ __launch_bounds__(256, 1) void gemm_large_kernel(
     }
   }
 #pragma unroll
-  for (int i = 0; i < 4 && !GR; ++i) {
-    const int blk = min((m0 >> 4) + 4 * wave + i, last_blk);
+  for (int i = 0; i < 2 && !GR; ++i) {
+    const int blk = min((m0 >> 4) + 2 * wave + i, last_blk);
     if constexpr (XT) {
       ra[i] = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(X + (size_t)blk * KS * 512), 0,
                                                 KS * 1024, 0x00020000);
@@ -137,7 +141,7 @@ __global__ __launch_bounds__(256, 1) void gemm_large_kernel(
   }
   if constexpr (XT) a_voff = lane * 16;
   else a_voff = ((lane & 15) * ldx + 8 * (lane >> 4)) * 2;
-  const int sb = min((n0 >> 6) + wave, last_sb);
+  const int sb = min((n0 >> 6) + (wave >> 1), last_sb);
   const __amdgpu_buffer_rsrc_t rb = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<bf16_t*>(W + (size_t)sb * KS * 2048), 0, KS * 4096, 0x00020000);
 
@@ -146,32 +150,34 @@ __global__ __launch_bounds__(256, 1) void gemm_large_kernel(
     if constexpr (GR) {
       const uint32_t dv = XT ? st * 1024u : st * 64u;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) dma16(ra[0], g_voff[i] + dv, so + (4 * wave + i) * 512);
+      for (int i = 0; i < 2; ++i) dma16(ra[0], g_voff[i] + dv, so + (2 * wave + i) * 512);
     } else {
       const uint32_t v = a_voff + (XT ? st * 1024u : st * 64u);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) dma16(ra[i], v, so + (4 * wave + i) * 512);
+      for (int i = 0; i < 2; ++i) dma16(ra[i], v, so + (2 * wave + i) * 512);
     }
   };
   auto issue_b = [&](int st) {
     bf16_t* so = smem + (st & (kLgStages - 1)) * kLgStageElems;
 #pragma unroll
-    for (int tt = 0; tt < 4; ++tt)
-      dma16(rb, st * 4096u + tt * 1024u + lane * 16, so + 16 * 512 + (wave * 4 + tt) * 512);
+    for (int t2 = 0; t2 < 2; ++t2) {
+      const int tt = 2 * (wave & 1) + t2;
+      dma16(rb, st * 4096u + tt * 1024u + lane * 16, so + 16 * 512 + ((wave >> 1) * 4 + tt) * 512);
+    }
   };
   // wait until stage st has landed.  When it is waited for, stage st + 1 is
   // fully issued and stage st + 2 only its A half (issue_b of a stage follows
-  // the barrier), so up to 8 + 4 younger loads may stay outstanding.
+  // the barrier), so up to 4 + 2 younger loads may stay outstanding.
   // every iteration issues a full stage (stages past the last one load zeros
   // or unused rows into a buffer nobody reads again), so when stage st is
   // waited for, stage st + 1 is fully issued and st + 2 only its A half
   auto wait_stage = [&](int) { wait_vmcnt<kLgDmaPerStage + kLgDmaPerStage / 2>(); };
 
-  f32x16 acc[4][4];
+  f32x16 acc[4][2];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int j = 0; j < 2; ++j)
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
@@ -180,15 +186,15 @@ __global__ __launch_bounds__(256, 1) void gemm_large_kernel(
   // B: n-tile nt is half (nt & 1) of superblock wn*2 + nt/2 (the gate or up
   // half for SwiGLU), fragments 2 (nt & 1) + {0, 1}.
   const int half = (lane >> 4) & 1, r16 = lane & 15, khi = lane >> 5;
-  int a_off[4], b_off[4];
+  int a_off[4], b_off[2];
 #pragma unroll
   for (int mt = 0; mt < 4; ++mt) a_off[mt] = (wm * 8 + 2 * mt + half) * 512 + r16 * 8;
 #pragma unroll
-  for (int nt = 0; nt < 4; ++nt)
-    b_off[nt] = 16 * 512 + ((wn * 2 + (nt >> 1)) * 4 + 2 * (nt & 1) + half) * 512 + r16 * 8;
+  for (int nt = 0; nt < 2; ++nt)
+    b_off[nt] = 16 * 512 + (wn * 4 + 2 * nt + half) * 512 + r16 * 8;
 
   struct Frags {
-    bf16x8v a[4], b[4];
+    bf16x8v a[4], b[2];
   };
   // operand runs of 16-k half kk of stage st: run quarter 2 kk + lane / 32
   auto read = [&](Frags& f, int st, int kk) {
@@ -196,13 +202,13 @@ __global__ __launch_bounds__(256, 1) void gemm_large_kernel(
 #pragma unroll
     for (int mt = 0; mt < 4; ++mt) f.a[mt] = *reinterpret_cast<const bf16x8v*>(so + a_off[mt]);
 #pragma unroll
-    for (int nt = 0; nt < 4; ++nt) f.b[nt] = *reinterpret_cast<const bf16x8v*>(so + b_off[nt]);
+    for (int nt = 0; nt < 2; ++nt) f.b[nt] = *reinterpret_cast<const bf16x8v*>(so + b_off[nt]);
   };
   auto mma = [&](const Frags& f) {
 #pragma unroll
     for (int mt = 0; mt < 4; ++mt)
 #pragma unroll
-      for (int nt = 0; nt < 4; ++nt)
+      for (int nt = 0; nt < 2; ++nt)
         acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[mt], f.b[nt], acc[mt][nt], 0, 0, 0);
   };
 
@@ -217,12 +223,12 @@ __global__ __launch_bounds__(256, 1) void gemm_large_kernel(
   // this way measured faster than issuing a stage's loads in one burst.
   auto interleave = [&](int nd) {
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
+    for (int i = 0; i < 6; ++i) {
       __builtin_amdgcn_sched_group_barrier(0x8, 1, 0);
       __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
       if (i < nd) __builtin_amdgcn_sched_group_barrier(0x10, 1, 0);
     }
-    __builtin_amdgcn_sched_group_barrier(0x8, 8, 0);
+    __builtin_amdgcn_sched_group_barrier(0x8, 2, 0);
   };
   Frags f0, f1;
   for (int st = 0; st < 3; ++st) {
@@ -236,7 +242,7 @@ __global__ __launch_bounds__(256, 1) void gemm_large_kernel(
     issue_a(kt + 3);
     read(f1, kt, 1);
     mma(f0);
-    interleave(4);
+    interleave(2);
     __builtin_amdgcn_sched_barrier(0);
     // (after the last stage this reads a stale buffer that is never used:
     // keeping the step unconditional keeps the LDS reads interleaved)
@@ -246,7 +252,7 @@ __global__ __launch_bounds__(256, 1) void gemm_large_kernel(
     issue_b(kt + 3);
     read(f0, kt + 1, 0);
     mma(f1);
-    interleave(4);
+    interleave(2);
     __builtin_amdgcn_sched_barrier(0);
   }
   wait_vmcnt<0>();
@@ -257,10 +263,9 @@ __global__ __launch_bounds__(256, 1) void gemm_large_kernel(
   auto row_of = [&](int mt, int e) { return m0 + wm * 128 + mt * 32 + 8 * (e >> 2) + 4 * khi + (e & 3); };
   if constexpr (EPI == 2) {
     const int F = N >> 1;
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int sbg = (n0 >> 6) + wn * 2 + j;
-      if (sbg > last_sb) continue;
+    {
+      const int sbg = (n0 >> 6) + wn, j = 0;
+      if (sbg <= last_sb) {
       const int f = sbg * 32 + col_l;
 #pragma unroll
       for (int mt = 0; mt < 4; ++mt)
@@ -275,6 +280,7 @@ __global__ __launch_bounds__(256, 1) void gemm_large_kernel(
             out_bf16[off] = f32_to_bf16(v);
           }
         }
+      }
     }
   } else if constexpr (EPI == 3) {
     // grouped down: row = entry ent0 + row of the expert -> (token, slot).
@@ -286,8 +292,8 @@ __global__ __launch_bounds__(256, 1) void gemm_large_kernel(
     int* t_row = reinterpret_cast<int*>(smem);
     float* t_wt = reinterpret_cast<float*>(smem) + kLgBM;
     {
-      const int row = m0 + threadIdx.x;  // 256 threads, one tile row each
-      if (row < rows) {
+      const int row = m0 + threadIdx.x;  // the first 256 threads, one tile row each
+      if (threadIdx.x < kLgBM && row < rows) {
         const int asg = g.assign[ent0 + row];
         const int tok = asg / g.k, slot = asg - tok * g.k;
         t_row[threadIdx.x] = slot * g.n + tok;
@@ -305,8 +311,8 @@ __global__ __launch_bounds__(256, 1) void gemm_large_kernel(
         const float wt = t_wt[lr];
         float* dst = out + (size_t)t_row[lr] * ldo;
 #pragma unroll
-        for (int nt = 0; nt < 4; ++nt) {
-          const int col = n0 + wn * 128 + nt * 32 + col_l;
+        for (int nt = 0; nt < 2; ++nt) {
+          const int col = n0 + wn * 64 + nt * 32 + col_l;
           if (col < N) dst[col] = acc[mt][nt][e] * wt;
         }
       }
@@ -318,12 +324,12 @@ __global__ __launch_bounds__(256, 1) void gemm_large_kernel(
     for (int mt = 0; mt < 4; ++mt) {
       const bool full = m0 + wm * 128 + mt * 32 + 32 <= M;
 #pragma unroll
-      for (int np = 0; np < 2; ++np) {
+      for (int np = 0; np < 1; ++np) {
         float old[2][16];
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
           const int nt = 2 * np + h;
-          const int col = n0 + wn * 128 + nt * 32 + col_l;
+          const int col = n0 + wn * 64 + nt * 32 + col_l;
 #pragma unroll
           for (int e = 0; e < 16; ++e) {
             old[h][e] = 0.f;
@@ -336,7 +342,7 @@ __global__ __launch_bounds__(256, 1) void gemm_large_kernel(
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
           const int nt = 2 * np + h;
-          const int col = n0 + wn * 128 + nt * 32 + col_l;
+          const int col = n0 + wn * 64 + nt * 32 + col_l;
 #pragma unroll
           for (int e = 0; e < 16; ++e) {
             const int row = row_of(mt, e);
@@ -357,7 +363,7 @@ hipError_t launch_gemm_large(int m, int n_out, int k, int ldx, int x_tiled, int 
                              hipStream_t st) {
   if (m == 0) return hipSuccess;
   const int tiles_m = (m + kLgBM - 1) / kLgBM, tiles_n = (n_out + kLgBN - 1) / kLgBN;
-  const dim3 grid(tiles_m * tiles_n), block(256);
+  const dim3 grid(tiles_m * tiles_n), block(64 * kLgWaves);
   float* of = reinterpret_cast<float*>(out);
   bf16_t* ob = reinterpret_cast<bf16_t*>(out);
   const GroupArgs none{};
@@ -382,7 +388,7 @@ hipError_t launch_gemm_grouped(int down, int m, int n_out, int k, const bf16_t* 
                                hipStream_t st) {
   if (m == 0 || max_tiles_m == 0) return hipSuccess;
   const int tiles_n = (n_out + kLgBN - 1) / kLgBN;
-  const dim3 grid(max_tiles_m * tiles_n), block(256);
+  const dim3 grid(max_tiles_m * tiles_n), block(64 * kLgWaves);
   if (down)
     hipLaunchKernelGGL((gemm_large_kernel<3, 0, 1>), grid, block, 0, st, x, k, m, w, n_out, k,
                        static_cast<float*>(out), n_out, nullptr, 0, max_tiles_m, tiles_n, g);
