@@ -124,13 +124,15 @@ DECODE_DIMS = [(8, 8, 128), (16, 8, 128), (32, 8, 128), (32, 4, 128),
 MODES = ["scale8", "scale32", "rise", "dominant"]
 
 
-@pytest.mark.parametrize("splits", [4, 1])
-@pytest.mark.parametrize("mode", MODES)
+# four splits for every mode; one split for the rise case (the within-split
+# rescale with a whole candidate in one split)
+MODE_SPLITS = [(m, 4) for m in MODES] + [("rise", 1)]
+
+
+@pytest.mark.parametrize("mode,splits", MODE_SPLITS)
 @pytest.mark.parametrize("hq,hkv,d", DECODE_DIMS)
 def test_decode_attention_softmax_edges(S, hq, hkv, d, mode, splits):
     sevo = S
-    if splits == 1 and mode != "rise":
-        pytest.skip("one split: the rise case covers the within-split rescale")
     lengths = [1024, 700, 1000, 333]
     pop = make_population(lengths, seed=hq * 131 + hkv * 7 + d)
     rng = np.random.default_rng([hq, hkv, d, MODES.index(mode), splits])
