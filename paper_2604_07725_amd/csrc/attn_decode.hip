@@ -579,18 +579,39 @@ __global__ __launch_bounds__(64) void attn_combine_kernel(const float* __restric
   int ns = (npg + chunk - 1) / chunk;
   ns = ns > S ? S : ns;
   const size_t base = ((size_t)i * hq + j) * S;
+  // splits in order, four splits' loads issued together (a load per split
+  // and pass would wait out one memory latency each)
   float M = -INFINITY;
-  for (int s = 0; s < ns; ++s) M = fmaxf(M, part_ml[(base + s) * 2]);
+  for (int s0 = 0; s0 < ns; s0 += 4) {
+    float mm[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) mm[j] = s0 + j < ns ? part_ml[(base + s0 + j) * 2] : -INFINITY;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) M = fmaxf(M, mm[j]);
+  }
   float L = 0.f, a[E];
 #pragma unroll
   for (int e = 0; e < E; ++e) a[e] = 0.f;
-  for (int s = 0; s < ns; ++s) {
-    const float ms = part_ml[(base + s) * 2];
-    if (ms == -INFINITY) continue;
-    const float f = exp2f(ms - M);
-    L += part_ml[(base + s) * 2 + 1] * f;
+  for (int s0 = 0; s0 < ns; s0 += 4) {
+    float ms[4], ls[4], ac[4][E];
 #pragma unroll
-    for (int e = 0; e < E; ++e) a[e] += part_acc[(base + s) * D + threadIdx.x + 64 * e] * f;
+    for (int j = 0; j < 4; ++j) {
+      ms[j] = -INFINITY;
+      if (s0 + j < ns) {
+        ms[j] = part_ml[(base + s0 + j) * 2];
+        ls[j] = part_ml[(base + s0 + j) * 2 + 1];
+#pragma unroll
+        for (int e = 0; e < E; ++e) ac[j][e] = part_acc[(base + s0 + j) * D + threadIdx.x + 64 * e];
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      if (ms[j] == -INFINITY) continue;
+      const float f = exp2f(ms[j] - M);
+      L += ls[j] * f;
+#pragma unroll
+      for (int e = 0; e < E; ++e) a[e] += ac[j][e] * f;
+    }
   }
   const float inv = L > 0.f ? 1.0f / L : 0.f;
   // row-major [n][hq][D], or the tiled activation layout of [n][hq D] (the

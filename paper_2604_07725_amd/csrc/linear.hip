@@ -215,7 +215,15 @@ __global__ __launch_bounds__(256) void linear_epilogue_kernel(const float* __res
   for (size_t g = (size_t)blockIdx.x * blockDim.x + threadIdx.x; g < total4;
        g += (size_t)gridDim.x * blockDim.x) {
     f32x4 a = f32x4{0.f, 0.f, 0.f, 0.f};
-    for (int s = 0; s < S; ++s) a += *reinterpret_cast<const f32x4*>(part + s * MN + g * 4);
+    for (int s0 = 0; s0 < S; s0 += 4) {  // split order; four splits' loads together
+      f32x4 p[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        if (s0 + j < S) p[j] = *reinterpret_cast<const f32x4*>(part + (s0 + j) * MN + g * 4);
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        if (s0 + j < S) a += p[j];
+    }
     f32x4* dst = reinterpret_cast<f32x4*>(out_f32 + g * 4);
     if (mode == 1) *dst = *dst + a;
     else *dst = a;

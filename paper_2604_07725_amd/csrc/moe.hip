@@ -39,8 +39,17 @@ __global__ __launch_bounds__(64) void moe_route_kernel(const float* __restrict__
     const int e = lane + 64 * i;
     float acc = -INFINITY;
     if (e < E) {
+      // split order; eight splits' loads issued together
       acc = 0.f;
-      for (int s = 0; s < S; ++s) acc += part[((size_t)s * n + t) * E + e];
+      for (int s0 = 0; s0 < S; s0 += 8) {
+        float p[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+          if (s0 + j < S) p[j] = part[((size_t)(s0 + j) * n + t) * E + e];
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+          if (s0 + j < S) acc += p[j];
+      }
     }
     v[i] = acc;
   }
@@ -454,7 +463,15 @@ __global__ __launch_bounds__(256) void moe_sum_slots_kernel(const float* __restr
   for (size_t g = (size_t)blockIdx.x * blockDim.x + threadIdx.x; g < total4;
        g += (size_t)gridDim.x * blockDim.x) {
     f32x4 acc = *reinterpret_cast<const f32x4*>(part + g * 4);
-    for (int j = 1; j < k; ++j) acc += *reinterpret_cast<const f32x4*>(part + j * plane + g * 4);
+    for (int j0 = 1; j0 < k; j0 += 8) {  // slot order; eight slots' loads together
+      f32x4 p[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        if (j0 + j < k) p[j] = *reinterpret_cast<const f32x4*>(part + (j0 + j) * plane + g * 4);
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        if (j0 + j < k) acc += p[j];
+    }
     *reinterpret_cast<f32x4*>(out + g * 4) = acc;
   }
 }

@@ -152,9 +152,22 @@ __global__ __launch_bounds__(64) void qk_norm_rope_append_kernel(RopeAppendArgs 
   const float* src = a.qkv + (size_t)i * qkv_ld + (size_t)hh * a.d;
   float u0 = 0.f, u1 = 0.f;
   if (act) {
-    for (int sp = 0; sp < a.qkv_splits; ++sp) {  // split-K partials, in split order
-      u0 += src[sp * split_stride + m];
-      u1 += src[sp * split_stride + m + half];
+    // split-K partials in split order; four splits' loads issued together
+    // (a load per iteration would wait out one memory latency per split)
+    for (int s0 = 0; s0 < a.qkv_splits; s0 += 4) {
+      float v0[4], v1[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        if (s0 + j < a.qkv_splits) {
+          v0[j] = src[(s0 + j) * split_stride + m];
+          v1[j] = src[(s0 + j) * split_stride + m + half];
+        }
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        if (s0 + j < a.qkv_splits) {
+          u0 += v0[j];
+          u1 += v1[j];
+        }
     }
   }
   rope_head(a, rope_token(a, i, m), i, hh, m, u0, u1);
