@@ -64,6 +64,8 @@ constexpr int kDppQuadXor1 = 0xB1;  // quad_perm [1,0,3,2]
 constexpr int kDppQuadXor2 = 0x4E;  // quad_perm [2,3,0,1]
 constexpr int kDppRowRor4 = 0x124;
 constexpr int kDppRowRor8 = 0x128;
+constexpr int kDppRowMirror = 0x140;      // lane i <- lane 15 - i of its row
+constexpr int kDppRowHalfMirror = 0x141;  // lane i <- lane 7 - i of its 8-lane half row
 
 // sum over the 4 lanes of each quad (every lane gets the result)
 __device__ __forceinline__ float quad_sum(float v) {

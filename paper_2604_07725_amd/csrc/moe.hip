@@ -75,19 +75,42 @@ __global__ __launch_bounds__(64) void moe_route_kernel(const float* __restrict__
         bi = e;
       }
     }
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-      const float ov = __shfl_xor(bv, o, kWave);
-      const int oi = __shfl_xor(bi, o, kWave);
+    // wave arg-max in registers: quads, 8-lane halves of rows and rows by
+    // DPP, then pairs of rows and the two halves of the wave by the permlane
+    // swaps (each step merges a lane's pair with another lane's; the merge is
+    // symmetric, so both lanes keep the same pair)
+    auto merge = [&](float ov, int oi) {
       if (oi != 0x7FFFFFFF && (bi == 0x7FFFFFFF || ov > bv || (ov == bv && oi < bi))) {
         bv = ov;
         bi = oi;
       }
+    };
+    auto dpp_step = [&](auto ctrl) {
+      constexpr int C = decltype(ctrl)::value;
+      merge(dpp<C>(bv), __builtin_amdgcn_update_dpp(0, bi, C, 0xF, 0xF, false));
+    };
+    dpp_step(std::integral_constant<int, kDppQuadXor1>{});
+    dpp_step(std::integral_constant<int, kDppQuadXor2>{});
+    dpp_step(std::integral_constant<int, kDppRowHalfMirror>{});
+    dpp_step(std::integral_constant<int, kDppRowMirror>{});
+    {
+      const auto pv = __builtin_amdgcn_permlane16_swap(__float_as_int(bv), __float_as_int(bv), false, false);
+      const auto pi = __builtin_amdgcn_permlane16_swap(bi, bi, false, false);
+      bv = __int_as_float(pv[0]);
+      bi = pi[0];
+      merge(__int_as_float(pv[1]), pi[1]);
+    }
+    {
+      const auto pv = __builtin_amdgcn_permlane32_swap(__float_as_int(bv), __float_as_int(bv), false, false);
+      const auto pi = __builtin_amdgcn_permlane32_swap(bi, bi, false, false);
+      bv = __int_as_float(pv[0]);
+      bi = pi[0];
+      merge(__int_as_float(pv[1]), pi[1]);
     }
     // lane 0's choice for every lane (the order is total unless a NaN is
     // involved; then lanes could disagree)
     bi = __builtin_amdgcn_readfirstlane(bi);
-    bv = __shfl(bv, 0, kWave);
+    bv = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(bv)));
 #pragma unroll
     for (int i = 0; i < kMoeMaxExperts / 64; ++i)
       if (lane + 64 * i == bi) taken |= 1u << i;
