@@ -192,6 +192,20 @@ typedef struct {
 } sevo_attn_args;
 
 sevo_status sevo_attn_decode(const sevo_attn_args* a, void* stream);
+
+/* Separate K and V pools in the plain paged layout, bf16
+ * [num_pages][n_kv_heads][16 slots][head_dim] each (slot-major rows), ->
+ * the fused pool above (dst kv_pool, 2 x the bytes of one source pool), so a
+ * caller that keeps the plain layout (for example one filled by another
+ * prefill engine) can hand its cache to the attention and the decode step of
+ * LLM aggregation (Recombination paragraph of the method section; Algorithm
+ * 1, aggregation line).  Pure data movement: every element is copied bit for
+ * bit.  head_dim 64 or 128 (else UNSUPPORTED); the three pools are
+ * caller-owned, 16-byte aligned, and dst must not overlap either source
+ * (INVALID_ARGUMENT).  num_pages 0 is a no-op.  Stream-ordered; not part of
+ * the decode step. */
+sevo_status sevo_pack_kv(const void* k_pool, const void* v_pool, int64_t num_pages,
+                         int32_t n_kv_heads, int32_t head_dim, void* kv_pool, void* stream);
 /* Split count the library uses when num_splits == 0. */
 int32_t sevo_attn_plan_splits(int32_t n, int32_t n_kv_heads, int32_t max_pages);
 /* Workspace for sevo_attn_decode with the given split count (0 = planned). */

@@ -46,6 +46,9 @@ struct RopeAppendArgs {
   const int32_t* row_of_token = nullptr;
 };
 hipError_t launch_qk_norm_rope_append(const RopeAppendArgs& a, hipStream_t st);
+// separate K, V pools [tiles][16][d] -> the fused pool [tiles][2][16 d]; d 64 or 128
+hipError_t launch_pack_kv(const bf16_t* k_src, const bf16_t* v_src, size_t tiles, int d,
+                          bf16_t* kv, hipStream_t st);
 hipError_t launch_fill_bf16(bf16_t* dst, int64_t count, uint64_t key, int64_t offset, float mul,
                             float add, int use_add, hipStream_t st);
 

@@ -139,6 +139,50 @@ __device__ __forceinline__ void rope_head(const RopeAppendArgs& a, const RopeTok
   }
 }
 
+// Separate K and V pools [page][head][16 slots][d] (row-major slots) -> the
+// fused pool [page][head][K tile | V tile] that the attention kernels read:
+// one workgroup (2 d threads) per (page, head) pair, grid-stride.  Every
+// thread moves 8 consecutive dims of one slot: K straight into its 32-dim
+// block (a 16-byte store), V through LDS so that the dim-major V tile is
+// written in 16-byte runs of 8 slots.
+__global__ __launch_bounds__(256) void pack_kv_kernel(const bf16_t* __restrict__ k_src,
+                                                      const bf16_t* __restrict__ v_src,
+                                                      size_t tiles, int d,
+                                                      bf16_t* __restrict__ kv) {
+  __shared__ __align__(16) bf16_t vt[kPage * 128];
+  const int t = threadIdx.x;
+  const int s = t / (d >> 3), e0 = (t % (d >> 3)) * 8;  // slot, first dim
+  const int e = t >> 1, h = t & 1;                      // V: dim, slot half
+  const size_t tile_elems = (size_t)kPage * d;
+  for (size_t tl = blockIdx.x; tl < tiles; tl += gridDim.x) {
+    const size_t src = tl * tile_elems + (size_t)s * d + e0;
+    const u32x4 kw = *reinterpret_cast<const u32x4*>(k_src + src);
+    const u32x4 vw = *reinterpret_cast<const u32x4*>(v_src + src);
+    bf16_t* kt = kv + tl * 2 * tile_elems;
+    *reinterpret_cast<u32x4*>(kt + ((e0 >> 5) * kPage + s) * 32 + (e0 & 31)) = kw;
+    __syncthreads();  // the previous tile's V reads are done
+    *reinterpret_cast<u32x4*>(vt + s * d + e0) = vw;
+    __syncthreads();
+    uint16_t r[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) r[j] = __builtin_bit_cast(uint16_t, vt[(8 * h + j) * d + e]);
+    u32x4 o;
+    o.x = r[0] | ((uint32_t)r[1] << 16);
+    o.y = r[2] | ((uint32_t)r[3] << 16);
+    o.z = r[4] | ((uint32_t)r[5] << 16);
+    o.w = r[6] | ((uint32_t)r[7] << 16);
+    *reinterpret_cast<u32x4*>(kt + tile_elems + e * kPage + 8 * h) = o;
+  }
+}
+
+hipError_t launch_pack_kv(const bf16_t* k_src, const bf16_t* v_src, size_t tiles, int d,
+                          bf16_t* kv, hipStream_t st) {
+  if (tiles == 0) return hipSuccess;
+  const unsigned grid = (unsigned)(tiles < 65536 ? tiles : 65536);
+  hipLaunchKernelGGL(pack_kv_kernel, dim3(grid), dim3(2 * d), 0, st, k_src, v_src, tiles, d, kv);
+  return hipGetLastError();
+}
+
 // One wave per (candidate, head); the QKV projection given as the fp32
 // split-K partials of the GEMM, summed here in split order.
 __global__ __launch_bounds__(64) void qk_norm_rope_append_kernel(RopeAppendArgs a) {

@@ -669,6 +669,32 @@ SEVO_API sevo_status sevo_pack_weight(const void* src, void* dst, int32_t n_out,
   return e == hipSuccess ? SEVO_OK : hip_fail(e, "sevo_pack_weight");
 }
 
+SEVO_API sevo_status sevo_pack_kv(const void* k_pool, const void* v_pool, int64_t num_pages,
+                                  int32_t n_kv_heads, int32_t head_dim, void* kv_pool,
+                                  void* stream) {
+  if (num_pages < 0 || n_kv_heads < 1)
+    return fail(SEVO_ERR_INVALID_ARGUMENT, "bad num_pages / n_kv_heads");
+  if (head_dim != 64 && head_dim != 128)
+    return fail(SEVO_ERR_UNSUPPORTED, "head_dim must be 64 or 128");
+  if (num_pages == 0) return SEVO_OK;
+  if (!k_pool || !v_pool || !kv_pool || !aligned16(k_pool) || !aligned16(v_pool) ||
+      !aligned16(kv_pool))
+    return fail(SEVO_ERR_INVALID_ARGUMENT, "null or misaligned pointer");
+  const size_t tiles = (size_t)num_pages * n_kv_heads;
+  const size_t src_bytes = tiles * SEVO_PAGE_SIZE * head_dim * 2;
+  const uintptr_t d0 = reinterpret_cast<uintptr_t>(kv_pool);
+  for (const void* p : {k_pool, v_pool}) {
+    const uintptr_t s0 = reinterpret_cast<uintptr_t>(p);
+    if (s0 < d0 + 2 * src_bytes && d0 < s0 + src_bytes)
+      return fail(SEVO_ERR_INVALID_ARGUMENT, "source and destination pools overlap");
+  }
+  hipError_t e = sevo::launch_pack_kv(static_cast<const sevo::bf16_t*>(k_pool),
+                                      static_cast<const sevo::bf16_t*>(v_pool), tiles, head_dim,
+                                      static_cast<sevo::bf16_t*>(kv_pool),
+                                      static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? SEVO_OK : hip_fail(e, "sevo_pack_kv");
+}
+
 static void fill_rope_args(const sevo_model* m, int layer, const float* qkv, int qkv_splits,
                            int n, const int32_t* pos, const int32_t* pt, int max_pages,
                            int64_t num_pages, void* q_out, void* kvp,

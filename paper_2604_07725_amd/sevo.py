@@ -133,6 +133,7 @@ _SIGS = {
     "sevo_linear_workspace_bytes": ([i32, i32, i32, i32], sz),
     "sevo_linear_plan": ([i32, i32, i32, i32, i32, C.POINTER(i32)], i32),
     "sevo_pack_weight": ([vp, vp, i32, i32, i32, vp], i32),
+    "sevo_pack_kv": ([vp, vp, i64, i32, i32, vp, vp], i32),
     "sevo_qk_norm_rope_append": ([vp, i32, vp, i32, vp, vp, i32, i64, vp, vp, vp], i32),
     "sevo_fill_normal_bf16": ([vp, i64, u64, i64, f32, f32, i32, vp], i32),
     "sevo_validate_paging": ([vp, vp, i32, i32, i64, vp], i32),
@@ -387,6 +388,16 @@ def sevo_pack_weight(src, kind=PACK_PLAIN, dst=None, stream=None):
         dst = torch.empty_like(src)
     _check(lib().sevo_pack_weight(_p(src), _p(dst), n_out, k, int(kind), _stream(stream)))
     return dst
+
+
+def sevo_pack_kv(k_pool, v_pool, kv_pool=None, stream=None):
+    """Plain K and V pools bf16 [pages, hkv, 16, d] -> the fused pool [pages, hkv, 2, 16 d]."""
+    pages, hkv, slots, d = k_pool.shape
+    if kv_pool is None:
+        kv_pool = torch.empty(pages, hkv, 2, slots * d, dtype=k_pool.dtype, device=k_pool.device)
+    _check(lib().sevo_pack_kv(_p(k_pool), _p(v_pool), pages, hkv, d, _p(kv_pool),
+                              _stream(stream)))
+    return kv_pool
 
 
 def sevo_qk_norm_rope_append(model, layer, qkv, positions, page_table, kv_pool, q_out=None,

@@ -225,6 +225,24 @@ def test_pack_weight_rejects_bad_arguments(kw, status):
 
 
 @pytest.mark.parametrize("kw,status", [
+    (dict(head_dim=96), sevo.UNSUPPORTED),
+    (dict(n_kv_heads=0), sevo.INVALID_ARGUMENT),
+    (dict(num_pages=-1), sevo.INVALID_ARGUMENT),
+    (dict(k_pool=0), sevo.INVALID_ARGUMENT),
+    (dict(v_pool=(1 << 22) + 8), sevo.INVALID_ARGUMENT),                 # misaligned
+    (dict(kv_pool=(1 << 20) + 4096), sevo.INVALID_ARGUMENT),             # overlaps k_pool
+    (dict(kv_pool=(1 << 22) - 8192), sevo.INVALID_ARGUMENT),             # overlaps v_pool
+    (dict(num_pages=0, k_pool=0, v_pool=0, kv_pool=0), sevo.OK),         # nothing to move
+])
+def test_pack_kv_rejects_bad_arguments(kw, status):
+    a = dict(k_pool=1 << 20, v_pool=1 << 22, num_pages=4, n_kv_heads=2, head_dim=64,
+             kv_pool=1 << 24)
+    a.update(kw)
+    assert sevo.lib().sevo_pack_kv(a["k_pool"], a["v_pool"], a["num_pages"], a["n_kv_heads"],
+                                   a["head_dim"], a["kv_pool"], None) == status
+
+
+@pytest.mark.parametrize("kw,status", [
     (dict(rows=-1), sevo.INVALID_ARGUMENT),
     (dict(cols=4094), sevo.INVALID_ARGUMENT),
     (dict(n_partials=17), sevo.INVALID_ARGUMENT),

@@ -41,6 +41,63 @@ def test_device_fill_equals_host_generator(S, count, offset, std, mean):
     np.testing.assert_array_equal(bf16_bits(t), synth.fill_bf16_bits(count, key, offset, std, mean))
 
 
+# ------------------------------------------------------------------ KV layout
+def _fused_from_plain(kp, vp):
+    """Host form of the fused pool from plain pools [P][hkv][16][d] (uint16
+    bit patterns), through the K and V tile offsets of the layout."""
+    P, hkv, slots, d = kp.shape
+    fused = np.zeros((P, hkv, 2, slots * d), np.uint16)
+    s, e = np.meshgrid(np.arange(slots), np.arange(d), indexing="ij")
+    fused[:, :, 0][:, :, od.k_tile_offset(s, e)] = kp
+    fused[:, :, 1][:, :, od.v_tile_offset(s, e)] = vp
+    return fused
+
+
+@pytest.mark.parametrize("pages,hkv,d", [(1, 1, 64), (37, 2, 64), (37, 8, 128), (5000, 4, 128)])
+def test_pack_kv_bit_exact(S, pages, hkv, d):
+    """Plain K and V pools to the fused pool: every element moved bit for bit
+    to its place in the K (32-dim blocks) and V (dim-major) tiles."""
+    sevo, _ = S
+    say(f"pack_kv pages={pages} hkv={hkv} d={d}")
+    rng = np.random.default_rng([pages, hkv, d])
+    kp = rng.integers(0, 1 << 16, size=(pages, hkv, 16, d), dtype=np.uint16)
+    vp = rng.integers(0, 1 << 16, size=(pages, hkv, 16, d), dtype=np.uint16)
+    kd = torch.from_numpy(kp.view(np.int16)).cuda().view(torch.bfloat16)
+    vd = torch.from_numpy(vp.view(np.int16)).cuda().view(torch.bfloat16)
+    out = torch.full((pages, hkv, 2, 16 * d), float("nan"), dtype=torch.bfloat16, device="cuda")
+    sevo.sevo_pack_kv(kd, vd, out)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(bf16_bits(out), _fused_from_plain(kp, vp))
+
+
+@pytest.mark.parametrize("hq,hkv,d", [(32, 8, 128), (16, 2, 64)])
+def test_attention_over_packed_plain_pools(S, hq, hkv, d):
+    """A cache kept in the plain layout (separate K and V pools, slot-major
+    rows), packed once, gives the oracle's attention over the candidates' keys."""
+    sevo, _ = S
+    lengths = [700, 1, 333, 1024, 65]
+    pop = make_population(lengths, seed=hq + d)
+    rng = np.random.default_rng([hq, hkv, d, 7])
+    kp = round_bf16(rng.standard_normal((pop.n_pages, hkv, 16, d))).astype(np.float32)
+    vp = round_bf16(rng.standard_normal((pop.n_pages, hkv, 16, d))).astype(np.float32)
+    q = round_bf16(rng.standard_normal((pop.n, hq, d))).astype(np.float32)
+    say(f"attention over packed plain pools hq={hq} hkv={hkv} d={d}")
+    kd = torch.from_numpy(kp).to(torch.bfloat16).cuda()
+    vd = torch.from_numpy(vp).to(torch.bfloat16).cuda()
+    kv = sevo.sevo_pack_kv(kd, vd)
+    out = sevo.sevo_attn_decode(torch.from_numpy(q).to(torch.bfloat16).cuda(), kv,
+                                torch.from_numpy(pop.page_table).cuda(),
+                                torch.from_numpy(pop.lengths).cuda())
+    torch.cuda.synchronize()
+    o = to_np(out)
+    for i, n in enumerate(lengths):
+        pages = pop.page_table[i, :(n + 15) // 16]
+        K = kp[pages].transpose(1, 0, 2, 3).reshape(hkv, -1, d)[:, :n].astype(np.float64)
+        V = vp[pages].transpose(1, 0, 2, 3).reshape(hkv, -1, d)[:, :n].astype(np.float64)
+        ref = od.attention_dense(q[i].astype(np.float64), K, V, d ** -0.5)
+        assert attn_rel_err(o[i], ref) <= min(ATTN_REL_TOL, 8e-3), i
+
+
 # ------------------------------------------------------------------ attention
 def _attn_case(S, shape, lengths, seed, num_splits=0, shuffle=True, pt_override=None):
     sevo, di = S
